@@ -1,0 +1,374 @@
+"""Pins for the float64 oracle: checks against what the paper and the
+mathematics fix, independent of the oracle's own code.
+
+Each pin is a function ``pin_xxx(lib_path=None)`` that raises AssertionError
+when the oracle disagrees.  test_oracle_pins.py runs them on the oracle;
+test_oracle_mutants.py runs them on deliberately broken copies of the oracle
+and requires every broken copy to fail at least one pin.
+
+What pins what (paper passages in brackets):
+  * gated linear attention, parallel form (QK^T (.) decay mask) V  [Sec. 2.1,
+    eq. linear_attn_parallel]: readout with lambda = 1 for any tau, C, and the
+    sum of all cached states;
+  * one state per token (tau <= 0, C >= T) equals lambda-weighted masked
+    attention, C = 1 equals lambda_0-weighted linear attention  [Sec. 3.2,
+    eq. capacity_bounded_output];
+  * brute force on membership lists: Alg. 2 replayed on lists of token ids
+    with a scalar argmin, outputs as sums over member tokens  [Alg. 2, Sec. 3.2];
+  * closed forms of the score: identical tokens, orthogonal keys, scalar states
+    (sign flips), scale invariance, 0 <= I <= 2, and the rank-one expansion of
+    the score  [eq. importance_score, RMSNorm remark of Sec. 3.1];
+  * hand-computed merge schedule on scalar states  (tests/golden/);
+  * conservation (counts, scores, states) and C-independence of boundaries.
+"""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+
+from oracle import OracleCache, oracle_forward
+from paper_2606_10650_amd.workloads import WORKLOADS, make_inputs, to_f64
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+# ----------------------------------------------------------------------------
+# independent helpers (no oracle code)
+# ----------------------------------------------------------------------------
+
+def cum_gate(g):
+    return np.cumsum(np.asarray(g, np.float64), axis=-1)
+
+
+def decay_mask(G):
+    """D[t, s] = exp(G_t - G_s) for s <= t, else 0 (G inclusive cumulative)."""
+    T = G.shape[0]
+    D = np.exp(np.minimum(G[:, None] - G[None, :], 0.0))
+    return np.tril(D) * np.tri(T)
+
+
+def gated_linear_attention(q, k, v, g):
+    """Textbook parallel form O = (Q K^T (.) M_decay) V of one head."""
+    D = decay_mask(cum_gate(g))
+    return ((q @ k.T) * D) @ v
+
+
+def replay_membership(b, merge, C):
+    """Replay the recorded decisions on lists of token ids (Alg. 2 with the
+    merges given).  Returns, per token t, the slots as lists of token ids."""
+    slots, hist = [], []
+    for t in range(len(b)):
+        if b[t]:
+            if len(slots) == C:
+                i = int(merge[t])
+                assert 0 <= i <= C - 2, f"t={t}: capacity reached but merge index {i}"
+                slots[i] = slots[i] + slots[i + 1]
+                del slots[i + 1]
+            else:
+                assert merge[t] == -1, f"t={t}: merge {merge[t]} below capacity"
+            slots.append([t])
+        else:
+            assert slots, "first token must open a state"
+            assert merge[t] == -1
+            slots[-1].append(t)
+        assert len(slots) <= C
+        hist.append([list(s) for s in slots])
+    return hist
+
+
+def brute_outputs(q, k, v, g, lam, hist):
+    """o_t = sum_j lam[t, j] sum_{s in slot j} exp(G_t - G_s) (q_t . k_s) v_s."""
+    G = cum_gate(g)
+    T = q.shape[0]
+    out = np.zeros((T, v.shape[1]))
+    for t in range(T):
+        for j, members in enumerate(hist[t]):
+            s = np.array(members)
+            w = np.exp(G[t] - G[s]) * (k[s] @ q[t])
+            lj = 1.0 if lam is None else lam[t, j]
+            out[t] += lj * (w @ v[s])
+    return out
+
+
+def rms_sq_norm(x2, D, eps_rms):
+    """||N(X)||^2 for ||X||^2 = x2 under RMSNorm over D entries."""
+    return x2 / (x2 / D + eps_rms)
+
+
+def score_rank_one(kt, vt, Sbar, eps, eps_rms):
+    """Score of token state k v^T against state Sbar via the rank-one expansion
+    ||N(s) - N(S)||^2 = a/rs^2 + b/rS^2 - 2 k^T S v/(rs rS)."""
+    D = Sbar.size
+    a = float(kt @ kt) * float(vt @ vt)
+    b = float((Sbar * Sbar).sum())
+    c = float(kt @ Sbar @ vt)
+    rs = np.sqrt(a / D + eps_rms)
+    rS = np.sqrt(b / D + eps_rms)
+    num = max(0.0, a / rs**2 + b / rS**2 - 2.0 * c / (rs * rS))
+    return np.sqrt(num) / (np.sqrt(b) / rS + eps)
+
+
+def f64_inputs(name, **kw):
+    w = WORKLOADS[name].replace(**kw) if kw else WORKLOADS[name]
+    x = make_inputs(w)
+    f = lambda a: to_f64(a, w.dtype)
+    return w, f(x["q"]), f(x["k"]), f(x["v"]), x["g"].astype(np.float64), f(x["lam"])
+
+
+# ----------------------------------------------------------------------------
+# pins
+# ----------------------------------------------------------------------------
+
+def pin_lambda_one_is_gated_linear_attention(lib_path=None):
+    """lambda = 1: the sum over states is the single gated state for any tau, C."""
+    w, q, k, v, g, _ = f64_inputs("cfg1", T=192)
+    ref = np.stack([gated_linear_attention(q[h], k[h], v[h], g[h]) for h in range(len(q))])
+    for C, tau in ((8, 0.5), (3, 0.5), (1, 0.5), (4, 0.0), (2, 0.3)):
+        r = oracle_forward(k, v, g, C, tau, q=q, lib_path=lib_path)
+        err = np.abs(r["out"] - ref).max() / np.abs(ref).max()
+        assert err < 1e-12, f"C={C} tau={tau}: rel err {err}"
+
+
+def pin_single_state_and_one_state_per_token(lib_path=None):
+    """C = 1 or tau = inf: o_t = lam_{t,0} q_t^T P_t.  tau <= 0 with C >= T:
+    o_t = sum_s lam_{t,s} exp(G_t - G_s) (q_t . k_s) v_s."""
+    w, q, k, v, g, _ = f64_inputs("cfg1", T=96)
+    rng = np.random.default_rng(7)
+    T = q.shape[1]
+    lam = 1.0 + 0.5 * rng.standard_normal((q.shape[0], T, T))
+    for h in range(q.shape[0]):
+        base = gated_linear_attention(q[h], k[h], v[h], g[h])
+        for C, tau in ((1, 0.5), (5, np.inf)):
+            r = oracle_forward(k[h:h + 1], v[h:h + 1], g[h:h + 1], C, tau, q=q[h:h + 1],
+                               lam=lam[h:h + 1, :, :C], lib_path=lib_path)
+            ref = lam[h, :, :1] * base
+            assert np.abs(r["out"][0] - ref).max() < 1e-12 * np.abs(ref).max(), (C, tau)
+            assert r["b"][0, 0] == 1 and r["b"][0, 1:].sum() == 0
+        r = oracle_forward(k[h:h + 1], v[h:h + 1], g[h:h + 1], T, 0.0, q=q[h:h + 1],
+                           lam=lam[h:h + 1], lib_path=lib_path)
+        D = decay_mask(cum_gate(g[h]))
+        ref = ((q[h] @ k[h].T) * D * lam[h]) @ v[h]
+        assert np.abs(r["out"][0] - ref).max() < 1e-12 * np.abs(ref).max()
+        assert r["b"][0].all() and (r["merge"][0] == -1).all()
+
+
+def pin_brute_force_membership(lib_path=None):
+    """Tiny inputs: outputs and merges equal a replay of Alg. 2 on lists of token
+    ids with a scalar argmin over (sum of scores)/(count)."""
+    for name, kw, C in (("cfg1", dict(T=160, dk=8, dv=8, n_seg=12), 4),
+                        ("cfg1_iid", dict(T=48, dk=4, dv=4), 3),
+                        ("cfg1", dict(T=64, dk=4, dv=6, n_seg=9), 2),
+                        ("cfg1", dict(T=80, dk=6, dv=4, n_seg=20, rho2=0.9), 5)):
+        w, q, k, v, g, lam = f64_inputs(name, C=C, **kw)
+        r = oracle_forward(k, v, g, C, w.tau, q=q, lam=lam, lib_path=lib_path)
+        for h in range(q.shape[0]):
+            b, merge, score = r["b"][h], r["merge"][h], r["score"][h]
+            hist = replay_membership(b, merge, C)
+            out = brute_outputs(q[h], k[h], v[h], g[h], lam[h], hist)
+            err = np.abs(out - r["out"][h]).max() / np.abs(out).max()
+            assert err < 1e-11, f"{name} C={C}: brute-force output rel err {err}"
+            # independent scalar Alg. 2 on membership lists
+            prev = []
+            for t in range(len(b)):
+                if b[t] and len(prev) == C:
+                    dens = [(sum(score[prev[i]]) + sum(score[prev[i + 1]])) /
+                            (len(prev[i]) + len(prev[i + 1])) for i in range(C - 1)]
+                    order = sorted(range(C - 1), key=lambda i: (dens[i], i))
+                    close = len(order) > 1 and dens[order[1]] - dens[order[0]] <= 1e-9 * abs(
+                        dens[order[0]])
+                    if not close:
+                        assert merge[t] == order[0], f"t={t}: merge {merge[t]} vs {order[0]}"
+                prev = hist[t]
+            # m_t and counts
+            assert all(len(hist[t]) == r["m"][h, t] for t in range(len(b)))
+
+
+def pin_score_identical_tokens(lib_path=None):
+    """Identical tokens, no decay: the newest state after n tokens is n s, so
+    I_{n+1} = sqrt(a) |1/r_1 - n/r_n| / (n sqrt(a)/r_n + eps) with
+    r_x = sqrt(x^2 a / D + eps_rms).  eps_rms is chosen comparable to a/D so
+    that its handling matters."""
+    dk, dv, T = 3, 2, 7
+    kv = np.array([0.3, -0.2, 0.1])
+    vv = np.array([0.05, 0.02])
+    a = float(kv @ kv) * float(vv @ vv)
+    D = dk * dv
+    eps, eps_rms = 1e-3, a / D
+    k = np.tile(kv, (1, T, 1))
+    v = np.tile(vv, (1, T, 1))
+    g = np.zeros((1, T))
+    r = oracle_forward(k, v, g, 4, 10.0, lib_path=lib_path, eps=eps, eps_rms=eps_rms, full=True,
+                       q=np.ones((1, T, dk)))
+    r1 = np.sqrt(a / D + eps_rms)
+    for t in range(1, T):
+        n = t
+        rn = np.sqrt(n * n * a / D + eps_rms)
+        ref = np.sqrt(a) * abs(1.0 / r1 - n / rn) / (n * np.sqrt(a) / rn + eps)
+        assert abs(r["score"][0, t] - ref) < 1e-12, (t, r["score"][0, t], ref)
+    assert r["score"][0, 0] == 0.0 and r["b"][0, 0] == 1 and r["b"][0, 1:].sum() == 0
+
+
+def pin_score_orthogonal_key(lib_path=None):
+    """A key orthogonal to every key of the newest state gives k^T S v = 0, so
+    I = sqrt(|N(s)|^2 + |N(S)|^2) / (|N(S)| + eps); decay enters through S."""
+    dk, dv = 4, 3
+    k = np.array([[[1.0, 0, 0, 0], [0.6, 0.8, 0, 0], [0, 0, 1.0, 0], [0.8, 0, 0, 0.6]]])
+    v = np.array([[[1.0, 2.0, -1.0], [0.5, 1.0, 0.5], [-1.0, 0.3, 2.0], [0.2, 0.2, 0.2]]])
+    g = np.array([[0.0, -0.3, -0.7, -0.1]])
+    eps, eps_rms = 1e-4, 0.05
+    D = dk * dv
+    bo = np.array([[-1, 0, 1, 0]], np.int8)   # tokens 0-1 form one state, 2 opens one
+    r = oracle_forward(k, v, g, 3, 0.5, lib_path=lib_path, eps=eps, eps_rms=eps_rms,
+                       b_override=bo, q=np.ones((1, 4, dk)))
+    # token 2 against the decayed state of tokens 0, 1
+    S = np.exp(g[0, 1] + g[0, 2]) * np.outer(k[0, 0], v[0, 0]) + np.exp(g[0, 2]) * np.outer(
+        k[0, 1], v[0, 1])
+    s = np.outer(k[0, 2], v[0, 2])
+    ns2 = rms_sq_norm((s * s).sum(), D, eps_rms)
+    nS2 = rms_sq_norm((S * S).sum(), D, eps_rms)
+    ref = np.sqrt(ns2 + nS2) / (np.sqrt(nS2) + eps)
+    assert abs(r["score"][0, 2] - ref) < 1e-12, (r["score"][0, 2], ref)
+    # token 3 against the single-token state of token 2 (k orthogonal again)
+    S = np.exp(g[0, 3]) * s
+    s = np.outer(k[0, 3], v[0, 3])
+    ns2 = rms_sq_norm((s * s).sum(), D, eps_rms)
+    nS2 = rms_sq_norm((S * S).sum(), D, eps_rms)
+    ref3 = np.sqrt(ns2 + nS2) / (np.sqrt(nS2) + eps)
+    assert abs(r["score"][0, 3] - ref3) < 1e-12, (r["score"][0, 3], ref3)
+
+
+def pin_score_rank_one_expansion(lib_path=None):
+    """Every score equals the rank-one expansion of the definition, evaluated on
+    the decayed newest state rebuilt from the replayed membership lists."""
+    w, q, k, v, g, lam = f64_inputs("cfg1", T=96, dk=8, dv=8, n_seg=6)
+    eps, eps_rms = 1e-3, 2e-3
+    r = oracle_forward(k, v, g, 4, w.tau, q=q, lam=lam[:, :, :4], eps=eps, eps_rms=eps_rms,
+                       lib_path=lib_path)
+    G = cum_gate(g)
+    for h in range(q.shape[0]):
+        hist = replay_membership(r["b"][h], r["merge"][h], 4)
+        for t in range(1, q.shape[1]):
+            newest = hist[t - 1][-1]
+            S = sum(np.exp(G[h, t] - G[h, s]) * np.outer(k[h, s], v[h, s]) for s in newest)
+            ref = score_rank_one(k[h, t], v[h, t], S, eps, eps_rms)
+            assert abs(r["score"][h, t] - ref) < 1e-10, (h, t, r["score"][h, t], ref)
+            assert r["b"][h, t] == (1 if r["score"][h, t] >= w.tau else 0)
+
+
+def pin_scalar_states_sign_flips(lib_path=None):
+    """d_k = d_v = 1, eps = eps_rms = 0: N(x) = sign(x), so I = 0 when the token
+    state has the sign of the newest state and 2 otherwise.  Two schedules worked
+    out by hand in tests/golden/: sign flips with tau = 1 (merges at index 0 and
+    1), and tau = 2 (the equality case of I >= tau) with exactly tied densities."""
+    for fixture in ("scalar_sign_flips.json", "scalar_ties.json"):
+        with open(os.path.join(GOLDEN, fixture)) as fh:
+            gold = json.load(fh)
+        kk = np.array(gold["k"], np.float64)[None, :, None]
+        vv = np.array(gold["v"], np.float64)[None, :, None]
+        g = np.array(gold["g"], np.float64)[None, :]
+        q = np.ones_like(kk)
+        lam = np.tile(np.array(gold["lambda_row"], np.float64), (1, kk.shape[1], 1))
+        r = oracle_forward(kk, vv, g, gold["C"], gold["tau"], q=q, lam=lam, eps=0.0,
+                           eps_rms=0.0, lib_path=lib_path)
+        assert r["score"][0].tolist() == gold["score"], (fixture, r["score"][0].tolist())
+        assert r["b"][0].tolist() == gold["b"], (fixture, r["b"][0].tolist())
+        assert r["merge"][0].tolist() == gold["merge"], (fixture, r["merge"][0].tolist())
+        assert r["m"][0].tolist() == gold["m"], (fixture, r["m"][0].tolist())
+        c = r["cache"]
+        m = int(c.m[0])
+        assert c.n[0, :m].tolist() == gold["final_n"], (fixture, c.n[0].tolist())
+        assert c.ibar[0, :m].tolist() == gold["final_ibar"], (fixture, c.ibar[0].tolist())
+        assert np.allclose(c.S[0, :m, 0, 0], gold["final_S"], rtol=0, atol=1e-12), fixture
+        assert np.allclose(r["out"][0, :, 0], gold["out"], rtol=0, atol=1e-12), fixture
+
+
+def pin_score_scale_invariance_and_range(lib_path=None):
+    """With eps = eps_rms = 0 the score is invariant to positive scaling of all
+    values or all keys; with eps > 0 it stays in [0, 2)."""
+    w, q, k, v, g, _ = f64_inputs("cfg1_iid", T=64, dk=8, dv=8)
+    w2, q2, k2, v2, g2, _ = f64_inputs("cfg1", T=64, dk=8, dv=8, n_seg=4)
+    for (kk, vv, gg) in ((k, v, g), (k2, v2, g2)):
+        r0 = oracle_forward(kk, vv, gg, 4, 0.5, eps=0.0, eps_rms=0.0, full=False,
+                            lib_path=lib_path)
+        r1 = oracle_forward(kk * 3.7, vv * 0.01, gg, 4, 0.5, eps=0.0, eps_rms=0.0, full=False,
+                            lib_path=lib_path)
+        assert np.abs(r0["score"] - r1["score"]).max() < 1e-12
+        r2 = oracle_forward(kk, vv, gg, 4, 0.5, full=False, lib_path=lib_path)
+        assert r2["score"].min() >= 0.0 and r2["score"].max() < 2.0
+    # opposite states give the maximum 2/(1+eps) ... with eps = 0 exactly 2
+    kk = np.array([[[1.0, 0.0], [1.0, 0.0]]])
+    vv = np.array([[[0.5, 0.5], [-1.0, -1.0]]])
+    r = oracle_forward(kk, vv, np.zeros((1, 2)), 2, 0.5, eps=0.0, eps_rms=0.0, full=False,
+                       lib_path=lib_path)
+    assert abs(r["score"][0, 1] - 2.0) < 1e-15
+
+
+def pin_conservation(lib_path=None):
+    """Counts, scores and states are conserved by merging: sum_j n_j = t,
+    sum_j Ibar_j = sum_s I_s, m_t = min(#boundaries, C), #merges =
+    max(0, #boundaries - C), and sum_j S_j equals the single gated state."""
+    for name, C in (("cfg1", 3), ("cfg1_iid", 8), ("cfg1", 8)):
+        w, q, k, v, g, lam = f64_inputs(name, T=256)
+        r = oracle_forward(k, v, g, C, w.tau, q=q, lam=lam[:, :, :C], lib_path=lib_path)
+        c = r["cache"]
+        G = cum_gate(g)
+        T = q.shape[1]
+        for h in range(q.shape[0]):
+            m = c.m[h]
+            assert m == min(int(r["b"][h].sum()), C)
+            assert int((r["merge"][h] >= 0).sum()) == max(0, int(r["b"][h].sum()) - C)
+            assert c.n[h, :m].sum() == T and (c.n[h, :m] > 0).all()
+            assert abs(c.ibar[h, :m].sum() - r["score"][h].sum()) < 1e-9
+            P = np.einsum("s,sa,sb->ab", np.exp(G[h, -1] - G[h]), k[h], v[h])
+            assert np.abs(c.S[h, :m].sum(0) - P).max() < 1e-12 * np.abs(P).max()
+            mt = np.minimum(np.cumsum(r["b"][h]), C)
+            assert (r["m"][h] == mt).all()
+
+
+def pin_boundaries_independent_of_capacity(lib_path=None):
+    """Capacity merges never touch the newest state, so b and I are the same
+    for every C >= 2; decisions mode agrees with full mode."""
+    w, q, k, v, g, lam = f64_inputs("cfg1", T=384, n_seg=30, rho2=0.9)
+    ref = oracle_forward(k, v, g, 2, w.tau, q=q, lam=lam[:, :, :2], lib_path=lib_path)
+    for C in (3, 8, 384):
+        lamC = np.ones((q.shape[0], q.shape[1], C))
+        r = oracle_forward(k, v, g, C, w.tau, q=q, lam=lamC, lib_path=lib_path)
+        assert (r["b"] == ref["b"]).all() and np.array_equal(r["score"], ref["score"])
+        rd = oracle_forward(k, v, g, C, w.tau, full=False, lib_path=lib_path)
+        assert (rd["b"] == r["b"]).all() and (rd["merge"] == r["merge"]).all()
+        assert np.abs(rd["score"] - r["score"]).max() < 1e-12
+
+
+def pin_continuation(lib_path=None):
+    """prefill(x[:T]) equals prefill(x[:T1]) followed by prefill(x[T1:]) on the
+    returned cache."""
+    w, q, k, v, g, lam = f64_inputs("cfg1", T=200, n_seg=10)
+    C = 4
+    lam = lam[:, :, :C]
+    full = oracle_forward(k, v, g, C, w.tau, q=q, lam=lam, lib_path=lib_path)
+    for T1 in (1, 77, 199):
+        a = oracle_forward(k[:, :T1], v[:, :T1], g[:, :T1], C, w.tau, q=q[:, :T1],
+                           lam=lam[:, :T1], lib_path=lib_path)
+        b = oracle_forward(k[:, T1:], v[:, T1:], g[:, T1:], C, w.tau, q=q[:, T1:],
+                           lam=lam[:, T1:], cache=a["cache"], lib_path=lib_path)
+        assert (np.concatenate([a["b"], b["b"]], 1) == full["b"]).all()
+        assert (np.concatenate([a["merge"], b["merge"]], 1) == full["merge"]).all()
+        o = np.concatenate([a["out"], b["out"]], 1)
+        assert np.abs(o - full["out"]).max() < 1e-12 * np.abs(full["out"]).max()
+
+
+ALL_PINS = [
+    pin_lambda_one_is_gated_linear_attention,
+    pin_single_state_and_one_state_per_token,
+    pin_brute_force_membership,
+    pin_score_identical_tokens,
+    pin_score_orthogonal_key,
+    pin_score_rank_one_expansion,
+    pin_scalar_states_sign_flips,
+    pin_score_scale_invariance_and_range,
+    pin_conservation,
+    pin_boundaries_independent_of_capacity,
+    pin_continuation,
+]

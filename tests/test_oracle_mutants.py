@@ -1,0 +1,81 @@
+"""Every plausible mistake planted in a copy of the oracle must fail a pin.
+
+Each mutant is a textual edit of dla_oracle.c (a dropped term, a wrong sign or
+index, a transposed operand, a wrong reading of an algorithm step), compiled
+to a temporary library.  The pins of tests/pins.py are run against it and at
+least one must fail; otherwise the pins would not catch that mistake.  CPU only.
+"""
+import os
+import subprocess
+import tempfile
+
+import pytest
+
+from tests import pins
+
+SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "oracle",
+                   "dla_oracle.c")
+
+MUTANTS = {
+    "no_decay": ("S[j * D + i] *= alpha;", "S[j * D + i] *= 1.0;"),
+    "decay_only_newest": ("for (int32_t j = full ? 0 : (m > 0 ? m - 1 : 0); j < m; ++j)",
+                          "for (int32_t j = (m > 0 ? m - 1 : 0); j < m; ++j)"),
+    "score_sign": ("const double d = ns[i] - nS[i];", "const double d = ns[i] + nS[i];"),
+    "no_rmsnorm_on_state": ("nS[i] = S[i] / rS;", "nS[i] = S[i];"),
+    "score_denominator_token": ("return sqrt(dd) / (frob(nS, D) + eps);",
+                                "return sqrt(dd) / (frob(ns, D) + eps);"),
+    "rms_not_mean": ("const double rS = sqrt(SS / (double)D + eps_rms);",
+                     "const double rS = sqrt(SS + eps_rms);"),
+    "threshold_strict": ("b = (I >= tau) ? 1 : 0;", "b = (I > tau) ? 1 : 0;"),
+    "argmax": ("if (dens[i] < dens[best]) best = i;", "if (dens[i] > dens[best]) best = i;"),
+    "argmin_last_tie": ("if (dens[i] < dens[best]) best = i;",
+                        "if (dens[i] <= dens[best]) best = i;"),
+    "density_product": ("(double)(n[i] + n[i + 1]);", "(double)(n[i] * n[i + 1]);"),
+    "density_no_count": ("dens[i] = (ibar[i] + ibar[i + 1]) / (double)(n[i] + n[i + 1]);",
+                         "dens[i] = (ibar[i] + ibar[i + 1]);"),
+    "merge_overwrites": ("S[best * D + i] += S[(best + 1) * D + i];",
+                         "S[best * D + i] = S[(best + 1) * D + i];"),
+    "merge_counts_not_summed": ("n[best] += n[best + 1];", "n[best] += 0;"),
+    "new_state_score_zero": ("ibar[m] = I;", "ibar[m] = 0.0;"),
+    "accumulate_score_dropped": ("ibar[m - 1] += I;", "ibar[m - 1] += 0.0;"),
+    # Alg. 1 read literally: the token is merged into the newest state and also appended
+    "double_count_token": ("      memcpy(S + (int64_t)m * D, s, sizeof(double) * D);",
+                           "      if (m > 0)\n"
+                           "        for (int64_t i = 0; i < D; ++i) S[(int64_t)(m - 1) * D + i] += s[i];\n"
+                           "      memcpy(S + (int64_t)m * D, s, sizeof(double) * D);"),
+    "readout_transposed": ("ot[c] += w * Sj[a * dv + c];", "ot[c] += w * Sj[c * dk + a];"),
+    "lambda_recency_index": ("lam[t * C + j]", "lam[t * C + (m - 1 - j)]"),
+    "readout_skips_newest": ("for (int32_t j = 0; j < m; ++j) {\n        const double lj",
+                             "for (int32_t j = 0; j + 1 < m; ++j) {\n        const double lj"),
+    "token_state_outer_swapped": ("s[a * dv + c] = kt[a] * vt[c];",
+                                  "s[a * dv + c] = kt[c % dk] * vt[a % dv];"),
+    # the just-closed state left out of the merge candidates
+    "candidates_exclude_closed": ("for (int32_t i = 0; i + 1 < C; ++i) {\n          dens[i]",
+                                  "for (int32_t i = 0; i + 2 < C; ++i) {\n          dens[i]"),
+    "c1_not_forced": ("      if (C == 1) {\n        b = 0;", "      if (C == 0) {\n        b = 0;"),
+}
+
+
+@pytest.fixture(scope="module")
+def src():
+    with open(SRC) as fh:
+        return fh.read()
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_fails_a_pin(name, src, tmp_path):
+    old, new = MUTANTS[name]
+    assert src.count(old) >= 1, f"mutation site for {name} not found"
+    mutated = src.replace(old, new, 1)
+    c = tmp_path / "mut.c"
+    c.write_text(mutated)
+    lib = str(tmp_path / "libmut.so")
+    subprocess.run(["gcc", "-O1", "-std=c11", "-fopenmp", "-shared", "-fPIC", str(c), "-o", lib,
+                    "-lm"], check=True)
+    failed = []
+    for pin in pins.ALL_PINS:
+        try:
+            pin(lib_path=lib)
+        except (AssertionError, ValueError, IndexError):
+            failed.append(pin.__name__)
+    assert failed, f"mutant {name} passes every pin"

@@ -1,0 +1,9 @@
+"""The float64 oracle against its pins (CPU only)."""
+import pytest
+
+from tests import pins
+
+
+@pytest.mark.parametrize("pin", pins.ALL_PINS, ids=lambda f: f.__name__)
+def test_pin(pin):
+    pin()
