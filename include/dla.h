@@ -1,0 +1,168 @@
+/*
+ * dla.h -- C ABI of libdla, the MI355X (gfx950) implementation of the Dynamic
+ * Linear Attention (DLA) layer forward of arXiv 2606.10650: information-aware
+ * dynamic state merging (Sec. 3.1, Alg. 1) and capacity-bounded memory with a
+ * multi-state readout (Sec. 3.2, Alg. 2, eq. capacity_bounded_output).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Plain pointers and sizes only.  Every array argument is DEVICE memory owned
+ *   by the caller; the library never allocates, frees or keeps a pointer after a
+ *   call returns.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All work
+ *   is enqueued on it; calls return after enqueueing.
+ * - Synchronous argument errors return a status and enqueue nothing.  A launch
+ *   failure returns DLA_ERR_HIP.  dla_get_last_error() returns the status of the
+ *   calling thread's last call.  Nothing is thrown across the ABI.
+ * - Calls on different caches may run concurrently; calls on one cache must be
+ *   ordered (same stream, or synchronised by the caller).
+ * - Shapes come from the cache descriptor: batch B, heads H, capacity C, key
+ *   and value head dimensions d_k, d_v.  Supported: d_k, d_v in {64, 128},
+ *   1 <= C <= 1024, B*H >= 1.
+ * - Token tensors are row-major [B][H][T][d] (d fastest); log_gate is
+ *   [B][H][T] float32 (the per-token log-decay g_t <= 0 of the base model:
+ *   every state decays by exp(g_t) at token t, the caller owns g_t <= 0);
+ *   lambda is [B][H][T][C] in the input dtype, lambda[t][j] weights the state
+ *   at chronological position j (0 = oldest) of the cache after token t is
+ *   absorbed (eq. capacity_bounded_output; entries j >= m_t are ignored), NULL
+ *   means lambda = 1.
+ * - Per-token exports (each nullable): boundary int8 in {0,1} (b_t of Sec. 3.1;
+ *   1 at the first token of an empty cache), merge_idx int32 (the chronological
+ *   index i* in the pre-merge cache of the left state of the adjacent pair
+ *   merged at token t by Alg. 2, or -1), score float32 (the State Information
+ *   Score I_t of eq. importance_score; 0 at the first token of an empty cache).
+ * - Overrides (each nullable, [B][H][T]): boundary_override -1 = decide, 0/1 =
+ *   force b_t; merge_override -1 = decide, else force i* in [0, C-2].  An
+ *   out-of-range merge override is ignored (the merge is decided) and sets
+ *   DLA_FLAG_BAD_MERGE_OVERRIDE in the cache's device flags.  Overrides do not
+ *   apply to the first token of an empty cache, and C = 1 forces b_t = 0 after
+ *   it (no adjacent pair exists).
+ */
+#ifndef DLA_H
+#define DLA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DLA_OK = 0,
+  DLA_ERR_INVALID_ARG = 1,    /* null pointer, bad size, bad dtype, T < 0 */
+  DLA_ERR_UNSUPPORTED = 2,    /* head dimension or capacity outside the supported set */
+  DLA_ERR_CACHE_MISMATCH = 3, /* descriptor differs from the one the cache was made with */
+  DLA_ERR_HIP = 4,            /* a HIP runtime call or kernel launch failed */
+  DLA_ERR_WORKSPACE = 5       /* workspace missing or smaller than required */
+} dla_status;
+
+typedef enum { DLA_F32 = 0, DLA_BF16 = 1 } dla_dtype;
+
+/* Shape of a state cache. */
+typedef struct {
+  int32_t B, H, C, d_k, d_v;
+} dla_cache_desc;
+
+/* Layer parameters.  tau: boundary threshold (b_t = [I_t >= tau], Sec. 3.1);
+ * eps: the epsilon of the score's denominator (eq. importance_score);
+ * eps_rms: the epsilon of the RMSNorm applied to both states before scoring
+ * (unit weight, over all d_k*d_v entries).  flags: DLA_SKIP_READOUT builds the
+ * cache and the exports but computes no output (out may be NULL). */
+typedef struct {
+  float tau;
+  float eps;
+  float eps_rms;
+  uint32_t flags;
+} dla_params;
+
+#define DLA_SKIP_READOUT 1u
+
+/* Device flags kept in the cache header (read with dla_cache_flags). */
+#define DLA_FLAG_BAD_MERGE_OVERRIDE 1u
+
+/*
+ * State cache (Sec. 3.2: chronological states with token counts n_i and
+ * aggregated scores I_i, at most C of them), one per head.
+ *
+ * Layout of the cache buffer (all offsets in bytes, see dla_cache_layout):
+ *   header  [0, 256): uint32 magic 0x31414C44 ('DLA1'), uint32 version,
+ *           int32 B, H, C, d_k, d_v, uint32 device flags, zero padding.
+ *   per-head metadata at meta_offset + h * meta_stride, h = b*H + head:
+ *           int32 m (live states), int32 0, double G (sum of all absorbed
+ *           log-decays), int64 tokens absorbed, int64 0,
+ *           double F[C] (frame of each live state), double Ibar[C] (aggregated
+ *           score), int32 n[C] (token count), int32 perm[C] (physical slot of
+ *           each logical state; entries m..C-1 list the free slots).
+ *           Arrays are in chronological order (index 0 = oldest).
+ *   states  at states_offset: float32 [B*H][C][d_k][d_v] by physical slot.
+ *           The true state of logical state j is exp(G - F[j]) * stored slot
+ *           perm[j] (states decay lazily: a slot is rescaled only when written).
+ */
+typedef struct {
+  size_t meta_offset;
+  size_t meta_stride;
+  size_t states_offset;
+  size_t total_bytes;
+} dla_cache_layout;
+
+/* Fill *layout for a descriptor.  Host only, no device work. */
+dla_status dla_cache_layout_of(const dla_cache_desc* desc, dla_cache_layout* layout);
+
+/* Two-call cache set-up.  With dev_buf == NULL: write the required size to
+ * *bytes.  With a device buffer of at least *bytes bytes: enqueue its
+ * initialisation to an empty cache (m = 0 for every head) on `stream`. */
+dla_status dla_state_cache_alloc(const dla_cache_desc* desc, void* dev_buf, size_t* bytes,
+                                 void* stream);
+
+/* Copy the cache's device flags to *flags and clear them.  Synchronises
+ * `stream`. */
+dla_status dla_cache_flags(const dla_cache_desc* desc, void* cache, uint32_t* flags,
+                           void* stream);
+
+/* Workspace that dla_prefill needs for T tokens. */
+dla_status dla_prefill_workspace_size(const dla_cache_desc* desc, int32_t T, size_t* bytes);
+
+/*
+ * Prefill: absorb T tokens per head into the cache, in order, computing for
+ * each token the score, the boundary decision, any capacity merge, and the
+ * readout o_t = sum_j lambda[t][j] q_t^T S_j over the cache after token t
+ * (eq. capacity_bounded_output; the first token of an empty cache opens a
+ * state).  Continues from whatever the cache holds: prefill of T1 tokens
+ * followed by prefill of T2 tokens equals prefill of T1 + T2 tokens.
+ *
+ * q (nullable with DLA_SKIP_READOUT), k: [B][H][T][d_k] in_dtype;
+ * v: [B][H][T][d_v] in_dtype; log_gate: [B][H][T] float32; lambda: see above;
+ * out: [B][H][T][d_v] out_dtype (nullable with DLA_SKIP_READOUT);
+ * exports and overrides: see above.  workspace: at least
+ * dla_prefill_workspace_size() bytes of device memory, 256-byte aligned.
+ * T = 0 is a no-op.
+ */
+dla_status dla_prefill(const dla_cache_desc* desc, void* cache, const void* q, const void* k,
+                       const void* v, const float* log_gate, const void* lambda, int32_t T,
+                       dla_dtype in_dtype, const dla_params* params, void* out,
+                       dla_dtype out_dtype, int8_t* boundary, int32_t* merge_idx, float* score,
+                       const int8_t* boundary_override, const int32_t* merge_override,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Decode step: absorb one token per head (the prefill semantics with T = 1),
+ * streaming every live state once.  q, k: [B][H][d_k]; v, out: [B][H][d_v];
+ * log_gate: [B][H]; lambda: [B][H][C] (nullable); exports and overrides:
+ * [B][H] (nullable).  Needs no workspace.
+ */
+dla_status dla_decode_step(const dla_cache_desc* desc, void* cache, const void* q, const void* k,
+                           const void* v, const float* log_gate, const void* lambda,
+                           dla_dtype in_dtype, const dla_params* params, void* out,
+                           dla_dtype out_dtype, int8_t* boundary, int32_t* merge_idx,
+                           float* score, const int8_t* boundary_override,
+                           const int32_t* merge_override, void* stream);
+
+const char* dla_status_string(dla_status s);
+dla_status dla_get_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DLA_H */

@@ -1,0 +1,232 @@
+// Host side of libdla: argument validation, cache set-up and the launch
+// sequence of each entry point.  Every entry point enqueues on the caller's
+// stream and never allocates device memory.
+#include <string.h>
+
+#include "dla_common.h"
+#include "prefill.h"
+#include "decode.h"
+
+namespace dla {
+
+
+
+__global__ void cache_init_kernel(char* cache, dla_cache_desc d, size_t meta_offset,
+                                  size_t meta_stride) {
+  const int h = blockIdx.x;
+  if (h == 0 && threadIdx.x == 0) {
+    CacheHeader* hd = reinterpret_cast<CacheHeader*>(cache);
+    hd->magic = kMagic;
+    hd->version = kVersion;
+    hd->B = d.B;
+    hd->H = d.H;
+    hd->C = d.C;
+    hd->dk = d.d_k;
+    hd->dv = d.d_v;
+    hd->flags = 0u;
+  }
+  Meta M = meta_at(cache + meta_offset + (size_t)h * meta_stride, d.C);
+  if (threadIdx.x == 0) {
+    *M.m = 0;
+    *reinterpret_cast<int32_t*>(cache + meta_offset + (size_t)h * meta_stride + 4) = 0;
+    *M.G = 0.0;
+    *M.tokens = 0;
+    *reinterpret_cast<int64_t*>(cache + meta_offset + (size_t)h * meta_stride + 24) = 0;
+  }
+  for (int j = threadIdx.x; j < d.C; j += blockDim.x) {
+    M.F[j] = 0.0;
+    M.ibar[j] = 0.0;
+    M.n[j] = 0;
+    M.perm[j] = j;
+  }
+}
+
+__global__ void flags_clear_kernel(char* cache) {
+  if (threadIdx.x == 0) reinterpret_cast<CacheHeader*>(cache)->flags = 0u;
+}
+
+}  // namespace dla
+
+using namespace dla;
+
+static thread_local dla_status g_last = DLA_OK;
+
+static dla_status ret(dla_status s) {
+  g_last = s;
+  return s;
+}
+
+static dla_status check_desc(const dla_cache_desc* d) {
+  if (!d) return DLA_ERR_INVALID_ARG;
+  if (d->B < 1 || d->H < 1 || d->C < 1) return DLA_ERR_INVALID_ARG;
+  if (d->C > 1024) return DLA_ERR_UNSUPPORTED;
+  if ((d->d_k != 64 && d->d_k != 128) || (d->d_v != 64 && d->d_v != 128))
+    return DLA_ERR_UNSUPPORTED;
+  if ((int64_t)d->B * d->H > (int64_t)1 << 24) return DLA_ERR_UNSUPPORTED;
+  return DLA_OK;
+}
+
+static bool dtype_ok(dla_dtype t) { return t == DLA_F32 || t == DLA_BF16; }
+
+extern "C" {
+
+const char* dla_status_string(dla_status s) {
+  switch (s) {
+    case DLA_OK: return "ok";
+    case DLA_ERR_INVALID_ARG: return "invalid argument";
+    case DLA_ERR_UNSUPPORTED: return "unsupported shape";
+    case DLA_ERR_CACHE_MISMATCH: return "cache does not match the descriptor";
+    case DLA_ERR_HIP: return "HIP runtime error";
+    case DLA_ERR_WORKSPACE: return "workspace missing or too small";
+  }
+  return "unknown status";
+}
+
+dla_status dla_get_last_error(void) { return g_last; }
+
+dla_status dla_cache_layout_of(const dla_cache_desc* desc, dla_cache_layout* layout) {
+  dla_status s = check_desc(desc);
+  if (s != DLA_OK) return ret(s);
+  if (!layout) return ret(DLA_ERR_INVALID_ARG);
+  *layout = layout_of(*desc);
+  return ret(DLA_OK);
+}
+
+dla_status dla_state_cache_alloc(const dla_cache_desc* desc, void* dev_buf, size_t* bytes,
+                                 void* stream) {
+  dla_status s = check_desc(desc);
+  if (s != DLA_OK) return ret(s);
+  if (!bytes) return ret(DLA_ERR_INVALID_ARG);
+  const dla_cache_layout L = layout_of(*desc);
+  if (!dev_buf) {
+    *bytes = L.total_bytes;
+    return ret(DLA_OK);
+  }
+  if (*bytes < L.total_bytes) return ret(DLA_ERR_INVALID_ARG);
+  const int nh = desc->B * desc->H;
+  hipLaunchKernelGGL(cache_init_kernel, dim3(nh), dim3(256), 0, (hipStream_t)stream,
+                     (char*)dev_buf, *desc, L.meta_offset, L.meta_stride);
+  if (hipGetLastError() != hipSuccess) return ret(DLA_ERR_HIP);
+  return ret(DLA_OK);
+}
+
+dla_status dla_cache_flags(const dla_cache_desc* desc, void* cache, uint32_t* flags,
+                           void* stream) {
+  dla_status s = check_desc(desc);
+  if (s != DLA_OK) return ret(s);
+  if (!cache || !flags) return ret(DLA_ERR_INVALID_ARG);
+  CacheHeader hd;
+  hipStream_t st = (hipStream_t)stream;
+  if (hipMemcpyAsync(&hd, cache, sizeof(hd), hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return ret(DLA_ERR_HIP);
+  if (hd.magic != kMagic || hd.B != desc->B || hd.H != desc->H || hd.C != desc->C ||
+      hd.dk != desc->d_k || hd.dv != desc->d_v)
+    return ret(DLA_ERR_CACHE_MISMATCH);
+  *flags = hd.flags;
+  hipLaunchKernelGGL(flags_clear_kernel, dim3(1), dim3(64), 0, st, (char*)cache);
+  if (hipGetLastError() != hipSuccess || hipStreamSynchronize(st) != hipSuccess)
+    return ret(DLA_ERR_HIP);
+  return ret(DLA_OK);
+}
+
+dla_status dla_prefill_workspace_size(const dla_cache_desc* desc, int32_t T, size_t* bytes) {
+  dla_status s = check_desc(desc);
+  if (s != DLA_OK) return ret(s);
+  if (!bytes || T < 0) return ret(DLA_ERR_INVALID_ARG);
+  *bytes = prefill_workspace_bytes(*desc, T);
+  return ret(DLA_OK);
+}
+
+dla_status dla_prefill(const dla_cache_desc* desc, void* cache, const void* q, const void* k,
+                       const void* v, const float* log_gate, const void* lambda, int32_t T,
+                       dla_dtype in_dtype, const dla_params* params, void* out,
+                       dla_dtype out_dtype, int8_t* boundary, int32_t* merge_idx, float* score,
+                       const int8_t* boundary_override, const int32_t* merge_override,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+  dla_status s = check_desc(desc);
+  if (s != DLA_OK) return ret(s);
+  if (!params || T < 0 || !dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return ret(DLA_ERR_INVALID_ARG);
+  const bool skip = (params->flags & DLA_SKIP_READOUT) != 0;
+  if (!cache || !k || !v || !log_gate) return ret(DLA_ERR_INVALID_ARG);
+  if (!skip && (!q || !out)) return ret(DLA_ERR_INVALID_ARG);
+  if (T == 0) return ret(DLA_OK);
+  if ((int64_t)desc->B * desc->H * (int64_t)T * (desc->C > 128 ? desc->C : 128) >
+      ((int64_t)1 << 40))
+    return ret(DLA_ERR_UNSUPPORTED);
+  const size_t need = prefill_workspace_bytes(*desc, T);
+  if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 255u))
+    return ret(DLA_ERR_WORKSPACE);
+  PrefillArgs a;
+  memset(&a, 0, sizeof(a));
+  const dla_cache_layout L = layout_of(*desc);
+  a.desc = *desc;
+  a.cache = (char*)cache;
+  a.meta_offset = L.meta_offset;
+  a.meta_stride = L.meta_stride;
+  a.states_offset = L.states_offset;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.g = log_gate;
+  a.lam = lambda;
+  a.out = skip ? nullptr : out;
+  a.b_out = boundary;
+  a.merge_out = merge_idx;
+  a.score_out = score;
+  a.b_ovr = boundary_override;
+  a.m_ovr = merge_override;
+  a.T = T;
+  a.tau = params->tau;
+  a.eps = params->eps;
+  a.eps_rms = params->eps_rms;
+  a.skip_readout = skip ? 1 : 0;
+  a.in_dtype = in_dtype;
+  a.out_dtype = out_dtype;
+  a.workspace = (char*)workspace;
+  if (launch_prefill(a, (hipStream_t)stream) != hipSuccess) return ret(DLA_ERR_HIP);
+  return ret(DLA_OK);
+}
+
+dla_status dla_decode_step(const dla_cache_desc* desc, void* cache, const void* q, const void* k,
+                           const void* v, const float* log_gate, const void* lambda,
+                           dla_dtype in_dtype, const dla_params* params, void* out,
+                           dla_dtype out_dtype, int8_t* boundary, int32_t* merge_idx,
+                           float* score, const int8_t* boundary_override,
+                           const int32_t* merge_override, void* stream) {
+  dla_status s = check_desc(desc);
+  if (s != DLA_OK) return ret(s);
+  if (!params || !dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return ret(DLA_ERR_INVALID_ARG);
+  const bool skip = (params->flags & DLA_SKIP_READOUT) != 0;
+  if (!cache || !k || !v || !log_gate) return ret(DLA_ERR_INVALID_ARG);
+  if (!skip && (!q || !out)) return ret(DLA_ERR_INVALID_ARG);
+  const dla_cache_layout L = layout_of(*desc);
+  DecodeArgs a;
+  memset(&a, 0, sizeof(a));
+  a.cache = (char*)cache;
+  a.meta_offset = L.meta_offset;
+  a.meta_stride = L.meta_stride;
+  a.states_offset = L.states_offset;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.g = log_gate;
+  a.lam = lambda;
+  a.out = out;
+  a.b_out = boundary;
+  a.merge_out = merge_idx;
+  a.score_out = score;
+  a.b_ovr = boundary_override;
+  a.m_ovr = merge_override;
+  a.C = desc->C;
+  a.tau = params->tau;
+  a.eps = params->eps;
+  a.eps_rms = params->eps_rms;
+  a.skip_readout = skip ? 1 : 0;
+  if (launch_decode(a, desc->B * desc->H, desc->d_k, desc->d_v, in_dtype, out_dtype,
+                    (hipStream_t)stream) != hipSuccess)
+    return ret(DLA_ERR_HIP);
+  return ret(DLA_OK);
+}
+
+}  // extern "C"

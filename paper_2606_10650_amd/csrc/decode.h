@@ -1,0 +1,29 @@
+// Decode step entry (internal).
+#pragma once
+#include "dla_common.h"
+
+namespace dla {
+
+struct DecodeArgs {
+  char* cache;
+  size_t meta_offset, meta_stride, states_offset;
+  const void* q;
+  const void* k;
+  const void* v;
+  const float* g;
+  const void* lam;
+  void* out;
+  int8_t* b_out;
+  int32_t* merge_out;
+  float* score_out;
+  const int8_t* b_ovr;
+  const int32_t* m_ovr;
+  int C;
+  float tau, eps, eps_rms;
+  int skip_readout;
+};
+
+hipError_t launch_decode(const DecodeArgs& a, int nheads, int dk, int dv, dla_dtype in,
+                         dla_dtype out, hipStream_t s);
+
+}  // namespace dla

@@ -1,0 +1,357 @@
+// Decode step of the DLA layer: one token per head against a resident cache.
+//
+// One 256-thread workgroup per head.  The step is bound by HBM bandwidth: every
+// live state (d_k x d_v float32) is streamed once for the readout
+// o = sum_j lambda_j q^T S_j (eq. capacity_bounded_output), and at most two
+// states are written (the accumulated newest state, or the merged pair of
+// Alg. 2 and the new state).  States decay lazily: a slot stores S~ with the
+// true state exp(G - F_j) S~, so untouched states are never rewritten.
+//
+// Thread mapping inside a state: float4 index tid + 256 r of the row-major
+// d_k x d_v array, i.e. thread tid owns the 4 columns 4*(tid % (d_v/4)) .. +3
+// of the rows (tid / (d_v/4)) + r * (256 / (d_v/4)).  Loads are fully coalesced.
+#include "decode.h"
+
+namespace dla {
+
+
+
+template <int DK, int DV>
+struct StateTile {
+  static constexpr int CQ = DV / 4;      // float4 per row
+  static constexpr int RG = 256 / CQ;    // row groups
+  static constexpr int RPT = DK / RG;    // rows per thread
+  static constexpr int NV = RPT;         // float4 per thread
+};
+
+template <int DK, int DV, typename Tin, typename Tout>
+__global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
+  using ST = StateTile<DK, DV>;
+  constexpr int D = DK * DV;
+  const int h = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int C = a.C;
+  const int cq = tid % ST::CQ;
+  const int rg = tid / ST::CQ;
+
+  extern __shared__ double smem[];
+  double* sF = smem;                                    // [C]
+  double* sI = sF + C;                                  // [C]
+  int32_t* sN = reinterpret_cast<int32_t*>(sI + C);     // [C]
+  int32_t* sP = sN + C;                                 // [C]
+  float* sLam = reinterpret_cast<float*>(sP + C);       // [C]
+  __shared__ float sq[DK], sk[DK], sv[DV];
+  __shared__ float red[8];
+  __shared__ float sOut[ST::RG][DV];
+  __shared__ double sArg[8];
+  __shared__ int sArgI[8];
+  __shared__ double sScal[4];
+  __shared__ int sDec[4];
+
+  const Tin* q = static_cast<const Tin*>(a.q) + (size_t)h * DK;
+  const Tin* k = static_cast<const Tin*>(a.k) + (size_t)h * DK;
+  const Tin* v = static_cast<const Tin*>(a.v) + (size_t)h * DV;
+  for (int i = tid; i < DK; i += 256) {
+    sk[i] = to_f32(k[i]);
+    sq[i] = a.skip_readout ? 0.f : to_f32(q[i]);
+  }
+  for (int i = tid; i < DV; i += 256) sv[i] = to_f32(v[i]);
+
+  char* mbase = a.cache + a.meta_offset + (size_t)h * a.meta_stride;
+  Meta M = meta_at(mbase, C);
+  const int m = min(max(*M.m, 0), C);
+  const double G0 = *M.G;
+  for (int j = tid; j < C; j += 256) {
+    sF[j] = M.F[j];
+    sI[j] = M.ibar[j];
+    sN[j] = M.n[j];
+    sP[j] = min(max(M.perm[j], 0), C - 1);
+    sLam[j] = a.lam ? to_f32(static_cast<const Tin*>(a.lam)[(size_t)h * C + j]) : 1.f;
+  }
+  __syncthreads();
+
+  const double Gn = G0 + (double)a.g[h];
+  float* states = reinterpret_cast<float*>(a.cache + a.states_offset) + (size_t)h * C * D;
+
+  // |k|^2, |v|^2, q.k
+  float kk = 0.f, vv = 0.f, qk = 0.f;
+  if (tid < 64) {
+    for (int i = tid; i < DK; i += 64) {
+      kk += sk[i] * sk[i];
+      qk += sq[i] * sk[i];
+    }
+    for (int i = tid; i < DV; i += 64) vv += sv[i] * sv[i];
+  }
+
+  // newest state in registers, and the two scalars b = |S~|^2, c = k^T S~ v
+  float4 Sopen[ST::NV];
+  float ct = 0.f, bt = 0.f;
+  if (m > 0) {
+    const float4* src = reinterpret_cast<const float4*>(states + (size_t)sP[m - 1] * D);
+    float4 vq = reinterpret_cast<const float4*>(sv)[cq];
+#pragma unroll
+    for (int r = 0; r < ST::NV; ++r) {
+      Sopen[r] = src[tid + 256 * r];
+      const float kr = sk[rg + ST::RG * r];
+      const float4 s = Sopen[r];
+      ct += kr * (s.x * vq.x + s.y * vq.y + s.z * vq.z + s.w * vq.w);
+      bt += s.x * s.x + s.y * s.y + s.z * s.z + s.w * s.w;
+    }
+  }
+  block_sum2_256(ct, bt, red);
+  float kk2 = kk, vv2 = vv;
+  block_sum2_256(kk2, vv2, red);
+  float qk2 = qk, dummy = 0.f;
+  block_sum2_256(qk2, dummy, red);
+
+  // score and boundary decision (one thread, float64 scalars)
+  if (tid == 0) {
+    double I = 0.0;
+    int b = 1;
+    if (m > 0) {
+      const double f = exp(Gn - sF[m - 1]);
+      const double a2 = (double)kk2 * (double)vv2;
+      I = info_score(a2, f * f * (double)bt, f * (double)ct, (double)D, a.eps, a.eps_rms);
+      b = (I >= (double)a.tau) ? 1 : 0;
+      if (a.b_ovr && a.b_ovr[h] != -1) b = a.b_ovr[h] ? 1 : 0;
+      if (C == 1) b = 0;
+    }
+    sScal[0] = I;
+    sDec[0] = b;
+  }
+  __syncthreads();
+  const int b = sDec[0];
+  const double I = sScal[0];
+
+  // Alg. 2: lowest-density adjacent pair when a new state opens in a full cache
+  int istar = -1;
+  if (b && m == C) {
+    double best = INFINITY;
+    int bi = 0x7fffffff;
+    for (int i = tid; i + 1 < C; i += 256) {
+      const double d = (sI[i] + sI[i + 1]) / (double)(sN[i] + sN[i + 1]);
+      if (d < best) {
+        best = d;
+        bi = i;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const double ob = __shfl_xor(best, o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      if (ob < best || (ob == best && oi < bi)) {
+        best = ob;
+        bi = oi;
+      }
+    }
+    if ((tid & 63) == 0) {
+      sArg[tid >> 6] = best;
+      sArgI[tid >> 6] = bi;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      double bb = sArg[0];
+      int ii = sArgI[0];
+      for (int w = 1; w < 4; ++w)
+        if (sArg[w] < bb || (sArg[w] == bb && sArgI[w] < ii)) {
+          bb = sArg[w];
+          ii = sArgI[w];
+        }
+      if (a.m_ovr && a.m_ovr[h] != -1) {
+        const int f = a.m_ovr[h];
+        if (f >= 0 && f <= C - 2)
+          ii = f;
+        else
+          atomicOr(&reinterpret_cast<CacheHeader*>(a.cache)->flags, DLA_FLAG_BAD_MERGE_OVERRIDE);
+      }
+      sDec[1] = ii;
+    }
+    __syncthreads();
+    istar = sDec[1];
+  }
+  const int m_post = b ? (istar >= 0 ? m : m + 1) : m;
+
+  // stream every live state: readout partials and the state writes
+  float o4[4] = {0.f, 0.f, 0.f, 0.f};
+  float qr[ST::NV];
+#pragma unroll
+  for (int r = 0; r < ST::NV; ++r) qr[r] = sq[rg + ST::RG * r];
+
+  for (int j = 0; j < m; ++j) {
+    const bool is_open = (j == m - 1);
+    float4 X[ST::NV];
+    if (is_open) {
+#pragma unroll
+      for (int r = 0; r < ST::NV; ++r) X[r] = Sopen[r];
+    } else {
+      const float4* src = reinterpret_cast<const float4*>(states + (size_t)sP[j] * D);
+#pragma unroll
+      for (int r = 0; r < ST::NV; ++r) X[r] = src[tid + 256 * r];
+    }
+    const int post = (istar >= 0 && j > istar) ? j - 1 : j;
+    const float w = a.skip_readout ? 0.f : sLam[post] * __expf((float)(Gn - sF[j]));
+    float y0 = 0.f, y1 = 0.f, y2 = 0.f, y3 = 0.f;
+#pragma unroll
+    for (int r = 0; r < ST::NV; ++r) {
+      y0 += qr[r] * X[r].x;
+      y1 += qr[r] * X[r].y;
+      y2 += qr[r] * X[r].z;
+      y3 += qr[r] * X[r].w;
+    }
+    o4[0] += w * y0;
+    o4[1] += w * y1;
+    o4[2] += w * y2;
+    o4[3] += w * y3;
+
+    if (j == istar) {
+      // merged pair: frame of the later state, S~ = exp(F_{i+1} - F_i) S~_i + S~_{i+1}
+      const int j2 = j + 1;
+      float4 Y[ST::NV];
+      if (j2 == m - 1) {
+#pragma unroll
+        for (int r = 0; r < ST::NV; ++r) Y[r] = Sopen[r];
+      } else {
+        const float4* src = reinterpret_cast<const float4*>(states + (size_t)sP[j2] * D);
+#pragma unroll
+        for (int r = 0; r < ST::NV; ++r) Y[r] = src[tid + 256 * r];
+      }
+      const float w2 = a.skip_readout ? 0.f : sLam[j] * __expf((float)(Gn - sF[j2]));
+      const float e = __expf((float)(sF[j2] - sF[j]));
+      float z0 = 0.f, z1 = 0.f, z2 = 0.f, z3 = 0.f;
+      float4* dst = reinterpret_cast<float4*>(states + (size_t)sP[j] * D);
+#pragma unroll
+      for (int r = 0; r < ST::NV; ++r) {
+        z0 += qr[r] * Y[r].x;
+        z1 += qr[r] * Y[r].y;
+        z2 += qr[r] * Y[r].z;
+        z3 += qr[r] * Y[r].w;
+        float4 s;
+        s.x = e * X[r].x + Y[r].x;
+        s.y = e * X[r].y + Y[r].y;
+        s.z = e * X[r].z + Y[r].z;
+        s.w = e * X[r].w + Y[r].w;
+        dst[tid + 256 * r] = s;
+      }
+      o4[0] += w2 * z0;
+      o4[1] += w2 * z1;
+      o4[2] += w2 * z2;
+      o4[3] += w2 * z3;
+      ++j;  // the pair is done
+    } else if (is_open && !b) {
+      // accumulate: S~' = exp(Gn - F) S~ + k v^T in frame Gn
+      const float f = __expf((float)(Gn - sF[j]));
+      const float4 vq = reinterpret_cast<const float4*>(sv)[cq];
+      float4* dst = reinterpret_cast<float4*>(states + (size_t)sP[j] * D);
+#pragma unroll
+      for (int r = 0; r < ST::NV; ++r) {
+        const float kr = sk[rg + ST::RG * r];
+        float4 s;
+        s.x = f * X[r].x + kr * vq.x;
+        s.y = f * X[r].y + kr * vq.y;
+        s.z = f * X[r].z + kr * vq.z;
+        s.w = f * X[r].w + kr * vq.w;
+        dst[tid + 256 * r] = s;
+      }
+    }
+  }
+
+  // new state k v^T (frame Gn) in the slot freed by the merge or the first free slot
+  if (b) {
+    const int phys = (istar >= 0) ? sP[istar + 1] : sP[m];
+    const float4 vq = reinterpret_cast<const float4*>(sv)[cq];
+    float4* dst = reinterpret_cast<float4*>(states + (size_t)phys * D);
+#pragma unroll
+    for (int r = 0; r < ST::NV; ++r) {
+      const float kr = sk[rg + ST::RG * r];
+      dst[tid + 256 * r] = make_float4(kr * vq.x, kr * vq.y, kr * vq.z, kr * vq.w);
+    }
+  }
+
+  // the new token's own contribution lambda_{m'-1} (q.k) v, then reduce the partials
+  if (!a.skip_readout) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) sOut[rg][4 * cq + c] = o4[c];
+    __syncthreads();
+    if (tid < DV) {
+      float acc = 0.f;
+#pragma unroll
+      for (int g2 = 0; g2 < ST::RG; ++g2) acc += sOut[g2][tid];
+      acc += sLam[m_post - 1] * qk2 * sv[tid];
+      static_cast<Tout*>(a.out)[(size_t)h * DV + tid] = from_f32<Tout>(acc);
+    }
+  }
+
+  // exports
+  if (tid == 0) {
+    if (a.b_out) a.b_out[h] = (int8_t)b;
+    if (a.merge_out) a.merge_out[h] = istar;
+    if (a.score_out) a.score_out[h] = (float)I;
+  }
+
+  // metadata update (chronological arrays, parallel over slots)
+  __syncthreads();
+  if (!b) {
+    if (tid == 0) {
+      M.F[m - 1] = Gn;
+      M.n[m - 1] = sN[m - 1] + 1;
+      M.ibar[m - 1] = sI[m - 1] + I;
+    }
+  } else {
+    if (istar >= 0) {
+      // merge istar, istar+1; shift later states down; freed slot goes to perm[m-1]
+      for (int j = tid; j < C; j += 256) {
+        if (j == istar) {
+          M.F[j] = sF[j + 1];
+          M.n[j] = sN[j] + sN[j + 1];
+          M.ibar[j] = sI[j] + sI[j + 1];
+        } else if (j > istar && j < m - 1) {
+          M.F[j] = sF[j + 1];
+          M.n[j] = sN[j + 1];
+          M.ibar[j] = sI[j + 1];
+          M.perm[j] = sP[j + 1];
+        } else if (j == m - 1) {
+          // the new state takes the freed slot
+          M.perm[j] = sP[istar + 1];
+          M.F[j] = Gn;
+          M.n[j] = 1;
+          M.ibar[j] = I;
+        }
+      }
+    } else if (tid == 0) {
+      M.F[m] = Gn;
+      M.n[m] = 1;
+      M.ibar[m] = I;
+    }
+    if (tid == 0) *M.m = m_post;
+  }
+  if (tid == 0) {
+    *M.G = Gn;
+    *M.tokens += 1;
+  }
+}
+
+template <int DK, int DV>
+static hipError_t launch_decode_dims(const DecodeArgs& a, int nheads, dla_dtype in, dla_dtype out,
+                                     hipStream_t s) {
+  const size_t shm = (size_t)a.C * (8 + 8 + 4 + 4 + 4);
+  if (in == DLA_F32 && out == DLA_F32)
+    hipLaunchKernelGGL((decode_kernel<DK, DV, float, float>), dim3(nheads), dim3(256), shm, s, a);
+  else if (in == DLA_F32 && out == DLA_BF16)
+    hipLaunchKernelGGL((decode_kernel<DK, DV, float, bf16_t>), dim3(nheads), dim3(256), shm, s, a);
+  else if (in == DLA_BF16 && out == DLA_F32)
+    hipLaunchKernelGGL((decode_kernel<DK, DV, bf16_t, float>), dim3(nheads), dim3(256), shm, s, a);
+  else
+    hipLaunchKernelGGL((decode_kernel<DK, DV, bf16_t, bf16_t>), dim3(nheads), dim3(256), shm, s,
+                       a);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode(const DecodeArgs& a, int nheads, int dk, int dv, dla_dtype in,
+                         dla_dtype out, hipStream_t s) {
+  if (dk == 128 && dv == 128) return launch_decode_dims<128, 128>(a, nheads, in, out, s);
+  if (dk == 64 && dv == 64) return launch_decode_dims<64, 64>(a, nheads, in, out, s);
+  if (dk == 128 && dv == 64) return launch_decode_dims<128, 64>(a, nheads, in, out, s);
+  return launch_decode_dims<64, 128>(a, nheads, in, out, s);
+}
+
+}  // namespace dla

@@ -1,0 +1,125 @@
+// Internal definitions shared by the libdla HIP sources (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dla.h"
+
+namespace dla {
+
+constexpr uint32_t kMagic = 0x31414C44u;  // 'DLA1'
+constexpr uint32_t kVersion = 1u;
+constexpr size_t kHeaderBytes = 256;
+
+struct CacheHeader {
+  uint32_t magic;
+  uint32_t version;
+  int32_t B, H, C, dk, dv;
+  uint32_t flags;
+};
+
+__host__ __device__ inline size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+__host__ __device__ inline size_t meta_stride(int C) {
+  return round_up(32 + 24 * (size_t)C, 256);
+}
+
+// Per-head metadata (chronological arrays).  See dla.h for the byte layout.
+struct Meta {
+  int32_t* m;
+  double* G;
+  int64_t* tokens;
+  double* F;
+  double* ibar;
+  int32_t* n;
+  int32_t* perm;
+};
+
+__host__ __device__ inline Meta meta_at(char* base, int C) {
+  Meta r;
+  r.m = reinterpret_cast<int32_t*>(base);
+  r.G = reinterpret_cast<double*>(base + 8);
+  r.tokens = reinterpret_cast<int64_t*>(base + 16);
+  r.F = reinterpret_cast<double*>(base + 32);
+  r.ibar = r.F + C;
+  r.n = reinterpret_cast<int32_t*>(r.ibar + C);
+  r.perm = r.n + C;
+  return r;
+}
+
+inline dla_cache_layout layout_of(const dla_cache_desc& d) {
+  dla_cache_layout L;
+  const size_t nh = (size_t)d.B * d.H;
+  L.meta_offset = kHeaderBytes;
+  L.meta_stride = meta_stride(d.C);
+  L.states_offset = round_up(L.meta_offset + nh * L.meta_stride, 256);
+  L.total_bytes = L.states_offset + nh * (size_t)d.C * d.d_k * d.d_v * sizeof(float);
+  return L;
+}
+
+// ---------------------------------------------------------------------------
+// element types: float32, or bfloat16 kept as raw 16-bit patterns
+// ---------------------------------------------------------------------------
+struct bf16_t {
+  uint16_t x;
+};
+
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(bf16_t v) {
+  return __uint_as_float(static_cast<uint32_t>(v.x) << 16);
+}
+
+template <typename T>
+__device__ __forceinline__ T from_f32(float v);
+template <>
+__device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <>
+__device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) {
+  // round to nearest even (inputs here are finite)
+  uint32_t u = __float_as_uint(v);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  bf16_t r;
+  r.x = static_cast<uint16_t>(u >> 16);
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+// wavefront (64 lanes) and block reductions
+// ---------------------------------------------------------------------------
+template <typename T>
+__device__ __forceinline__ T wave_sum(T v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Sum of two values over a 256-thread block; every thread gets the result.
+// red must hold 8 floats.
+__device__ __forceinline__ void block_sum2_256(float& a, float& b, float* red) {
+  a = wave_sum(a);
+  b = wave_sum(b);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) {
+    red[w] = a;
+    red[4 + w] = b;
+  }
+  __syncthreads();
+  a = (red[0] + red[1]) + (red[2] + red[3]);
+  b = (red[4] + red[5]) + (red[6] + red[7]);
+}
+
+// The State Information Score from the three scalars of a rank-one token
+// state s = k v^T against a state S:  a = |k|^2 |v|^2, b = |S|^2, c = k^T S v.
+// With RMSNorm N(X) = X / sqrt(|X|^2/D + eps_rms):
+//   |N(s) - N(S)|^2 = a/rs^2 + b/rS^2 - 2c/(rs rS),   |N(S)| = sqrt(b)/rS.
+__device__ __forceinline__ double info_score(double a, double b, double c, double D, double eps,
+                                             double eps_rms) {
+  const double rs2 = a / D + eps_rms;
+  const double rS2 = b / D + eps_rms;
+  const double num = a / rs2 + b / rS2 - 2.0 * c / sqrt(rs2 * rS2);
+  return sqrt(num > 0.0 ? num : 0.0) / (sqrt(b / rS2) + eps);
+}
+
+}  // namespace dla

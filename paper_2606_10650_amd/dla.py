@@ -1,0 +1,280 @@
+"""Python binding of libdla (ctypes).  Argument marshalling only: every step of
+the layer runs in the HIP kernels of libdla.so; torch provides device memory and
+the current stream.  The library must be built (python -m
+paper_2606_10650_amd.build); a missing library is an error, there is no
+fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Optional
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdla.so")
+_lib = None
+
+DLA_OK, DLA_ERR_INVALID_ARG, DLA_ERR_UNSUPPORTED, DLA_ERR_CACHE_MISMATCH, DLA_ERR_HIP, \
+    DLA_ERR_WORKSPACE = range(6)
+DLA_F32, DLA_BF16 = 0, 1
+DLA_SKIP_READOUT = 1
+DLA_FLAG_BAD_MERGE_OVERRIDE = 1
+
+EXPORTED = ("dla_cache_layout_of", "dla_state_cache_alloc", "dla_cache_flags",
+            "dla_prefill_workspace_size", "dla_prefill", "dla_decode_step", "dla_status_string",
+            "dla_get_last_error")
+
+
+class CacheDesc(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("C", ctypes.c_int32),
+                ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32)]
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("tau", ctypes.c_float), ("eps", ctypes.c_float), ("eps_rms", ctypes.c_float),
+                ("flags", ctypes.c_uint32)]
+
+
+class Layout(ctypes.Structure):
+    _fields_ = [("meta_offset", ctypes.c_size_t), ("meta_stride", ctypes.c_size_t),
+                ("states_offset", ctypes.c_size_t), ("total_bytes", ctypes.c_size_t)]
+
+
+class DLAError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} ({status})")
+
+
+def lib():
+    """Load libdla.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
+                               "`python -m paper_2606_10650_amd.build`")
+        L = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.c_void_p
+        I = ctypes.c_int
+        L.dla_cache_layout_of.argtypes = [ctypes.POINTER(CacheDesc), ctypes.POINTER(Layout)]
+        L.dla_state_cache_alloc.argtypes = [ctypes.POINTER(CacheDesc), P,
+                                            ctypes.POINTER(ctypes.c_size_t), P]
+        L.dla_cache_flags.argtypes = [ctypes.POINTER(CacheDesc), P, ctypes.POINTER(ctypes.c_uint32),
+                                      P]
+        L.dla_prefill_workspace_size.argtypes = [ctypes.POINTER(CacheDesc), ctypes.c_int32,
+                                                 ctypes.POINTER(ctypes.c_size_t)]
+        L.dla_prefill.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, ctypes.c_int32, I,
+                                  ctypes.POINTER(Params), P, I, P, P, P, P, P, P, ctypes.c_size_t, P]
+        L.dla_decode_step.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, I,
+                                      ctypes.POINTER(Params), P, I, P, P, P, P, P, P]
+        L.dla_status_string.argtypes = [I]
+        L.dla_status_string.restype = ctypes.c_char_p
+        L.dla_get_last_error.argtypes = []
+        for name in ("dla_cache_layout_of", "dla_state_cache_alloc", "dla_cache_flags",
+                     "dla_prefill_workspace_size", "dla_prefill", "dla_decode_step",
+                     "dla_get_last_error"):
+            getattr(L, name).restype = I
+        _lib = L
+    return _lib
+
+
+def status_string(s: int) -> str:
+    return lib().dla_status_string(int(s)).decode()
+
+
+def _check(status: int, what: str):
+    if status != DLA_OK:
+        raise DLAError(status, what)
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t == torch.float32:
+        return DLA_F32
+    if t == torch.bfloat16:
+        return DLA_BF16
+    raise ValueError(f"unsupported dtype {t}")
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device) -> ctypes.c_void_p:
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+@dataclasses.dataclass
+class StateCache:
+    """A device state cache (Sec. 3.2) for B*H heads of capacity C."""
+    B: int
+    H: int
+    C: int
+    d_k: int
+    d_v: int
+    buf: "object"  # torch uint8 tensor on the device
+
+    @property
+    def desc(self) -> CacheDesc:
+        return CacheDesc(self.B, self.H, self.C, self.d_k, self.d_v)
+
+    @property
+    def device(self):
+        return self.buf.device
+
+
+def cache_layout(B, H, C, d_k, d_v) -> Layout:
+    L = Layout()
+    _check(lib().dla_cache_layout_of(ctypes.byref(CacheDesc(B, H, C, d_k, d_v)), ctypes.byref(L)),
+           "dla_cache_layout_of")
+    return L
+
+
+def cache_alloc(B: int, H: int, C: int, d_k: int, d_v: int, device="cuda") -> StateCache:
+    """Allocate and initialise an empty cache (two-call dla_state_cache_alloc)."""
+    torch = _torch()
+    d = CacheDesc(B, H, C, d_k, d_v)
+    n = ctypes.c_size_t(0)
+    _check(lib().dla_state_cache_alloc(ctypes.byref(d), None, ctypes.byref(n), None),
+           "dla_state_cache_alloc(size)")
+    buf = torch.empty(n.value, dtype=torch.uint8, device=device)
+    _check(lib().dla_state_cache_alloc(ctypes.byref(d), _ptr(buf), ctypes.byref(n),
+                                       _stream(buf.device)), "dla_state_cache_alloc")
+    return StateCache(B, H, C, d_k, d_v, buf)
+
+
+def cache_flags(cache: StateCache) -> int:
+    f = ctypes.c_uint32(0)
+    _check(lib().dla_cache_flags(ctypes.byref(cache.desc), _ptr(cache.buf), ctypes.byref(f),
+                                 _stream(cache.device)), "dla_cache_flags")
+    return int(f.value)
+
+
+def workspace_bytes(cache: StateCache, T: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().dla_prefill_workspace_size(ctypes.byref(cache.desc), int(T), ctypes.byref(n)),
+           "dla_prefill_workspace_size")
+    return int(n.value)
+
+
+def _params(tau, eps, eps_rms, skip_readout):
+    return Params(float(tau), float(eps), float(eps_rms), DLA_SKIP_READOUT if skip_readout else 0)
+
+
+def prefill(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5, eps: float = 1e-6,
+            eps_rms: float = 1e-6, out=None, out_dtype=None, skip_readout: bool = False,
+            boundary=None, merge_idx=None, score=None, boundary_override=None,
+            merge_override=None, workspace=None, want_exports: bool = True):
+    """Absorb T tokens per head.  q, k: [B, H, T, d_k]; v: [B, H, T, d_v]; g:
+    [B, H, T] float32; lam: [B, H, T, C] or None.  Returns (out, boundary,
+    merge_idx, score); exports not requested are None."""
+    torch = _torch()
+    B, H, C = cache.B, cache.H, cache.C
+    T = k.shape[2]
+    dev = cache.device
+    assert k.shape == (B, H, T, cache.d_k) and v.shape == (B, H, T, cache.d_v), (k.shape, v.shape)
+    assert g.shape == (B, H, T) and g.dtype == torch.float32
+    for t in (q, k, v, g, lam, boundary_override, merge_override):
+        assert t is None or (t.is_contiguous() and t.device == dev)
+    if q is not None:
+        assert q.shape == (B, H, T, cache.d_k) and q.dtype == k.dtype
+    if lam is not None:
+        assert lam.shape == (B, H, T, C) and lam.dtype == k.dtype
+    if out is None and not skip_readout:
+        out = torch.empty((B, H, T, cache.d_v), dtype=out_dtype or k.dtype, device=dev)
+    if want_exports:
+        boundary = boundary if boundary is not None else torch.empty((B, H, T), dtype=torch.int8,
+                                                                      device=dev)
+        merge_idx = merge_idx if merge_idx is not None else torch.empty((B, H, T),
+                                                                        dtype=torch.int32,
+                                                                        device=dev)
+        score = score if score is not None else torch.empty((B, H, T), dtype=torch.float32,
+                                                            device=dev)
+    wsb = workspace_bytes(cache, T)
+    if workspace is None or workspace.numel() < wsb:
+        workspace = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
+    p = _params(tau, eps, eps_rms, skip_readout)
+    st = lib().dla_prefill(ctypes.byref(cache.desc), _ptr(cache.buf), _ptr(q), _ptr(k), _ptr(v),
+                           _ptr(g), _ptr(lam), int(T), _dtype_code(k.dtype), ctypes.byref(p),
+                           _ptr(out), _dtype_code(out.dtype) if out is not None else DLA_F32,
+                           _ptr(boundary), _ptr(merge_idx), _ptr(score), _ptr(boundary_override),
+                           _ptr(merge_override), _ptr(workspace), workspace.numel(),
+                           _stream(dev))
+    _check(st, "dla_prefill")
+    return out, boundary, merge_idx, score
+
+
+def decode_step(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5, eps: float = 1e-6,
+                eps_rms: float = 1e-6, out=None, out_dtype=None, skip_readout: bool = False,
+                boundary=None, merge_idx=None, score=None, boundary_override=None,
+                merge_override=None, want_exports: bool = True):
+    """Absorb one token per head.  q, k: [B, H, d_k]; v: [B, H, d_v]; g: [B, H];
+    lam: [B, H, C] or None."""
+    torch = _torch()
+    B, H, C = cache.B, cache.H, cache.C
+    dev = cache.device
+    assert k.shape == (B, H, cache.d_k) and v.shape == (B, H, cache.d_v)
+    assert g.shape == (B, H) and g.dtype == torch.float32
+    for t in (q, k, v, g, lam, boundary_override, merge_override):
+        assert t is None or (t.is_contiguous() and t.device == dev)
+    if lam is not None:
+        assert lam.shape == (B, H, C) and lam.dtype == k.dtype
+    if out is None and not skip_readout:
+        out = torch.empty((B, H, cache.d_v), dtype=out_dtype or k.dtype, device=dev)
+    if want_exports:
+        boundary = boundary if boundary is not None else torch.empty((B, H), dtype=torch.int8,
+                                                                      device=dev)
+        merge_idx = merge_idx if merge_idx is not None else torch.empty((B, H), dtype=torch.int32,
+                                                                        device=dev)
+        score = score if score is not None else torch.empty((B, H), dtype=torch.float32,
+                                                            device=dev)
+    p = _params(tau, eps, eps_rms, skip_readout)
+    st = lib().dla_decode_step(ctypes.byref(cache.desc), _ptr(cache.buf), _ptr(q), _ptr(k),
+                               _ptr(v), _ptr(g), _ptr(lam), _dtype_code(k.dtype), ctypes.byref(p),
+                               _ptr(out), _dtype_code(out.dtype) if out is not None else DLA_F32,
+                               _ptr(boundary), _ptr(merge_idx), _ptr(score),
+                               _ptr(boundary_override), _ptr(merge_override), _stream(dev))
+    _check(st, "dla_decode_step")
+    return out, boundary, merge_idx, score
+
+
+def cache_export(cache: StateCache, heads=None) -> dict:
+    """Read a cache back to host memory and decode its layout: per head m, G,
+    tokens, and in chronological order F, Ibar, n, and the true (decayed)
+    states exp(G - F_j) S~_perm[j] as float64 [n_heads, C, d_k, d_v] (entries
+    j >= m are zero)."""
+    L = cache_layout(cache.B, cache.H, cache.C, cache.d_k, cache.d_v)
+    raw = cache.buf.cpu().numpy()
+    nh = cache.B * cache.H
+    heads = list(range(nh)) if heads is None else list(heads)
+    C, dk, dv = cache.C, cache.d_k, cache.d_v
+    res = {"m": np.zeros(len(heads), np.int32), "G": np.zeros(len(heads)),
+           "tokens": np.zeros(len(heads), np.int64), "F": np.zeros((len(heads), C)),
+           "ibar": np.zeros((len(heads), C)), "n": np.zeros((len(heads), C), np.int32),
+           "perm": np.zeros((len(heads), C), np.int32),
+           "S": np.zeros((len(heads), C, dk, dv)), "flags": int(raw[28:32].view(np.uint32)[0])}
+    states = raw[L.states_offset:].view(np.float32).reshape(nh, C, dk, dv)
+    for i, h in enumerate(heads):
+        base = L.meta_offset + h * L.meta_stride
+        mb = raw[base:base + L.meta_stride]
+        m = int(mb[0:4].view(np.int32)[0])
+        res["m"][i] = m
+        res["G"][i] = mb[8:16].view(np.float64)[0]
+        res["tokens"][i] = mb[16:24].view(np.int64)[0]
+        F = mb[32:32 + 8 * C].view(np.float64)
+        res["F"][i] = F
+        res["ibar"][i] = mb[32 + 8 * C:32 + 16 * C].view(np.float64)
+        res["n"][i] = mb[32 + 16 * C:32 + 20 * C].view(np.int32)
+        perm = mb[32 + 20 * C:32 + 24 * C].view(np.int32)
+        res["perm"][i] = perm
+        for j in range(m):
+            res["S"][i, j] = np.exp(res["G"][i] - F[j]) * states[h, perm[j]].astype(np.float64)
+    return res

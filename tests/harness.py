@@ -1,0 +1,106 @@
+"""Shared helpers of the GPU parity tests: move seeded inputs to the device, run
+the float64 oracle, derive near-tie overrides, and compare.
+
+Parity protocol.  The oracle runs first.  Where its decision is within rounding
+of the other outcome -- a score within DELTA_B of tau, or a capacity merge whose
+two lowest pair densities differ by less than DELTA_M relative -- the oracle's
+decision is passed to the HIP path as an override.  Every other boundary and
+merge index, the state counts and token counts must then match bit for bit, and
+outputs must match within the tolerance of the input dtype.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import OracleCache, oracle_forward
+from paper_2606_10650_amd.workloads import to_f64
+
+DELTA_B = 1e-4   # |I - tau| below this is a near tie (GPU score error is ~1e-6)
+DELTA_M = 1e-5   # relative density gap below this is a near tie
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def torch_mod():
+    import torch
+    return torch
+
+
+def dev_tensor(a: np.ndarray, dtype: str, shape, device="cuda"):
+    torch = torch_mod()
+    if dtype == "bf16":
+        t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return t.reshape(shape).to(device)
+
+
+def inputs_to_device(w, x, B, H, device="cuda"):
+    T = x["k"].shape[1]
+    q = dev_tensor(x["q"], w.dtype, (B, H, T, w.dk), device) if "q" in x else None
+    k = dev_tensor(x["k"], w.dtype, (B, H, T, w.dk), device)
+    v = dev_tensor(x["v"], w.dtype, (B, H, T, w.dv), device)
+    torch = torch_mod()
+    g = torch.from_numpy(np.ascontiguousarray(x["g"], np.float32)).reshape(B, H, T).to(device)
+    lam = dev_tensor(x["lam"], w.dtype, (B, H, T, w.C), device) if "lam" in x else None
+    return q, k, v, g, lam
+
+
+def f64(x, w):
+    return {k: (to_f64(x[k], w.dtype) if k in ("q", "k", "v", "lam") else
+                (x[k].astype(np.float64) if k == "g" else x[k])) for k in x}
+
+
+def run_oracle(w, x, C=None, tau=None, full=True, cache=None, b_override=None, m_override=None):
+    xf = f64(x, w)
+    return oracle_forward(xf["k"], xf["v"], xf["g"], C or w.C, w.tau if tau is None else tau,
+                          q=xf.get("q") if full else None, lam=xf.get("lam") if full else None,
+                          full=full, cache=cache, b_override=b_override, m_override=m_override)
+
+
+def near_tie_overrides(ref, b_override=None, m_override=None):
+    """Overrides that pin the oracle's decision wherever it is a near tie."""
+    bo = np.full(ref["b"].shape, -1, np.int8) if b_override is None else b_override.copy()
+    mo = np.full(ref["merge"].shape, -1, np.int32) if m_override is None else m_override.copy()
+    nb = ref["margin_b"] < DELTA_B
+    nm = ref["margin_m"] < DELTA_M
+    bo[nb] = ref["b"][nb]
+    mo[nm] = ref["merge"][nm]
+    return bo, mo, int(nb.sum()), int(nm.sum())
+
+
+def assert_decisions(gpu_b, gpu_m, ref, what=""):
+    gb = np.asarray(gpu_b).reshape(ref["b"].shape)
+    gm = np.asarray(gpu_m).reshape(ref["merge"].shape)
+    bad = np.argwhere(gb != ref["b"])
+    assert len(bad) == 0, f"{what}: boundary mismatch at (head, t) {bad[:5].tolist()}"
+    bad = np.argwhere(gm != ref["merge"])
+    assert len(bad) == 0, (f"{what}: merge mismatch at {bad[:5].tolist()}: gpu "
+                           f"{gm[tuple(bad[0])]} ref {ref['merge'][tuple(bad[0])]}")
+
+
+def assert_outputs(o_gpu, o_ref, tol, what=""):
+    """||o_gpu - o_ref|| <= tol * max(||o_ref_t||, rms_t ||o_ref_t||) per token."""
+    og = np.asarray(o_gpu, np.float64).reshape(o_ref.shape)
+    err = np.linalg.norm(og - o_ref, axis=-1)
+    nrm = np.linalg.norm(o_ref, axis=-1)
+    rms = np.sqrt((nrm ** 2).mean(axis=-1, keepdims=True))
+    ratio = err / (tol * np.maximum(nrm, rms))
+    worst = np.unravel_index(np.argmax(ratio), ratio.shape)
+    assert ratio.max() <= 1.0, (f"{what}: output error {err[worst]:.3e} at {worst} exceeds "
+                                f"{tol} x {max(nrm[worst], rms[worst[0], 0]):.3e}")
+    return float((err / np.maximum(nrm, rms)).max())
+
+
+def assert_cache(exp, ref_cache: OracleCache, tol, heads=None, what=""):
+    heads = range(len(exp["m"])) if heads is None else heads
+    for i, h in enumerate(heads):
+        m = int(ref_cache.m[h])
+        assert exp["m"][i] == m, f"{what}: head {h} m {exp['m'][i]} vs {m}"
+        assert (exp["n"][i, :m] == ref_cache.n[h, :m]).all(), f"{what}: head {h} counts"
+        ib = ref_cache.ibar[h, :m]
+        assert np.allclose(exp["ibar"][i, :m], ib, rtol=1e-5, atol=1e-6), f"{what}: head {h} Ibar"
+        for j in range(m):
+            Sr = ref_cache.S[h, j]
+            e = np.linalg.norm(exp["S"][i, j] - Sr)
+            assert e <= tol * max(np.linalg.norm(Sr), 1e-30), \
+                f"{what}: head {h} state {j} rel err {e / np.linalg.norm(Sr):.3e}"

@@ -1,0 +1,87 @@
+"""The C ABI without a GPU: the header compiles as C, libdla.so loads and
+exports every entry point the header declares, and host-side argument checks
+return their status codes without touching a device."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dla.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(dla_[a-z_]+)\s*\(", src)))
+
+
+def test_header_compiles_as_c(tmp_path):
+    c = tmp_path / "t.c"
+    c.write_text('#include "dla.h"\nint main(void){dla_cache_desc d={1,1,1,64,64};(void)d;return 0;}\n')
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"),
+                    "-fsyntax-only", str(c)], check=True)
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_2606_10650_amd import dla
+    lib = dla.lib()
+    names = _declared()
+    assert "dla_prefill" in names and "dla_decode_step" in names
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in dla.h but not exported"
+    assert set(dla.EXPORTED) == set(names)
+
+
+def test_host_side_errors():
+    from paper_2606_10650_amd import dla
+    L = dla.lib()
+    lay = dla.Layout()
+    bad = [dla.CacheDesc(1, 1, 8, 96, 64), dla.CacheDesc(1, 1, 2000, 64, 64)]
+    for d in bad:
+        assert L.dla_cache_layout_of(ctypes.byref(d), ctypes.byref(lay)) == dla.DLA_ERR_UNSUPPORTED
+    d = dla.CacheDesc(0, 1, 8, 64, 64)
+    assert L.dla_cache_layout_of(ctypes.byref(d), ctypes.byref(lay)) == dla.DLA_ERR_INVALID_ARG
+    d = dla.CacheDesc(2, 3, 8, 64, 128)
+    assert L.dla_cache_layout_of(ctypes.byref(d), ctypes.byref(lay)) == dla.DLA_OK
+    assert lay.total_bytes == lay.states_offset + 6 * 8 * 64 * 128 * 4
+    n = ctypes.c_size_t(0)
+    assert L.dla_state_cache_alloc(ctypes.byref(d), None, ctypes.byref(n), None) == dla.DLA_OK
+    assert n.value == lay.total_bytes
+    p = dla.Params(0.5, 1e-6, 1e-6, 0)
+    fake = ctypes.c_void_p(0x1000)
+    # missing k
+    st = L.dla_prefill(ctypes.byref(d), fake, fake, None, fake, fake, None, 10, 1, ctypes.byref(p),
+                       fake, 1, None, None, None, None, None, fake, 1 << 30, None)
+    assert st == dla.DLA_ERR_INVALID_ARG
+    assert L.dla_get_last_error() == dla.DLA_ERR_INVALID_ARG
+    # workspace too small
+    st = L.dla_prefill(ctypes.byref(d), fake, fake, fake, fake, fake, None, 10, 1, ctypes.byref(p),
+                       fake, 1, None, None, None, None, None, fake, 16, None)
+    assert st == dla.DLA_ERR_WORKSPACE
+    # bad dtype
+    st = L.dla_prefill(ctypes.byref(d), fake, fake, fake, fake, fake, None, 10, 7, ctypes.byref(p),
+                       fake, 1, None, None, None, None, None, fake, 1 << 30, None)
+    assert st == dla.DLA_ERR_INVALID_ARG
+    # T = 0 is a no-op
+    st = L.dla_prefill(ctypes.byref(d), fake, fake, fake, fake, fake, None, 0, 1, ctypes.byref(p),
+                       fake, 1, None, None, None, None, None, None, 0, None)
+    assert st == dla.DLA_OK
+    # decode without q but with readout
+    st = L.dla_decode_step(ctypes.byref(d), fake, None, fake, fake, fake, None, 1,
+                           ctypes.byref(p), fake, 1, None, None, None, None, None, None)
+    assert st == dla.DLA_ERR_INVALID_ARG
+    assert dla.status_string(dla.DLA_ERR_WORKSPACE) == "workspace missing or too small"
+    ws = ctypes.c_size_t(0)
+    assert L.dla_prefill_workspace_size(ctypes.byref(d), 1000, ctypes.byref(ws)) == dla.DLA_OK
+    assert ws.value >= 6 * 1000 * 12
+
+
+def test_missing_library_fails_loudly(tmp_path, monkeypatch):
+    from paper_2606_10650_amd import dla
+    monkeypatch.setattr(dla, "_lib", None)
+    monkeypatch.setattr(dla, "_LIB_PATH", str(tmp_path / "nope.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        dla.lib()

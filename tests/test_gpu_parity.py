@@ -1,0 +1,239 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle on
+the same seeded inputs.  Decisions bit-exact (near ties pinned to the oracle's
+choice), outputs within 1e-4 (float32 inputs) or 2e-2 (bfloat16 inputs)
+relative, final cache states within 1e-4, token counts exact."""
+import numpy as np
+import pytest
+
+from tests import harness as H
+from paper_2606_10650_amd.workloads import WORKLOADS, make_inputs, make_decode_tokens
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _dla():
+    from paper_2606_10650_amd import dla
+    return dla
+
+
+def _report(tag, **kw):
+    print(f"[{tag}] " + " ".join(f"{k}={v}" for k, v in kw.items()), flush=True)
+
+
+def _prefill_case(w, C=None, tau=None, T_split=None):
+    torch = _torch()
+    dla = _dla()
+    C = C or w.C
+    tau = w.tau if tau is None else tau
+    w = w.replace(C=C, tau=tau)
+    x = make_inputs(w)
+    ref = H.run_oracle(w, x)
+    bo, mo, nb, nm = H.near_tie_overrides(ref)
+    _report("prefill", case=w.label, near_b=nb, near_m=nm, boundaries=int(ref["b"].sum()),
+            merges=int((ref["merge"] >= 0).sum()))
+    q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    cache = dla.cache_alloc(w.B, w.H, C, w.dk, w.dv)
+    shp = (w.B, w.H, w.T)
+    bo_d = torch.from_numpy(bo).reshape(shp).cuda()
+    mo_d = torch.from_numpy(mo).reshape(shp).cuda()
+    if T_split is None:
+        out, b, mi, sc = dla.prefill(cache, q, k, v, g, lam, tau=tau, boundary_override=bo_d,
+                                     merge_override=mo_d)
+    else:
+        parts = []
+        s0 = 0
+        for s1 in list(T_split) + [w.T]:
+            sl = slice(s0, s1)
+            parts.append(dla.prefill(cache, q[:, :, sl].contiguous(), k[:, :, sl].contiguous(),
+                                     v[:, :, sl].contiguous(), g[:, :, sl].contiguous(),
+                                     lam[:, :, sl].contiguous(), tau=tau,
+                                     boundary_override=bo_d[:, :, sl].contiguous(),
+                                     merge_override=mo_d[:, :, sl].contiguous()))
+            s0 = s1
+        out, b, mi, sc = (torch.cat([p[i] for p in parts], dim=2) for i in range(4))
+    torch.cuda.synchronize()
+    nh = w.B * w.H
+    H.assert_decisions(b.cpu().numpy().reshape(nh, -1), mi.cpu().numpy().reshape(nh, -1), ref,
+                       w.label)
+    serr = np.abs(sc.cpu().numpy().reshape(nh, -1) - ref["score"]).max()
+    assert serr < H.DELTA_B / 10, f"score error {serr}"
+    rel = H.assert_outputs(out.float().cpu().numpy().reshape(nh, w.T, w.dv), ref["out"],
+                           H.TOL[w.dtype], w.label)
+    exp = dla.cache_export(cache)
+    H.assert_cache(exp, ref["cache"], 1e-4, what=w.label)
+    assert (exp["tokens"] == w.T).all()
+    _report("prefill-ok", case=w.label, max_score_err=f"{serr:.2e}", max_rel_out=f"{rel:.2e}")
+
+
+def test_prefill_cfg1():
+    _prefill_case(WORKLOADS["cfg1"])
+
+
+def test_prefill_cfg1_iid_merges_every_token():
+    _prefill_case(WORKLOADS["cfg1_iid"])
+
+
+def test_prefill_cfg1_capacity_one_and_threshold_zero():
+    _prefill_case(WORKLOADS["cfg1"], C=1)
+    _prefill_case(WORKLOADS["cfg1"].replace(T=300), C=300, tau=0.0)
+
+
+def test_prefill_bf16_geometric_segments_ragged():
+    # cfg2 distributions at a size the oracle finishes in seconds: 1000 tokens
+    # (7 chunks + a ragged tail of 104), capacity reached
+    _prefill_case(WORKLOADS["cfg2"].replace(B=1, H=4, T=1000, C=12))
+
+
+def test_prefill_bf16_spans_and_bursts():
+    _prefill_case(WORKLOADS["cfg3"].replace(B=1, H=3, T=2600, C=24, span_mean=200.0))
+
+
+def test_prefill_bf16_many_segments_slow_decay():
+    _prefill_case(WORKLOADS["cfg4"].replace(B=1, H=2, T=3000, C=40, n_seg=200))
+
+
+def test_prefill_mixed_head_dims():
+    _prefill_case(WORKLOADS["cfg2"].replace(B=1, H=2, T=700, C=9, dk=64, dv=128))
+    _prefill_case(WORKLOADS["cfg2"].replace(B=2, H=1, T=500, C=7, dk=128, dv=64))
+
+
+def test_prefill_continuation():
+    _prefill_case(WORKLOADS["cfg2"].replace(B=1, H=2, T=900, C=10), T_split=[1, 300, 301, 640])
+    _prefill_case(WORKLOADS["cfg1_iid"].replace(T=200), T_split=[57, 128])
+
+
+def test_decode_steps_from_empty_match_oracle():
+    """T decode steps from an empty cache equal the oracle's recurrence."""
+    torch = _torch()
+    dla = _dla()
+    for w in (WORKLOADS["cfg1"].replace(T=256), WORKLOADS["cfg1_iid"].replace(T=96),
+              WORKLOADS["cfg2"].replace(B=1, H=2, T=200, C=6)):
+        x = make_inputs(w)
+        ref = H.run_oracle(w, x)
+        bo, mo, nb, nm = H.near_tie_overrides(ref)
+        _report("decode", case=w.label, near_b=nb, near_m=nm)
+        q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+        cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+        bo_d = torch.from_numpy(bo).reshape(w.B, w.H, w.T).cuda()
+        mo_d = torch.from_numpy(mo).reshape(w.B, w.H, w.T).cuda()
+        outs, bs, ms, ss = [], [], [], []
+        for t in range(w.T):
+            o, b, mi, sc = dla.decode_step(cache, q[:, :, t].contiguous(), k[:, :, t].contiguous(),
+                                           v[:, :, t].contiguous(), g[:, :, t].contiguous(),
+                                           lam[:, :, t].contiguous(),
+                                           boundary_override=bo_d[:, :, t].contiguous(),
+                                           merge_override=mo_d[:, :, t].contiguous())
+            outs.append(o)
+            bs.append(b)
+            ms.append(mi)
+            ss.append(sc)
+        torch.cuda.synchronize()
+        nh = w.B * w.H
+        out = torch.stack(outs, 2).float().cpu().numpy().reshape(nh, w.T, w.dv)
+        b = torch.stack(bs, 2).cpu().numpy().reshape(nh, w.T)
+        mi = torch.stack(ms, 2).cpu().numpy().reshape(nh, w.T)
+        H.assert_decisions(b, mi, ref, w.label)
+        H.assert_outputs(out, ref["out"], H.TOL[w.dtype], w.label)
+        H.assert_cache(dla.cache_export(cache), ref["cache"], 1e-4, what=w.label)
+
+
+def test_prefill_then_decode_continuation():
+    """prefill(T1) followed by decode steps equals the oracle over all tokens."""
+    torch = _torch()
+    dla = _dla()
+    w = WORKLOADS["cfg2"].replace(B=1, H=2, T=420, C=8)
+    x = make_inputs(w)
+    ref = H.run_oracle(w, x)
+    bo, mo, _, _ = H.near_tie_overrides(ref)
+    q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    bo_d = torch.from_numpy(bo).reshape(1, 2, w.T).cuda()
+    mo_d = torch.from_numpy(mo).reshape(1, 2, w.T).cuda()
+    T1 = 389
+    cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+    o1, b1, m1, _ = dla.prefill(cache, q[:, :, :T1].contiguous(), k[:, :, :T1].contiguous(),
+                                v[:, :, :T1].contiguous(), g[:, :, :T1].contiguous(),
+                                lam[:, :, :T1].contiguous(), boundary_override=bo_d[:, :, :T1].contiguous(),
+                                merge_override=mo_d[:, :, :T1].contiguous())
+    outs, bs, ms = [o1], [b1], [m1]
+    for t in range(T1, w.T):
+        o, b, mi, _ = dla.decode_step(cache, q[:, :, t].contiguous(), k[:, :, t].contiguous(),
+                                      v[:, :, t].contiguous(), g[:, :, t].contiguous(),
+                                      lam[:, :, t].contiguous(),
+                                      boundary_override=bo_d[:, :, t].contiguous(),
+                                      merge_override=mo_d[:, :, t].contiguous())
+        outs.append(o.unsqueeze(2))
+        bs.append(b.unsqueeze(2))
+        ms.append(mi.unsqueeze(2))
+    torch.cuda.synchronize()
+    out = torch.cat(outs, 2).float().cpu().numpy().reshape(2, w.T, w.dv)
+    H.assert_decisions(torch.cat(bs, 2).cpu().numpy().reshape(2, -1),
+                       torch.cat(ms, 2).cpu().numpy().reshape(2, -1), ref, "prefill+decode")
+    H.assert_outputs(out, ref["out"], H.TOL[w.dtype], "prefill+decode")
+    H.assert_cache(dla.cache_export(cache), ref["cache"], 1e-4, what="prefill+decode")
+
+
+def test_forced_overrides_match_oracle():
+    """Random forced boundaries and merge indices take the same path on both sides."""
+    torch = _torch()
+    dla = _dla()
+    w = WORKLOADS["cfg2"].replace(B=1, H=2, T=600, C=6)
+    x = make_inputs(w)
+    rng = np.random.default_rng(11)
+    bo = np.where(rng.random((2, w.T)) < 0.08, 1, -1).astype(np.int8)
+    bo[rng.random((2, w.T)) < 0.05] = 0
+    mo = np.where(rng.random((2, w.T)) < 0.5, rng.integers(0, w.C - 1, (2, w.T)), -1).astype(np.int32)
+    ref = H.run_oracle(w, x, b_override=bo, m_override=mo)
+    bo2, mo2, _, _ = H.near_tie_overrides(ref, bo, mo)
+    q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+    out, b, mi, sc = dla.prefill(cache, q, k, v, g, lam,
+                                 boundary_override=torch.from_numpy(bo2).reshape(1, 2, -1).cuda(),
+                                 merge_override=torch.from_numpy(mo2).reshape(1, 2, -1).cuda())
+    torch.cuda.synchronize()
+    H.assert_decisions(b.cpu().numpy().reshape(2, -1), mi.cpu().numpy().reshape(2, -1), ref, "forced")
+    H.assert_outputs(out.float().cpu().numpy().reshape(2, w.T, w.dv), ref["out"], H.TOL["bf16"],
+                     "forced")
+    assert dla.cache_flags(cache) == 0
+
+
+def test_bad_merge_override_sets_flag_and_is_ignored():
+    torch = _torch()
+    dla = _dla()
+    w = WORKLOADS["cfg1_iid"].replace(T=40)
+    x = make_inputs(w)
+    ref = H.run_oracle(w, x)
+    bo, mo, _, _ = H.near_tie_overrides(ref)
+    mo[:, 20] = 99   # out of range: decided freely, flag raised
+    q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+    out, b, mi, sc = dla.prefill(cache, q, k, v, g, lam,
+                                 boundary_override=torch.from_numpy(bo).reshape(1, 2, -1).cuda(),
+                                 merge_override=torch.from_numpy(mo).reshape(1, 2, -1).cuda())
+    torch.cuda.synchronize()
+    H.assert_decisions(b.cpu().numpy().reshape(2, -1), mi.cpu().numpy().reshape(2, -1), ref, "bad")
+    assert dla.cache_flags(cache) == dla.DLA_FLAG_BAD_MERGE_OVERRIDE
+    assert dla.cache_flags(cache) == 0   # cleared by the read
+
+
+def test_skip_readout_builds_the_same_cache():
+    torch = _torch()
+    dla = _dla()
+    w = WORKLOADS["cfg2"].replace(B=1, H=2, T=530, C=7)
+    x = make_inputs(w)
+    ref = H.run_oracle(w, x)
+    bo, mo, _, _ = H.near_tie_overrides(ref)
+    q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+    _, b, mi, _ = dla.prefill(cache, None, k, v, g, None, skip_readout=True,
+                              boundary_override=torch.from_numpy(bo).reshape(1, 2, -1).cuda(),
+                              merge_override=torch.from_numpy(mo).reshape(1, 2, -1).cuda())
+    torch.cuda.synchronize()
+    H.assert_decisions(b.cpu().numpy().reshape(2, -1), mi.cpu().numpy().reshape(2, -1), ref, "skip")
+    H.assert_cache(dla.cache_export(cache), ref["cache"], 1e-4, what="skip")
