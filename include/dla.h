@@ -68,13 +68,20 @@ typedef struct {
  * eps: the epsilon of the score's denominator (eq. importance_score);
  * eps_rms: the epsilon of the RMSNorm applied to both states before scoring
  * (unit weight, over all d_k*d_v entries).  flags: DLA_SKIP_READOUT builds the
- * cache and the exports but computes no output (out may be NULL). */
+ * cache and the exports but computes no output (out may be NULL).
+ * stage_events: NULL, or DLA_PREFILL_STAGES + 1 hipEvent_t handles (created by
+ * the caller) that dla_prefill records on its stream before its first stage and
+ * after each stage (token frames, boundary scan, readout + state update), for
+ * timing the stages; dla_decode_step ignores it. */
 typedef struct {
   float tau;
   float eps;
   float eps_rms;
   uint32_t flags;
+  void* const* stage_events;
 } dla_params;
+
+#define DLA_PREFILL_STAGES 3
 
 #define DLA_SKIP_READOUT 1u
 
@@ -120,8 +127,9 @@ dla_status dla_state_cache_alloc(const dla_cache_desc* desc, void* dev_buf, size
 dla_status dla_cache_flags(const dla_cache_desc* desc, void* cache, uint32_t* flags,
                            void* stream);
 
-/* Workspace that dla_prefill needs for T tokens. */
-dla_status dla_prefill_workspace_size(const dla_cache_desc* desc, int32_t T, size_t* bytes);
+/* Workspace that dla_prefill needs for T tokens of the given input dtype. */
+dla_status dla_prefill_workspace_size(const dla_cache_desc* desc, int32_t T, dla_dtype in_dtype,
+                                      size_t* bytes);
 
 /*
  * Prefill: absorb T tokens per head into the cache, in order, computing for

@@ -130,11 +130,12 @@ dla_status dla_cache_flags(const dla_cache_desc* desc, void* cache, uint32_t* fl
   return ret(DLA_OK);
 }
 
-dla_status dla_prefill_workspace_size(const dla_cache_desc* desc, int32_t T, size_t* bytes) {
+dla_status dla_prefill_workspace_size(const dla_cache_desc* desc, int32_t T, dla_dtype in_dtype,
+                                      size_t* bytes) {
   dla_status s = check_desc(desc);
   if (s != DLA_OK) return ret(s);
-  if (!bytes || T < 0) return ret(DLA_ERR_INVALID_ARG);
-  *bytes = prefill_workspace_bytes(*desc, T);
+  if (!bytes || T < 0 || !dtype_ok(in_dtype)) return ret(DLA_ERR_INVALID_ARG);
+  *bytes = prefill_workspace_bytes(*desc, T, in_dtype);
   return ret(DLA_OK);
 }
 
@@ -154,7 +155,7 @@ dla_status dla_prefill(const dla_cache_desc* desc, void* cache, const void* q, c
   if ((int64_t)desc->B * desc->H * (int64_t)T * (desc->C > 128 ? desc->C : 128) >
       ((int64_t)1 << 40))
     return ret(DLA_ERR_UNSUPPORTED);
-  const size_t need = prefill_workspace_bytes(*desc, T);
+  const size_t need = prefill_workspace_bytes(*desc, T, in_dtype);
   if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 255u))
     return ret(DLA_ERR_WORKSPACE);
   PrefillArgs a;
@@ -184,7 +185,8 @@ dla_status dla_prefill(const dla_cache_desc* desc, void* cache, const void* q, c
   a.in_dtype = in_dtype;
   a.out_dtype = out_dtype;
   a.workspace = (char*)workspace;
-  if (launch_prefill(a, (hipStream_t)stream) != hipSuccess) return ret(DLA_ERR_HIP);
+  if (launch_prefill(a, (hipStream_t)stream, params->stage_events) != hipSuccess)
+    return ret(DLA_ERR_HIP);
   return ret(DLA_OK);
 }
 

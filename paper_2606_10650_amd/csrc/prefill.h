@@ -32,16 +32,23 @@ struct PrefillArgs {
 //                           T: it starts a state that is never merged away;
 //                           t' in (t, T): its state was merged into its left
 //                           neighbour at token t' (Alg. 2)
-//   init   per head: int32 m0, int32 pad, double F0[C], int32 perm0[C],
-//          int32 death0[C] (death token of the states present before the call)
+//   init   per head: int32 m0, int32 pad, double G0, double F0[C], int32 perm0[C],
+//          int32 death0[C] (the cache's metadata before the call, and the death
+//          token of the states present before the call)
+//   shadow [nh][C][d_v/32][d_k/16][2][32][8] elements of the input dtype: a copy
+//          of each state (by physical slot) in the per-lane order of the MFMA
+//          A operand, for the readout stage
 struct PrefillWS {
   double* Gtok;
   int32_t* death;
   char* init;
   size_t init_stride;
+  char* shadow;
 };
 
-__host__ __device__ inline size_t ws_init_stride(int C) { return round_up(8 + 16 * (size_t)C, 256); }
+__host__ __device__ inline size_t ws_init_stride(int C) { return round_up(16 + 16 * (size_t)C, 256); }
+
+__host__ __device__ inline size_t dtype_bytes(dla_dtype t) { return t == DLA_F32 ? 4 : 2; }
 
 __host__ __device__ inline PrefillWS ws_layout(char* base, int nh, int T, int C) {
   PrefillWS w;
@@ -52,19 +59,23 @@ __host__ __device__ inline PrefillWS ws_layout(char* base, int nh, int T, int C)
   off = round_up(off + (size_t)nh * T * sizeof(int32_t), 256);
   w.init = base + off;
   w.init_stride = ws_init_stride(C);
+  off = round_up(off + (size_t)nh * w.init_stride, 256);
+  w.shadow = base + off;
   return w;
 }
 
-inline size_t prefill_workspace_bytes(const dla_cache_desc& d, int T) {
+inline size_t prefill_workspace_bytes(const dla_cache_desc& d, int T, dla_dtype in) {
   const size_t nh = (size_t)d.B * d.H;
   size_t off = round_up(nh * T * sizeof(double), 256);
   off = round_up(off + nh * T * sizeof(int32_t), 256);
-  off += nh * ws_init_stride(d.C);
+  off = round_up(off + nh * ws_init_stride(d.C), 256);
+  off += nh * (size_t)d.C * d.d_k * d.d_v * dtype_bytes(in);
   return off;
 }
 
 struct InitView {
   int32_t* m0;
+  double* G0;
   double* F0;
   int32_t* perm0;
   int32_t* death0;
@@ -74,8 +85,9 @@ __host__ __device__ inline InitView init_at(const PrefillWS& w, int h, int C) {
   char* p = w.init + (size_t)h * w.init_stride;
   InitView v;
   v.m0 = reinterpret_cast<int32_t*>(p);
-  v.F0 = reinterpret_cast<double*>(p + 8);
-  v.perm0 = reinterpret_cast<int32_t*>(p + 8 + 8 * (size_t)C);
+  v.G0 = reinterpret_cast<double*>(p + 8);
+  v.F0 = reinterpret_cast<double*>(p + 16);
+  v.perm0 = reinterpret_cast<int32_t*>(p + 16 + 8 * (size_t)C);
   v.death0 = v.perm0 + C;
   return v;
 }
@@ -84,12 +96,18 @@ hipError_t launch_prefill_prep(const PrefillArgs& a, hipStream_t s);
 hipError_t launch_prefill_scan(const PrefillArgs& a, hipStream_t s);
 hipError_t launch_prefill_readout(const PrefillArgs& a, hipStream_t s);
 
-inline hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s) {
-  hipError_t e = launch_prefill_prep(a, s);
-  if (e != hipSuccess) return e;
-  e = launch_prefill_scan(a, s);
-  if (e != hipSuccess) return e;
-  return launch_prefill_readout(a, s);
+// Stages in order; ev (nullable) receives an event before the first stage and
+// after each stage.
+inline hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s, void* const* ev) {
+  hipError_t (*stages[DLA_PREFILL_STAGES])(const PrefillArgs&, hipStream_t) = {
+      launch_prefill_prep, launch_prefill_scan, launch_prefill_readout};
+  if (ev && hipEventRecord((hipEvent_t)ev[0], s) != hipSuccess) return hipErrorInvalidValue;
+  for (int i = 0; i < DLA_PREFILL_STAGES; ++i) {
+    hipError_t e = stages[i](a, s);
+    if (e != hipSuccess) return e;
+    if (ev && hipEventRecord((hipEvent_t)ev[i + 1], s) != hipSuccess) return hipErrorInvalidValue;
+  }
+  return hipSuccess;
 }
 
 }  // namespace dla

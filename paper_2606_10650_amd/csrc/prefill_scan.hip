@@ -30,7 +30,10 @@ __global__ __launch_bounds__(256) void prefill_prep_kernel(PrefillArgs a, Prefil
   InitView iv = init_at(w, h, C);
   const int m0 = min(max(*M.m, 0), C);
   const double G0 = *M.G;
-  if (tid == 0) *iv.m0 = m0;
+  if (tid == 0) {
+    *iv.m0 = m0;
+    *iv.G0 = G0;
+  }
   for (int j = tid; j < C; j += 256) {
     iv.F0[j] = M.F[j];
     iv.perm0[j] = M.perm[j];

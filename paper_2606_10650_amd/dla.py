@@ -34,7 +34,10 @@ class CacheDesc(ctypes.Structure):
 
 class Params(ctypes.Structure):
     _fields_ = [("tau", ctypes.c_float), ("eps", ctypes.c_float), ("eps_rms", ctypes.c_float),
-                ("flags", ctypes.c_uint32)]
+                ("flags", ctypes.c_uint32), ("stage_events", ctypes.c_void_p)]
+
+
+PREFILL_STAGES = ("frames", "scan", "readout")
 
 
 class Layout(ctypes.Structure):
@@ -63,7 +66,7 @@ def lib():
                                             ctypes.POINTER(ctypes.c_size_t), P]
         L.dla_cache_flags.argtypes = [ctypes.POINTER(CacheDesc), P, ctypes.POINTER(ctypes.c_uint32),
                                       P]
-        L.dla_prefill_workspace_size.argtypes = [ctypes.POINTER(CacheDesc), ctypes.c_int32,
+        L.dla_prefill_workspace_size.argtypes = [ctypes.POINTER(CacheDesc), ctypes.c_int32, I,
                                                  ctypes.POINTER(ctypes.c_size_t)]
         L.dla_prefill.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, ctypes.c_int32, I,
                                   ctypes.POINTER(Params), P, I, P, P, P, P, P, P, ctypes.c_size_t, P]
@@ -158,21 +161,31 @@ def cache_flags(cache: StateCache) -> int:
     return int(f.value)
 
 
-def workspace_bytes(cache: StateCache, T: int) -> int:
+def workspace_bytes(cache: StateCache, T: int, dtype=None) -> int:
+    """Prefill workspace for T tokens of input dtype (torch dtype, default bf16)."""
+    code = DLA_BF16 if dtype is None else _dtype_code(dtype)
     n = ctypes.c_size_t(0)
-    _check(lib().dla_prefill_workspace_size(ctypes.byref(cache.desc), int(T), ctypes.byref(n)),
-           "dla_prefill_workspace_size")
+    _check(lib().dla_prefill_workspace_size(ctypes.byref(cache.desc), int(T), code,
+                                            ctypes.byref(n)), "dla_prefill_workspace_size")
     return int(n.value)
 
 
-def _params(tau, eps, eps_rms, skip_readout):
-    return Params(float(tau), float(eps), float(eps_rms), DLA_SKIP_READOUT if skip_readout else 0)
+def _params(tau, eps, eps_rms, skip_readout, stage_events=None):
+    p = Params(float(tau), float(eps), float(eps_rms), DLA_SKIP_READOUT if skip_readout else 0,
+               None)
+    if stage_events is not None:
+        # torch.cuda.Event objects (enable_timing=True); keep the array alive in p
+        assert len(stage_events) == len(PREFILL_STAGES) + 1
+        arr = (ctypes.c_void_p * len(stage_events))(*[e.cuda_event for e in stage_events])
+        p._events_keepalive = arr
+        p.stage_events = ctypes.cast(arr, ctypes.c_void_p)
+    return p
 
 
 def prefill(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5, eps: float = 1e-6,
             eps_rms: float = 1e-6, out=None, out_dtype=None, skip_readout: bool = False,
             boundary=None, merge_idx=None, score=None, boundary_override=None,
-            merge_override=None, workspace=None, want_exports: bool = True):
+            merge_override=None, workspace=None, want_exports: bool = True, stage_events=None):
     """Absorb T tokens per head.  q, k: [B, H, T, d_k]; v: [B, H, T, d_v]; g:
     [B, H, T] float32; lam: [B, H, T, C] or None.  Returns (out, boundary,
     merge_idx, score); exports not requested are None."""
@@ -198,10 +211,12 @@ def prefill(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5, eps: f
                                                                         device=dev)
         score = score if score is not None else torch.empty((B, H, T), dtype=torch.float32,
                                                             device=dev)
-    wsb = workspace_bytes(cache, T)
+    wsb = workspace_bytes(cache, T, k.dtype)
     if workspace is None or workspace.numel() < wsb:
         workspace = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
-    p = _params(tau, eps, eps_rms, skip_readout)
+    for e in stage_events or ():
+        e.record()   # make sure the event exists before the library records it
+    p = _params(tau, eps, eps_rms, skip_readout, stage_events)
     st = lib().dla_prefill(ctypes.byref(cache.desc), _ptr(cache.buf), _ptr(q), _ptr(k), _ptr(v),
                            _ptr(g), _ptr(lam), int(T), _dtype_code(k.dtype), ctypes.byref(p),
                            _ptr(out), _dtype_code(out.dtype) if out is not None else DLA_F32,

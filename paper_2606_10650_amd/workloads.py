@@ -196,6 +196,20 @@ def lambda_weights(w: Workload, h: int) -> np.ndarray:
     return _rng(w.seed, 0, h, _S_W).standard_normal((w.C, w.dk))
 
 
+def _parallel(fn, n):
+    """Run fn(i) for i < n on a thread pool (numpy releases the GIL in the bulk
+    kernels used here); results are written in place, so the order is free."""
+    import concurrent.futures as cf
+    import os
+    workers = max(1, min(n, int(os.environ.get("DLA_GEN_THREADS", os.cpu_count() or 1)), 16))
+    if workers == 1:
+        for i in range(n):
+            fn(i)
+        return
+    with cf.ThreadPoolExecutor(workers) as ex:
+        list(ex.map(fn, range(n)))
+
+
 def make_inputs(w: Workload, heads: Optional[list] = None, with_lambda: bool = True,
                 with_q: bool = True):
     """Draw the inputs of a prefill workload.
@@ -218,10 +232,10 @@ def make_inputs(w: Workload, heads: Optional[list] = None, with_lambda: bool = T
         out["q"] = np.empty((n, w.T, w.dk), sdt)
     if with_lambda:
         out["lam"] = np.empty((n, w.T, w.C), sdt)
-    plans = {}
-    for i, (b, h) in enumerate(heads):
-        if b not in plans:
-            plans[b] = segment_plan(w, b)
+    plans = {b: segment_plan(w, b) for b in sorted({b for b, _ in heads})}
+
+    def one(i):
+        b, h = heads[i]
         seg, rho2 = plans[b]
         k, v, q, g = _head_tokens(w, b, h, seg, rho2)
         out["k"][i] = store(k, w.dtype)
@@ -233,6 +247,8 @@ def make_inputs(w: Workload, heads: Optional[list] = None, with_lambda: bool = T
             # lambda is drawn from the stored (rounded) query, as a layer would see it
             qs = to_f64(out["q"][i], w.dtype) if with_q else q
             out["lam"][i] = store(1.0 + 0.5 * (qs @ lambda_weights(w, h).T), w.dtype)
+
+    _parallel(one, n)
     return out
 
 
@@ -259,3 +275,37 @@ def make_decode_tokens(w: Workload, steps: Optional[int] = None, heads: Optional
                               w.dtype)
     out["heads"] = list(heads)
     return out
+
+
+def make_prefix_torch(w: Workload, device, with_q: bool = False):
+    """Device-side draw of a prefill workload's k, v, g (and q) with the same
+    recipe as make_inputs, from torch's generator seeded with w.seed: for
+    prefixes too large to draw on the host (B*H*T in the billions).  Values
+    differ from make_inputs' numpy streams; the segment plan is the same.
+    Returns bf16/f32 tensors [B, H, T, d] and g [B, H, T] float32."""
+    import torch
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(w.seed) * 1000003 + 17)
+    k = torch.empty((w.B, w.H, w.T, w.dk), dtype=tdt, device=device)
+    v = torch.empty((w.B, w.H, w.T, w.dv), dtype=tdt, device=device)
+    q = torch.empty((w.B, w.H, w.T, w.dk), dtype=tdt, device=device) if with_q else None
+    g = torch.empty((w.B, w.H, w.T), dtype=torch.float32, device=device)
+    for b in range(w.B):
+        seg_np, rho_np = segment_plan(w, b)
+        seg = torch.from_numpy(seg_np).to(device)
+        a = torch.from_numpy(np.sqrt(rho_np)).to(device=device, dtype=torch.float32)[None, :, None]
+        c = torch.from_numpy(np.sqrt(1.0 - rho_np)).to(device=device,
+                                                     dtype=torch.float32)[None, :, None]
+        nseg = int(seg_np.max()) + 1
+        mu_k = torch.randn((w.H, nseg, w.dk), generator=gen, device=device)
+        mu_v = torch.randn((w.H, nseg, w.dv), generator=gen, device=device)
+        kk = a * mu_k[:, seg] + c * torch.randn((w.H, w.T, w.dk), generator=gen, device=device)
+        k[b] = (kk / kk.norm(dim=-1, keepdim=True)).to(tdt)
+        v[b] = (a * mu_v[:, seg] + c * torch.randn((w.H, w.T, w.dv), generator=gen,
+                                                   device=device)).to(tdt)
+        g[b] = torch.rand((w.H, w.T), generator=gen, device=device) * w.g_lo
+        if with_q:
+            qq = torch.randn((w.H, w.T, w.dk), generator=gen, device=device)
+            q[b] = (qq / qq.norm(dim=-1, keepdim=True)).to(tdt)
+    return q, k, v, g
