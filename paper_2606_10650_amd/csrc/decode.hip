@@ -157,6 +157,8 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
           bb = sArg[w];
           ii = sArgI[w];
         }
+      // no comparable density (NaN scores from non-finite inputs): the first pair
+      if (ii < 0 || ii > C - 2) ii = 0;
       if (a.m_ovr && a.m_ovr[h] != -1) {
         const int f = a.m_ovr[h];
         if (f >= 0 && f <= C - 2)

@@ -5,15 +5,31 @@
 // token in float64, and a copy of the cache's per-head metadata as it was
 // before the call (later stages overwrite the cache).
 //
-// Stage 2 (scan, one workgroup per head, sequential over tokens): the newest
-// state lives in registers (float32, 64 values per thread for d = 128).  Per
-// token: the two scalars b = |S|^2 and c = k^T S v (one block reduction), the
-// score in float64 from its rank-one closed form, the boundary, and -- when a
-// new state opens in a full cache -- the argmin over the C-1 adjacent pair
-// densities kept in LDS.  Emits b_t, merge index and score per token, and the
-// death token of every state leader (the token at which Alg. 2 merged that
-// state into its left neighbour), from which the readout stage reconstructs the
-// chronological index of every state at every token without a replay.
+// Stage 2 (scan, one workgroup per head, sequential over chunks of 64 tokens).
+// The decisions are sequential -- whether token t opens a state depends on the
+// newest state, which depends on every earlier decision -- but within a chunk
+// the score of token t against a newest state that started at position p has a
+// closed form in a few chunk-wide tables, so each chunk costs a handful of
+// dense MFMA products plus a short pointer chase:
+//   * P[s][t] = (k_s . k_t)(v_s . v_t)  (Gram products, MFMA), a_t = P[t][t];
+//   * c0[t] = k_t^T S_0 v_t against the newest state S_0 at the chunk start
+//     (MFMA with S_0 split into three bf16 terms, exact to float32 rounding);
+//   * R[p][t] = sum_{s=p}^{t-1} exp(G_t - G_s) P[t][s], so that k_t^T S v_t for
+//     the state S of tokens p..t-1 is R[p][t] (plus the decayed c0 term when
+//     the state began before the chunk);
+//   * |S|^2 follows the recurrence b <- alpha^2 (b + 2c + a), evaluated for
+//     all t at once as a wavefront scan of affine maps.
+// The score (rank-one closed form of the RMS-normalised distance, Sec. 3.1)
+// and the boundary test then hold for every token of a row at once; a ballot
+// finds the first boundary, which starts the next row.  Each boundary runs the
+// capacity schedule of Alg. 2 on the (count, score) pairs in LDS.  At the
+// chunk end the newest state (float32 MFMA accumulators, one 32-row band of
+// d_k per wave) is advanced by the chunk's tokens.  Emits b_t, merge index and
+// score per token, and the death token of every state leader (the token at
+// which Alg. 2 merged that state into its left neighbour), from which the
+// readout stage reconstructs the chronological index of every state at every
+// token without a replay.
+#include "mfma.h"
 #include "prefill.h"
 
 namespace dla {
@@ -73,275 +89,543 @@ hipError_t launch_prefill_prep(const PrefillArgs& a, hipStream_t s) {
 // ---------------------------------------------------------------------------
 // stage 2
 // ---------------------------------------------------------------------------
-template <int DK, int DV>
-struct ScanTile {
-  static constexpr int CQ = DV / 4;
-  static constexpr int RG = 256 / CQ;
-  static constexpr int NV = DK / RG;
+constexpr int SL = 64;  // tokens per scan chunk (one per lane of a wavefront)
+
+typedef unsigned int u32x4s __attribute__((ext_vector_type(4)));
+
+template <int DK, int DV, typename Tin>
+struct ScanP {
+  static constexpr int K16 = SL * DK * (int)sizeof(Tin) / 16 / 256;  // 16-byte K pieces per thread
+  static constexpr int V16 = SL * DV * (int)sizeof(Tin) / 16 / 256;
+  static size_t smem_bytes(int C) {
+    size_t off = (size_t)SL * (DK + DV) * sizeof(Tin);  // sK, sV
+    off += (size_t)SL * (SL + 1) * 4;                   // sP
+    off += (size_t)SL * SL * 4;                         // sR
+    off += (size_t)8 * SL * 4;                          // sPart[4], sQ[4]
+    off += (size_t)SL * 4 * 8;                          // float rows
+    off += (size_t)SL * 4 * 3 + SL * 2;                 // int rows, int8 rows
+    off = round_up(off, 8);
+    off += (size_t)C * (8 + 4 + 4) + 64;
+    return round_up(off, 16);
+  }
 };
+
+// Score of a rank-one token state (|k|^2|v|^2 = a) against a state S with
+// |S|^2 = b and k^T S v = c, both RMS-normalised (closed form of the
+// State Information Score).
+__device__ __forceinline__ float score_f(float a, float b, float c, float D, float eps,
+                                         float eps_rms) {
+  const float rs2 = a / D + eps_rms;
+  const float rS2 = b / D + eps_rms;
+  const float num = a / rs2 + b / rS2 - 2.f * c * rsqrtf(rs2 * rS2);
+  return sqrtf(fmaxf(num, 0.f)) / (sqrtf(b / rS2) + eps);
+}
 
 template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, PrefillWS w) {
-  using ST = ScanTile<DK, DV>;
+  using FR = Frag<Tin>;
+  using FT = typename FR::T;
+  using P = ScanP<DK, DV, Tin>;
   constexpr int D = DK * DV;
+  constexpr int NB = DK / 32;  // 32-row bands of d_k: band b is held by wave b
+  constexpr int NJ = DV / 32;  // 32-column tiles of d_v
+  constexpr int KSK = DK / 16, KSV = DV / 16;
+  constexpr int K16 = P::K16, V16 = P::V16;
   const int h = blockIdx.x;
   const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wv = tid >> 6;
+  const int half = lane >> 5;
+  const int l32 = lane & 31;
   const int C = a.desc.C;
   const int T = a.T;
-  const int cq = tid % ST::CQ;
-  const int rg = tid / ST::CQ;
+  const size_t tok0 = (size_t)h * T;
+  const float Df = (float)D;
 
-  extern __shared__ double smem[];
-  double* sI = smem;                                     // [C] aggregated scores
-  int32_t* sN = reinterpret_cast<int32_t*>(sI + C);      // [C] token counts
-  int32_t* sLead = sN + C;                               // [C] leader token of each state
-  __shared__ float sk[2][DK], sv[2][DV];
-  __shared__ float red[16];
-  __shared__ double sDecI;
-  __shared__ int sDec[2];
-  __shared__ double sArg[4];
-  __shared__ int sArgI[4];
+  extern __shared__ __align__(16) char smem[];
+  Tin* sK = reinterpret_cast<Tin*>(smem);
+  Tin* sV = sK + SL * DK;
+  float* sP = reinterpret_cast<float*>(sV + SL * DV);  // [SL][SL+1]
+  float* sR = sP + SL * (SL + 1);                      // [SL][SL], R[p][t]
+  float* sPart = sR + SL * SL;                         // [4][SL]
+  float* sQ = sPart + 4 * SL;                          // [4][SL]
+  float* sGc = sQ + 4 * SL;    // G_t - G(chunk start), float
+  float* sA = sGc + SL;        // exp(sGc[t])
+  float* sAl2 = sA + SL;       // alpha_t^2
+  float* sDe = sAl2 + SL;      // exp(G_end - G_t)
+  float* sa = sDe + SL;        // |k_t|^2 |v_t|^2
+  float* sc0 = sa + SL;        // k_t^T S_0 v_t
+  float* sIo = sc0 + SL;       // scores
+  float* sRed = sIo + SL;      // reductions (8 floats used)
+  int32_t* sMo = reinterpret_cast<int32_t*>(sRed + SL);  // merge overrides
+  int32_t* sMout = sMo + SL;                             // merge indices
+  int32_t* sDC = sMout + SL;                             // death tokens of the chunk's tokens
+  int8_t* sBo = reinterpret_cast<int8_t*>(sDC + SL);     // boundary overrides
+  int8_t* sBout = sBo + SL;                              // boundaries
+  char* q8 = reinterpret_cast<char*>(sBout + SL);
+  double* sIb = reinterpret_cast<double*>(smem + round_up((size_t)(q8 - smem), 8));  // [C]
+  int32_t* sN = reinterpret_cast<int32_t*>(sIb + C);  // [C]
+  int32_t* sLead = sN + C;                            // [C]
+  int32_t* sMisc = sLead + C;                         // m, p_last
 
   Meta M = meta_at(a.cache + a.meta_offset + (size_t)h * a.meta_stride, C);
   InitView iv = init_at(w, h, C);
   const int m0 = min(max(*M.m, 0), C);
-  int m = m0;
   for (int j = tid; j < C; j += 256) {
-    sI[j] = M.ibar[j];
+    sIb[j] = M.ibar[j];
     sN[j] = M.n[j];
     sLead[j] = j - m0;
   }
+  if (tid == 0) sMisc[0] = m0;
 
-  const float* states = reinterpret_cast<const float*>(a.cache + a.states_offset) +
-                        (size_t)h * C * D;
-  float4 S[ST::NV];
-  double Fo = 0.0;
-  if (m0 > 0) {
-    const float4* src =
-        reinterpret_cast<const float4*>(states + (size_t)min(max(M.perm[m0 - 1], 0), C - 1) * D);
+  // newest state at the start of the call, true (decayed) values, as MFMA
+  // accumulators: wave b < NB holds rows 32b.. of d_k, all d_v columns
+  f32x16 S[NJ];
 #pragma unroll
-    for (int r = 0; r < ST::NV; ++r) S[r] = src[tid + 256 * r];
-    Fo = M.F[m0 - 1];
-  } else {
+  for (int nj = 0; nj < NJ; ++nj) S[nj] = zero16();
+  const double G0 = *M.G;
+  if (m0 > 0 && wv < NB) {
+    const float* src = reinterpret_cast<const float*>(a.cache + a.states_offset) +
+                       ((size_t)h * C + min(max(M.perm[m0 - 1], 0), C - 1)) * D;
+    const float f = (float)exp(G0 - M.F[m0 - 1]);
 #pragma unroll
-    for (int r = 0; r < ST::NV; ++r) S[r] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int nj = 0; nj < NJ; ++nj)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        S[nj][r] = f * src[(size_t)(32 * wv + out_row(r, lane)) * DV + 32 * nj + l32];
   }
-
-  const Tin* kin = static_cast<const Tin*>(a.k) + (size_t)h * T * DK;
-  const Tin* vin = static_cast<const Tin*>(a.v) + (size_t)h * T * DV;
-  const double* Gt = w.Gtok + (size_t)h * T;
-  int32_t* death = w.death + (size_t)h * T;
-  const size_t tok0 = (size_t)h * T;
-
-  // token 0 into LDS
-  if (tid < DK) sk[0][tid] = to_f32(kin[tid]);
-  if (tid >= 128 && tid - 128 < DV) sv[0][tid - 128] = to_f32(vin[tid - 128]);
-
-  for (int t = 0; t < T; ++t) {
-    const int buf = t & 1;
-    // prefetch the next token
-    float pk = 0.f, pv = 0.f;
-    if (t + 1 < T) {
-      if (tid < DK) pk = to_f32(kin[(size_t)(t + 1) * DK + tid]);
-      if (tid >= 128 && tid - 128 < DV) pv = to_f32(vin[(size_t)(t + 1) * DV + tid - 128]);
-    }
-    const double G = Gt[t];
-    __syncthreads();
-
-    const float4 v4 = reinterpret_cast<const float4*>(sv[buf])[cq];
-    float ct = 0.f, bt = 0.f;
+  auto state_norm2 = [&]() -> float {  // |S|^2 over the block
+    float x = 0.f;
+    if (wv < NB) {
 #pragma unroll
-    for (int r = 0; r < ST::NV; ++r) {
-      const float kr = sk[buf][rg + ST::RG * r];
-      const float4 s = S[r];
-      ct += kr * (s.x * v4.x + s.y * v4.y + s.z * v4.z + s.w * v4.w);
-      bt += s.x * s.x + s.y * s.y + s.z * s.z + s.w * s.w;
-    }
-    float kk = 0.f, vv = 0.f;
-    if (tid < DK) kk = sk[buf][tid] * sk[buf][tid];
-    if (tid < DV) vv = sv[buf][tid] * sv[buf][tid];
-    ct = wave_sum(ct);
-    bt = wave_sum(bt);
-    kk = wave_sum(kk);
-    vv = wave_sum(vv);
-    if ((tid & 63) == 0) {
-      red[(tid >> 6)] = ct;
-      red[4 + (tid >> 6)] = bt;
-      red[8 + (tid >> 6)] = kk;
-      red[12 + (tid >> 6)] = vv;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      double I = 0.0;
-      int b = 1;
-      if (m > 0) {
-        const float c = (red[0] + red[1]) + (red[2] + red[3]);
-        const float bb = (red[4] + red[5]) + (red[6] + red[7]);
-        const float k2 = (red[8] + red[9]) + (red[10] + red[11]);
-        const float v2 = (red[12] + red[13]) + (red[14] + red[15]);
-        const double f = exp(G - Fo);
-        I = info_score((double)k2 * (double)v2, f * f * (double)bb, f * (double)c, (double)D,
-                       a.eps, a.eps_rms);
-        b = (I >= (double)a.tau) ? 1 : 0;
-        if (a.b_ovr && a.b_ovr[tok0 + t] != -1) b = a.b_ovr[tok0 + t] ? 1 : 0;
-        if (C == 1) b = 0;
-      }
-      sDecI = I;
-      sDec[0] = b;
-    }
-    __syncthreads();
-    const int b = sDec[0];
-    const double I = sDecI;
-
-    int istar = -1;
-    if (b && m == C) {
-      double best = INFINITY;
-      int bi = 0x7fffffff;
-      for (int i = tid; i + 1 < C; i += 256) {
-        const double d = (sI[i] + sI[i + 1]) / (double)(sN[i] + sN[i + 1]);
-        if (d < best) {
-          best = d;
-          bi = i;
-        }
-      }
+      for (int nj = 0; nj < NJ; ++nj)
 #pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        const double ob = __shfl_xor(best, o, 64);
-        const int oi = __shfl_xor(bi, o, 64);
-        if (ob < best || (ob == best && oi < bi)) {
-          best = ob;
-          bi = oi;
-        }
-      }
-      if ((tid & 63) == 0) {
-        sArg[tid >> 6] = best;
-        sArgI[tid >> 6] = bi;
-      }
-      __syncthreads();
-      if (tid == 0) {
-        double bb = sArg[0];
-        int ii = sArgI[0];
-        for (int q = 1; q < 4; ++q)
-          if (sArg[q] < bb || (sArg[q] == bb && sArgI[q] < ii)) {
-            bb = sArg[q];
-            ii = sArgI[q];
+        for (int r = 0; r < 16; ++r) x += S[nj][r] * S[nj][r];
+    }
+    x = wave_sum(x);
+    __syncthreads();
+    if (lane == 0) sRed[wv] = x;
+    __syncthreads();
+    const float b = (sRed[0] + sRed[1]) + (sRed[2] + sRed[3]);
+    __syncthreads();
+    return b;
+  };
+  float b0 = state_norm2();
+
+  const Tin* Kin = static_cast<const Tin*>(a.k) + tok0 * DK;
+  const Tin* Vin = static_cast<const Tin*>(a.v) + tok0 * DV;
+  const double* Gtok = w.Gtok + tok0;
+  int32_t* death = w.death + tok0;
+  constexpr int KROW16 = DK * (int)sizeof(Tin) / 16;  // 16-byte pieces per key row
+  constexpr int VROW16 = DV * (int)sizeof(Tin) / 16;
+  u32x4s pk[K16], pv[V16];
+  auto prefetch = [&](int c0n) __attribute__((always_inline)) {
+    const int nr = min(SL, T - c0n);
+#pragma unroll
+    for (int u = 0; u < K16; ++u) {
+      const int pi = tid + 256 * u;
+      const int r = min(pi / KROW16, nr - 1);
+      pk[u] = reinterpret_cast<const u32x4s*>(Kin + (size_t)(c0n + r) * DK)[pi % KROW16];
+    }
+#pragma unroll
+    for (int u = 0; u < V16; ++u) {
+      const int pi = tid + 256 * u;
+      const int r = min(pi / VROW16, nr - 1);
+      pv[u] = reinterpret_cast<const u32x4s*>(Vin + (size_t)(c0n + r) * DV)[pi % VROW16];
+    }
+  };
+  prefetch(0);
+  double Gprev = G0;
+  const float tau = a.tau;
+
+  for (int c0 = 0; c0 < T; c0 += SL) {
+    const int nrow = min(SL, T - c0);
+    // ------------------------------------------------ stage the chunk
+#pragma unroll
+    for (int u = 0; u < K16; ++u) {
+      const int pi = tid + 256 * u;
+      const u32x4s z = {0u, 0u, 0u, 0u};
+      reinterpret_cast<u32x4s*>(sK)[pi] = (pi / KROW16 < nrow) ? pk[u] : z;
+    }
+#pragma unroll
+    for (int u = 0; u < V16; ++u) {
+      const int pi = tid + 256 * u;
+      const u32x4s z = {0u, 0u, 0u, 0u};
+      reinterpret_cast<u32x4s*>(sV)[pi] = (pi / VROW16 < nrow) ? pv[u] : z;
+    }
+    if (c0 + SL < T) prefetch(c0 + SL);
+    if (tid < SL) {
+      const int t = tid;
+      const int tc = min(t, nrow - 1);
+      const double Gt = Gtok[c0 + tc];
+      const float gc = (float)(Gt - Gprev);
+      sGc[t] = gc;
+      sA[t] = __expf(gc);
+      // alpha_t^2 = exp(2 g_t); only tokens of the chunk read their predecessor
+      const float gprev = (t == 0 || t >= nrow) ? 0.f : (float)(Gtok[c0 + t - 1] - Gprev);
+      sAl2[t] = (t < nrow) ? __expf(2.f * (gc - gprev)) : 0.f;
+      sDe[t] = (t < nrow) ? (float)exp(Gtok[c0 + nrow - 1] - Gt) : 0.f;
+      sBo[t] = (a.b_ovr && t < nrow) ? a.b_ovr[tok0 + c0 + t] : (int8_t)-1;
+      sMo[t] = (a.m_ovr && t < nrow) ? a.m_ovr[tok0 + c0 + t] : -1;
+      sDC[t] = -1;
+      sBout[t] = 0;
+      sMout[t] = -1;
+      sIo[t] = 0.f;
+    }
+    __syncthreads();
+
+    // ------------------------------------------------ Gram products and the carry term
+    {
+      // P tile (tr, tc) = (K K^T) (.) (V V^T)
+      const int tr = wv >> 1, tcl = wv & 1;
+      f32x16 kk = zero16(), vv = zero16();
+      const Tin* ka = sK + (32 * tr + l32) * DK;
+      const Tin* kb = sK + (32 * tcl + l32) * DK;
+#pragma unroll
+      for (int ks = 0; ks < KSK; ++ks)
+        FR::mma(kk, FR::load(ka + 16 * ks + 8 * half), FR::load(kb + 16 * ks + 8 * half));
+      const Tin* va = sV + (32 * tr + l32) * DV;
+      const Tin* vb = sV + (32 * tcl + l32) * DV;
+#pragma unroll
+      for (int ks = 0; ks < KSV; ++ks)
+        FR::mma(vv, FR::load(va + 16 * ks + 8 * half), FR::load(vb + 16 * ks + 8 * half));
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sP[(32 * tr + out_row(r, lane)) * (SL + 1) + 32 * tcl + l32] = kk[r] * vv[r];
+    }
+    if (wv < NB) {
+      // partial over this wave's band of d_k: sum_i sum_j k_t[i] S0[i][j] v_t[j]
+      float part[2] = {0.f, 0.f};
+#pragma unroll
+      for (int nj = 0; nj < NJ; ++nj) {
+        // A = S0^T (rows j, K = i) straight from the accumulator layout, in three
+        // bf16 terms; B = K^T with the matching permutation of i
+        FT ah[2], am[2], al[2];
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+          float x[8], r1[8], r2[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) x[e] = S[nj][8 * st + e];
+          ah[st] = FR::from_floats(x);
+          if constexpr (sizeof(Tin) == 2) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) r1[e] = x[e] - (float)ah[st][e];
+            am[st] = FR::from_floats(r1);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) r2[e] = r1[e] - (float)am[st][e];
+            al[st] = FR::from_floats(r2);
           }
-        if (a.m_ovr && a.m_ovr[tok0 + t] != -1) {
-          const int f = a.m_ovr[tok0 + t];
-          if (f >= 0 && f <= C - 2)
-            ii = f;
-          else
-            atomicOr(&reinterpret_cast<CacheHeader*>(a.cache)->flags,
-                     DLA_FLAG_BAD_MERGE_OVERRIDE);
         }
-        sDec[1] = ii;
-        // the state right of the pair dies at token t
-        const int lead = sLead[ii + 1];
-        if (lead >= 0)
-          death[lead] = t;
-        else
-          iv.death0[lead + m0] = t;
-      }
-      __syncthreads();
-      istar = sDec[1];
-      // merge istar and istar+1, shift the later states down (C <= 1024: at most
-      // 4 entries per thread, all read before any is written)
-      double nI[4];
-      int nN[4], nL[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int j = tid + 256 * u;
-        if (j >= istar && j + 1 < m) {
-          nI[u] = (j == istar) ? sI[j] + sI[j + 1] : sI[j + 1];
-          nN[u] = (j == istar) ? sN[j] + sN[j + 1] : sN[j + 1];
-          nL[u] = (j == istar) ? sLead[j] : sLead[j + 1];
-        }
-      }
-      __syncthreads();
+        for (int tn = 0; tn < 2; ++tn) {
+          f32x16 y = zero16();
+          const Tin* krow = sK + (32 * tn + l32) * DK + 32 * wv + 4 * half;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int j = tid + 256 * u;
-        if (j >= istar && j + 1 < m) {
-          sI[j] = nI[u];
-          sN[j] = nN[u];
-          sLead[j] = nL[u];
+          for (int st = 0; st < 2; ++st) {
+            float kx[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) kx[e] = to_f32(krow[16 * st + 8 * (e >> 2) + (e & 3)]);
+            const FT kb = FR::from_floats(kx);
+            if constexpr (sizeof(Tin) == 2) {
+              FR::mma(y, al[st], kb);
+              FR::mma(y, am[st], kb);
+            }
+            FR::mma(y, ah[st], kb);
+          }
+          const Tin* vrow = sV + (32 * tn + l32) * DV + 32 * nj;
+          float sacc = 0.f;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) sacc += y[r] * to_f32(vrow[out_row(r, lane)]);
+          part[tn] += sacc;
         }
       }
-      __syncthreads();
-      m -= 1;
+#pragma unroll
+      for (int tn = 0; tn < 2; ++tn) {
+        const float tot = part[tn] + __shfl_xor(part[tn], 32, 64);
+        if (half == 0) sPart[wv * SL + 32 * tn + l32] = tot;
+      }
     }
+    __syncthreads();
 
-    const float4 vq = v4;
-    if (!b) {
-      const float f = (float)exp(G - Fo);
+    // ------------------------------------------------ tables: a_t, c0[t], R[p][t]
+    if (tid < SL) {
+      float c = 0.f;
 #pragma unroll
-      for (int r = 0; r < ST::NV; ++r) {
-        const float kr = sk[buf][rg + ST::RG * r];
-        S[r].x = f * S[r].x + kr * vq.x;
-        S[r].y = f * S[r].y + kr * vq.y;
-        S[r].z = f * S[r].z + kr * vq.z;
-        S[r].w = f * S[r].w + kr * vq.w;
-      }
-      if (tid == 0) {
-        sN[m - 1] += 1;
-        sI[m - 1] += I;
-        death[t] = -1;
-      }
-    } else {
+      for (int b = 0; b < NB; ++b) c += sPart[b * SL + tid];
+      sc0[tid] = c;
+      sa[tid] = sP[tid * (SL + 1) + tid];
+    }
+    {
+      // wave q: partial suffix sums over s in [16q, 16q+16) for row t = lane
+      const int t = lane;
+      const int q = wv;
+      float part = 0.f;
+      const float gt = sGc[t];
 #pragma unroll
-      for (int r = 0; r < ST::NV; ++r) {
-        const float kr = sk[buf][rg + ST::RG * r];
-        S[r] = make_float4(kr * vq.x, kr * vq.y, kr * vq.z, kr * vq.w);
+      for (int i = 15; i >= 0; --i) {
+        const int s = 16 * q + i;
+        if (s < t) part += __expf(gt - sGc[s]) * sP[t * (SL + 1) + s];
+        sR[s * SL + t] = (s < t) ? part : 0.f;
       }
-      if (tid == 0) {
-        sN[m] = 1;
-        sI[m] = I;
-        sLead[m] = t;
-        death[t] = T;
+      sQ[q * SL + t] = part;
+    }
+    __syncthreads();
+    {
+      const int t = lane;
+      const int q = wv;
+      float tail = 0.f;
+      for (int q2 = q + 1; q2 < 4; ++q2) tail += sQ[q2 * SL + t];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int s = 16 * q + i;
+        if (s < t) sR[s * SL + t] += tail;
       }
-      m += 1;
     }
-    Fo = G;
-    if (tid == 0) {
-      if (a.b_out) a.b_out[tok0 + t] = (int8_t)b;
-      if (a.merge_out) a.merge_out[tok0 + t] = istar;
-      if (a.score_out) a.score_out[tok0 + t] = (float)I;
+    __syncthreads();
+
+    // ------------------------------------------------ decisions (wave 0)
+    if (wv == 0) {
+      const int t = lane;
+      const float at = sa[t];
+      const float c0t = sc0[t];
+      const float At = sA[t];
+      const float al2n = (t + 1 < SL) ? sAl2[t + 1] : 0.f;  // alpha^2 of token t+1
+      int mcur = sMisc[0];
+      int p = -1;  // start of the newest state: -1 = before the chunk
+      int plast = -1;
+      if (mcur == 0) {
+        // the first token of an empty cache opens a state with score 0
+        if (lane == 0) {
+          sBout[0] = 1;
+          sIo[0] = 0.f;
+          sMout[0] = -1;
+          sN[0] = 1;
+          sIb[0] = 0.0;
+          sLead[0] = c0;
+          sDC[0] = T;
+        }
+        mcur = 1;
+        p = 0;
+        plast = 0;
+      }
+      while (true) {
+        const int first = p + 1;  // first token scored against this state
+        float ct;
+        if (p < 0)
+          ct = At * c0t + sR[t];  // R[0][t]
+        else
+          ct = (t > p) ? sR[p * SL + t] : 0.f;
+        // |S|^2 before token t: b(t+1) = alpha_{t+1}^2 (b(t) + 2 c(t) + a_t), b(first) = binit
+        const float binit = (p < 0) ? sA[0] * sA[0] * b0 : 0.f;
+        const int ustart = (p < 0) ? 0 : p;
+        float Am = 1.f, Bm = 0.f;
+        if (t >= ustart) {
+          Am = al2n;
+          Bm = al2n * (2.f * ct + at);
+        }
+        // inclusive scan of the affine maps x -> Am x + Bm over lanes
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const float Ao = __shfl_up(Am, o, 64);
+          const float Bo = __shfl_up(Bm, o, 64);
+          if (lane >= o) {
+            Bm = Am * Bo + Bm;
+            Am = Am * Ao;
+          }
+        }
+        const float bnext = Am * binit + Bm;  // b(t+1)
+        float bt = __shfl_up(bnext, 1, 64);
+        if (t == ustart) bt = binit;
+        if (p < 0 && t == 0) bt = binit;
+        const bool valid = (t < nrow) && (t >= first);
+        const float It = valid ? score_f(at, bt, ct, Df, a.eps, a.eps_rms) : 0.f;
+        int bd = (It >= tau) ? 1 : 0;
+        if (sBo[t] != -1) bd = sBo[t] ? 1 : 0;
+        if (C == 1) bd = 0;
+        const uint64_t mask = __ballot(valid && bd);
+        const int tstar = mask ? (__ffsll((unsigned long long)mask) - 1) : nrow;
+        // tokens first .. tstar-1 join the newest state
+        const bool joins = valid && t < tstar;
+        if (joins) sIo[t] = It;
+        double sI = joins ? (double)It : 0.0;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) sI += __shfl_xor(sI, o, 64);
+        if (lane == 0 && tstar > first) {
+          sN[mcur - 1] += tstar - first;
+          sIb[mcur - 1] += sI;
+        }
+        if (tstar >= nrow) break;
+        // boundary at tstar: Alg. 2 when the cache is full, then a new state
+        const float Istar = __shfl(It, tstar, 64);
+        int istar = -1;
+        if (mcur == C) {
+          double best = INFINITY;
+          int bi = 0x7fffffff;
+          for (int i = lane; i + 1 < C; i += 64) {
+            const double d = (sIb[i] + sIb[i + 1]) / (double)(sN[i] + sN[i + 1]);
+            if (d < best) {
+              best = d;
+              bi = i;
+            }
+          }
+#pragma unroll
+          for (int o = 32; o > 0; o >>= 1) {
+            const double ob = __shfl_xor(best, o, 64);
+            const int oi = __shfl_xor(bi, o, 64);
+            if (ob < best || (ob == best && oi < bi)) {
+              best = ob;
+              bi = oi;
+            }
+          }
+          // no comparable density (NaN scores from non-finite inputs): the first
+          // pair, as a sequential argmin that starts at index 0 would pick
+          istar = (bi >= 0 && bi <= C - 2) ? bi : 0;
+          const int fo = sMo[tstar];
+          if (fo != -1) {
+            if (fo >= 0 && fo <= C - 2)
+              istar = fo;
+            else if (lane == 0)
+              atomicOr(&reinterpret_cast<CacheHeader*>(a.cache)->flags, DLA_FLAG_BAD_MERGE_OVERRIDE);
+          }
+          // the state right of the pair dies at token c0 + tstar
+          const int ld = sLead[istar + 1];
+          if (lane == 0) {
+            if (ld >= c0)
+              sDC[ld - c0] = c0 + tstar;
+            else if (ld >= 0)
+              death[ld] = c0 + tstar;
+            else
+              iv.death0[ld + m0] = c0 + tstar;
+          }
+          // merge istar, istar+1 and shift the later states down, 64 entries at a
+          // time in increasing order (a block's writes never touch entries that a
+          // later block still has to read)
+          for (int j0 = istar; j0 + 1 < mcur; j0 += 64) {
+            const int j = j0 + lane;
+            const bool act = j + 1 < mcur;
+            double nI = 0.0;
+            int nN = 0, nL = 0;
+            if (act) {
+              nI = (j == istar) ? sIb[j] + sIb[j + 1] : sIb[j + 1];
+              nN = (j == istar) ? sN[j] + sN[j + 1] : sN[j + 1];
+              nL = (j == istar) ? sLead[j] : sLead[j + 1];
+            }
+            __builtin_amdgcn_wave_barrier();
+            if (act) {
+              sIb[j] = nI;
+              sN[j] = nN;
+              sLead[j] = nL;
+            }
+            __builtin_amdgcn_wave_barrier();
+          }
+          mcur -= 1;
+        }
+        if (lane == 0) {
+          sBout[tstar] = 1;
+          sIo[tstar] = Istar;
+          sMout[tstar] = istar;
+          sN[mcur] = 1;
+          sIb[mcur] = (double)Istar;
+          sLead[mcur] = c0 + tstar;
+          sDC[tstar] = T;
+        }
+        mcur += 1;
+        p = tstar;
+        plast = tstar;
+      }
+      if (lane == 0) {
+        sMisc[0] = mcur;
+        sMisc[1] = plast;
+      }
     }
-    // next token into the other buffer
-    if (t + 1 < T) {
-      if (tid < DK) sk[buf ^ 1][tid] = pk;
-      if (tid >= 128 && tid - 128 < DV) sv[buf ^ 1][tid - 128] = pv;
+    __syncthreads();
+
+    // ------------------------------------------------ advance the newest state
+    const int plast = sMisc[1];
+    if (wv < NB) {
+      const float sc = (plast < 0) ? sA[nrow - 1] : 0.f;
+#pragma unroll
+      for (int nj = 0; nj < NJ; ++nj)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) S[nj][r] *= sc;
+      const int s0 = (plast < 0) ? 0 : plast;
+#pragma unroll
+      for (int st = 0; st < SL / 16; ++st) {
+        if (16 * st + 15 < s0 || 16 * st >= nrow) continue;  // wave-uniform
+        float kt[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int s = 16 * st + 8 * half + e;
+          kt[e] = (s >= s0 && s < nrow) ? sDe[s] * to_f32(sK[s * DK + 32 * wv + l32]) : 0.f;
+        }
+        FT khi = FR::from_floats(kt), kmi, klo;
+        if constexpr (sizeof(Tin) == 2) {
+          float r1[8], r2[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) r1[e] = kt[e] - (float)khi[e];
+          kmi = FR::from_floats(r1);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) r2[e] = r1[e] - (float)kmi[e];
+          klo = FR::from_floats(r2);
+        }
+#pragma unroll
+        for (int nj = 0; nj < NJ; ++nj) {
+          float vx[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) vx[e] = to_f32(sV[(16 * st + 8 * half + e) * DV + 32 * nj + l32]);
+          const FT vb = FR::from_floats(vx);
+          if constexpr (sizeof(Tin) == 2) {
+            FR::mma(S[nj], klo, vb);
+            FR::mma(S[nj], kmi, vb);
+          }
+          FR::mma(S[nj], khi, vb);
+        }
+      }
     }
+    b0 = state_norm2();  // contains barriers; also orders the exports below
+    if (tid < nrow) {
+      const int t = tid;
+      death[c0 + t] = sDC[t];
+      if (a.b_out) a.b_out[tok0 + c0 + t] = sBout[t];
+      if (a.merge_out) a.merge_out[tok0 + c0 + t] = sMout[t];
+      if (a.score_out) a.score_out[tok0 + c0 + t] = sIo[t];
+    }
+    Gprev = Gtok[c0 + nrow - 1];
   }
   __syncthreads();
-  for (int j = tid; j < m; j += 256) {
+  const int mfin = sMisc[0];
+  for (int j = tid; j < mfin; j += 256) {
     M.n[j] = sN[j];
-    M.ibar[j] = sI[j];
+    M.ibar[j] = sIb[j];
   }
 }
 
 template <int DK, int DV>
-static void launch_scan_dims(const PrefillArgs& a, const PrefillWS& w, int nh, hipStream_t s) {
-  const size_t shm = (size_t)a.desc.C * (8 + 4 + 4);
-  if (a.in_dtype == DLA_F32)
-    hipLaunchKernelGGL((prefill_scan_kernel<DK, DV, float>), dim3(nh), dim3(256), shm, s, a, w);
-  else
-    hipLaunchKernelGGL((prefill_scan_kernel<DK, DV, bf16_t>), dim3(nh), dim3(256), shm, s, a, w);
+static hipError_t launch_scan_dims(const PrefillArgs& a, const PrefillWS& w, int nh,
+                                   hipStream_t s) {
+  if (a.in_dtype == DLA_F32) {
+    auto k = prefill_scan_kernel<DK, DV, float>;
+    const size_t shm = ScanP<DK, DV, float>::smem_bytes(a.desc.C);
+    if (shm > 160 * 1024) return hipErrorInvalidValue;
+    hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+    hipLaunchKernelGGL(k, dim3(nh), dim3(256), shm, s, a, w);
+  } else {
+    auto k = prefill_scan_kernel<DK, DV, bf16_t>;
+    const size_t shm = ScanP<DK, DV, bf16_t>::smem_bytes(a.desc.C);
+    if (shm > 160 * 1024) return hipErrorInvalidValue;
+    hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+    hipLaunchKernelGGL(k, dim3(nh), dim3(256), shm, s, a, w);
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_prefill_scan(const PrefillArgs& a, hipStream_t s) {
   const int nh = a.desc.B * a.desc.H;
   PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C);
   const int dk = a.desc.d_k, dv = a.desc.d_v;
-  if (dk == 128 && dv == 128)
-    launch_scan_dims<128, 128>(a, w, nh, s);
-  else if (dk == 64 && dv == 64)
-    launch_scan_dims<64, 64>(a, w, nh, s);
-  else if (dk == 128 && dv == 64)
-    launch_scan_dims<128, 64>(a, w, nh, s);
-  else
-    launch_scan_dims<64, 128>(a, w, nh, s);
-  return hipGetLastError();
+  if (dk == 128 && dv == 128) return launch_scan_dims<128, 128>(a, w, nh, s);
+  if (dk == 64 && dv == 64) return launch_scan_dims<64, 64>(a, w, nh, s);
+  if (dk == 128 && dv == 64) return launch_scan_dims<128, 64>(a, w, nh, s);
+  return launch_scan_dims<64, 128>(a, w, nh, s);
 }
 
 }  // namespace dla
