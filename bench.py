@@ -35,10 +35,59 @@ sys.path.insert(0, ROOT)
 METRIC = "DLA layer fwd tokens/sec (prefill) + decode-step µs; % of HBM/MFMA roofline"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+PROFILES = os.path.join(ROOT, "profiles")
+# sources whose kernels the counter summaries describe
+KERNEL_SOURCES = {
+    "prefill_readout_kernel": ["prefill_readout.hip", "prefill.h", "mfma.h", "dla_common.h"],
+    "decode_kernel": ["decode.hip", "decode.h", "dla_common.h"],
+}
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def source_digest(kernel: str) -> str:
+    """sha256 over the sources of a kernel, to tell whether a counter summary
+    still describes the code being timed."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2606_10650_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def counter_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` on `workload` from the committed
+    rocprofv3 counter summary (FETCH_SIZE + WRITE_SIZE, scaled by the copy-kernel
+    calibration), or None when there is none for the current sources."""
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_counters.md")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if line.startswith("- ") and ": " in line:
+            k, v = line[2:].split(": ", 1)
+            kv[k.strip()] = v.strip().strip("`")
+    if kv.get("source_sha256") != source_digest(kernel):
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_probe(args, torch):
+    """A plain device copy of known size, to calibrate the FETCH_SIZE and
+    WRITE_SIZE counters against bytes moved."""
+    n = args.copy_probe_mib << 20
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n, "launches": 5}), flush=True)
 
 
 def prefill_bench(args, torch, dla, W):
@@ -108,7 +157,8 @@ def prefill_bench(args, torch, dla, W):
         "roofline": {"kernel": "prefill_readout_kernel", "bound": "mfma",
                      "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None, "flops_per_launch": flops,
+                     "traffic": counter_traffic("prefill_readout_kernel", W.name),
+                     "flops_per_launch": flops,
                      "flops_per_launch_at_m_eq_C": flops_cap},
         "decisions": {"boundaries": int(b.sum()), "merges": int(mm.sum()),
                       "mean_live_states": round(float(m_t.mean()), 2)},
@@ -177,7 +227,8 @@ def decode_bench(args, torch, dla, W):
         "boundaries": nb, "merges": nm,
         "roofline": {"kernel": "decode_kernel", "bound": "hbm", "achieved": round(ach, 1),
                      "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
-                     "traffic": None, "bytes_per_launch": bytes_step},
+                     "traffic": counter_traffic("decode_kernel", W.name),
+                     "bytes_per_launch": bytes_step},
     }
 
 
@@ -195,10 +246,9 @@ def cpu_baseline(args, W):
     dt = time.perf_counter() - t0
     return {"value": round(Ts / dt, 2), "unit": "tokens/s", "cores": oracle_threads(),
             "kind": "oracle",
-            "sample": (f"float64 oracle, sequence 0 of the prefill workload, all {W.H} heads, first "
-                       f"{Ts} of {W.T} tokens ({dt:.1f} s); tokens/s counts sequence tokens (all "
-                       f"heads); the sample holds fewer live states than the full sequence, so it "
-                       f"overstates the oracle's full-workload rate")}
+            "sample": (f"float64 oracle, sequence 0 of the prefill workload ({W.H} heads, first "
+                       f"{Ts} of {W.T} tokens, {dt:.1f} s); tokens/s counts sequence tokens "
+                       f"(all heads of a token together), comparable with value / B")}
 
 
 def main():
@@ -210,7 +260,9 @@ def main():
     ap.add_argument("--decode-steps", type=int, default=256)
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-tokens", type=int, default=4096)
+    ap.add_argument("--cpu-tokens", type=int, default=16384)
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the DLA layer shards over (batch, head) with no "
@@ -218,6 +270,9 @@ def main():
               file=sys.stderr)
         sys.exit(2)
     import torch
+    if args.copy_probe_mib:
+        copy_probe(args, torch)
+        return
     from paper_2606_10650_amd import dla
     from paper_2606_10650_amd.workloads import WORKLOADS
     W = WORKLOADS[args.workload]
