@@ -18,7 +18,9 @@
  *   ordered (same stream, or synchronised by the caller).
  * - Shapes come from the cache descriptor: batch B, heads H, capacity C, key
  *   and value head dimensions d_k, d_v.  Supported: d_k, d_v in {64, 128},
- *   1 <= C <= 1024, B*H >= 1.
+ *   1 <= C <= 1024, B*H >= 1; dla_prefill with float32 inputs and d_k = 128
+ *   supports C <= 977 (its per-workgroup working set must fit in 160 KiB of
+ *   LDS) and returns DLA_ERR_UNSUPPORTED above that.
  * - Token tensors are row-major [B][H][T][d] (d fastest); log_gate is
  *   [B][H][T] float32 (the per-token log-decay g_t <= 0 of the base model:
  *   every state decays by exp(g_t) at token t, the caller owns g_t <= 0);

@@ -152,6 +152,7 @@ dla_status dla_prefill(const dla_cache_desc* desc, void* cache, const void* q, c
   if (!cache || !k || !v || !log_gate) return ret(DLA_ERR_INVALID_ARG);
   if (!skip && (!q || !out)) return ret(DLA_ERR_INVALID_ARG);
   if (T == 0) return ret(DLA_OK);
+  if (!prefill_readout_supported(*desc, in_dtype)) return ret(DLA_ERR_UNSUPPORTED);
   if ((int64_t)desc->B * desc->H * (int64_t)T * (desc->C > 128 ? desc->C : 128) >
       ((int64_t)1 << 40))
     return ret(DLA_ERR_UNSUPPORTED);

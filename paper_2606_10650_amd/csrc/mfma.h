@@ -81,6 +81,41 @@ __device__ __forceinline__ f32x16 zero16() {
   return r;
 }
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));  // 16 bytes, first-class
+
+// element e of a 16-byte piece of elements of type Tin
+template <typename Tin>
+__device__ __forceinline__ Tin piece_elem(const u32x4& v, int e);
+template <>
+__device__ __forceinline__ bf16_t piece_elem<bf16_t>(const u32x4& v, int e) {
+  bf16_t r;
+  r.x = static_cast<uint16_t>(v[e >> 1] >> (16 * (e & 1)));
+  return r;
+}
+template <>
+__device__ __forceinline__ float piece_elem<float>(const u32x4& v, int e) {
+  return __uint_as_float(v[e]);
+}
+
+// 8 operand values from two runs of 4 consecutive elements (each run aligned
+// to 4 elements)
+template <typename Tin>
+__device__ __forceinline__ typename Frag<Tin>::T load_4x2(const Tin* p0, const Tin* p1);
+template <>
+__device__ __forceinline__ bf16x8 load_4x2<bf16_t>(const bf16_t* p0, const bf16_t* p1) {
+  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  const bf16x4 lo = *reinterpret_cast<const bf16x4*>(p0);
+  const bf16x4 hi = *reinterpret_cast<const bf16x4*>(p1);
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+template <>
+__device__ __forceinline__ f32x8 load_4x2<float>(const float* p0, const float* p1) {
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  const f32x4 lo = *reinterpret_cast<const f32x4*>(p0);
+  const f32x4 hi = *reinterpret_cast<const f32x4*>(p1);
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
 // row (within the 32-row tile) of output element r held by lane l
 __device__ __forceinline__ int out_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 

@@ -95,6 +95,8 @@ __host__ __device__ inline InitView init_at(const PrefillWS& w, int h, int C) {
 hipError_t launch_prefill_prep(const PrefillArgs& a, hipStream_t s);
 hipError_t launch_prefill_scan(const PrefillArgs& a, hipStream_t s);
 hipError_t launch_prefill_readout(const PrefillArgs& a, hipStream_t s);
+// whether the readout stage's working set fits in LDS for this shape
+bool prefill_readout_supported(const dla_cache_desc& d, dla_dtype in_dtype);
 
 // Stages in order; ev (nullable) receives an event before the first stage and
 // after each stage.

@@ -91,14 +91,20 @@ hipError_t launch_prefill_prep(const PrefillArgs& a, hipStream_t s) {
 // ---------------------------------------------------------------------------
 constexpr int SL = 64;  // tokens per scan chunk (one per lane of a wavefront)
 
-typedef unsigned int u32x4s __attribute__((ext_vector_type(4)));
+typedef u32x4 u32x4s;
 
 template <int DK, int DV, typename Tin>
 struct ScanP {
-  static constexpr int K16 = SL * DK * (int)sizeof(Tin) / 16 / 256;  // 16-byte K pieces per thread
-  static constexpr int V16 = SL * DV * (int)sizeof(Tin) / 16 / 256;
+  static constexpr int E = (int)sizeof(Tin);
+  static constexpr int EPP = 16 / E;                // elements per 16 bytes
+  static constexpr int K16 = SL * DK * E / 16 / 256;  // 16-byte K pieces per thread
+  static constexpr int V16 = SL * DV * E / 16 / 256;
+  // LDS row strides (elements), padded by 16 bytes so that lanes reading
+  // consecutive rows hit distinct banks
+  static constexpr int KRS = DK + EPP;  // sK  [SL][KRS]
+  static constexpr int VRS = DV + EPP;  // sV  [SL][VRS]
   static size_t smem_bytes(int C) {
-    size_t off = (size_t)SL * (DK + DV) * sizeof(Tin);  // sK, sV
+    size_t off = (size_t)SL * (KRS + VRS) * E;          // sK, sV
     off += (size_t)SL * (SL + 1) * 4;                   // sP
     off += (size_t)SL * SL * 4;                         // sR
     off += (size_t)8 * SL * 4;                          // sPart[4], sQ[4]
@@ -143,9 +149,10 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
   const float Df = (float)D;
 
   extern __shared__ __align__(16) char smem[];
-  Tin* sK = reinterpret_cast<Tin*>(smem);
-  Tin* sV = sK + SL * DK;
-  float* sP = reinterpret_cast<float*>(sV + SL * DV);  // [SL][SL+1]
+  constexpr int KRS = P::KRS, VRS = P::VRS;
+  Tin* sK = reinterpret_cast<Tin*>(smem);  // keys of the chunk, row-major
+  Tin* sV = sK + SL * KRS;                 // values, row-major
+  float* sP = reinterpret_cast<float*>(sV + SL * VRS);  // [SL][SL+1]
   float* sR = sP + SL * (SL + 1);                      // [SL][SL], R[p][t]
   float* sPart = sR + SL * SL;                         // [4][SL]
   float* sQ = sPart + 4 * SL;                          // [4][SL]
@@ -244,14 +251,18 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
 #pragma unroll
     for (int u = 0; u < K16; ++u) {
       const int pi = tid + 256 * u;
+      const int r = pi / KROW16, pc = pi % KROW16;
       const u32x4s z = {0u, 0u, 0u, 0u};
-      reinterpret_cast<u32x4s*>(sK)[pi] = (pi / KROW16 < nrow) ? pk[u] : z;
+      const u32x4s val = (r < nrow) ? pk[u] : z;
+      *reinterpret_cast<u32x4s*>(sK + r * KRS + pc * P::EPP) = val;
     }
 #pragma unroll
     for (int u = 0; u < V16; ++u) {
       const int pi = tid + 256 * u;
+      const int r = pi / VROW16, pc = pi % VROW16;
       const u32x4s z = {0u, 0u, 0u, 0u};
-      reinterpret_cast<u32x4s*>(sV)[pi] = (pi / VROW16 < nrow) ? pv[u] : z;
+      const u32x4s val = (r < nrow) ? pv[u] : z;
+      *reinterpret_cast<u32x4s*>(sV + r * VRS + pc * P::EPP) = val;
     }
     if (c0 + SL < T) prefetch(c0 + SL);
     if (tid < SL) {
@@ -279,13 +290,13 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
       // P tile (tr, tc) = (K K^T) (.) (V V^T)
       const int tr = wv >> 1, tcl = wv & 1;
       f32x16 kk = zero16(), vv = zero16();
-      const Tin* ka = sK + (32 * tr + l32) * DK;
-      const Tin* kb = sK + (32 * tcl + l32) * DK;
+      const Tin* ka = sK + (32 * tr + l32) * KRS;
+      const Tin* kb = sK + (32 * tcl + l32) * KRS;
 #pragma unroll
       for (int ks = 0; ks < KSK; ++ks)
         FR::mma(kk, FR::load(ka + 16 * ks + 8 * half), FR::load(kb + 16 * ks + 8 * half));
-      const Tin* va = sV + (32 * tr + l32) * DV;
-      const Tin* vb = sV + (32 * tcl + l32) * DV;
+      const Tin* va = sV + (32 * tr + l32) * VRS;
+      const Tin* vb = sV + (32 * tcl + l32) * VRS;
 #pragma unroll
       for (int ks = 0; ks < KSV; ++ks)
         FR::mma(vv, FR::load(va + 16 * ks + 8 * half), FR::load(vb + 16 * ks + 8 * half));
@@ -318,20 +329,19 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
 #pragma unroll
         for (int tn = 0; tn < 2; ++tn) {
           f32x16 y = zero16();
-          const Tin* krow = sK + (32 * tn + l32) * DK + 32 * wv + 4 * half;
+          const Tin* krow = sK + (32 * tn + l32) * KRS + 32 * wv + 4 * half;
 #pragma unroll
           for (int st = 0; st < 2; ++st) {
-            float kx[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) kx[e] = to_f32(krow[16 * st + 8 * (e >> 2) + (e & 3)]);
-            const FT kb = FR::from_floats(kx);
+            // k index 16 st + 8 (e / 4) + 4 h + e % 4 of the band, as in the
+            // accumulator layout of S0
+            const FT kb = load_4x2<Tin>(krow + 16 * st, krow + 16 * st + 8);
             if constexpr (sizeof(Tin) == 2) {
               FR::mma(y, al[st], kb);
               FR::mma(y, am[st], kb);
             }
             FR::mma(y, ah[st], kb);
           }
-          const Tin* vrow = sV + (32 * tn + l32) * DV + 32 * nj;
+          const Tin* vrow = sV + (32 * tn + l32) * VRS + 32 * nj;
           float sacc = 0.f;
 #pragma unroll
           for (int r = 0; r < 16; ++r) sacc += y[r] * to_f32(vrow[out_row(r, lane)]);
@@ -551,34 +561,42 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
 #pragma unroll
       for (int st = 0; st < SL / 16; ++st) {
         if (16 * st + 15 < s0 || 16 * st >= nrow) continue;  // wave-uniform
+        // element e of half h <-> token 16 st + 8 h + e; A = K~^T (rows of this
+        // wave's band of d_k), B = V (32 columns per tile)
+        // (padded rows: the lanes of a half read consecutive columns of one row,
+        // the two halves rows 8 apart, which fall in disjoint banks)
         float kt[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const int s = 16 * st + 8 * half + e;
-          kt[e] = (s >= s0 && s < nrow) ? sDe[s] * to_f32(sK[s * DK + 32 * wv + l32]) : 0.f;
+          kt[e] = (s >= s0 && s < nrow) ? sDe[s] * to_f32(sK[s * KRS + 32 * wv + l32]) : 0.f;
         }
-        FT khi = FR::from_floats(kt), kmi, klo;
-        if constexpr (sizeof(Tin) == 2) {
-          float r1[8], r2[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) r1[e] = kt[e] - (float)khi[e];
-          kmi = FR::from_floats(r1);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) r2[e] = r1[e] - (float)kmi[e];
-          klo = FR::from_floats(r2);
-        }
+        FT vb[NJ];
 #pragma unroll
         for (int nj = 0; nj < NJ; ++nj) {
           float vx[8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) vx[e] = to_f32(sV[(16 * st + 8 * half + e) * DV + 32 * nj + l32]);
-          const FT vb = FR::from_floats(vx);
-          if constexpr (sizeof(Tin) == 2) {
-            FR::mma(S[nj], klo, vb);
-            FR::mma(S[nj], kmi, vb);
-          }
-          FR::mma(S[nj], khi, vb);
+          for (int e = 0; e < 8; ++e) vx[e] = to_f32(sV[(16 * st + 8 * half + e) * VRS + 32 * nj + l32]);
+          vb[nj] = FR::from_floats(vx);
         }
+        const FT khi = FR::from_floats(kt);
+        if constexpr (sizeof(Tin) == 2) {
+          // three bf16 terms carry the float32 value of K~; each term runs over
+          // all column tiles before the next, so no MFMA waits on its predecessor
+          float r1[8], r2[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) r1[e] = kt[e] - (float)khi[e];
+          const FT kmi = FR::from_floats(r1);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) r2[e] = r1[e] - (float)kmi[e];
+          const FT klo = FR::from_floats(r2);
+#pragma unroll
+          for (int nj = 0; nj < NJ; ++nj) FR::mma(S[nj], klo, vb[nj]);
+#pragma unroll
+          for (int nj = 0; nj < NJ; ++nj) FR::mma(S[nj], kmi, vb[nj]);
+        }
+#pragma unroll
+        for (int nj = 0; nj < NJ; ++nj) FR::mma(S[nj], khi, vb[nj]);
       }
     }
     b0 = state_norm2();  // contains barriers; also orders the exports below
