@@ -131,7 +131,8 @@ def prefill_bench(args, torch, dla, W):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    ns = len(dla.PREFILL_STAGES)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(ns + 1)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -139,17 +140,17 @@ def prefill_bench(args, torch, dla, W):
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms = (t1 - t0) * 1e3 / args.steps
-    stages = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(3)] for e in evs])
+    stages = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(ns)] for e in evs])
     st_ms = stages.mean(axis=0)
 
-    # algorithmic work of the readout + state-update kernel, from this run's exports:
-    # sum over tokens of 2 m_t d_k d_v (readout over live states) + 2 d_k d_v (accumulate)
+    # algorithmic work of the readout kernel, from this run's exports: the sum
+    # over tokens of 2 m_t d_k d_v (the readout over the m_t live states)
     b = bnd.cpu().numpy().reshape(B * H, T).astype(np.int64)
     mm = (mrg.cpu().numpy().reshape(B * H, T) >= 0).astype(np.int64)
     m_t = np.cumsum(b, axis=1) - np.cumsum(mm, axis=1)
-    flops = 2.0 * W.dk * W.dv * (m_t.sum() + m_t.size)
-    flops_cap = 2.0 * W.dk * W.dv * (W.C + 1) * m_t.size
-    achieved = flops / (st_ms[2] * 1e-3) / 1e12
+    flops = 2.0 * W.dk * W.dv * m_t.sum()
+    flops_cap = 2.0 * W.dk * W.dv * W.C * m_t.size
+    achieved = flops / (st_ms[3] * 1e-3) / 1e12
     return {
         "ms_per_step": ms,
         "value": B * T / (ms * 1e-3),

@@ -18,9 +18,9 @@
  *   ordered (same stream, or synchronised by the caller).
  * - Shapes come from the cache descriptor: batch B, heads H, capacity C, key
  *   and value head dimensions d_k, d_v.  Supported: d_k, d_v in {64, 128},
- *   1 <= C <= 1024, B*H >= 1; dla_prefill with float32 inputs and d_k = 128
- *   supports C <= 977 (its per-workgroup working set must fit in 160 KiB of
- *   LDS) and returns DLA_ERR_UNSUPPORTED above that.
+ *   1 <= C <= 1024, B*H >= 1.  dla_prefill returns DLA_ERR_UNSUPPORTED when a
+ *   stage's per-workgroup working set would not fit in 160 KiB of LDS (float32
+ *   inputs with d_k = 128 and C above about 900).
  * - Token tensors are row-major [B][H][T][d] (d fastest); log_gate is
  *   [B][H][T] float32 (the per-token log-decay g_t <= 0 of the base model:
  *   every state decays by exp(g_t) at token t, the caller owns g_t <= 0);
@@ -73,8 +73,11 @@ typedef struct {
  * cache and the exports but computes no output (out may be NULL).
  * stage_events: NULL, or DLA_PREFILL_STAGES + 1 hipEvent_t handles (created by
  * the caller) that dla_prefill records on its stream before its first stage and
- * after each stage (token frames, boundary scan, readout + state update), for
- * timing the stages; dla_decode_step ignores it. */
+ * after each stage (token frames, boundary scan, state update, readout), for
+ * timing the stages; dla_decode_step ignores it.  A prefill whose state copies
+ * exceed the workspace budget (see dla_prefill_workspace_size) runs the update
+ * and readout stages segment by segment, alternating; the last two events then
+ * follow the last update and the last readout. */
 typedef struct {
   float tau;
   float eps;
@@ -83,7 +86,7 @@ typedef struct {
   void* const* stage_events;
 } dla_params;
 
-#define DLA_PREFILL_STAGES 3
+#define DLA_PREFILL_STAGES 4
 
 #define DLA_SKIP_READOUT 1u
 
@@ -129,9 +132,15 @@ dla_status dla_state_cache_alloc(const dla_cache_desc* desc, void* dev_buf, size
 dla_status dla_cache_flags(const dla_cache_desc* desc, void* cache, uint32_t* flags,
                            void* stream);
 
-/* Workspace that dla_prefill needs for T tokens of the given input dtype. */
+/* Workspace that dla_prefill needs for T tokens of the given input dtype and
+ * params flags (DLA_SKIP_READOUT needs less: no state copies).  Besides O(T)
+ * bytes per head (token frames, death tokens) and O(C) per head and chunk of
+ * 512 tokens (256 for float32 inputs; the state list of every chunk), the
+ * readout needs copies of the states in the input dtype: up to C per head and
+ * chunk, d_k*d_v elements each.  They are bounded to 8 GiB per call: above
+ * that the call is split into segments of whole chunks that reuse the space. */
 dla_status dla_prefill_workspace_size(const dla_cache_desc* desc, int32_t T, dla_dtype in_dtype,
-                                      size_t* bytes);
+                                      uint32_t flags, size_t* bytes);
 
 /*
  * Prefill: absorb T tokens per head into the cache, in order, computing for

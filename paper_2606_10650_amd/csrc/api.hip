@@ -131,11 +131,11 @@ dla_status dla_cache_flags(const dla_cache_desc* desc, void* cache, uint32_t* fl
 }
 
 dla_status dla_prefill_workspace_size(const dla_cache_desc* desc, int32_t T, dla_dtype in_dtype,
-                                      size_t* bytes) {
+                                      uint32_t flags, size_t* bytes) {
   dla_status s = check_desc(desc);
   if (s != DLA_OK) return ret(s);
   if (!bytes || T < 0 || !dtype_ok(in_dtype)) return ret(DLA_ERR_INVALID_ARG);
-  *bytes = prefill_workspace_bytes(*desc, T, in_dtype);
+  *bytes = prefill_workspace_bytes(*desc, T, in_dtype, (flags & DLA_SKIP_READOUT) == 0);
   return ret(DLA_OK);
 }
 
@@ -152,11 +152,11 @@ dla_status dla_prefill(const dla_cache_desc* desc, void* cache, const void* q, c
   if (!cache || !k || !v || !log_gate) return ret(DLA_ERR_INVALID_ARG);
   if (!skip && (!q || !out)) return ret(DLA_ERR_INVALID_ARG);
   if (T == 0) return ret(DLA_OK);
-  if (!prefill_readout_supported(*desc, in_dtype)) return ret(DLA_ERR_UNSUPPORTED);
+  if (!prefill_chunks_supported(*desc, in_dtype)) return ret(DLA_ERR_UNSUPPORTED);
   if ((int64_t)desc->B * desc->H * (int64_t)T * (desc->C > 128 ? desc->C : 128) >
       ((int64_t)1 << 40))
     return ret(DLA_ERR_UNSUPPORTED);
-  const size_t need = prefill_workspace_bytes(*desc, T, in_dtype);
+  const size_t need = prefill_workspace_bytes(*desc, T, in_dtype, !skip);
   if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 255u))
     return ret(DLA_ERR_WORKSPACE);
   PrefillArgs a;

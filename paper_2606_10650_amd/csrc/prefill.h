@@ -1,4 +1,5 @@
-// Prefill entry (internal): arguments, workspace layout and launchers.
+// Prefill entry (internal): arguments, workspace layout, segment plan and
+// launchers.
 #pragma once
 #include "dla_common.h"
 
@@ -26,6 +27,61 @@ struct PrefillArgs {
   char* workspace;
 };
 
+// ---------------------------------------------------------------------------
+// Readout chunks and segments.
+//
+// Stages 3 (state update) and 4 (readout) work on chunks of RL tokens.  The
+// update stage walks the chunks in order and records, for every chunk, the
+// list of states present at its start; every state it rebuilds gets a fresh
+// object in a per-head pool holding a bfloat16 (or float32) copy of the state
+// in MFMA operand order.  The readout stage then runs every chunk in parallel
+// against the pool.  A chunk creates at most C objects, so the pool holds up to
+// C objects per chunk; to bound its size the call is split into segments of at
+// most nch_seg chunks (update, then readout, per segment), and each segment
+// starts its pool afresh with copies of the states present at its start.
+// ---------------------------------------------------------------------------
+constexpr int NWAVE = 8;  // waves per workgroup of the update and readout stages
+constexpr int NTHR = 64 * NWAVE;
+constexpr int NC = 32;    // value columns per workgroup
+constexpr size_t kPoolBudget = (size_t)8 << 30;  // bytes of state copies per segment
+
+// token tiles of 32 per wave in the readout stage: two for 16-bit inputs, one
+// for float32 inputs (whose operands take twice the registers and LDS)
+__host__ __device__ constexpr int readout_nt(int elem_bytes) { return elem_bytes == 2 ? 2 : 1; }
+__host__ __device__ constexpr int chunk_len(int elem_bytes) {
+  return 32 * NWAVE * readout_nt(elem_bytes);
+}
+
+struct SegPlan {
+  int RL;       // tokens per chunk
+  int nch;      // chunks in the call
+  int nch_seg;  // chunks per segment
+  int nseg;     // segments
+  int P_cap;    // pool objects per head (0 without a readout)
+};
+
+inline size_t dtype_bytes(dla_dtype t) { return t == DLA_F32 ? 4 : 2; }
+
+inline SegPlan seg_plan(const dla_cache_desc& d, int T, dla_dtype in, bool readout) {
+  SegPlan p;
+  const int E = (int)dtype_bytes(in);
+  p.RL = chunk_len(E);
+  p.nch = T > 0 ? (T + p.RL - 1) / p.RL : 0;
+  if (!readout || p.nch == 0) {
+    p.nch_seg = p.nch > 0 ? p.nch : 1;
+    p.nseg = 1;
+    p.P_cap = 0;
+    return p;
+  }
+  const size_t per_chunk = (size_t)d.B * d.H * d.C * d.d_k * d.d_v * E;
+  int fit = (int)(kPoolBudget / per_chunk);
+  if (fit < 1) fit = 1;
+  p.nseg = (p.nch + fit - 1) / fit;
+  p.nch_seg = (p.nch + p.nseg - 1) / p.nseg;
+  p.P_cap = d.C * p.nch_seg;
+  return p;
+}
+
 // Workspace regions (per head, 256-byte aligned):
 //   Gtok   double [nh][T]   cumulative log-decay after each token (global frame)
 //   death  int32  [nh][T]   -1: token t is not the first token of a state;
@@ -35,22 +91,38 @@ struct PrefillArgs {
 //   init   per head: int32 m0, int32 pad, double G0, double F0[C], int32 perm0[C],
 //          int32 death0[C] (the cache's metadata before the call, and the death
 //          token of the states present before the call)
-//   shadow [nh][C][d_v/32][d_k/16][2][32][8] elements of the input dtype: a copy
-//          of each state (by physical slot) in the per-lane order of the MFMA
-//          A operand, for the readout stage
+//   carry  per head: int32 m, int32 pad, double F[C], int32 perm[C], int32 lead[C]
+//          (update-stage bookkeeping handed from one segment to the next)
+//   lists  [nh][nch] chunk lists: int32 m at offset 0, then from offset 16 one
+//          ListEntry per state present at the chunk start, in chronological order
+//   pool   [nh][P_cap] state copies, each [d_v/32][d_k/16][2][32][8] elements of
+//          the input dtype: the per-lane order of the MFMA A operand for one
+//          32-column group, so a lane reads its operand with 16-byte loads
+struct ListEntry {
+  int32_t obj;  // pool object holding the state's copy
+  int32_t dt;   // token at which Alg. 2 merges the state away (T: never)
+  double F;     // frame: the true state is exp(G - F) times the stored one
+};
+
 struct PrefillWS {
   double* Gtok;
   int32_t* death;
   char* init;
   size_t init_stride;
-  char* shadow;
+  char* carry;
+  size_t carry_stride;
+  char* lists;
+  size_t list_stride;
+  char* pool;
 };
 
 __host__ __device__ inline size_t ws_init_stride(int C) { return round_up(16 + 16 * (size_t)C, 256); }
+__host__ __device__ inline size_t ws_carry_stride(int C) { return round_up(8 + 16 * (size_t)C, 256); }
+__host__ __device__ inline size_t ws_list_stride(int C) {
+  return round_up(16 + sizeof(ListEntry) * (size_t)C, 256);
+}
 
-__host__ __device__ inline size_t dtype_bytes(dla_dtype t) { return t == DLA_F32 ? 4 : 2; }
-
-__host__ __device__ inline PrefillWS ws_layout(char* base, int nh, int T, int C) {
+__host__ __device__ inline PrefillWS ws_layout(char* base, int nh, int T, int C, int nch) {
   PrefillWS w;
   size_t off = 0;
   w.Gtok = reinterpret_cast<double*>(base + off);
@@ -60,16 +132,25 @@ __host__ __device__ inline PrefillWS ws_layout(char* base, int nh, int T, int C)
   w.init = base + off;
   w.init_stride = ws_init_stride(C);
   off = round_up(off + (size_t)nh * w.init_stride, 256);
-  w.shadow = base + off;
+  w.carry = base + off;
+  w.carry_stride = ws_carry_stride(C);
+  off = round_up(off + (size_t)nh * w.carry_stride, 256);
+  w.lists = base + off;
+  w.list_stride = ws_list_stride(C);
+  off = round_up(off + (size_t)nh * nch * w.list_stride, 256);
+  w.pool = base + off;
   return w;
 }
 
-inline size_t prefill_workspace_bytes(const dla_cache_desc& d, int T, dla_dtype in) {
+inline size_t prefill_workspace_bytes(const dla_cache_desc& d, int T, dla_dtype in, bool readout) {
   const size_t nh = (size_t)d.B * d.H;
+  const SegPlan p = seg_plan(d, T, in, readout);
   size_t off = round_up(nh * T * sizeof(double), 256);
   off = round_up(off + nh * T * sizeof(int32_t), 256);
   off = round_up(off + nh * ws_init_stride(d.C), 256);
-  off += nh * (size_t)d.C * d.d_k * d.d_v * dtype_bytes(in);
+  off = round_up(off + nh * ws_carry_stride(d.C), 256);
+  off = round_up(off + nh * (size_t)p.nch * ws_list_stride(d.C), 256);
+  off += nh * (size_t)p.P_cap * d.d_k * d.d_v * dtype_bytes(in);
   return off;
 }
 
@@ -92,24 +173,57 @@ __host__ __device__ inline InitView init_at(const PrefillWS& w, int h, int C) {
   return v;
 }
 
+struct CarryView {
+  int32_t* m;
+  double* F;
+  int32_t* perm;
+  int32_t* lead;
+};
+
+__host__ __device__ inline CarryView carry_at(const PrefillWS& w, int h, int C) {
+  char* p = w.carry + (size_t)h * w.carry_stride;
+  CarryView v;
+  v.m = reinterpret_cast<int32_t*>(p);
+  v.F = reinterpret_cast<double*>(p + 8);
+  v.perm = reinterpret_cast<int32_t*>(p + 8 + 8 * (size_t)C);
+  v.lead = v.perm + C;
+  return v;
+}
+
+__host__ __device__ inline char* list_at(const PrefillWS& w, int h, int c, int nch) {
+  return w.lists + ((size_t)h * nch + c) * w.list_stride;
+}
+
 hipError_t launch_prefill_prep(const PrefillArgs& a, hipStream_t s);
 hipError_t launch_prefill_scan(const PrefillArgs& a, hipStream_t s);
-hipError_t launch_prefill_readout(const PrefillArgs& a, hipStream_t s);
-// whether the readout stage's working set fits in LDS for this shape
-bool prefill_readout_supported(const dla_cache_desc& d, dla_dtype in_dtype);
+hipError_t launch_prefill_update(const PrefillArgs& a, const SegPlan& p, int seg, hipStream_t s);
+hipError_t launch_prefill_readout(const PrefillArgs& a, const SegPlan& p, int seg, hipStream_t s);
+// whether the update and readout stages' working sets fit in LDS for this shape
+bool prefill_chunks_supported(const dla_cache_desc& d, dla_dtype in_dtype);
 
-// Stages in order; ev (nullable) receives an event before the first stage and
-// after each stage.
+// Stages in order, segment by segment; ev (nullable) receives an event before
+// the first stage and after the token frames, the scan, the state updates and
+// the readouts.  With one segment the four intervals time the four stages
+// exactly; with several, updates and readouts alternate and the last two
+// events follow the last update and the last readout.
 inline hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s, void* const* ev) {
-  hipError_t (*stages[DLA_PREFILL_STAGES])(const PrefillArgs&, hipStream_t) = {
-      launch_prefill_prep, launch_prefill_scan, launch_prefill_readout};
-  if (ev && hipEventRecord((hipEvent_t)ev[0], s) != hipSuccess) return hipErrorInvalidValue;
-  for (int i = 0; i < DLA_PREFILL_STAGES; ++i) {
-    hipError_t e = stages[i](a, s);
-    if (e != hipSuccess) return e;
-    if (ev && hipEventRecord((hipEvent_t)ev[i + 1], s) != hipSuccess) return hipErrorInvalidValue;
+  const SegPlan p = seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout);
+  auto rec = [&](int i) -> hipError_t {
+    if (ev && hipEventRecord((hipEvent_t)ev[i], s) != hipSuccess) return hipErrorInvalidValue;
+    return hipSuccess;
+  };
+  hipError_t e;
+  if ((e = rec(0)) != hipSuccess) return e;
+  if ((e = launch_prefill_prep(a, s)) != hipSuccess) return e;
+  if ((e = rec(1)) != hipSuccess) return e;
+  if ((e = launch_prefill_scan(a, s)) != hipSuccess) return e;
+  if ((e = rec(2)) != hipSuccess) return e;
+  for (int seg = 0; seg < p.nseg; ++seg) {
+    if ((e = launch_prefill_update(a, p, seg, s)) != hipSuccess) return e;
+    if (seg == p.nseg - 1 && (e = rec(3)) != hipSuccess) return e;
+    if (!a.skip_readout && (e = launch_prefill_readout(a, p, seg, s)) != hipSuccess) return e;
   }
-  return hipSuccess;
+  return rec(4);
 }
 
 }  // namespace dla

@@ -81,7 +81,8 @@ __global__ __launch_bounds__(256) void prefill_prep_kernel(PrefillArgs a, Prefil
 
 hipError_t launch_prefill_prep(const PrefillArgs& a, hipStream_t s) {
   const int nh = a.desc.B * a.desc.H;
-  PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C);
+  PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C,
+                          seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout).nch);
   hipLaunchKernelGGL(prefill_prep_kernel, dim3(nh), dim3(256), 0, s, a, w);
   return hipGetLastError();
 }
@@ -638,7 +639,8 @@ static hipError_t launch_scan_dims(const PrefillArgs& a, const PrefillWS& w, int
 
 hipError_t launch_prefill_scan(const PrefillArgs& a, hipStream_t s) {
   const int nh = a.desc.B * a.desc.H;
-  PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C);
+  PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C,
+                          seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout).nch);
   const int dk = a.desc.d_k, dv = a.desc.d_v;
   if (dk == 128 && dv == 128) return launch_scan_dims<128, 128>(a, w, nh, s);
   if (dk == 64 && dv == 64) return launch_scan_dims<64, 64>(a, w, nh, s);

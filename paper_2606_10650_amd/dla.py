@@ -37,7 +37,7 @@ class Params(ctypes.Structure):
                 ("flags", ctypes.c_uint32), ("stage_events", ctypes.c_void_p)]
 
 
-PREFILL_STAGES = ("frames", "scan", "readout")
+PREFILL_STAGES = ("frames", "scan", "update", "readout")
 
 
 class Layout(ctypes.Structure):
@@ -67,7 +67,7 @@ def lib():
         L.dla_cache_flags.argtypes = [ctypes.POINTER(CacheDesc), P, ctypes.POINTER(ctypes.c_uint32),
                                       P]
         L.dla_prefill_workspace_size.argtypes = [ctypes.POINTER(CacheDesc), ctypes.c_int32, I,
-                                                 ctypes.POINTER(ctypes.c_size_t)]
+                                                 ctypes.c_uint32, ctypes.POINTER(ctypes.c_size_t)]
         L.dla_prefill.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, ctypes.c_int32, I,
                                   ctypes.POINTER(Params), P, I, P, P, P, P, P, P, ctypes.c_size_t, P]
         L.dla_decode_step.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, I,
@@ -161,11 +161,12 @@ def cache_flags(cache: StateCache) -> int:
     return int(f.value)
 
 
-def workspace_bytes(cache: StateCache, T: int, dtype=None) -> int:
+def workspace_bytes(cache: StateCache, T: int, dtype=None, skip_readout: bool = False) -> int:
     """Prefill workspace for T tokens of input dtype (torch dtype, default bf16)."""
     code = DLA_BF16 if dtype is None else _dtype_code(dtype)
     n = ctypes.c_size_t(0)
     _check(lib().dla_prefill_workspace_size(ctypes.byref(cache.desc), int(T), code,
+                                            DLA_SKIP_READOUT if skip_readout else 0,
                                             ctypes.byref(n)), "dla_prefill_workspace_size")
     return int(n.value)
 
@@ -211,7 +212,7 @@ def prefill(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5, eps: f
                                                                         device=dev)
         score = score if score is not None else torch.empty((B, H, T), dtype=torch.float32,
                                                             device=dev)
-    wsb = workspace_bytes(cache, T, k.dtype)
+    wsb = workspace_bytes(cache, T, k.dtype, skip_readout)
     if workspace is None or workspace.numel() < wsb:
         workspace = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
     for e in stage_events or ():

@@ -75,7 +75,7 @@ def test_host_side_errors():
     assert st == dla.DLA_ERR_INVALID_ARG
     assert dla.status_string(dla.DLA_ERR_WORKSPACE) == "workspace missing or too small"
     ws = ctypes.c_size_t(0)
-    assert L.dla_prefill_workspace_size(ctypes.byref(d), 1000, 1, ctypes.byref(ws)) == dla.DLA_OK
+    assert L.dla_prefill_workspace_size(ctypes.byref(d), 1000, 1, 0, ctypes.byref(ws)) == dla.DLA_OK
     assert ws.value >= 6 * 1000 * 12
 
 
