@@ -40,16 +40,18 @@ struct PrefillArgs {
 // most nch_seg chunks (update, then readout, per segment), and each segment
 // starts its pool afresh with copies of the states present at its start.
 // ---------------------------------------------------------------------------
-constexpr int NWAVE = 8;  // waves per workgroup of the update and readout stages
+constexpr int NWAVE = 8;  // waves per workgroup of the update stage
 constexpr int NTHR = 64 * NWAVE;
+constexpr int RWAVE = 8;  // waves per workgroup of the readout stage (two per SIMD)
+constexpr int RTHR = 64 * RWAVE;
 constexpr int NC = 32;    // value columns per workgroup
 constexpr size_t kPoolBudget = (size_t)8 << 30;  // bytes of state copies per segment
 
-// token tiles of 32 per wave in the readout stage: two for 16-bit inputs, one
-// for float32 inputs (whose operands take twice the registers and LDS)
+// token tiles of 32 per readout wave: two for 16-bit inputs, one for float32
+// inputs (whose operands take twice the registers and LDS)
 __host__ __device__ constexpr int readout_nt(int elem_bytes) { return elem_bytes == 2 ? 2 : 1; }
 __host__ __device__ constexpr int chunk_len(int elem_bytes) {
-  return 32 * NWAVE * readout_nt(elem_bytes);
+  return 32 * RWAVE * readout_nt(elem_bytes);
 }
 
 struct SegPlan {

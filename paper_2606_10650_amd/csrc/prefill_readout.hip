@@ -9,17 +9,20 @@
 //   * inter-chunk part: every state S_j present at the chunk start contributes
 //     lambda[t][x_j(t)] exp(G_t - F_j) q_t^T S~_j, x_j(t) being its chronological
 //     index at token t: the number of live states up to it, a state living while
-//     its death token is later than t.  The tile S~_j^T Q^T (32 columns x 32
-//     tokens, K = d_k) is an MFMA chain; each lane owns one token of a tile, so
-//     the weight is a per-lane scalar applied to the chain's result.  States
-//     are streamed from the pool three ahead through registers and a
-//     double-buffered LDS ring (one barrier per state); each wave reads a
-//     state's operand from LDS once for all of its tiles.
+//     its death token is later than t (a state merged away is weighted as the
+//     state that absorbed it).  The tile S~_j^T Q^T (32 columns x 32 tokens,
+//     K = d_k) is an MFMA chain; each lane owns one token of a tile, so the
+//     weight is a per-lane scalar applied to the chain's result.  States are
+//     streamed from the pool two per step through a 4-slot LDS ring, six
+//     states ahead in registers, with one barrier per step; each wave reads a
+//     state's operand from LDS once for all of its tiles.  The lambda weights
+//     are gathered two states ahead.
 //   * intra-chunk part: (Q K^T (.) M) V with M[t][s] = [s <= t] exp(G_t - G_s)
-//     lambda[t][slot_t(s)] over the chunk's own keys, staged 32 tokens at a
-//     time in LDS.  slot_t(s) is uniform over a key block unless a live state
-//     leader starts inside it, so lambda is gathered once per (token, block) in
-//     the common case.
+//     lambda[t][slot_t(s)] over the chunk's own keys.  Each wave loads the key
+//     rows of a block of 32 tokens straight into MFMA operand registers, one
+//     block ahead, so this part has no barriers.  slot_t(s) is uniform over a
+//     block unless a live state leader starts inside it, so lambda is gathered
+//     once per (token, block) in the common case.
 // Workgroups are dealt to the 8 XCDs round-robin by id; the mapping puts the
 // column groups and neighbouring chunks of one head on one XCD, so the chunk's
 // queries, keys and lambda rows, and the state copies that neighbouring chunks
@@ -31,31 +34,39 @@ namespace dla {
 template <int DK, typename Tin>
 struct RO : ChunkP<DK, Tin> {
   using B = ChunkP<DK, Tin>;
-  static constexpr size_t RING_BYTES = 2 * (size_t)B::SLICE16 * 16;
-  static constexpr size_t KB_BYTES = 2 * (size_t)B::KBUF * B::E;
-  // the ring (inter part) and the key blocks (intra part) share LDS
-  static constexpr size_t SHARED_BYTES = RING_BYTES > KB_BYTES ? RING_BYTES : KB_BYTES;
+  // inter phase: state ring (two steps of two states)
+  static constexpr int NSLOT = 4;
+  static constexpr size_t RING_BYTES = NSLOT * (size_t)B::SLICE16 * 16;
+  static constexpr size_t INTER_BYTES = RING_BYTES;
+  // intra phase: key ring + lambda window
+  static constexpr int KSLOT = 4;
+  static constexpr size_t KRING_BYTES = (KSLOT * (size_t)B::KBUF * B::E + 15) / 16 * 16;
+  __host__ __device__ static size_t region_bytes(int lw) {
+    const size_t intra = KRING_BYTES + (size_t)B::RL * (lw > 0 ? lw + 1 : 0) * B::E;
+    return round_up(INTER_BYTES > intra ? INTER_BYTES : intra, 16);
+  }
   static size_t smem_bytes(int C, int lw) {
-    size_t off = round_up(SHARED_BYTES, 16);
-    off += (size_t)NC * B::VTS * B::E;                    // sVt
-    off += (size_t)B::RL * (lw > 0 ? lw + 1 : 0) * B::E;  // lambda window
+    size_t off = region_bytes(lw);
+    off += (size_t)NC * B::VTS * B::E;  // sVt
     off = round_up(off, 16);
     off += (size_t)B::RL * (8 + 4 * 6);  // sG sRf sBf sDeath sLeadU sLeadD sAold
-    off += (size_t)(C + 4) * 4 * 2;      // sSf, sObj (padded past the last state)
-    off += (size_t)C * 4;                // sDt
+    off += (size_t)(C + 8) * 4 * 3;      // sSf, sObj, sDt (padded past the last state)
     return round_up(off, 16);
   }
 };
 
-// Token tile of wave wv: with two tiles per wave, wave p owns tiles p and
-// 2 NWAVE - 1 - p, so the causal intra-chunk work is the same for every wave.
+// Token tile of wave wv: tiles come in mirrored pairs, wave p owning tiles
+// 2 RWAVE q + p and 2 RWAVE q + 2 RWAVE - 1 - p of pair q, so every wave has
+// the same causal intra-chunk work, and at every key block the same number of
+// tiles still to serve.
 template <int NT>
 __device__ __forceinline__ int tile_of(int wv, int nt) {
-  return nt == 0 ? wv : 2 * NWAVE - 1 - wv;
+  const int base = 2 * RWAVE * (nt >> 1);
+  return (nt & 1) ? base + 2 * RWAVE - 1 - wv : base + wv;
 }
 
 template <int DK, int DV, typename Tin, typename Tout>
-__global__ __launch_bounds__(NTHR) void prefill_readout_kernel(PrefillArgs a, PrefillWS w,
+__global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, PrefillWS w,
                                                                SegPlan plan, int seg, int lw) {
   using FR = Frag<Tin>;
   using FT = typename FR::T;
@@ -64,6 +75,7 @@ __global__ __launch_bounds__(NTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   constexpr int NCG = DV / NC;
   constexpr int KS = P::KS;
   constexpr int RL = P::RL;
+  constexpr int EPP = P::EPP;
   const int nh = a.desc.B * a.desc.H;
   const int cs = seg * plan.nch_seg;
   const int nchs = min(plan.nch, cs + plan.nch_seg) - cs;
@@ -83,15 +95,15 @@ __global__ __launch_bounds__(NTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   const int T = a.T;
 
   extern __shared__ __align__(16) char smem[];
-  u32x4* ring = reinterpret_cast<u32x4*>(smem);  // 2 state slices (inter part)
-  Tin* kbuf = reinterpret_cast<Tin*>(smem);      // 2 key blocks (intra part)
-  Tin* sVt = reinterpret_cast<Tin*>(smem + round_up(P::SHARED_BYTES, 16));  // [NC][VTS]
-  Tin* sLamW = sVt + NC * P::VTS;  // [RL][lw + 1] lambda window
+  // inter phase
+  u32x4* ring = reinterpret_cast<u32x4*>(smem);                   // NSLOT state slices
+  // intra phase (same bytes)
+  Tin* kring = reinterpret_cast<Tin*>(smem);                      // KSLOT x [32][KRS] keys
+  Tin* sLamW = reinterpret_cast<Tin*>(smem + P::KRING_BYTES);     // [RL][lw + 1] lambda
   const int lws = lw + 1;
-  double* sG = reinterpret_cast<double*>(smem + round_up(
-      round_up(P::SHARED_BYTES, 16) +
-          ((size_t)NC * P::VTS + (size_t)RL * (lw > 0 ? lws : 0)) * P::E,
-      16));
+  const size_t rgn = P::region_bytes(lw);
+  Tin* sVt = reinterpret_cast<Tin*>(smem + rgn);                  // [NC][VTS] values
+  double* sG = reinterpret_cast<double*>(smem + round_up(rgn + (size_t)NC * P::VTS * P::E, 16));
   float* sRf = reinterpret_cast<float*>(sG + RL);  // exp(G_t - G_ref)
   float* sBf = sRf + RL;                            // exp(G_blockend - G_s)
   int32_t* sDeath = reinterpret_cast<int32_t*>(sBf + RL);
@@ -99,12 +111,11 @@ __global__ __launch_bounds__(NTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   int32_t* sLeadD = sLeadU + RL;  //                   death token
   int32_t* sAold = sLeadD + RL;   // old states alive at each token of the chunk
   float* sSf = reinterpret_cast<float*>(sAold + RL);  // exp(G_ref - F_j); 0 for j >= m
-  int32_t* sObj = reinterpret_cast<int32_t*>(sSf + C + 4);
-  int32_t* sDt = sObj + C + 4;
+  int32_t* sObj = reinterpret_cast<int32_t*>(sSf + C + 8);
+  int32_t* sDt = sObj + C + 8;
   __shared__ int sCnt[2];
   __shared__ int sBlk[RL / 32 + 1];
 
-  const double G0 = *init_at(w, h, C).G0;
   const double* Gtok = w.Gtok + (size_t)h * T;
   const int32_t* death = w.death + (size_t)h * T;
   const Tin* Kin = static_cast<const Tin*>(a.k) + (size_t)h * T * DK;
@@ -116,45 +127,92 @@ __global__ __launch_bounds__(NTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   const int c0 = c * RL;
   const int nrow = min(RL, T - c0);
   const int nblk = (nrow + 31) >> 5;
-  const double Gref = (c0 == 0) ? G0 : Gtok[c0 - 1];
 
-  // the chunk's state list
+  // ------------------------------------------------ set-up: every load first
   const char* lst = list_at(w, h, c, plan.nch);
-  const int m = min(max(*reinterpret_cast<const int32_t*>(lst), 0), C);
-  {
-    const ListEntry* ent = reinterpret_cast<const ListEntry*>(lst + 16);
-    for (int j = tid; j < m + 4; j += NTHR) {
-      if (j < m) {
-        const ListEntry le = ent[j];
-        sObj[j] = min(max(le.obj, 0), plan.P_cap - 1);
-        sDt[j] = le.dt;
-        sSf[j] = __expf((float)(Gref - le.F));
-      } else {
-        sObj[j] = 0;
-        sSf[j] = 0.f;
-      }
-    }
-  }
-  for (int i2 = tid; i2 < RL; i2 += NTHR) {
-    const int ic = min(i2, nrow - 1);
-    const double Gi = Gtok[c0 + ic];
-    const int be = min(32 * (i2 >> 5) + 31, nrow - 1);
-    sG[i2] = Gi;
-    sRf[i2] = __expf((float)(Gi - Gref));
-    sBf[i2] = __expf((float)(Gtok[c0 + be] - Gi));
-    sDeath[i2] = (i2 < nrow) ? death[c0 + i2] : -1;
-  }
-  // this group's value columns of the chunk, transposed (sVt[c][r])
-  {
-    constexpr int PER_ROW16 = NC * P::E / 16;
-    for (int idx = tid; idx < RL * PER_ROW16; idx += NTHR) {
-      const int r = idx / PER_ROW16, p = idx % PER_ROW16;
-      u32x4 val = {0u, 0u, 0u, 0u};
-      if (r < nrow)
-        val = *reinterpret_cast<const u32x4*>(Vin + (size_t)(c0 + r) * DV + cg * NC + p * P::EPP);
+  const ListEntry* ent = reinterpret_cast<const ListEntry*>(lst + 16);
+  constexpr int EPT = 1024 / RTHR;  // list entries per thread (C <= 1024)
+  ListEntry le[EPT];
 #pragma unroll
-      for (int e = 0; e < P::EPP; ++e) sVt[(p * P::EPP + e) * P::VTS + r] = piece_elem<Tin>(val, e);
+  for (int u = 0; u < EPT; ++u) {
+    const int j = tid + RTHR * u;
+    if (j < C) le[u] = ent[j];  // entries past m are read but not used
+  }
+  const int m = min(max(*reinterpret_cast<const int32_t*>(lst), 0), C);
+  const double Gref = (c0 == 0) ? *init_at(w, h, C).G0 : Gtok[c0 - 1];
+  constexpr int TPT = (RL + RTHR - 1) / RTHR;
+  double gi_[TPT], gb_[TPT];
+  int dth_[TPT];
+#pragma unroll
+  for (int u = 0; u < TPT; ++u) {
+    const int t = tid + RTHR * u;
+    const int ic = min(t, nrow - 1);
+    const int be = min(32 * (t >> 5) + 31, nrow - 1);
+    gi_[u] = Gtok[c0 + ic];
+    gb_[u] = Gtok[c0 + be];
+    dth_[u] = (t < nrow) ? death[c0 + t] : -1;
+  }
+  constexpr int PER_ROW16 = NC * P::E / 16;
+  constexpr int VPT = RL * PER_ROW16 / RTHR;
+  u32x4 vp_[VPT];
+#pragma unroll
+  for (int u = 0; u < VPT; ++u) {
+    const int idx = tid + RTHR * u;
+    const int r = idx / PER_ROW16, p = idx % PER_ROW16;
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    vp_[u] = (r < nrow)
+                 ? *reinterpret_cast<const u32x4*>(Vin + (size_t)(c0 + r) * DV + cg * NC + p * EPP)
+                 : z;
+  }
+  int tr[NT];
+  bool rv[NT];
+  FT qf[NT][KS];
+  f32x16 acc[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    tr[nt] = 32 * tile_of<NT>(wv, nt) + l32;
+    rv[nt] = tr[nt] < nrow;
+    acc[nt] = zero16();
+    const Tin* qrow = Qin + (size_t)(c0 + (rv[nt] ? tr[nt] : 0)) * DK;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qf[nt][ks] = rv[nt] ? FR::load(qrow + 16 * ks + 8 * half) : FR::zero();
+  }
+  // ... then the LDS tables
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    const int j = tid + RTHR * u;
+    if (j < m) {
+      sObj[j] = min(max(le[u].obj, 0), plan.P_cap - 1);
+      sDt[j] = le[u].dt;
+      sSf[j] = __expf((float)(Gref - le[u].F));
+    } else if (j < C + 8) {
+      sObj[j] = 0;
+      sDt[j] = 0;
+      sSf[j] = 0.f;
     }
+  }
+  for (int j = max(C, RTHR * EPT) + tid; j < C + 8; j += RTHR) {  // padding past RTHR * EPT
+    sObj[j] = 0;
+    sDt[j] = 0;
+    sSf[j] = 0.f;
+  }
+#pragma unroll
+  for (int u = 0; u < TPT; ++u) {
+    const int t = tid + RTHR * u;
+    if (t < RL) {
+      sG[t] = gi_[u];
+      sRf[t] = __expf((float)(gi_[u] - Gref));
+      sBf[t] = __expf((float)(gb_[u] - gi_[u]));
+      sDeath[t] = dth_[u];
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < VPT; ++u) {
+    const int idx = tid + RTHR * u;
+    const int r = idx / PER_ROW16, p = idx % PER_ROW16;
+#pragma unroll
+    for (int e = 0; e < EPP; ++e) sVt[(p * EPP + e) * P::VTS + r] = piece_elem<Tin>(vp_[u], e);
   }
   __syncthreads();
   // compact list of the chunk's state leaders (wave 0)
@@ -176,7 +234,7 @@ __global__ __launch_bounds__(NTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   __syncthreads();
   const int nLead = sCnt[0];
   // first leader of each 32-token block (the leader list is in token order)
-  for (int sb = tid; sb <= RL / 32; sb += NTHR) {
+  for (int sb = tid; sb <= RL / 32; sb += RTHR) {
     int lo = 0, hi = nLead;
     while (lo < hi) {
       const int mid = (lo + hi) >> 1;
@@ -185,34 +243,22 @@ __global__ __launch_bounds__(NTHR) void prefill_readout_kernel(PrefillArgs a, Pr
     sBlk[sb] = lo;
   }
 
-  // this wave's token tiles
-  int tr[NT];
-  bool rv[NT];
-  FT qf[NT][KS];
-  f32x16 acc[NT];
-  int cnt[NT];
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    tr[nt] = 32 * tile_of<NT>(wv, nt) + l32;
-    rv[nt] = tr[nt] < nrow;
-    acc[nt] = zero16();
-    cnt[nt] = 0;
-    const Tin* qrow = Qin + (size_t)(c0 + (rv[nt] ? tr[nt] : 0)) * DK;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qf[nt][ks] = rv[nt] ? FR::load(qrow + 16 * ks + 8 * half) : FR::zero();
-  }
-
   // ------------------------------------------------ inter-chunk readout
-  // Each thread loads its share of a state's slice three states ahead (named
-  // register buffers, constant indexing), writes it to the ring, and after one
-  // barrier every wave reads the state's operand from LDS once for its tiles.
-  // Per step the loads are issued in a fixed order (lambda of the next state,
-  // then the prefetch), so waiting for one never waits for the other.
+  // Step J handles states 2J and 2J+1: the registers loaded two steps earlier
+  // go to ring slots 2 (J & 1) and 2 (J & 1) + 1, the lambda weights of states
+  // 2J+2 and 2J+3 are read and the slices of states 2J+4 and 2J+5 requested,
+  // and after one barrier every wave reads the two operands from LDS.  Steps
+  // run in pairs over named register buffers (constant indexing); steps past
+  // the last state have sSf = 0.
+  // The weight of state j at token t is lambda[t][x], x = (live states up to
+  // j) - 1 (a state merged away at or before t is weighted as the live state
+  // that absorbed it).
+  int cnt[NT];  // live states up to the last state whose weight was read
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) cnt[nt] = 0;
   if (m > 0) {
     float rf[NT];
     const Tin* lp[NT];
-    Tin lamC[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       rf[nt] = rv[nt] ? sRf[tr[nt]] : 0.f;
@@ -221,83 +267,115 @@ __global__ __launch_bounds__(NTHR) void prefill_readout_kernel(PrefillArgs a, Pr
       lp[nt] = Lin ? Lin + (size_t)(c0 + (rv[nt] ? tr[nt] : 0)) * C : Kin;
     }
     constexpr int SL16 = P::SLICE16;
-    constexpr int V16 = (SL16 + NTHR - 1) / NTHR;
-    u32x4 preA[V16], preB[V16], preC[V16];
-    auto prefetch = [&](int j, u32x4(&pr)[V16]) __attribute__((always_inline)) {
-      const u32x4* src = reinterpret_cast<const u32x4*>(
-          pool_slice<Tin>(w.pool, h, plan.P_cap, sObj[min(j, m - 1)], cg, NCG, P::SLICE));
+    constexpr int V16 = (SL16 + RTHR - 1) / RTHR;
+    struct Pre {
+      u32x4 x[2][V16];
+    };
+    Pre preA, preB;
+    auto prefetch2 = [&](int jb, Pre& pr) __attribute__((always_inline)) {
 #pragma unroll
-      for (int u = 0; u < V16; ++u) {
-        const int pi = tid + NTHR * u;
-        if (SL16 % NTHR == 0 || pi < SL16) pr[u] = src[pi];
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const u32x4* src = reinterpret_cast<const u32x4*>(pool_slice<Tin>(
+            w.pool, h, plan.P_cap, sObj[min(jb + s2, m - 1)], cg, NCG, P::SLICE));
+#pragma unroll
+        for (int u = 0; u < V16; ++u) {
+          const int pi = tid + RTHR * u;
+          if (SL16 % RTHR == 0 || pi < SL16) pr.x[s2][u] = src[pi];
+        }
       }
     };
-    // first lambda, then the first three states: the steady-state order
-    {
-      const int d0 = sDt[0];
+    // weight of state j at each tile token: advance the live count, then gather
+    auto lam_req = [&](int j, Tin (&lv)[NT]) __attribute__((always_inline)) {
+      const int dj = sDt[min(j, C + 7)];
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        cnt[nt] = (d0 > c0 + tr[nt]) ? 1 : 0;
-        lamC[nt] = lp[nt][Lin ? max(cnt[nt] - 1, 0) : 0];
+        cnt[nt] += (j < m && dj > c0 + tr[nt]) ? 1 : 0;
+        lv[nt] = lp[nt][Lin ? max(cnt[nt] - 1, 0) : 0];
       }
-    }
-    prefetch(0, preA);
-    prefetch(1, preB);
-    prefetch(2, preC);
-    auto step = [&](int j, u32x4(&pr)[V16]) __attribute__((always_inline)) {
-      u32x4* rb = ring + (j & 1) * SL16;
+    };
+    Tin lamC0[NT], lamC1[NT];
+    lam_req(0, lamC0);
+    lam_req(1, lamC1);
+    prefetch2(0, preA);
+    prefetch2(2, preB);
+    // The tiles are staggered: after the MFMA chain of tile k of state j comes
+    // the weighting of tile k - 1 (of state j - 1 for k = 0), so every FMA runs
+    // while the matrix core works on an independent chain.
+    f32x16 f[NT];
+    float wP = 0.f;  // weight of the last tile's pending chain result
 #pragma unroll
-      for (int u = 0; u < V16; ++u) {
-        const int pi = tid + NTHR * u;
-        if (SL16 % NTHR == 0 || pi < SL16) rb[pi] = pr[u];
+    for (int nt = 0; nt < NT; ++nt) f[nt] = zero16();
+    // sched_group_barrier masks: 0x008 MFMA, 0x002 VALU, 0x100 LDS read
+    auto interleave = [&]() __attribute__((always_inline)) {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
       }
-      // lambda of state j + 1: raw values, converted when used
-      const int jn = min(j + 1, m - 1);
-      const int dn = sDt[jn];
-      int cntN[NT];
-      Tin lamN[NT];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        cntN[nt] = cnt[nt] + ((j + 1 < m && dn > c0 + tr[nt]) ? 1 : 0);
-        lamN[nt] = lp[nt][Lin ? max(cntN[nt] - 1, 0) : 0];
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      prefetch(j + 3, pr);
-      __builtin_amdgcn_sched_barrier(0);
-      __syncthreads();
-      // weights of state j (a step past the last state has sSf = 0)
-      const float sf = sSf[j];
-      float wgt[NT];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) wgt[nt] = (Lin ? to_f32(lamC[nt]) : 1.f) * rf[nt] * sf;
-      // the state's operand, read from LDS once for all token tiles
-      const Tin* A = reinterpret_cast<const Tin*>(rb);
+    };
+    auto sub = [&](const Tin* A, float sf, const Tin (&lc)[NT]) __attribute__((always_inline)) {
       FT sa[KS];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) sa[ks] = FR::load(A + ((ks * 2 + half) * 32 + l32) * 8);
-      f32x16 f[NT];
+      float wg[NT];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) f[nt] = zero16();
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) FR::mma(f[nt], sa[ks], qf[nt][ks]);
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[nt][r] += wgt[nt] * f[nt][r];
+      for (int nt = 0; nt < NT; ++nt) wg[nt] = (Lin ? to_f32(lc[nt]) : 1.f) * rf[nt] * sf;
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        cnt[nt] = cntN[nt];
-        lamC[nt] = lamN[nt];
+        // f[nt] held tile nt of the previous state, weighted one tile ago; the
+        // chain's MFMAs alternate with the FMAs of that weighting
+        f[nt] = zero16();
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) FR::mma(f[nt], sa[ks], qf[nt][ks]);
+        const int pt = nt == 0 ? NT - 1 : nt - 1;
+        const float wq = nt == 0 ? wP : wg[nt - 1];
+        if (NT > 1 || nt > 0) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[pt][r] += wq * f[pt][r];
+        }
+        interleave();
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if constexpr (NT == 1) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[0][r] += wg[0] * f[0][r];
+      }
+      wP = wg[NT - 1];
+    };
+    auto step = [&](int J, Pre& pr) __attribute__((always_inline)) {
+      u32x4* rb = ring + (J & 1) * 2 * SL16;
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+        for (int u = 0; u < V16; ++u) {
+          const int pi = tid + RTHR * u;
+          if (SL16 % RTHR == 0 || pi < SL16) rb[s2 * SL16 + pi] = pr.x[s2][u];
+        }
+      Tin lamN0[NT], lamN1[NT];
+      lam_req(2 * J + 2, lamN0);
+      lam_req(2 * J + 3, lamN1);
+      __builtin_amdgcn_sched_barrier(0);
+      prefetch2(2 * J + 4, pr);
+      __builtin_amdgcn_sched_barrier(0);
+      __syncthreads();
+      const Tin* A = reinterpret_cast<const Tin*>(rb);
+      sub(A, sSf[2 * J], lamC0);
+      __builtin_amdgcn_sched_barrier(0);
+      sub(A + P::SLICE, sSf[2 * J + 1], lamC1);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        lamC0[nt] = lamN0[nt];
+        lamC1[nt] = lamN1[nt];
       }
     };
-    // whole triples: every step issues the same memory operations, so the
-    // compiler keeps three prefetches in flight across iterations
-    for (int j0 = 0; j0 < m; j0 += 3) {
-      step(j0, preA);
-      step(j0 + 1, preB);
-      step(j0 + 2, preC);
+    for (int J0 = 0; 2 * J0 < m; J0 += 2) {
+      step(J0, preA);
+      step(J0 + 1, preB);
+    }
+    if constexpr (NT > 1) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[NT - 1][r] += wP * f[NT - 1][r];
     }
   }
   // old states alive at each of this wave's tokens (chronological index of
@@ -305,110 +383,123 @@ __global__ __launch_bounds__(NTHR) void prefill_readout_kernel(PrefillArgs a, Pr
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt)
     if (rv[nt]) sAold[tr[nt]] = cnt[nt];
-  __syncthreads();  // the ring is no longer read
+  __syncthreads();  // the state ring and the lambda blocks are no longer read
 
   // lambda window of every token: lambda[t][Aold_t - 1 + x] for x < lw, the
-  // weights of the states that hold the chunk's own tokens
+  // weights of the states that hold the chunk's own tokens.  Consecutive lanes
+  // read consecutive entries of a row; every load is issued before the stores.
   if (Lin && lw > 0) {
-    for (int idx = tid; idx < nrow * lw; idx += NTHR) {
-      const int t = idx / lw, x = idx - t * lw;
-      const int j = min(max(sAold[t] - 1 + x, 0), C - 1);
-      sLamW[t * lws + x] = Lin[(size_t)(c0 + t) * C + j];
+    constexpr int WPT = RL * 32 / RTHR;
+    Tin lv[WPT];
+    const int nwin = nrow * lw;
+#pragma unroll
+    for (int u = 0; u < WPT; ++u) {
+      const int idx = tid + RTHR * u;
+      if (idx < nwin) {
+        const int t = idx / lw, x = idx - t * lw;
+        lv[u] = Lin[(size_t)(c0 + t) * C + min(max(sAold[t] - 1 + x, 0), C - 1)];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < WPT; ++u) {
+      const int idx = tid + RTHR * u;
+      if (idx < nwin) {
+        const int t = idx / lw, x = idx - t * lw;
+        sLamW[t * lws + x] = lv[u];
+      }
     }
   }
 
   // ------------------------------------------------------- key-block loop
-  const bool kstager = tid >= NTHR / 2;
-  const int ktid = tid - NTHR / 2;
-  u32x4 kpre[P::KPT];
-  auto kload = [&](int sb) __attribute__((always_inline)) {
+  // The chunk's keys pass through a KSLOT-slot LDS ring, 32 tokens per block,
+  // two blocks ahead in registers; every thread loads one 16-byte piece per
+  // block (consecutive threads, consecutive pieces of a row).  Block sb + 1 is
+  // stored at iteration sb, replacing block sb - 3, whose readers all passed
+  // the barrier of iteration sb - 2.
+  constexpr int KPT = (32 * P::KROW16 + RTHR - 1) / RTHR;
+  u32x4 kA[KPT], kB[KPT];
+  auto kload = [&](int sb, u32x4 (&kr)[KPT]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < P::KPT; ++u) {
-      const int pi = ktid + (NTHR / 2) * u;
+    for (int u = 0; u < KPT; ++u) {
+      const int pi = tid + RTHR * u;
       const int r = pi / P::KROW16, pc = pi % P::KROW16;
       const int tok = 32 * sb + r;
-      u32x4 z = {0u, 0u, 0u, 0u};
-      if (r < 32 && tok < nrow)
-        z = *reinterpret_cast<const u32x4*>(Kin + (size_t)(c0 + tok) * DK + pc * P::EPP);
-      kpre[u] = z;
+      const u32x4 z = {0u, 0u, 0u, 0u};
+      kr[u] = (r < 32 && tok < nrow)
+                  ? *reinterpret_cast<const u32x4*>(Kin + (size_t)(c0 + tok) * DK + pc * EPP)
+                  : z;
     }
   };
-  auto kstore = [&](Tin* kb) __attribute__((always_inline)) {
+  auto kstore = [&](int sb, const u32x4 (&kr)[KPT]) __attribute__((always_inline)) {
+    Tin* kb = kring + (sb % P::KSLOT) * P::KBUF;
 #pragma unroll
-    for (int u = 0; u < P::KPT; ++u) {
-      const int pi = ktid + (NTHR / 2) * u;
+    for (int u = 0; u < KPT; ++u) {
+      const int pi = tid + RTHR * u;
       const int r = pi / P::KROW16, pc = pi % P::KROW16;
-      if (r < 32) *reinterpret_cast<u32x4*>(kb + r * P::KRS + pc * P::EPP) = kpre[u];
+      if (r < 32) *reinterpret_cast<u32x4*>(kb + r * P::KRS + pc * EPP) = kr[u];
     }
   };
   int before[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) before[nt] = 0;
-  int maxtile = 0;
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) maxtile = max(maxtile, tile_of<NT>(wv, nt));
-  if (kstager) kload(0);
-  for (int sb = 0; sb < nblk; ++sb) {
-    Tin* kb = kbuf + (sb & 1) * P::KBUF;
-    if (kstager) {
-      kstore(kb);
-      if (sb + 1 < nblk) kload(sb + 1);
-    }
-    __syncthreads();
-    if (sb > maxtile) continue;
-    const Tin* krow = kb + l32 * P::KRS + 8 * half;
+  auto block = [&](int sb) __attribute__((always_inline)) {
+    const Tin* krow = kring + (sb % P::KSLOT) * P::KBUF + l32 * P::KRS + 8 * half;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int ti = tile_of<NT>(wv, nt);
       if (sb > ti || 32 * ti >= nrow) continue;
+      __builtin_amdgcn_sched_barrier(0);
       const int trn = tr[nt];
       const int tabs = c0 + trn;
       const int Aold = cnt[nt];
       const Tin* lrow = Lin ? Lin + (size_t)(c0 + (rv[nt] ? trn : 0)) * C : nullptr;
       const Tin* lwin = sLamW + trn * lws;
-      // weight of the state at window position x (x = live in-chunk leaders
-      // up to the key token): from the window, else from the lambda row
+      // weight of the state at window position x (x = live in-chunk leaders up
+      // to the key token): from the window, else from the lambda row
+      // (the window read is unconditional and the row read separate, so the
+      // two never merge into one generic-address load)
       auto lam_at = [&](int x) __attribute__((always_inline)) -> float {
         if (!lrow || !rv[nt]) return 1.f;
-        if (x < lw) return to_f32(lwin[x]);
-        return to_f32(lrow[min(max(Aold - 1 + x, 0), C - 1)]);
+        float v = lw > 0 ? to_f32(lwin[min(x, lw - 1)]) : 0.f;
+        if (x >= lw) v = to_f32(lrow[min(max(Aold - 1 + x, 0), C - 1)]);
+        return v;
       };
+      // P^T tile: rows = the block's key tokens, columns = the tile's tokens
+      f32x16 pt = zero16();
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) FR::mma(pt, FR::load(krow + 16 * ks), qf[nt][ks]);
       // leaders inside block sb that are live at token t, as a bit mask
       uint32_t word = 0u;
       for (int k2 = sBlk[sb]; k2 < sBlk[sb + 1]; ++k2)
         if (sLeadD[k2] > tabs) word |= 1u << (sLeadU[k2] & 31);
-      // P^T tile: rows = the block's key tokens, columns = this tile's tokens
-      f32x16 pt = zero16();
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) FR::mma(pt, FR::load(krow + 16 * ks), qf[nt][ks]);
-      // weights, in place
+      // live leaders at key rows <= so = rb + 4 half of the block, with rb =
+      // 8 (r / 4) + r % 4 a constant per accumulator element: ww holds the mask
+      // shifted so that the count is a popcount under a constant mask
+      const uint32_t ww = half ? word : (word << 4);
+      auto upto = [&](int r) __attribute__((always_inline)) -> int {
+        const int rb = 8 * (r >> 2) + (r & 3);
+        return __popc(ww & (0xFFFFFFFFu >> (27 - rb)));
+      };
       if (sb < ti) {
         // the whole block precedes the token: one decay factor per lane, and
         // lambda uniform unless a live leader starts inside the block
         const float f1 = rv[nt] ? __expf((float)(sG[trn] - sG[32 * sb + 31])) : 0.f;
         if ((word & ~1u) == 0u) {
-          const float f = f1 * lam_at(before[nt] + (int)(word & 1u));
+          const float fw = f1 * lam_at(before[nt] + (int)(word & 1u));
 #pragma unroll
-          for (int r = 0; r < 16; ++r) pt[r] *= f * sBf[32 * sb + out_row(r, lane)];
+          for (int r = 0; r < 16; ++r) pt[r] *= fw * sBf[32 * sb + out_row(r, lane)];
         } else {
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int so = out_row(r, lane);
-            const int cl = before[nt] + __popc(word & (0xFFFFFFFFu >> (31 - so)));
-            pt[r] *= f1 * lam_at(cl) * sBf[32 * sb + so];
-          }
+          for (int r = 0; r < 16; ++r)
+            pt[r] *= f1 * lam_at(before[nt] + upto(r)) * sBf[32 * sb + out_row(r, lane)];
         }
       } else {
         // the token's own block: causal mask and decay per element
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int so = out_row(r, lane);
-          const int s = 32 * sb + so;
+          const int s = 32 * sb + out_row(r, lane);
           float wgt = 0.f;
-          if (rv[nt] && s <= trn) {
-            const int cl = before[nt] + __popc(word & (0xFFFFFFFFu >> (31 - so)));
-            wgt = lam_at(cl) * __expf((float)(sG[trn] - sG[s]));
-          }
+          if (rv[nt] && s <= trn) wgt = lam_at(before[nt] + upto(r)) * __expf((float)(sG[trn] - sG[s]));
           pt[r] *= wgt;
         }
       }
@@ -424,6 +515,21 @@ __global__ __launch_bounds__(NTHR) void prefill_readout_kernel(PrefillArgs a, Pr
         FR::mma(acc[nt], load_4x2<Tin>(vp, vp + 8), FR::from_floats(pw));
       }
     }
+  };
+  kload(0, kA);
+  kload(1, kB);
+  kstore(0, kA);
+  kload(2, kA);
+  for (int sb = 0; sb < nblk; sb += 2) {
+    kstore(sb + 1, kB);  // (past the last block: zeros into a free slot)
+    kload(sb + 3, kB);
+    __syncthreads();
+    block(sb);
+    if (sb + 1 >= nblk) break;
+    kstore(sb + 2, kA);
+    kload(sb + 4, kA);
+    __syncthreads();
+    block(sb + 1);
   }
 
   // outputs
@@ -462,7 +568,7 @@ static hipError_t launch_readout_t(const PrefillArgs& a, const SegPlan& p, int s
     if (hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm) !=
         hipSuccess)
       return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(NTHR), shm, s, a, w, p, seg, lw);
+    hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(RTHR), shm, s, a, w, p, seg, lw);
     return hipGetLastError();
   };
   if (a.out_dtype == DLA_F32) return launch(prefill_readout_kernel<DK, DV, Tin, float>);
