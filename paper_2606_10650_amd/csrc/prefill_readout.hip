@@ -39,7 +39,7 @@ struct RO : ChunkP<DK, Tin> {
   static constexpr size_t RING_BYTES = NSLOT * (size_t)B::SLICE16 * 16;
   static constexpr size_t INTER_BYTES = RING_BYTES;
   // intra phase: key ring + lambda window
-  static constexpr int KSLOT = 4;
+  static constexpr int KSLOT = 6;
   static constexpr size_t KRING_BYTES = (KSLOT * (size_t)B::KBUF * B::E + 15) / 16 * 16;
   __host__ __device__ static size_t region_bytes(int lw) {
     const size_t intra = KRING_BYTES + (size_t)B::RL * (lw > 0 ? lw + 1 : 0) * B::E;
@@ -49,7 +49,7 @@ struct RO : ChunkP<DK, Tin> {
     size_t off = region_bytes(lw);
     off += (size_t)NC * B::VTS * B::E;  // sVt
     off = round_up(off, 16);
-    off += (size_t)B::RL * (8 + 4 * 6);  // sG sRf sBf sDeath sLeadU sLeadD sAold
+    off += (size_t)B::RL * 4 * 7;  // sGc sRf sBf sDeath sLeadU sLeadD sAold
     off += (size_t)(C + 8) * 4 * 3;      // sSf, sObj, sDt (padded past the last state)
     return round_up(off, 16);
   }
@@ -103,8 +103,8 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   const int lws = lw + 1;
   const size_t rgn = P::region_bytes(lw);
   Tin* sVt = reinterpret_cast<Tin*>(smem + rgn);                  // [NC][VTS] values
-  double* sG = reinterpret_cast<double*>(smem + round_up(rgn + (size_t)NC * P::VTS * P::E, 16));
-  float* sRf = reinterpret_cast<float*>(sG + RL);  // exp(G_t - G_ref)
+  float* sGc = reinterpret_cast<float*>(smem + round_up(rgn + (size_t)NC * P::VTS * P::E, 16));
+  float* sRf = sGc + RL;                            // exp(G_t - G_ref)
   float* sBf = sRf + RL;                            // exp(G_blockend - G_s)
   int32_t* sDeath = reinterpret_cast<int32_t*>(sBf + RL);
   int32_t* sLeadU = sDeath + RL;  // in-chunk leaders: position in the chunk
@@ -201,7 +201,7 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   for (int u = 0; u < TPT; ++u) {
     const int t = tid + RTHR * u;
     if (t < RL) {
-      sG[t] = gi_[u];
+      sGc[t] = (float)(gi_[u] - Gref);  // G_t - G_ref
       sRf[t] = __expf((float)(gi_[u] - Gref));
       sBf[t] = __expf((float)(gb_[u] - gi_[u]));
       sDeath[t] = dth_[u];
@@ -412,10 +412,10 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
 
   // ------------------------------------------------------- key-block loop
   // The chunk's keys pass through a KSLOT-slot LDS ring, 32 tokens per block,
-  // two blocks ahead in registers; every thread loads one 16-byte piece per
+  // four blocks ahead in registers; every thread loads its 16-byte pieces of a
   // block (consecutive threads, consecutive pieces of a row).  Block sb + 1 is
-  // stored at iteration sb, replacing block sb - 3, whose readers all passed
-  // the barrier of iteration sb - 2.
+  // stored at iteration sb into the slot of block sb + 1 - KSLOT, whose readers
+  // all passed the barrier of iteration sb + 2 - KSLOT <= sb - 1.
   constexpr int KPT = (32 * P::KROW16 + RTHR - 1) / RTHR;
   u32x4 kA[KPT], kB[KPT];
   auto kload = [&](int sb, u32x4 (&kr)[KPT]) __attribute__((always_inline)) {
@@ -480,12 +480,16 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
         const int rb = 8 * (r >> 2) + (r & 3);
         return __popc(ww & (0xFFFFFFFFu >> (27 - rb)));
       };
+      // lambda is uniform over the block unless a live leader starts after its
+      // first row
+      const bool uni = (word & ~1u) == 0u;
+      const float lu = uni ? lam_at(before[nt] + (int)(word & 1u)) : 0.f;
       if (sb < ti) {
-        // the whole block precedes the token: one decay factor per lane, and
-        // lambda uniform unless a live leader starts inside the block
-        const float f1 = rv[nt] ? __expf((float)(sG[trn] - sG[32 * sb + 31])) : 0.f;
-        if ((word & ~1u) == 0u) {
-          const float fw = f1 * lam_at(before[nt] + (int)(word & 1u));
+        // the whole block precedes the token: decay exp(G_t - G_end) per lane
+        // times exp(G_end - G_s) per row (both at most 1)
+        const float f1 = rv[nt] ? __expf(sGc[trn] - sGc[32 * sb + 31]) : 0.f;
+        if (uni) {
+          const float fw = f1 * lu;
 #pragma unroll
           for (int r = 0; r < 16; ++r) pt[r] *= fw * sBf[32 * sb + out_row(r, lane)];
         } else {
@@ -494,13 +498,13 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
             pt[r] *= f1 * lam_at(before[nt] + upto(r)) * sBf[32 * sb + out_row(r, lane)];
         }
       } else {
-        // the token's own block: causal mask and decay per element
+        // the token's own block: causal mask, decay exp(G_t - G_s) per element
+        const float gt = sGc[trn];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int s = 32 * sb + out_row(r, lane);
-          float wgt = 0.f;
-          if (rv[nt] && s <= trn) wgt = lam_at(before[nt] + upto(r)) * __expf((float)(sG[trn] - sG[s]));
-          pt[r] *= wgt;
+          const float lr = uni ? lu : lam_at(before[nt] + upto(r));
+          pt[r] *= (rv[nt] && s <= trn) ? lr * __expf(gt - sGc[s]) : 0.f;
         }
       }
       before[nt] += __popc(word);
@@ -516,20 +520,35 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
       }
     }
   };
+  u32x4 kC[KPT], kD[KPT];
   kload(0, kA);
   kload(1, kB);
+  kload(2, kC);
+  kload(3, kD);
   kstore(0, kA);
-  kload(2, kA);
-  for (int sb = 0; sb < nblk; sb += 2) {
-    kstore(sb + 1, kB);  // (past the last block: zeros into a free slot)
-    kload(sb + 3, kB);
+  kload(4, kA);
+  // iteration sb stores block sb + 1 (loaded four iterations earlier) and
+  // requests block sb + 5 into the same registers
+  for (int sb = 0; sb < nblk; sb += 4) {
+    kstore(sb + 1, kB);
+    kload(sb + 5, kB);
     __syncthreads();
     block(sb);
     if (sb + 1 >= nblk) break;
-    kstore(sb + 2, kA);
-    kload(sb + 4, kA);
+    kstore(sb + 2, kC);
+    kload(sb + 6, kC);
     __syncthreads();
     block(sb + 1);
+    if (sb + 2 >= nblk) break;
+    kstore(sb + 3, kD);
+    kload(sb + 7, kD);
+    __syncthreads();
+    block(sb + 2);
+    if (sb + 3 >= nblk) break;
+    kstore(sb + 4, kA);
+    kload(sb + 8, kA);
+    __syncthreads();
+    block(sb + 3);
   }
 
   // outputs
