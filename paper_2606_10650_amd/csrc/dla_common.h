@@ -94,6 +94,92 @@ __device__ __forceinline__ T wave_sum(T v) {
   return v;
 }
 
+// ---------------------------------------------------------------------------
+// DPP lane moves (GFX9 controls): row_shr:n = 0x110 + n, wave_shr:1 = 0x138,
+// row_bcast:15 = 0x142 (to rows 1 and 3), row_bcast:31 = 0x143 (to rows 2
+// and 3).  A lane with no source lane, or outside the row mask, gets `old`.
+// Scans built from them compose the earlier lanes into each lane with the
+// classic row_shr 1/2/4/8 + row_bcast 15/31 ladder; lane 63 ends with the whole
+// wavefront.
+// ---------------------------------------------------------------------------
+template <int CTRL, int RMASK>
+__device__ __forceinline__ float dpp_f(float old, float x) {
+  return __int_as_float(
+      __builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(x), CTRL, RMASK, 0xF, false));
+}
+template <int CTRL, int RMASK>
+__device__ __forceinline__ int dpp_i(int old, int x) {
+  return __builtin_amdgcn_update_dpp(old, x, CTRL, RMASK, 0xF, false);
+}
+template <int CTRL, int RMASK>
+__device__ __forceinline__ double dpp_d(double old, double x) {
+  const long long o = __double_as_longlong(old), v = __double_as_longlong(x);
+  const int lo = dpp_i<CTRL, RMASK>((int)o, (int)v);
+  const int hi = dpp_i<CTRL, RMASK>((int)(o >> 32), (int)(v >> 32));
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+__device__ __forceinline__ double readlane_d(double x, int l) {
+  const long long v = __double_as_longlong(x);
+  const int lo = __builtin_amdgcn_readlane((int)v, l);
+  const int hi = __builtin_amdgcn_readlane((int)(v >> 32), l);
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
+// Inclusive scan of affine maps x -> A x + B over the lanes: lane i ends with
+// map_i o ... o map_0.
+template <int CTRL, int RMASK>
+__device__ __forceinline__ void affine_step(float& A, float& B) {
+  const float Ao = dpp_f<CTRL, RMASK>(1.f, A);
+  const float Bo = dpp_f<CTRL, RMASK>(0.f, B);
+  B = A * Bo + B;
+  A = A * Ao;
+}
+__device__ __forceinline__ void wave_scan_affine(float& A, float& B) {
+  affine_step<0x111, 0xF>(A, B);
+  affine_step<0x112, 0xF>(A, B);
+  affine_step<0x114, 0xF>(A, B);
+  affine_step<0x118, 0xF>(A, B);
+  affine_step<0x142, 0xA>(A, B);
+  affine_step<0x143, 0xC>(A, B);
+}
+
+// Sum of a double over the wavefront (every lane gets it).
+template <int CTRL, int RMASK>
+__device__ __forceinline__ void sum_step_d(double& x) {
+  x += dpp_d<CTRL, RMASK>(0.0, x);
+}
+__device__ __forceinline__ double wave_sum_d(double x) {
+  sum_step_d<0x111, 0xF>(x);
+  sum_step_d<0x112, 0xF>(x);
+  sum_step_d<0x114, 0xF>(x);
+  sum_step_d<0x118, 0xF>(x);
+  sum_step_d<0x142, 0xA>(x);
+  sum_step_d<0x143, 0xC>(x);
+  return readlane_d(x, 63);
+}
+
+// Lowest value over the wavefront, ties to the lowest index (every lane gets
+// both).
+template <int CTRL, int RMASK>
+__device__ __forceinline__ void argmin_step(double& best, int& bi) {
+  const double ob = dpp_d<CTRL, RMASK>(INFINITY, best);
+  const int oi = dpp_i<CTRL, RMASK>(0x7fffffff, bi);
+  if (ob < best || (ob == best && oi < bi)) {
+    best = ob;
+    bi = oi;
+  }
+}
+__device__ __forceinline__ void wave_argmin_d(double& best, int& bi) {
+  argmin_step<0x111, 0xF>(best, bi);
+  argmin_step<0x112, 0xF>(best, bi);
+  argmin_step<0x114, 0xF>(best, bi);
+  argmin_step<0x118, 0xF>(best, bi);
+  argmin_step<0x142, 0xA>(best, bi);
+  argmin_step<0x143, 0xC>(best, bi);
+  best = readlane_d(best, 63);
+  bi = __builtin_amdgcn_readlane(bi, 63);
+}
+
 // Sum of two values over a 256-thread block; every thread gets the result.
 // red must hold 8 floats.
 __device__ __forceinline__ void block_sum2_256(float& a, float& b, float* red) {

@@ -104,8 +104,10 @@ struct ScanP {
   // consecutive rows hit distinct banks
   static constexpr int KRS = DK + EPP;  // sK  [SL][KRS]
   static constexpr int VRS = DV + EPP;  // sV  [SL][VRS]
+  static constexpr int TRS = SL + EPP;  // sKt [DK][TRS], sVt [DV][TRS] (transposed)
   static size_t smem_bytes(int C) {
     size_t off = (size_t)SL * (KRS + VRS) * E;          // sK, sV
+    off += (size_t)(DK + DV) * TRS * E;                 // sKt, sVt
     off += (size_t)SL * (SL + 1) * 4;                   // sP
     off += (size_t)SL * SL * 4;                         // sR
     off += (size_t)8 * SL * 4;                          // sPart[4], sQ[4]
@@ -153,7 +155,9 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
   constexpr int KRS = P::KRS, VRS = P::VRS;
   Tin* sK = reinterpret_cast<Tin*>(smem);  // keys of the chunk, row-major
   Tin* sV = sK + SL * KRS;                 // values, row-major
-  float* sP = reinterpret_cast<float*>(sV + SL * VRS);  // [SL][SL+1]
+  Tin* sKt = sV + SL * VRS;                // keys, transposed [DK][TRS]
+  Tin* sVt = sKt + DK * P::TRS;            // values, transposed [DV][TRS]
+  float* sP = reinterpret_cast<float*>(sVt + DV * P::TRS);  // [SL][SL+1]
   float* sR = sP + SL * (SL + 1);                      // [SL][SL], R[p][t]
   float* sPart = sR + SL * SL;                         // [4][SL]
   float* sQ = sPart + 4 * SL;                          // [4][SL]
@@ -175,6 +179,7 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
   int32_t* sN = reinterpret_cast<int32_t*>(sIb + C);  // [C]
   int32_t* sLead = sN + C;                            // [C]
   int32_t* sMisc = sLead + C;                         // m, p_last
+  __shared__ double sGlast[1];
 
   Meta M = meta_at(a.cache + a.meta_offset + (size_t)h * a.meta_stride, C);
   InitView iv = init_at(w, h, C);
@@ -226,20 +231,32 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
   int32_t* death = w.death + tok0;
   constexpr int KROW16 = DK * (int)sizeof(Tin) / 16;  // 16-byte pieces per key row
   constexpr int VROW16 = DV * (int)sizeof(Tin) / 16;
+  // Next-chunk registers: lane tid % SL holds token row tid % SL, pieces
+  // tid / SL + 4 u of its key and value rows (so the transposed copies are
+  // written with consecutive lanes on consecutive tokens), and threads tid < SL
+  // hold the token's cumulative log-decay and overrides.
   u32x4s pk[K16], pv[V16];
+  double gpre = 0.0;
+  int bpre = -1, mpre = -1;
   auto prefetch = [&](int c0n) __attribute__((always_inline)) {
     const int nr = min(SL, T - c0n);
 #pragma unroll
     for (int u = 0; u < K16; ++u) {
       const int pi = tid + 256 * u;
-      const int r = min(pi / KROW16, nr - 1);
-      pk[u] = reinterpret_cast<const u32x4s*>(Kin + (size_t)(c0n + r) * DK)[pi % KROW16];
+      const int r = min(pi % SL, nr - 1);
+      pk[u] = reinterpret_cast<const u32x4s*>(Kin + (size_t)(c0n + r) * DK)[pi / SL];
     }
 #pragma unroll
     for (int u = 0; u < V16; ++u) {
       const int pi = tid + 256 * u;
-      const int r = min(pi / VROW16, nr - 1);
-      pv[u] = reinterpret_cast<const u32x4s*>(Vin + (size_t)(c0n + r) * DV)[pi % VROW16];
+      const int r = min(pi % SL, nr - 1);
+      pv[u] = reinterpret_cast<const u32x4s*>(Vin + (size_t)(c0n + r) * DV)[pi / SL];
+    }
+    if (tid < SL) {
+      const int t = min(tid, nr - 1);
+      gpre = Gtok[c0n + t];
+      bpre = (a.b_ovr && tid < nr) ? a.b_ovr[tok0 + c0n + tid] : (int8_t)-1;
+      mpre = (a.m_ovr && tid < nr) ? a.m_ovr[tok0 + c0n + tid] : -1;
     }
   };
   prefetch(0);
@@ -252,39 +269,47 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
 #pragma unroll
     for (int u = 0; u < K16; ++u) {
       const int pi = tid + 256 * u;
-      const int r = pi / KROW16, pc = pi % KROW16;
+      const int r = pi % SL, pc = pi / SL;
       const u32x4s z = {0u, 0u, 0u, 0u};
       const u32x4s val = (r < nrow) ? pk[u] : z;
       *reinterpret_cast<u32x4s*>(sK + r * KRS + pc * P::EPP) = val;
+#pragma unroll
+      for (int e = 0; e < P::EPP; ++e) sKt[(pc * P::EPP + e) * P::TRS + r] = piece_elem<Tin>(val, e);
     }
 #pragma unroll
     for (int u = 0; u < V16; ++u) {
       const int pi = tid + 256 * u;
-      const int r = pi / VROW16, pc = pi % VROW16;
+      const int r = pi % SL, pc = pi / SL;
       const u32x4s z = {0u, 0u, 0u, 0u};
       const u32x4s val = (r < nrow) ? pv[u] : z;
       *reinterpret_cast<u32x4s*>(sV + r * VRS + pc * P::EPP) = val;
+#pragma unroll
+      for (int e = 0; e < P::EPP; ++e) sVt[(pc * P::EPP + e) * P::TRS + r] = piece_elem<Tin>(val, e);
     }
-    if (c0 + SL < T) prefetch(c0 + SL);
     if (tid < SL) {
+      // log-decay offsets from the chunk start; the last token's G is the
+      // next chunk's start
       const int t = tid;
-      const int tc = min(t, nrow - 1);
-      const double Gt = Gtok[c0 + tc];
+      const double Gt = gpre;
+      const double Glast = __shfl(gpre, nrow - 1, 64);
       const float gc = (float)(Gt - Gprev);
+      const float gcp = __shfl_up(gc, 1, 64);  // token t - 1 (t >= 1)
       sGc[t] = gc;
       sA[t] = __expf(gc);
       // alpha_t^2 = exp(2 g_t); only tokens of the chunk read their predecessor
-      const float gprev = (t == 0 || t >= nrow) ? 0.f : (float)(Gtok[c0 + t - 1] - Gprev);
-      sAl2[t] = (t < nrow) ? __expf(2.f * (gc - gprev)) : 0.f;
-      sDe[t] = (t < nrow) ? (float)exp(Gtok[c0 + nrow - 1] - Gt) : 0.f;
-      sBo[t] = (a.b_ovr && t < nrow) ? a.b_ovr[tok0 + c0 + t] : (int8_t)-1;
-      sMo[t] = (a.m_ovr && t < nrow) ? a.m_ovr[tok0 + c0 + t] : -1;
+      sAl2[t] = (t < nrow) ? __expf(2.f * (t == 0 ? gc : gc - gcp)) : 0.f;
+      sDe[t] = (t < nrow) ? __expf((float)(Glast - Gt)) : 0.f;
+      sBo[t] = (int8_t)bpre;
+      sMo[t] = mpre;
       sDC[t] = -1;
       sBout[t] = 0;
       sMout[t] = -1;
       sIo[t] = 0.f;
+      if (t == 0) sGlast[0] = Glast;
     }
     __syncthreads();
+    const double Gnext = sGlast[0];  // G after the chunk's last token
+    if (c0 + SL < T) prefetch(c0 + SL);
 
     // ------------------------------------------------ Gram products and the carry term
     {
@@ -342,10 +367,16 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
             }
             FR::mma(y, ah[st], kb);
           }
-          const Tin* vrow = sV + (32 * tn + l32) * VRS + 32 * nj;
+          // v_t[j] for the rows j = 8 q + 4 h + (0..3) of the tile held by the lane
+          const Tin* vrow = sV + (32 * tn + l32) * VRS + 32 * nj + 4 * half;
           float sacc = 0.f;
 #pragma unroll
-          for (int r = 0; r < 16; ++r) sacc += y[r] * to_f32(vrow[out_row(r, lane)]);
+          for (int q4 = 0; q4 < 4; ++q4) {
+            float vx[4];
+            load4f(vrow + 8 * q4, vx);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) sacc += y[4 * q4 + e] * vx[e];
+          }
           part[tn] += sacc;
         }
       }
@@ -434,17 +465,9 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
           Bm = al2n * (2.f * ct + at);
         }
         // inclusive scan of the affine maps x -> Am x + Bm over lanes
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const float Ao = __shfl_up(Am, o, 64);
-          const float Bo = __shfl_up(Bm, o, 64);
-          if (lane >= o) {
-            Bm = Am * Bo + Bm;
-            Am = Am * Ao;
-          }
-        }
+        wave_scan_affine(Am, Bm);
         const float bnext = Am * binit + Bm;  // b(t+1)
-        float bt = __shfl_up(bnext, 1, 64);
+        float bt = dpp_f<0x138, 0xF>(binit, bnext);  // lane t - 1
         if (t == ustart) bt = binit;
         if (p < 0 && t == 0) bt = binit;
         const bool valid = (t < nrow) && (t >= first);
@@ -457,9 +480,7 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
         // tokens first .. tstar-1 join the newest state
         const bool joins = valid && t < tstar;
         if (joins) sIo[t] = It;
-        double sI = joins ? (double)It : 0.0;
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) sI += __shfl_xor(sI, o, 64);
+        const double sI = wave_sum_d(joins ? (double)It : 0.0);
         if (lane == 0 && tstar > first) {
           sN[mcur - 1] += tstar - first;
           sIb[mcur - 1] += sI;
@@ -478,15 +499,7 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
               bi = i;
             }
           }
-#pragma unroll
-          for (int o = 32; o > 0; o >>= 1) {
-            const double ob = __shfl_xor(best, o, 64);
-            const int oi = __shfl_xor(bi, o, 64);
-            if (ob < best || (ob == best && oi < bi)) {
-              best = ob;
-              bi = oi;
-            }
-          }
+          wave_argmin_d(best, bi);
           // no comparable density (NaN scores from non-finite inputs): the first
           // pair, as a sequential argmin that starts at index 0 would pick
           istar = (bi >= 0 && bi <= C - 2) ? bi : 0;
@@ -563,23 +576,19 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
       for (int st = 0; st < SL / 16; ++st) {
         if (16 * st + 15 < s0 || 16 * st >= nrow) continue;  // wave-uniform
         // element e of half h <-> token 16 st + 8 h + e; A = K~^T (rows of this
-        // wave's band of d_k), B = V (32 columns per tile)
-        // (padded rows: the lanes of a half read consecutive columns of one row,
-        // the two halves rows 8 apart, which fall in disjoint banks)
+        // wave's band of d_k), B = V (32 columns per tile), both read from the
+        // transposed copies, 8 consecutive tokens per 16-byte load
+        const int sb0 = 16 * st + 8 * half;
+        const FT kraw = FR::load(sKt + (32 * wv + l32) * P::TRS + sb0);
         float kt[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const int s = 16 * st + 8 * half + e;
-          kt[e] = (s >= s0 && s < nrow) ? sDe[s] * to_f32(sK[s * KRS + 32 * wv + l32]) : 0.f;
+          // (sDe is 0 past the chunk's last token)
+          kt[e] = (sb0 + e >= s0) ? sDe[sb0 + e] * (float)kraw[e] : 0.f;
         }
         FT vb[NJ];
 #pragma unroll
-        for (int nj = 0; nj < NJ; ++nj) {
-          float vx[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) vx[e] = to_f32(sV[(16 * st + 8 * half + e) * VRS + 32 * nj + l32]);
-          vb[nj] = FR::from_floats(vx);
-        }
+        for (int nj = 0; nj < NJ; ++nj) vb[nj] = FR::load(sVt + (32 * nj + l32) * P::TRS + sb0);
         const FT khi = FR::from_floats(kt);
         if constexpr (sizeof(Tin) == 2) {
           // three bf16 terms carry the float32 value of K~; each term runs over
@@ -608,7 +617,7 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
       if (a.merge_out) a.merge_out[tok0 + c0 + t] = sMout[t];
       if (a.score_out) a.score_out[tok0 + c0 + t] = sIo[t];
     }
-    Gprev = Gtok[c0 + nrow - 1];
+    Gprev = Gnext;
   }
   __syncthreads();
   const int mfin = sMisc[0];
