@@ -82,6 +82,7 @@ __device__ __forceinline__ f32x16 zero16() {
 }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));  // 16 bytes, first-class
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 // element e of a 16-byte piece of elements of type Tin
 template <typename Tin>

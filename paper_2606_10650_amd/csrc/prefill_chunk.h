@@ -22,7 +22,6 @@ struct ChunkP {
   static constexpr int KRS = DK + EPP;        // key block, row-major [32][KRS]
   static constexpr int KBUF = 32 * KRS;
   static constexpr int KROW16 = DK * E / 16;  // 16-byte pieces per key row
-  static constexpr int KPT = (32 * KROW16 + NTHR / 2 - 1) / (NTHR / 2);  // per staging thread
 };
 
 // Slice of pool object `obj` of head h for column group cg.  Element (k, c) of

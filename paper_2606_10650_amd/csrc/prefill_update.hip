@@ -9,29 +9,64 @@
 //     consumes;
 //   * the states alive after the chunk are rebuilt from the old states they
 //     absorbed (Alg. 2 merges: sums of adjacent states) plus, for states that
-//     hold tokens of the chunk, sum_s exp(G_end - G_s) k_s v_s^T over their
+//     hold tokens of the chunk, sum_s k_s (exp(G_end - G_s) v_s)^T over their
 //     consecutive token range (the update rule of Sec. 3.1 with the gated
-//     decay of every state).  K~ = exp(G_end - G_s) k_s is split into three
-//     bf16 terms so the MFMA product is exact to float32 rounding.  Each
-//     rebuilt state is stored in frame G_end: the float32 master in its cache
-//     slot, and a copy in MFMA operand order as a new pool object.  States
-//     that nothing touched keep their slot, frame and object (lazy decay).
+//     decay of every state).  The decayed values are staged in LDS as three
+//     bf16 terms whose sum is their float32 value, so the MFMA products with
+//     the raw bf16 keys are exact to float32 rounding.  The waves split the
+//     chunk's tokens into consecutive parts; each reads its keys straight from
+//     global memory several 16-token groups ahead, with no barrier inside the
+//     part.  Each rebuilt state is stored in frame G_end: the float32 master
+//     in its cache slot, and a copy in MFMA operand order as a new pool
+//     object.  States that nothing touched keep their slot, frame and object
+//     (lazy decay).
 // Slots of states merged away, and free slots, are reused by new states; the
 // per-head permutation maps chronological states to slots.
 #include "prefill_chunk.h"
 
 namespace dla {
 
+// Geometry of the update stage.  The workgroup's 8 waves form NSET sets of
+// NBAND waves; wave (set, band) owns rows 32 band .. 32 band + 31 of d_k and the
+// set-th of NSET consecutive parts of the chunk's tokens.
+template <int DK, typename Tin>
+struct UpdP {
+  using CP = ChunkP<DK, Tin>;
+  static constexpr int E = CP::E;
+  static constexpr int RL = CP::RL;
+  static constexpr int EPP = CP::EPP;
+  static constexpr int VTS = CP::VTS;
+  static constexpr int NTERM = E == 2 ? 3 : 1;   // bf16 terms that carry a float32 value
+  static constexpr int TS = NC * VTS;            // elements per term
+  static constexpr int NBAND = DK / 32;
+  static constexpr int NSET = NWAVE / NBAND;
+  static constexpr int PART = RL / NSET;         // tokens per part
+  static constexpr int KD = E == 2 ? 8 : 4;      // key groups in flight per wave
+  static constexpr int KW = E == 2 ? 4 : 8;      // 32-bit key loads per lane and group
+  static constexpr int TPW = E == 2 ? 2 : 1;     // tokens per 32-bit word of staged values
+  static constexpr int NPIECE = NC / EPP;        // 16-byte pieces of a token's 32 values
+  static constexpr int VIPT = RL / TPW * NPIECE / NTHR;  // staging items per thread
+  static constexpr size_t VBYTES = (size_t)NTERM * TS * E;
+  static_assert(RL / TPW * NPIECE == VIPT * NTHR, "staging items");
+  static_assert(PART % 16 == 0 && KD % 2 == 0, "part geometry");
+  // the staged values' region also holds the chunk's leader tables before the
+  // values are staged, and the partial sums of ranges that cross a part
+  // boundary after the last use of the values
+  static_assert(VBYTES >= (size_t)3 * RL * 4 && VBYTES >= (size_t)NWAVE * 64 * 16 * 4, "aliases");
+};
+
 template <int DK, typename Tin>
 static size_t update_smem_bytes(int C) {
-  using P = ChunkP<DK, Tin>;
-  size_t off = (size_t)NC * P::VTS * P::E;   // sVt
-  off += 2 * (size_t)P::KBUF * P::E;         // key blocks
-  off = round_up(off, 16);
-  off += (size_t)P::RL * 4 * 4;              // sDecE sDeath sLeadU sLeadD
-  off += (size_t)C * 8;                      // sF
-  off += (size_t)C * 4 * 14 + 64;            // int arrays, reduction scratch
+  using U = UpdP<DK, Tin>;
+  size_t off = round_up(U::VBYTES, 16);  // staged values (and their aliases)
+  off += (size_t)C * 8;                  // sF
+  off += (size_t)C * 4 * 13 + 64;        // int arrays, reduction scratch
   return round_up(off, 16);
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, int bytes) {
+  // raw buffer: loads at byte offsets >= bytes return zero
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
 }
 
 template <int DK, int DV, typename Tin>
@@ -39,10 +74,12 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
                                                               SegPlan plan, int seg) {
   using FR = Frag<Tin>;
   using FT = typename FR::T;
-  using P = ChunkP<DK, Tin>;
+  using U = UpdP<DK, Tin>;
   constexpr int D = DK * DV;
   constexpr int NCG = DV / NC;
-  constexpr int RL = P::RL;
+  constexpr int RL = U::RL;
+  constexpr int E = U::E;
+  constexpr int VTS = U::VTS;
   const int nh = a.desc.B * a.desc.H;
   // XCD-aware mapping: workgroups are dealt to the 8 XCDs round-robin by id, so
   // the column groups of one head get the same id modulo 8 and share an L2 for
@@ -54,7 +91,7 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
   if (h >= nh) return;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wv = tid >> 6;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int half = lane >> 5;
   const int l32 = lane & 31;
   const int C = a.desc.C;
@@ -65,18 +102,17 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
   const bool copies = plan.P_cap > 0;  // pool objects for a readout stage
 
   extern __shared__ __align__(16) char smem[];
-  Tin* sVt = reinterpret_cast<Tin*>(smem);  // [NC][VTS] values, transposed
-  Tin* kbuf = sVt + NC * P::VTS;            // 2 key blocks of KBUF elements
-  float* sDecE = reinterpret_cast<float*>(
-      smem + round_up(((size_t)NC * P::VTS + 2 * (size_t)P::KBUF) * P::E, 16));  // exp(G_end - G_s)
-  int32_t* sDeath = reinterpret_cast<int32_t*>(sDecE + RL);
+  // [NTERM][NC][VTS]: exp(G_end - G_s) v_s of the group's columns, transposed
+  // (for 16-bit inputs as three bf16 terms, largest first)
+  Tin* sV = reinterpret_cast<Tin*>(smem);
+  int32_t* sDeath = reinterpret_cast<int32_t*>(smem);  // aliases, see UpdP
   int32_t* sLeadU = sDeath + RL;  // in-chunk leaders: position in the chunk
   int32_t* sLeadD = sLeadU + RL;  //                   death token
-  double* sF = reinterpret_cast<double*>(sLeadD + RL);
+  float* xbuf = reinterpret_cast<float*>(smem);
+  double* sF = reinterpret_cast<double*>(smem + round_up(U::VBYTES, 16));
   int32_t* sPerm = reinterpret_cast<int32_t*>(sF + C);
   int32_t* sLead = sPerm + C;
-  int32_t* sDt = sLead + C;
-  int32_t* sObj = sDt + C;
+  int32_t* sObj = sLead + C;
   int32_t* eJa = sObj + C;
   int32_t* eJb = eJa + C;
   int32_t* eR0 = eJb + C;
@@ -88,6 +124,8 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
   int32_t* eObj = eChg + C;
   int32_t* eTmp = eObj + C;
   int32_t* red = eTmp + C;
+  int32_t* sDt = eTmp;  // death token of each state present (until the alive sets)
+  int32_t* eMO = eTmp;  // states rebuilt from old states only (after the pool objects)
   __shared__ int sCnt[2];
 
   InitView iv = init_at(w, h, C);
@@ -119,7 +157,7 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
   const Tin* Kin = static_cast<const Tin*>(a.k) + (size_t)h * T * DK;
   const Tin* Vin = static_cast<const Tin*>(a.v) + (size_t)h * T * DV;
   auto obj_slice = [&](int obj) -> Tin* {
-    return pool_slice<Tin>(w.pool, h, plan.P_cap, obj, cg, NCG, P::SLICE);
+    return pool_slice<Tin>(w.pool, h, plan.P_cap, obj, cg, NCG, U::CP::SLICE);
   };
 
   // copies of the states present at the segment start
@@ -140,37 +178,70 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
     }
   }
 
-  // band of d_k rows owned by this wave; the waves form NWAVE / NBAND groups
-  // and group 0 does the arithmetic
-  constexpr int NBAND = DK / 32;
-  const int ib = 32 * (wv % NBAND);
-  const bool band = wv < NBAND;
-  // decayed old states j = ja..jb (float32 masters) added to a band accumulator
+  constexpr int NBAND = U::NBAND;
+  constexpr int NSET = U::NSET;
+  const int band = wv % NBAND;
+  const int ib = 32 * band;
+  const int set = wv / NBAND;
+  // Band accesses of a float32 master go through a buffer resource based at the
+  // band's first element: lane offset (4 half d_v + l32) * 4 bytes, element r
+  // at row 8 (r / 4) + r % 4 further (the 8 (r / 4) rows in the scalar offset)
+  const int voff_lane = (4 * half * DV + l32) * 4;
+  // (slot and object numbers are wave-uniform: read them into scalars so the
+  // resources live in scalar registers)
+  auto band_rsrc = [&](int phys) __attribute__((always_inline)) {
+    phys = __builtin_amdgcn_readfirstlane(phys);
+    return buffer_rsrc(states + (size_t)phys * D + (size_t)ib * DV + cg * NC, 32 * DV * 4);
+  };
+  // decayed old states j = ja..jb (float32 masters) added to a band accumulator,
+  // two states' loads in flight at a time
   auto add_old = [&](f32x16& acc16, int ja, int jb, double Gend) __attribute__((always_inline)) {
-    for (int j = ja; j <= jb; ++j) {
-      const float* src = states + (size_t)sPerm[j] * D + cg * NC + l32;
-      // all 16 loads in flight before the first use
-      float x[16];
+    for (int j = ja; j <= jb; j += 2) {
+      const bool two = j + 1 <= jb;
+      const __amdgpu_buffer_rsrc_t r0 = band_rsrc(sPerm[j]);
+      const __amdgpu_buffer_rsrc_t r1 = band_rsrc(sPerm[two ? j + 1 : j]);
+      float x[16], y[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) x[r] = src[(size_t)(ib + out_row(r, lane)) * DV];
-      const float f = __expf((float)(Gend - sF[j]));
+      for (int r = 0; r < 16; ++r)
+        x[r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                                             r0, voff_lane + (r & 3) * DV * 4, (r >> 2) * 8 * DV * 4, 0));
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc16[r] += f * x[r];
+      for (int r = 0; r < 16; ++r)
+        y[r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                                             r1, voff_lane + (r & 3) * DV * 4, (r >> 2) * 8 * DV * 4, 0));
+      const float f0 = __expf((float)(Gend - sF[j]));
+      const float f1 = two ? __expf((float)(Gend - sF[j + 1])) : 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc16[r] += f0 * x[r];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc16[r] += f1 * y[r];
     }
   };
-  // store a band of a state: float32 master, and its copy when obj >= 0
+  // store a band of a state: float32 master, and its copy when obj >= 0 (the
+  // copy's 8-byte pieces at ((ib / 8 + g4) * 256 + l32 * 8 + 4 half) elements)
   auto store_state = [&](const f32x16& acc16, int phys, int obj) __attribute__((always_inline)) {
-    float* dst = states + (size_t)phys * D + cg * NC + l32;
+    const __amdgpu_buffer_rsrc_t rs = band_rsrc(phys);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) dst[(size_t)(ib + out_row(r, lane)) * DV] = acc16[r];
+    for (int r = 0; r < 16; ++r)
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc16[r]), rs,
+                                            voff_lane + (r & 3) * DV * 4, (r >> 2) * 8 * DV * 4, 0);
+    obj = __builtin_amdgcn_readfirstlane(obj);
     if (obj >= 0) {
-      Tin* sh = obj_slice(obj);
+      const __amdgpu_buffer_rsrc_t ro = buffer_rsrc(obj_slice(obj), U::CP::SLICE * E);
+      const int voff = (l32 * 8 + 4 * half) * E;
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
-        const int ks = (ib >> 4) + (g4 >> 1);
-        Tin* d4 = sh + ((ks * 2 + (g4 & 1)) * 32 + l32) * 8 + 4 * half;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) d4[q] = from_f32<Tin>(acc16[4 * g4 + q]);
+        const int soff = ((ib >> 3) + g4) * 256 * E;
+        if constexpr (E == 2) {
+          typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+          const bf16x4 v4 = {(__bf16)acc16[4 * g4], (__bf16)acc16[4 * g4 + 1], (__bf16)acc16[4 * g4 + 2],
+                             (__bf16)acc16[4 * g4 + 3]};
+          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v4), ro, voff, soff, 0);
+        } else {
+          const u32x4 v4 = {__float_as_uint(acc16[4 * g4]), __float_as_uint(acc16[4 * g4 + 1]),
+                            __float_as_uint(acc16[4 * g4 + 2]), __float_as_uint(acc16[4 * g4 + 3])};
+          __builtin_amdgcn_raw_buffer_store_b128(v4, ro, voff, soff, 0);
+        }
       }
     }
   };
@@ -179,30 +250,34 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
     const int c0 = c * RL;
     const int nrow = min(RL, T - c0);
     const int c1 = c0 + nrow;
-    const int nblk = (nrow + 31) >> 5;
     const double Gend = Gtok[c1 - 1];
     // copies of this chunk's rebuilt states are read by the next chunk of the
     // segment only
     const bool make_obj = copies && c + 1 < ce;
     __syncthreads();
-    for (int i = tid; i < RL; i += NTHR) {
-      sDecE[i] = (i < nrow) ? __expf((float)(Gend - Gtok[c0 + i])) : 0.f;
-      sDeath[i] = (i < nrow) ? death[c0 + i] : -1;
-    }
+    for (int i = tid; i < RL; i += NTHR) sDeath[i] = (i < nrow) ? death[c0 + i] : -1;
     for (int j = tid; j < m; j += NTHR) {
       const int ld = sLead[j];
       sDt[j] = (ld >= 0) ? death[ld] : iv.death0[ld + m0];
     }
-    // this group's value columns of the chunk, transposed (sVt[c][r])
+    // the chunk's values (this group's columns) and log-decays: loads issued
+    // now, staged in LDS once the leader tables no longer need the region.
+    // Item i covers TPW consecutive tokens and one 16-byte piece.
+    u32x4 vraw[U::VIPT][U::TPW];
+    double vg[U::VIPT][U::TPW];
     {
-      constexpr int PER_ROW16 = NC * P::E / 16;
-      for (int idx = tid; idx < RL * PER_ROW16; idx += NTHR) {
-        const int r = idx / PER_ROW16, p = idx % PER_ROW16;
-        u32x4 val = {0u, 0u, 0u, 0u};
-        if (r < nrow)
-          val = *reinterpret_cast<const u32x4*>(Vin + (size_t)(c0 + r) * DV + cg * NC + p * P::EPP);
+      const __amdgpu_buffer_rsrc_t vr = buffer_rsrc(Vin + (size_t)c0 * DV, nrow * DV * E);
 #pragma unroll
-        for (int e = 0; e < P::EPP; ++e) sVt[(p * P::EPP + e) * P::VTS + r] = piece_elem<Tin>(val, e);
+      for (int u = 0; u < U::VIPT; ++u) {
+        const int item = tid + NTHR * u;
+        const int tp = item % (RL / U::TPW), p = item / (RL / U::TPW);
+#pragma unroll
+        for (int t = 0; t < U::TPW; ++t) {
+          const int tok = U::TPW * tp + t;
+          vraw[u][t] = __builtin_amdgcn_raw_buffer_load_b128(
+              vr, (tok * DV + cg * NC + p * U::EPP) * E, 0, 0);
+          vg[u][t] = Gtok[c0 + min(tok, nrow - 1)];
+        }
       }
     }
     __syncthreads();
@@ -298,7 +373,42 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
         eChg[e] = ch_[u];
       }
     }
-    __syncthreads();
+
+    // ------------------------------------------------------ staged values
+    // exp(G_end - G_s) v_s, rounded to the input type's terms (three bf16 terms
+    // whose sum is the float32 product, so the MFMA products below are those of
+    // float32 values); tokens past the chunk end hold zero
+#pragma unroll
+    for (int u = 0; u < U::VIPT; ++u) {
+      const int item = tid + NTHR * u;
+      const int tp = item % (RL / U::TPW), p = item / (RL / U::TPW);
+      float ef[U::TPW];
+#pragma unroll
+      for (int t = 0; t < U::TPW; ++t)
+        ef[t] = (U::TPW * tp + t < nrow) ? __expf((float)(Gend - vg[u][t])) : 0.f;
+      if constexpr (E == 2) {
+        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+        uint32_t* row = reinterpret_cast<uint32_t*>(sV + (p * U::EPP) * VTS) + tp;
+#pragma unroll
+        for (int q = 0; q < U::EPP; ++q) {
+          const float x0 = ef[0] * to_f32(piece_elem<bf16_t>(vraw[u][0], q));
+          const float x1 = ef[1] * to_f32(piece_elem<bf16_t>(vraw[u][1], q));
+          const bf16x2 hi = {(__bf16)x0, (__bf16)x1};
+          const float y0 = x0 - (float)hi[0], y1 = x1 - (float)hi[1];
+          const bf16x2 mid = {(__bf16)y0, (__bf16)y1};
+          const bf16x2 lo = {(__bf16)(y0 - (float)mid[0]), (__bf16)(y1 - (float)mid[1])};
+          uint32_t* r = row + q * (VTS / 2);
+          r[0] = __builtin_bit_cast(uint32_t, hi);
+          r[U::TS / 2] = __builtin_bit_cast(uint32_t, mid);
+          r[U::TS] = __builtin_bit_cast(uint32_t, lo);
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < U::EPP; ++q)
+          sV[(p * U::EPP + q) * VTS + tp] = ef[0] * piece_elem<float>(vraw[u][0], q);
+      }
+    }
+
     // pool objects of the rebuilt states, in chronological order
     const int nchg = block_excl_count(ne, [&](int e) { return eChg[e] != 0; }, eTmp, red);
     // (next_obj + nchg <= P_cap: a segment starts with at most C objects and
@@ -306,108 +416,210 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
     for (int e = tid; e < ne; e += NTHR)
       eObj[e] = (eChg[e] && make_obj && next_obj + eTmp[e] < plan.P_cap) ? next_obj + eTmp[e] : -1;
     __syncthreads();
-
-    // ------------------------------- states changed by merges of old states only
-    // (rebuilt first: they read old slots that new states may reuse)
-    if (band) {
-      for (int e = 0; e < nAO; ++e) {
-        if (!eChg[e] || eR1[e] >= eR0[e]) continue;
-        f32x16 u16 = zero16();
-        add_old(u16, eJa[e], eJb[e], Gend);
-        store_state(u16, ePhys[e], eObj[e]);
+    // the token ranges: the newest old state's (when it takes chunk tokens),
+    // then the new leaders', tiling the chunk
+    const int rfirst = (nAO > 0 && eR1[nAO - 1] >= eR0[nAO - 1]) ? nAO - 1 : nAO;
+    const int ncont = rfirst < nAO ? 1 : 0;
+    // states changed by merges of old states only (wave 0)
+    if (wv == 0) {
+      int n = 0;
+      for (int base = 0; base < nAO; base += 64) {
+        const int e = base + lane;
+        const bool f = e < nAO && eChg[e] != 0 && eR1[e] < eR0[e];
+        const uint64_t bal = __ballot(f);
+        if (f) eMO[n + __popcll(bal & ((1ull << lane) - 1ull))] = e;
+        n += __popcll(bal);
       }
+      if (lane == 0) sCnt[1] = n;
     }
+    __syncthreads();
+    const int nMO = sCnt[1];
 
-    // ------------------------------------------------------- key-block loop
-    // keys are staged by the upper half of the workgroup (waves that never
-    // store to global memory inside the loop, so waiting for a prefetch never
-    // waits for state stores)
-    const bool kstager = tid >= NTHR / 2;
-    const int ktid = tid - NTHR / 2;
-    u32x4 kpre[P::KPT];
-    auto kload = [&](int sb) __attribute__((always_inline)) {
-#pragma unroll
-      for (int u = 0; u < P::KPT; ++u) {
-        const int pi = ktid + (NTHR / 2) * u;
-        const int r = pi / P::KROW16, pc = pi % P::KROW16;
-        const int tok = 32 * sb + r;
-        u32x4 z = {0u, 0u, 0u, 0u};
-        if (r < 32 && tok < nrow)
-          z = *reinterpret_cast<const u32x4*>(Kin + (size_t)(c0 + tok) * DK + pc * P::EPP);
-        kpre[u] = z;
+    // -------------------------------------- sums of old states (Alg. 2 merges)
+    // Item 0 is the newest old group when it takes chunk tokens: its decayed
+    // old states start the accumulator of the set that owns token 0.  The
+    // other items are the states rebuilt from old states only, stored here.
+    // Every read of an old slot completes before the barrier below, so slots
+    // of merged-away states can take new states afterwards.
+    f32x16 acc = zero16();
+    for (int i = set; i < ncont + nMO; i += NSET) {
+      const int e = i < ncont ? rfirst : eMO[i - ncont];
+      f32x16 u16 = zero16();
+      add_old(u16, eJa[e], eJb[e], Gend);
+      if (i < ncont)
+        acc = u16;
+      else
+        store_state(u16, ePhys[e], eObj[e]);
+    }
+    __syncthreads();
+
+    // ------------------------------------------------------- token ranges
+    // Each set walks the 16-token groups of its part.  The MFMA A operand is
+    // K^T (32 rows of d_k by 16 tokens, zero outside the current range), read
+    // from global memory KD groups ahead; B is the staged values.  A range
+    // that ends in the part is stored when it ends; a range that reaches past
+    // the part is finished by the set where it started, with the partial sums
+    // of the later sets.
+    const int ps = set * U::PART;
+    const int pe = min(ps + U::PART, nrow);
+    int inR = -1, outR = -1;
+    f32x16 xacc = zero16();
+    if (ps < nrow && rfirst < ne) {
+      // the range holding token ps: the last one starting at or before it
+      int cnt = 0;
+      for (int base = rfirst; base < ne; base += 64) {
+        const int e = base + lane;
+        const uint64_t bal = __ballot(e < ne && eR0[e] <= ps);
+        cnt += __popcll(bal);
+        if (bal != ~0ull) break;
       }
-    };
-    auto kstore = [&](Tin* kb) __attribute__((always_inline)) {
+      int rc = max(rfirst + cnt - 1, rfirst);
+      int r0c = __builtin_amdgcn_readfirstlane(eR0[rc]);
+      int r1c = __builtin_amdgcn_readfirstlane(eR1[rc]);
+      if (r0c < ps) inR = rc;
+
+      const __amdgpu_buffer_rsrc_t kr = buffer_rsrc(Kin + (size_t)c0 * DK, nrow * DK * E);
+      const bool odd = (l32 & 1) != 0;
+      // 16-bit keys: lane pair (2i, 2i + 1) of a half reads the 32-bit words
+      // holding rows ib + 2i, ib + 2i + 1 of tokens s0 .. s0 + 3 (even lane) and
+      // s0 + 4 .. s0 + 7 (odd lane), and the pair swaps halves; float32 keys:
+      // the lane reads its row of the 8 tokens
+      auto kload = [&](int g, uint32_t (&dst)[U::KW]) __attribute__((always_inline)) {
+        const int s0 = 16 * g + 8 * half;
+        if constexpr (E == 2) {
+          const int off = ((s0 + (odd ? 4 : 0)) * DK + ib + (l32 & ~1)) * 2;
 #pragma unroll
-      for (int u = 0; u < P::KPT; ++u) {
-        const int pi = ktid + (NTHR / 2) * u;
-        const int r = pi / P::KROW16, pc = pi % P::KROW16;
-        if (r < 32) *reinterpret_cast<u32x4*>(kb + r * P::KRS + pc * P::EPP) = kpre[u];
-      }
-    };
-    // the first range of chunk tokens: the newest old state's, unless a new
-    // leader that stays alive starts the chunk
-    int rc = (nAO > 0 && eR1[nAO - 1] >= eR0[nAO - 1]) ? nAO - 1 : nAO;
-    f32x16 uacc = zero16();
-    // nothing issued before the loop is outstanding inside it (vmcnt(0)), so the
-    // only memory operations a wave waits for there are its own
-    __builtin_amdgcn_s_waitcnt(0x0F70);
-    if (kstager) kload(0);
-    for (int sb = 0; sb < nblk; ++sb) {
-      Tin* kb = kbuf + (sb & 1) * P::KBUF;
-      if (kstager) {
-        kstore(kb);
-        if (sb + 1 < nblk) kload(sb + 1);
-      }
-      __syncthreads();
-      // the block's share of every changed state (this wave's band of d_k)
-      if (band && rc < ne) {
-        const int bs = 32 * sb, be = min(bs + 32, nrow);
-        while (true) {
-          const int r0 = max(eR0[rc], bs), r1 = min(eR1[rc], be - 1);
+          for (int u = 0; u < 4; ++u) dst[u] = __builtin_amdgcn_raw_buffer_load_b32(kr, off + u * DK * 2, 0, 0);
+        } else {
+          const int off = (s0 * DK + ib + l32) * 4;
 #pragma unroll
-          for (int g = 0; g < 2; ++g) {
-            const int gs = bs + 16 * g;
-            if (gs > r1 || gs + 15 < r0) continue;
-            // element e of half h <-> token gs + 8 h + e
-            const int s0 = gs + 8 * half;
-            const FT bv = FR::load(sVt + l32 * P::VTS + s0);
-            // A = K~^T: column ib + l32 of the block's rows s0 .. s0 + 7 (the lanes
-            // of a half read consecutive columns; the halves rows 8 apart, in
-            // disjoint banks)
-            const Tin* kc = kb + (s0 - bs) * P::KRS + ib + l32;
-            float kx[8];
+          for (int u = 0; u < 8; ++u) dst[u] = __builtin_amdgcn_raw_buffer_load_b32(kr, off + u * DK * 4, 0, 0);
+        }
+      };
+      auto kfrag = [&](const uint32_t (&r)[U::KW]) __attribute__((always_inline)) -> FT {
+        if constexpr (E == 2) {
+          const uint32_t L0 = __builtin_amdgcn_perm(r[1], r[0], 0x05040100u);  // low halves
+          const uint32_t L1 = __builtin_amdgcn_perm(r[3], r[2], 0x05040100u);
+          const uint32_t H0 = __builtin_amdgcn_perm(r[1], r[0], 0x07060302u);  // high halves
+          const uint32_t H1 = __builtin_amdgcn_perm(r[3], r[2], 0x07060302u);
+          // quad_perm [1, 0, 3, 2]: swap with the pair's other lane
+          const uint32_t R0 = (uint32_t)__builtin_amdgcn_mov_dpp((int)(odd ? L0 : H0), 0xB1, 0xF, 0xF, false);
+          const uint32_t R1 = (uint32_t)__builtin_amdgcn_mov_dpp((int)(odd ? L1 : H1), 0xB1, 0xF, 0xF, false);
+          u32x4 wq;
+          wq[0] = odd ? R0 : L0;
+          wq[1] = odd ? R1 : L1;
+          wq[2] = odd ? H0 : R0;
+          wq[3] = odd ? H1 : R1;
+          return __builtin_bit_cast(FT, wq);
+        } else {
+          FT out;
 #pragma unroll
-            for (int e8 = 0; e8 < 8; ++e8) {
-              const int s = s0 + e8;
-              kx[e8] = (s >= r0 && s <= r1) ? sDecE[s] * to_f32(kc[e8 * P::KRS]) : 0.f;
-            }
-            if constexpr (sizeof(Tin) == 4) {
-              FR::mma(uacc, FR::from_floats(kx), bv);
-            } else {
-              // three bf16 terms carry the float32 value of K~
-              float q1[8], q2[8];
-              const FT hi = FR::from_floats(kx);
+          for (int e = 0; e < 8; ++e) out[e] = __uint_as_float(r[e]);
+          return out;
+        }
+      };
+      // zero the A elements of tokens outside [r0, r1] (element e <-> token s0 + e)
+      auto kmask = [&](FT av, int s0, int r0, int r1) __attribute__((always_inline)) -> FT {
+        if constexpr (E == 2) {
+          u32x4 wq = __builtin_bit_cast(u32x4, av);
 #pragma unroll
-              for (int e8 = 0; e8 < 8; ++e8) q1[e8] = kx[e8] - (float)hi[e8];
-              const FT mid = FR::from_floats(q1);
-#pragma unroll
-              for (int e8 = 0; e8 < 8; ++e8) q2[e8] = q1[e8] - (float)mid[e8];
-              const FT lo = FR::from_floats(q2);
-              FR::mma(uacc, lo, bv);
-              FR::mma(uacc, mid, bv);
-              FR::mma(uacc, hi, bv);
-            }
+          for (int q = 0; q < 4; ++q) {
+            const int t = s0 + 2 * q;
+            const uint32_t mk = ((t >= r0 && t <= r1) ? 0x0000FFFFu : 0u) |
+                                ((t + 1 >= r0 && t + 1 <= r1) ? 0xFFFF0000u : 0u);
+            wq[q] &= mk;
           }
-          if (eR1[rc] > be - 1) break;  // the range continues in the next block
-          // the range ends here: complete the state and store it
-          if (eJa[rc] >= 0) add_old(uacc, eJa[rc], eJb[rc], Gend);
-          store_state(uacc, ePhys[rc], eObj[rc]);
-          uacc = zero16();
+          return __builtin_bit_cast(FT, wq);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (s0 + e < r0 || s0 + e > r1) av[e] = 0.f;
+          return av;
+        }
+      };
+      struct BOp {
+        FT t[U::NTERM];
+      };
+      auto bload = [&](int g, BOp& b) __attribute__((always_inline)) {
+        const Tin* p = sV + l32 * VTS + 16 * g + 8 * half;
+#pragma unroll
+        for (int q = 0; q < U::NTERM; ++q) b.t[q] = FR::load(p + q * U::TS);
+      };
+      auto mma_all = [&](const FT& av, const BOp& b) __attribute__((always_inline)) {
+#pragma unroll
+        for (int q = U::NTERM - 1; q >= 0; --q) FR::mma(acc, av, b.t[q]);  // smallest term first
+      };
+      auto group = [&](int g, const FT& av, const BOp& b) __attribute__((always_inline)) {
+        const int gs = 16 * g, ge = gs + 15;
+        const int s0 = gs + 8 * half;
+        while (true) {
+          if (r0c > gs || r1c < ge)
+            mma_all(kmask(av, s0, r0c, r1c), b);
+          else
+            mma_all(av, b);
+          if (r1c > ge) break;  // the range continues in the next group
+          // the range ends here
+          if (rc == inR)
+            xacc = acc;
+          else
+            store_state(acc, ePhys[rc], eObj[rc]);
+          acc = zero16();
           ++rc;
-          if (rc >= ne || eR0[rc] >= be) break;
+          if (rc >= ne) break;
+          r0c = __builtin_amdgcn_readfirstlane(eR0[rc]);
+          r1c = __builtin_amdgcn_readfirstlane(eR1[rc]);
+          if (r0c > ge) break;
+        }
+      };
+
+      const int g0 = ps >> 4, g1 = (pe + 15) >> 4;
+      uint32_t kw[U::KD][U::KW];
+      BOp bb[2];
+#pragma unroll
+      for (int u = 0; u < U::KD; ++u)
+        if (g0 + u < g1) kload(g0 + u, kw[u]);
+      bload(g0, bb[0]);
+      for (int gb = g0; gb < g1; gb += U::KD) {
+#pragma unroll
+        for (int u = 0; u < U::KD; ++u) {
+          const int g = gb + u;
+          if (g < g1) {
+            if (g + 1 < g1) bload(g + 1, bb[(u + 1) & 1]);
+            const FT av = kfrag(kw[u]);
+            if (g + U::KD < g1) kload(g + U::KD, kw[u]);
+            group(g, av, bb[u & 1]);
+          }
         }
       }
+      if (rc < ne && r0c < pe && r1c >= pe) {  // the range reaches past the part
+        if (rc == inR)
+          xacc = acc;
+        else
+          outR = rc;
+      }
+    }
+    __syncthreads();  // every set is done with the staged values
+    if (inR >= 0) {
+      float4* xb = reinterpret_cast<float4*>(xbuf + wv * 1024);
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4)
+        xb[r4 * 64 + lane] = make_float4(xacc[4 * r4], xacc[4 * r4 + 1], xacc[4 * r4 + 2], xacc[4 * r4 + 3]);
+    }
+    __syncthreads();
+    if (outR >= 0) {
+      const int r1o = eR1[outR];
+      for (int q = set + 1; q < NSET && q * U::PART <= r1o; ++q) {
+        const float4* xb = reinterpret_cast<const float4*>(xbuf + (q * NBAND + band) * 1024);
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          const float4 x = xb[r4 * 64 + lane];
+          acc[4 * r4] += x.x;
+          acc[4 * r4 + 1] += x.y;
+          acc[4 * r4 + 2] += x.z;
+          acc[4 * r4 + 3] += x.w;
+        }
+      }
+      store_state(acc, ePhys[outR], eObj[outR]);
     }
     __syncthreads();
 
