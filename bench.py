@@ -38,7 +38,8 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 PROFILES = os.path.join(ROOT, "profiles")
 # sources whose kernels the counter summaries describe
 KERNEL_SOURCES = {
-    "prefill_readout_kernel": ["prefill_readout.hip", "prefill.h", "mfma.h", "dla_common.h"],
+    "prefill_readout_kernel": ["prefill_readout.hip", "prefill_chunk.h", "prefill.h", "mfma.h",
+                               "dla_common.h"],
     "decode_kernel": ["decode.hip", "decode.h", "dla_common.h"],
 }
 
