@@ -27,6 +27,8 @@
 // column groups and neighbouring chunks of one head on one XCD, so the chunk's
 // queries, keys and lambda rows, and the state copies that neighbouring chunks
 // share, are read from HBM once per L2.
+#include <type_traits>
+
 #include "prefill_chunk.h"
 
 namespace dla {
@@ -39,7 +41,8 @@ struct RO : ChunkP<DK, Tin> {
   static constexpr size_t RING_BYTES = NSLOT * (size_t)B::SLICE16 * 16;
   static constexpr size_t INTER_BYTES = RING_BYTES;
   // intra phase: key ring + lambda window
-  static constexpr int KSLOT = 6;
+  static constexpr int KU = B::E == 2 ? 4 : 2;  // key blocks per barrier
+  static constexpr int KSLOT = 2 * KU;
   static constexpr size_t KRING_BYTES = (KSLOT * (size_t)B::KBUF * B::E + 15) / 16 * 16;
   __host__ __device__ static size_t region_bytes(int lw) {
     const size_t intra = KRING_BYTES + (size_t)B::RL * (lw > 0 ? lw + 1 : 0) * B::E;
@@ -385,6 +388,43 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
     if (rv[nt]) sAold[tr[nt]] = cnt[nt];
   __syncthreads();  // the state ring and the lambda blocks are no longer read
 
+  // The chunk's keys pass through a 2 KU-slot LDS ring, 32 tokens per block;
+  // every thread loads its 16-byte pieces of a block (consecutive threads,
+  // consecutive pieces of a row).
+  constexpr int KPT = (32 * P::KROW16 + RTHR - 1) / RTHR;
+  auto kload = [&](int sb, u32x4 (&kr)[KPT]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < KPT; ++u) {
+      const int pi = tid + RTHR * u;
+      const int r = pi / P::KROW16, pc = pi % P::KROW16;
+      const int tok = 32 * sb + r;
+      const u32x4 z = {0u, 0u, 0u, 0u};
+      kr[u] = (r < 32 && tok < nrow)
+                  ? *reinterpret_cast<const u32x4*>(Kin + (size_t)(c0 + tok) * DK + pc * EPP)
+                  : z;
+    }
+  };
+  auto kstore = [&](int sb, const u32x4 (&kr)[KPT]) __attribute__((always_inline)) {
+    Tin* kb = kring + (sb % P::KSLOT) * P::KBUF;
+#pragma unroll
+    for (int u = 0; u < KPT; ++u) {
+      const int pi = tid + RTHR * u;
+      const int r = pi / P::KROW16, pc = pi % P::KROW16;
+      if (r < 32) *reinterpret_cast<u32x4*>(kb + r * P::KRS + pc * EPP) = kr[u];
+    }
+  };
+  u32x4 kq[P::KU][KPT];
+  // store blocks sb0 .. sb0 + KU - 1 (those in the chunk) from kq
+  auto kput = [&](int sb0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < P::KU; ++u)
+      if (sb0 + u < nblk) kstore(sb0 + u, kq[u]);
+  };
+  // the first KU blocks are requested before the lambda window is built
+#pragma unroll
+  for (int u = 0; u < P::KU; ++u)
+    if (u < nblk) kload(u, kq[u]);
+
   // lambda window of every token: lambda[t][Aold_t - 1 + x] for x < lw, the
   // weights of the states that hold the chunk's own tokens.  Consecutive lanes
   // read consecutive entries of a row; every load is issued before the stores.
@@ -411,46 +451,60 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   }
 
   // ------------------------------------------------------- key-block loop
-  // The chunk's keys pass through a KSLOT-slot LDS ring, 32 tokens per block,
-  // four blocks ahead in registers; every thread loads its 16-byte pieces of a
-  // block (consecutive threads, consecutive pieces of a row).  Block sb + 1 is
-  // stored at iteration sb into the slot of block sb + 1 - KSLOT, whose readers
-  // all passed the barrier of iteration sb + 2 - KSLOT <= sb - 1.
-  constexpr int KPT = (32 * P::KROW16 + RTHR - 1) / RTHR;
-  u32x4 kA[KPT], kB[KPT];
-  auto kload = [&](int sb, u32x4 (&kr)[KPT]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int u = 0; u < KPT; ++u) {
-      const int pi = tid + RTHR * u;
-      const int r = pi / P::KROW16, pc = pi % P::KROW16;
-      const int tok = 32 * sb + r;
-      const u32x4 z = {0u, 0u, 0u, 0u};
-      kr[u] = (r < 32 && tok < nrow)
-                  ? *reinterpret_cast<const u32x4*>(Kin + (size_t)(c0 + tok) * DK + pc * EPP)
-                  : z;
-    }
-  };
-  auto kstore = [&](int sb, const u32x4 (&kr)[KPT]) __attribute__((always_inline)) {
-    Tin* kb = kring + (sb % P::KSLOT) * P::KBUF;
-#pragma unroll
-    for (int u = 0; u < KPT; ++u) {
-      const int pi = tid + RTHR * u;
-      const int r = pi / P::KROW16, pc = pi % P::KROW16;
-      if (r < 32) *reinterpret_cast<u32x4*>(kb + r * P::KRS + pc * EPP) = kr[u];
-    }
-  };
-  int before[NT];
+  int before[NT];  // live in-chunk leaders in the blocks before, at each tile token
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) before[nt] = 0;
-  auto block = [&](int sb) __attribute__((always_inline)) {
-    const Tin* krow = kring + (sb % P::KSLOT) * P::KBUF + l32 * P::KRS + 8 * half;
+  float gtok[NT];   // G_t - G_ref of each tile token
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
+  for (int nt = 0; nt < NT; ++nt) gtok[nt] = rv[nt] ? sGc[tr[nt]] : 0.f;
+  // Key block sb against the active tiles N0 .. N0 + NA - 1 of this wave (a
+  // uniform set: a tile is active while the block does not start after it).
+  // The key operand, the value operand, the rows' decays and the block's
+  // leaders are read once for all of them, and the tiles' MFMA chains are
+  // interleaved.
+  auto blockT = [&](auto n0_c, auto na_c, int sb) __attribute__((always_inline)) {
+    constexpr int N0 = decltype(n0_c)::value;
+    constexpr int NA = decltype(na_c)::value;
+    const Tin* krow = kring + (sb % P::KSLOT) * P::KBUF + l32 * P::KRS + 8 * half;
+    FT ka[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) ka[ks] = FR::load(krow + 16 * ks);
+    // P^T tiles: rows = the block's key tokens, columns = the tile's tokens
+    f32x16 pt[NA];
+#pragma unroll
+    for (int i = 0; i < NA; ++i) pt[i] = zero16();
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int i = 0; i < NA; ++i) FR::mma(pt[i], ka[ks], qf[N0 + i][ks]);
+    // values of the block's tokens in the permuted k order of the weights:
+    // element e of half h <-> token 16 st + 8 (e / 4) + 4 h + e % 4
+    FT va[2];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      const Tin* vp = sVt + l32 * P::VTS + 32 * sb + 16 * st + 4 * half;
+      va[st] = load_4x2<Tin>(vp, vp + 8);
+    }
+    float bf[16];  // exp(G_blockend - G_s) of each accumulator row
+#pragma unroll
+    for (int r = 0; r < 16; ++r) bf[r] = sBf[32 * sb + out_row(r, lane)];
+    const float gend = sGc[32 * sb + 31];
+    // leaders inside block sb that are live at each tile token, as bit masks
+    uint32_t word[NA];
+#pragma unroll
+    for (int i = 0; i < NA; ++i) word[i] = 0u;
+    for (int k2 = sBlk[sb]; k2 < sBlk[sb + 1]; ++k2) {
+      const int ldd = sLeadD[k2];
+      const uint32_t bit = 1u << (sLeadU[k2] & 31);
+#pragma unroll
+      for (int i = 0; i < NA; ++i)
+        if (ldd > c0 + tr[N0 + i]) word[i] |= bit;
+    }
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int nt = N0 + i;
       const int ti = tile_of<NT>(wv, nt);
-      if (sb > ti || 32 * ti >= nrow) continue;
-      __builtin_amdgcn_sched_barrier(0);
       const int trn = tr[nt];
-      const int tabs = c0 + trn;
       const int Aold = cnt[nt];
       const Tin* lrow = Lin ? Lin + (size_t)(c0 + (rv[nt] ? trn : 0)) * C : nullptr;
       const Tin* lwin = sLamW + trn * lws;
@@ -464,91 +518,85 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
         if (x >= lw) v = to_f32(lrow[min(max(Aold - 1 + x, 0), C - 1)]);
         return v;
       };
-      // P^T tile: rows = the block's key tokens, columns = the tile's tokens
-      f32x16 pt = zero16();
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) FR::mma(pt, FR::load(krow + 16 * ks), qf[nt][ks]);
-      // leaders inside block sb that are live at token t, as a bit mask
-      uint32_t word = 0u;
-      for (int k2 = sBlk[sb]; k2 < sBlk[sb + 1]; ++k2)
-        if (sLeadD[k2] > tabs) word |= 1u << (sLeadU[k2] & 31);
       // live leaders at key rows <= so = rb + 4 half of the block, with rb =
       // 8 (r / 4) + r % 4 a constant per accumulator element: ww holds the mask
       // shifted so that the count is a popcount under a constant mask
-      const uint32_t ww = half ? word : (word << 4);
+      const uint32_t ww = half ? word[i] : (word[i] << 4);
       auto upto = [&](int r) __attribute__((always_inline)) -> int {
         const int rb = 8 * (r >> 2) + (r & 3);
         return __popc(ww & (0xFFFFFFFFu >> (27 - rb)));
       };
       // lambda is uniform over the block unless a live leader starts after its
       // first row
-      const bool uni = (word & ~1u) == 0u;
-      const float lu = uni ? lam_at(before[nt] + (int)(word & 1u)) : 0.f;
+      const bool uni = (word[i] & ~1u) == 0u;
+      const float lu = uni ? lam_at(before[nt] + (int)(word[i] & 1u)) : 0.f;
       if (sb < ti) {
         // the whole block precedes the token: decay exp(G_t - G_end) per lane
         // times exp(G_end - G_s) per row (both at most 1)
-        const float f1 = rv[nt] ? __expf(sGc[trn] - sGc[32 * sb + 31]) : 0.f;
+        const float f1 = rv[nt] ? __expf(gtok[nt] - gend) : 0.f;
         if (uni) {
           const float fw = f1 * lu;
 #pragma unroll
-          for (int r = 0; r < 16; ++r) pt[r] *= fw * sBf[32 * sb + out_row(r, lane)];
+          for (int r = 0; r < 16; ++r) pt[i][r] *= fw * bf[r];
         } else {
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            pt[r] *= f1 * lam_at(before[nt] + upto(r)) * sBf[32 * sb + out_row(r, lane)];
+          for (int r = 0; r < 16; ++r) pt[i][r] *= f1 * lam_at(before[nt] + upto(r)) * bf[r];
         }
       } else {
         // the token's own block: causal mask, decay exp(G_t - G_s) per element
-        const float gt = sGc[trn];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int s = 32 * sb + out_row(r, lane);
           const float lr = uni ? lu : lam_at(before[nt] + upto(r));
-          pt[r] *= (rv[nt] && s <= trn) ? lr * __expf(gt - sGc[s]) : 0.f;
+          pt[i][r] *= (rv[nt] && s <= trn) ? lr * __expf(gtok[nt] - sGc[s]) : 0.f;
         }
       }
-      before[nt] += __popc(word);
-      // values of the block's tokens in the permuted k order of the weights:
-      // element e of half h <-> token 16 st + 8 (e / 4) + 4 h + e % 4
+      before[nt] += __popc(word[i]);
+    }
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int i = 0; i < NA; ++i) {
         float pw[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pw[e] = pt[8 * st + e];
-        const Tin* vp = sVt + l32 * P::VTS + 32 * sb + 16 * st + 4 * half;
-        FR::mma(acc[nt], load_4x2<Tin>(vp, vp + 8), FR::from_floats(pw));
+        for (int e = 0; e < 8; ++e) pw[e] = pt[i][8 * st + e];
+        FR::mma(acc[N0 + i], va[st], FR::from_floats(pw));
       }
+  };
+  // the active tiles at block sb: tile nt is active while sb <= its index and
+  // it starts inside the chunk; tiles are in increasing order
+  auto block = [&](int sb) __attribute__((always_inline)) {
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    const int t0 = tile_of<NT>(wv, 0);
+    const bool a0 = sb <= t0 && 32 * t0 < nrow;
+    if constexpr (NT == 2) {
+      const int t1 = tile_of<NT>(wv, 1);
+      const bool a1 = sb <= t1 && 32 * t1 < nrow;
+      if (a0 && a1)
+        blockT(I0{}, I2{}, sb);
+      else if (a1)
+        blockT(I1{}, I1{}, sb);
+      else if (a0)
+        blockT(I0{}, I1{}, sb);
+    } else {
+      if (a0) blockT(I0{}, I1{}, sb);
     }
   };
-  u32x4 kC[KPT], kD[KPT];
-  kload(0, kA);
-  kload(1, kB);
-  kload(2, kC);
-  kload(3, kD);
-  kstore(0, kA);
-  kload(4, kA);
-  // iteration sb stores block sb + 1 (loaded four iterations earlier) and
-  // requests block sb + 5 into the same registers
-  for (int sb = 0; sb < nblk; sb += 4) {
-    kstore(sb + 1, kB);
-    kload(sb + 5, kB);
+  // Each iteration requests the next KU blocks at its start and stores them at
+  // its end, after the arithmetic of its own KU blocks: no register buffer
+  // lives across the loop's back-edge, and the loads stay in flight over KU
+  // blocks of work.  The stores go to the slots of the previous iteration's
+  // blocks, whose readers all passed this iteration's barrier.
+  kput(0);
+  for (int sb0 = 0; sb0 < nblk; sb0 += P::KU) {
+#pragma unroll
+    for (int u = 0; u < P::KU; ++u)
+      if (sb0 + P::KU + u < nblk) kload(sb0 + P::KU + u, kq[u]);
     __syncthreads();
-    block(sb);
-    if (sb + 1 >= nblk) break;
-    kstore(sb + 2, kC);
-    kload(sb + 6, kC);
-    __syncthreads();
-    block(sb + 1);
-    if (sb + 2 >= nblk) break;
-    kstore(sb + 3, kD);
-    kload(sb + 7, kD);
-    __syncthreads();
-    block(sb + 2);
-    if (sb + 3 >= nblk) break;
-    kstore(sb + 4, kA);
-    kload(sb + 8, kA);
-    __syncthreads();
-    block(sb + 3);
+    for (int u = 0; u < P::KU && sb0 + u < nblk; ++u) block(sb0 + u);
+    kput(sb0 + P::KU);
   }
 
   // outputs
