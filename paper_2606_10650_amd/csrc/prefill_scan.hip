@@ -5,7 +5,8 @@
 // token in float64, and a copy of the cache's per-head metadata as it was
 // before the call (later stages overwrite the cache).
 //
-// Stage 2 (scan, one workgroup per head, sequential over chunks of 64 tokens).
+// Stage 2 (scan, one 8-wave workgroup per head, sequential over chunks of 64
+// tokens).
 // The decisions are sequential -- whether token t opens a state depends on the
 // newest state, which depends on every earlier decision -- but within a chunk
 // the score of token t against a newest state that started at position p has a
@@ -23,8 +24,8 @@
 // and the boundary test then hold for every token of a row at once; a ballot
 // finds the first boundary, which starts the next row.  Each boundary runs the
 // capacity schedule of Alg. 2 on the (count, score) pairs in LDS.  At the
-// chunk end the newest state (float32 MFMA accumulators, one 32-row band of
-// d_k per wave) is advanced by the chunk's tokens.  Emits b_t, merge index and
+// chunk end the newest state (float32 MFMA accumulators, 32 x 32 tiles spread
+// over the waves) is advanced by the chunk's tokens.  Emits b_t, merge index and
 // score per token, and the death token of every state leader (the token at
 // which Alg. 2 merged that state into its left neighbour), from which the
 // readout stage reconstructs the chronological index of every state at every
@@ -91,6 +92,8 @@ hipError_t launch_prefill_prep(const PrefillArgs& a, hipStream_t s) {
 // stage 2
 // ---------------------------------------------------------------------------
 constexpr int SL = 64;  // tokens per scan chunk (one per lane of a wavefront)
+constexpr int SWAVE = 8;  // waves per scan workgroup
+constexpr int STHR = 64 * SWAVE;
 
 typedef u32x4 u32x4s;
 
@@ -98,19 +101,23 @@ template <int DK, int DV, typename Tin>
 struct ScanP {
   static constexpr int E = (int)sizeof(Tin);
   static constexpr int EPP = 16 / E;                // elements per 16 bytes
-  static constexpr int K16 = SL * DK * E / 16 / 256;  // 16-byte K pieces per thread
-  static constexpr int V16 = SL * DV * E / 16 / 256;
+  static constexpr int K16 = SL * DK * E / 16 / STHR;  // 16-byte K pieces per thread
+  static constexpr int V16 = SL * DV * E / 16 / STHR;
   // LDS row strides (elements), padded by 16 bytes so that lanes reading
   // consecutive rows hit distinct banks
   static constexpr int KRS = DK + EPP;  // sK  [SL][KRS]
   static constexpr int VRS = DV + EPP;  // sV  [SL][VRS]
   static constexpr int TRS = SL + EPP;  // sKt [DK][TRS], sVt [DV][TRS] (transposed)
+  static constexpr int NTERM = E == 2 ? 3 : 1;  // bf16 terms that carry a float32 value
+  // sK, sV, sP and sVV are contiguous and dead once the tables are built; the
+  // decayed keys of the state advance (NTERM x [DK][TRS]) reuse their bytes
+  static constexpr size_t DEAD_BYTES = (size_t)SL * (KRS + VRS) * E + 2 * (size_t)SL * (SL + 1) * 4;
+  static_assert((size_t)NTERM * DK * TRS * E <= DEAD_BYTES, "decayed keys");
   static size_t smem_bytes(int C) {
-    size_t off = (size_t)SL * (KRS + VRS) * E;          // sK, sV
+    size_t off = DEAD_BYTES;                            // sK, sV, sP, sVV
     off += (size_t)(DK + DV) * TRS * E;                 // sKt, sVt
-    off += (size_t)SL * (SL + 1) * 4;                   // sP
     off += (size_t)SL * SL * 4;                         // sR
-    off += (size_t)8 * SL * 4;                          // sPart[4], sQ[4]
+    off += (size_t)2 * SWAVE * SL * 4;                  // sPart, sQ
     off += (size_t)SL * 4 * 8;                          // float rows
     off += (size_t)SL * 4 * 3 + SL * 2;                 // int rows, int8 rows
     off = round_up(off, 8);
@@ -131,13 +138,17 @@ __device__ __forceinline__ float score_f(float a, float b, float c, float D, flo
 }
 
 template <int DK, int DV, typename Tin>
-__global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, PrefillWS w) {
+__global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, PrefillWS w) {
   using FR = Frag<Tin>;
   using FT = typename FR::T;
   using P = ScanP<DK, DV, Tin>;
   constexpr int D = DK * DV;
-  constexpr int NB = DK / 32;  // 32-row bands of d_k: band b is held by wave b
+  constexpr int NB = DK / 32;  // 32-row bands of d_k
   constexpr int NJ = DV / 32;  // 32-column tiles of d_v
+  // state tiles (band b, column tile j), tile i = b + NB j: wave w holds tiles
+  // w, w + SWAVE, ... (all in band w % NB)
+  constexpr int NTILE = NB * NJ;
+  constexpr int NTW = (NTILE + SWAVE - 1) / SWAVE;
   constexpr int KSK = DK / 16, KSV = DV / 16;
   constexpr int K16 = P::K16, V16 = P::V16;
   const int h = blockIdx.x;
@@ -155,13 +166,15 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
   constexpr int KRS = P::KRS, VRS = P::VRS;
   Tin* sK = reinterpret_cast<Tin*>(smem);  // keys of the chunk, row-major
   Tin* sV = sK + SL * KRS;                 // values, row-major
-  Tin* sKt = sV + SL * VRS;                // keys, transposed [DK][TRS]
+  float* sP = reinterpret_cast<float*>(sV + SL * VRS);  // [SL][SL+1], (K K^T) tiles
+  float* sVV = sP + SL * (SL + 1);                      // [SL][SL+1], (V V^T) tiles
+  Tin* sKd = reinterpret_cast<Tin*>(smem);  // [NTERM][DK][TRS] decayed keys (alias)
+  Tin* sKt = reinterpret_cast<Tin*>(smem + P::DEAD_BYTES);  // keys, transposed [DK][TRS]
   Tin* sVt = sKt + DK * P::TRS;            // values, transposed [DV][TRS]
-  float* sP = reinterpret_cast<float*>(sVt + DV * P::TRS);  // [SL][SL+1]
-  float* sR = sP + SL * (SL + 1);                      // [SL][SL], R[p][t]
-  float* sPart = sR + SL * SL;                         // [4][SL]
-  float* sQ = sPart + 4 * SL;                          // [4][SL]
-  float* sGc = sQ + 4 * SL;    // G_t - G(chunk start), float
+  float* sR = reinterpret_cast<float*>(sVt + DV * P::TRS);  // [SL][SL], R[p][t]
+  float* sPart = sR + SL * SL;                          // [SWAVE][SL]
+  float* sQ = sPart + SWAVE * SL;                      // [SWAVE][SL]
+  float* sGc = sQ + SWAVE * SL;  // G_t - G(chunk start), float
   float* sA = sGc + SL;        // exp(sGc[t])
   float* sAl2 = sA + SL;       // alpha_t^2
   float* sDe = sAl2 + SL;      // exp(G_end - G_t)
@@ -184,7 +197,7 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
   Meta M = meta_at(a.cache + a.meta_offset + (size_t)h * a.meta_stride, C);
   InitView iv = init_at(w, h, C);
   const int m0 = min(max(*M.m, 0), C);
-  for (int j = tid; j < C; j += 256) {
+  for (int j = tid; j < C; j += STHR) {
     sIb[j] = M.ibar[j];
     sN[j] = M.n[j];
     sLead[j] = j - m0;
@@ -192,34 +205,42 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
   if (tid == 0) sMisc[0] = m0;
 
   // newest state at the start of the call, true (decayed) values, as MFMA
-  // accumulators: wave b < NB holds rows 32b.. of d_k, all d_v columns
-  f32x16 S[NJ];
+  // accumulators: S[k] is the wave's tile wv + SWAVE k (rows 32 band.. of d_k,
+  // columns 32 tj(k)..)
+  const int band = wv % NB;
+  auto tj = [&](int k) { return (wv + SWAVE * k) / NB; };
+  auto tok = [&](int k) { return wv + SWAVE * k < NTILE; };
+  f32x16 S[NTW];
 #pragma unroll
-  for (int nj = 0; nj < NJ; ++nj) S[nj] = zero16();
+  for (int k = 0; k < NTW; ++k) S[k] = zero16();
   const double G0 = *M.G;
-  if (m0 > 0 && wv < NB) {
+  if (m0 > 0) {
     const float* src = reinterpret_cast<const float*>(a.cache + a.states_offset) +
                        ((size_t)h * C + min(max(M.perm[m0 - 1], 0), C - 1)) * D;
     const float f = (float)exp(G0 - M.F[m0 - 1]);
 #pragma unroll
-    for (int nj = 0; nj < NJ; ++nj)
+    for (int k = 0; k < NTW; ++k)
+      if (tok(k)) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        S[nj][r] = f * src[(size_t)(32 * wv + out_row(r, lane)) * DV + 32 * nj + l32];
+        for (int r = 0; r < 16; ++r)
+          S[k][r] = f * src[(size_t)(32 * band + out_row(r, lane)) * DV + 32 * tj(k) + l32];
+      }
   }
   auto state_norm2 = [&]() -> float {  // |S|^2 over the block
     float x = 0.f;
-    if (wv < NB) {
 #pragma unroll
-      for (int nj = 0; nj < NJ; ++nj)
+    for (int k = 0; k < NTW; ++k)
+      if (tok(k)) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) x += S[nj][r] * S[nj][r];
-    }
+        for (int r = 0; r < 16; ++r) x += S[k][r] * S[k][r];
+      }
     x = wave_sum(x);
     __syncthreads();
     if (lane == 0) sRed[wv] = x;
     __syncthreads();
-    const float b = (sRed[0] + sRed[1]) + (sRed[2] + sRed[3]);
+    float b = 0.f;
+#pragma unroll
+    for (int i = 0; i < SWAVE; ++i) b += sRed[i];
     __syncthreads();
     return b;
   };
@@ -232,7 +253,7 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
   constexpr int KROW16 = DK * (int)sizeof(Tin) / 16;  // 16-byte pieces per key row
   constexpr int VROW16 = DV * (int)sizeof(Tin) / 16;
   // Next-chunk registers: lane tid % SL holds token row tid % SL, pieces
-  // tid / SL + 4 u of its key and value rows (so the transposed copies are
+  // tid / SL + SWAVE u of its key and value rows (so the transposed copies are
   // written with consecutive lanes on consecutive tokens), and threads tid < SL
   // hold the token's cumulative log-decay and overrides.
   u32x4s pk[K16], pv[V16];
@@ -242,13 +263,13 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
     const int nr = min(SL, T - c0n);
 #pragma unroll
     for (int u = 0; u < K16; ++u) {
-      const int pi = tid + 256 * u;
+      const int pi = tid + STHR * u;
       const int r = min(pi % SL, nr - 1);
       pk[u] = reinterpret_cast<const u32x4s*>(Kin + (size_t)(c0n + r) * DK)[pi / SL];
     }
 #pragma unroll
     for (int u = 0; u < V16; ++u) {
-      const int pi = tid + 256 * u;
+      const int pi = tid + STHR * u;
       const int r = min(pi % SL, nr - 1);
       pv[u] = reinterpret_cast<const u32x4s*>(Vin + (size_t)(c0n + r) * DV)[pi / SL];
     }
@@ -268,7 +289,7 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
     // ------------------------------------------------ stage the chunk
 #pragma unroll
     for (int u = 0; u < K16; ++u) {
-      const int pi = tid + 256 * u;
+      const int pi = tid + STHR * u;
       const int r = pi % SL, pc = pi / SL;
       const u32x4s z = {0u, 0u, 0u, 0u};
       const u32x4s val = (r < nrow) ? pk[u] : z;
@@ -278,7 +299,7 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
     }
 #pragma unroll
     for (int u = 0; u < V16; ++u) {
-      const int pi = tid + 256 * u;
+      const int pi = tid + STHR * u;
       const int r = pi % SL, pc = pi / SL;
       const u32x4s z = {0u, 0u, 0u, 0u};
       const u32x4s val = (r < nrow) ? pv[u] : z;
@@ -313,27 +334,35 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
 
     // ------------------------------------------------ Gram products and the carry term
     {
-      // P tile (tr, tc) = (K K^T) (.) (V V^T)
-      const int tr = wv >> 1, tcl = wv & 1;
-      f32x16 kk = zero16(), vv = zero16();
-      const Tin* ka = sK + (32 * tr + l32) * KRS;
-      const Tin* kb = sK + (32 * tcl + l32) * KRS;
+      // tile (tr, tc) of K K^T (waves 0..3, into sP) or of V V^T (waves 4..7,
+      // into sVV); the product P = (K K^T) (.) (V V^T) is formed where it is read
+      const int tq = wv & 3;
+      const int tr = tq >> 1, tcl = tq & 1;
+      f32x16 g = zero16();
+      if (wv < 4) {
+        const Tin* ka = sK + (32 * tr + l32) * KRS;
+        const Tin* kb = sK + (32 * tcl + l32) * KRS;
 #pragma unroll
-      for (int ks = 0; ks < KSK; ++ks)
-        FR::mma(kk, FR::load(ka + 16 * ks + 8 * half), FR::load(kb + 16 * ks + 8 * half));
-      const Tin* va = sV + (32 * tr + l32) * VRS;
-      const Tin* vb = sV + (32 * tcl + l32) * VRS;
+        for (int ks = 0; ks < KSK; ++ks)
+          FR::mma(g, FR::load(ka + 16 * ks + 8 * half), FR::load(kb + 16 * ks + 8 * half));
+      } else {
+        const Tin* va = sV + (32 * tr + l32) * VRS;
+        const Tin* vb = sV + (32 * tcl + l32) * VRS;
 #pragma unroll
-      for (int ks = 0; ks < KSV; ++ks)
-        FR::mma(vv, FR::load(va + 16 * ks + 8 * half), FR::load(vb + 16 * ks + 8 * half));
+        for (int ks = 0; ks < KSV; ++ks)
+          FR::mma(g, FR::load(va + 16 * ks + 8 * half), FR::load(vb + 16 * ks + 8 * half));
+      }
+      float* dst = wv < 4 ? sP : sVV;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sP[(32 * tr + out_row(r, lane)) * (SL + 1) + 32 * tcl + l32] = kk[r] * vv[r];
+      for (int r = 0; r < 16; ++r) dst[(32 * tr + out_row(r, lane)) * (SL + 1) + 32 * tcl + l32] = g[r];
     }
-    if (wv < NB) {
-      // partial over this wave's band of d_k: sum_i sum_j k_t[i] S0[i][j] v_t[j]
+    {
+      // partial over this wave's state tiles: sum_i sum_j k_t[i] S0[i][j] v_t[j]
       float part[2] = {0.f, 0.f};
 #pragma unroll
-      for (int nj = 0; nj < NJ; ++nj) {
+      for (int k = 0; k < NTW; ++k) {
+        if (!tok(k)) continue;
+        const int nj = tj(k);
         // A = S0^T (rows j, K = i) straight from the accumulator layout, in three
         // bf16 terms; B = K^T with the matching permutation of i
         FT ah[2], am[2], al[2];
@@ -341,7 +370,7 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
         for (int st = 0; st < 2; ++st) {
           float x[8], r1[8], r2[8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) x[e] = S[nj][8 * st + e];
+          for (int e = 0; e < 8; ++e) x[e] = S[k][8 * st + e];
           ah[st] = FR::from_floats(x);
           if constexpr (sizeof(Tin) == 2) {
 #pragma unroll
@@ -355,7 +384,7 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
 #pragma unroll
         for (int tn = 0; tn < 2; ++tn) {
           f32x16 y = zero16();
-          const Tin* krow = sK + (32 * tn + l32) * KRS + 32 * wv + 4 * half;
+          const Tin* krow = sK + (32 * tn + l32) * KRS + 32 * band + 4 * half;
 #pragma unroll
           for (int st = 0; st < 2; ++st) {
             // k index 16 st + 8 (e / 4) + 4 h + e % 4 of the band, as in the
@@ -392,20 +421,21 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
     if (tid < SL) {
       float c = 0.f;
 #pragma unroll
-      for (int b = 0; b < NB; ++b) c += sPart[b * SL + tid];
+      for (int b = 0; b < SWAVE; ++b) c += sPart[b * SL + tid];
       sc0[tid] = c;
-      sa[tid] = sP[tid * (SL + 1) + tid];
+      sa[tid] = sP[tid * (SL + 1) + tid] * sVV[tid * (SL + 1) + tid];
     }
     {
-      // wave q: partial suffix sums over s in [16q, 16q+16) for row t = lane
+      // wave q: partial suffix sums over s in [QS q, QS q + QS) for row t = lane
+      constexpr int QS = SL / SWAVE;
       const int t = lane;
       const int q = wv;
       float part = 0.f;
       const float gt = sGc[t];
 #pragma unroll
-      for (int i = 15; i >= 0; --i) {
-        const int s = 16 * q + i;
-        if (s < t) part += __expf(gt - sGc[s]) * sP[t * (SL + 1) + s];
+      for (int i = QS - 1; i >= 0; --i) {
+        const int s = QS * q + i;
+        if (s < t) part += __expf(gt - sGc[s]) * (sP[t * (SL + 1) + s] * sVV[t * (SL + 1) + s]);
         sR[s * SL + t] = (s < t) ? part : 0.f;
       }
       sQ[q * SL + t] = part;
@@ -414,17 +444,46 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
     {
       const int t = lane;
       const int q = wv;
+      constexpr int QS = SL / SWAVE;
       float tail = 0.f;
-      for (int q2 = q + 1; q2 < 4; ++q2) tail += sQ[q2 * SL + t];
+      for (int q2 = q + 1; q2 < SWAVE; ++q2) tail += sQ[q2 * SL + t];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int s = 16 * q + i;
+      for (int i = 0; i < QS; ++i) {
+        const int s = QS * q + i;
         if (s < t) sR[s * SL + t] += tail;
       }
     }
     __syncthreads();
 
     // ------------------------------------------------ decisions (wave 0)
+    // Meanwhile the waves on the other SIMDs (wave 4 shares wave 0's) stage the
+    // chunk's decayed keys exp(G_end - G_s) k_s for the state advance, split
+    // into NTERM terms of the input type, transposed: item (i, g) covers row i of
+    // d_k and tokens 8 g .. 8 g + 7 (zero past the chunk end, where sDe = 0).
+    if (wv != 0 && wv != 4) {
+      constexpr int NITEM = DK * (SL / 8);
+      const int hw = wv < 4 ? wv - 1 : wv - 2;  // 0 .. 5
+      for (int it = hw * 64 + lane; it < NITEM; it += 6 * 64) {
+        const int i = it / (SL / 8), g = it % (SL / 8);
+        const FT kraw = FR::load(sKt + i * P::TRS + 8 * g);
+        float x[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = sDe[8 * g + e] * (float)kraw[e];
+        Tin* dst = sKd + i * P::TRS + 8 * g;
+        const FT khi = FR::from_floats(x);
+        *reinterpret_cast<FT*>(dst) = khi;
+        if constexpr (sizeof(Tin) == 2) {
+          float r1[8], r2[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) r1[e] = x[e] - (float)khi[e];
+          const FT kmi = FR::from_floats(r1);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) r2[e] = r1[e] - (float)kmi[e];
+          *reinterpret_cast<FT*>(dst + DK * P::TRS) = kmi;
+          *reinterpret_cast<FT*>(dst + 2 * DK * P::TRS) = FR::from_floats(r2);
+        }
+      }
+    }
     if (wv == 0) {
       const int t = lane;
       const float at = sa[t];
@@ -565,48 +624,41 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
 
     // ------------------------------------------------ advance the newest state
     const int plast = sMisc[1];
-    if (wv < NB) {
+    {
       const float sc = (plast < 0) ? sA[nrow - 1] : 0.f;
 #pragma unroll
-      for (int nj = 0; nj < NJ; ++nj)
+      for (int k = 0; k < NTW; ++k)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) S[nj][r] *= sc;
+        for (int r = 0; r < 16; ++r) S[k][r] *= sc;
       const int s0 = (plast < 0) ? 0 : plast;
 #pragma unroll
       for (int st = 0; st < SL / 16; ++st) {
         if (16 * st + 15 < s0 || 16 * st >= nrow) continue;  // wave-uniform
         // element e of half h <-> token 16 st + 8 h + e; A = K~^T (rows of this
-        // wave's band of d_k), B = V (32 columns per tile), both read from the
-        // transposed copies, 8 consecutive tokens per 16-byte load
+        // wave's band of d_k, the staged terms), B = V (32 columns per tile),
+        // with the tokens before s0 masked out of V
         const int sb0 = 16 * st + 8 * half;
-        const FT kraw = FR::load(sKt + (32 * wv + l32) * P::TRS + sb0);
-        float kt[8];
+        FT ka[P::NTERM];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          // (sDe is 0 past the chunk's last token)
-          kt[e] = (sb0 + e >= s0) ? sDe[sb0 + e] * (float)kraw[e] : 0.f;
+        for (int q = 0; q < P::NTERM; ++q) ka[q] = FR::load(sKd + (q * DK + 32 * band + l32) * P::TRS + sb0);
+        const bool part = 16 * st < s0;  // wave-uniform
+        FT vb[NTW];
+#pragma unroll
+        for (int k = 0; k < NTW; ++k) {
+          vb[k] = tok(k) ? FR::load(sVt + (32 * tj(k) + l32) * P::TRS + sb0) : FR::zero();
+          if (part) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (sb0 + e < s0) vb[k][e] = FR::zero()[0];
+          }
         }
-        FT vb[NJ];
+        // smallest term first; each term runs over the column tiles before the
+        // next, so no MFMA waits on its predecessor
 #pragma unroll
-        for (int nj = 0; nj < NJ; ++nj) vb[nj] = FR::load(sVt + (32 * nj + l32) * P::TRS + sb0);
-        const FT khi = FR::from_floats(kt);
-        if constexpr (sizeof(Tin) == 2) {
-          // three bf16 terms carry the float32 value of K~; each term runs over
-          // all column tiles before the next, so no MFMA waits on its predecessor
-          float r1[8], r2[8];
+        for (int q = P::NTERM - 1; q >= 0; --q)
 #pragma unroll
-          for (int e = 0; e < 8; ++e) r1[e] = kt[e] - (float)khi[e];
-          const FT kmi = FR::from_floats(r1);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) r2[e] = r1[e] - (float)kmi[e];
-          const FT klo = FR::from_floats(r2);
-#pragma unroll
-          for (int nj = 0; nj < NJ; ++nj) FR::mma(S[nj], klo, vb[nj]);
-#pragma unroll
-          for (int nj = 0; nj < NJ; ++nj) FR::mma(S[nj], kmi, vb[nj]);
-        }
-#pragma unroll
-        for (int nj = 0; nj < NJ; ++nj) FR::mma(S[nj], khi, vb[nj]);
+          for (int k = 0; k < NTW; ++k)
+            if (tok(k)) FR::mma(S[k], ka[q], vb[k]);
       }
     }
     b0 = state_norm2();  // contains barriers; also orders the exports below
@@ -621,7 +673,7 @@ __global__ __launch_bounds__(256) void prefill_scan_kernel(PrefillArgs a, Prefil
   }
   __syncthreads();
   const int mfin = sMisc[0];
-  for (int j = tid; j < mfin; j += 256) {
+  for (int j = tid; j < mfin; j += STHR) {
     M.n[j] = sN[j];
     M.ibar[j] = sIb[j];
   }
@@ -635,13 +687,13 @@ static hipError_t launch_scan_dims(const PrefillArgs& a, const PrefillWS& w, int
     const size_t shm = ScanP<DK, DV, float>::smem_bytes(a.desc.C);
     if (shm > 160 * 1024) return hipErrorInvalidValue;
     hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
-    hipLaunchKernelGGL(k, dim3(nh), dim3(256), shm, s, a, w);
+    hipLaunchKernelGGL(k, dim3(nh), dim3(STHR), shm, s, a, w);
   } else {
     auto k = prefill_scan_kernel<DK, DV, bf16_t>;
     const size_t shm = ScanP<DK, DV, bf16_t>::smem_bytes(a.desc.C);
     if (shm > 160 * 1024) return hipErrorInvalidValue;
     hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
-    hipLaunchKernelGGL(k, dim3(nh), dim3(256), shm, s, a, w);
+    hipLaunchKernelGGL(k, dim3(nh), dim3(STHR), shm, s, a, w);
   }
   return hipGetLastError();
 }
