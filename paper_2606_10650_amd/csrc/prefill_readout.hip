@@ -118,6 +118,7 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   int32_t* sDt = sObj + C + 8;
   __shared__ int sCnt[2];
   __shared__ int sBlk[RL / 32 + 1];
+  __shared__ int sWsum[RWAVE];
 
   const double* Gtok = w.Gtok + (size_t)h * T;
   const int32_t* death = w.death + (size_t)h * T;
@@ -204,6 +205,7 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   for (int u = 0; u < TPT; ++u) {
     const int t = tid + RTHR * u;
     if (t < RL) {
+      sAold[t] = 0;                     // death counts first (see below)
       sGc[t] = (float)(gi_[u] - Gref);  // G_t - G_ref
       sRf[t] = __expf((float)(gi_[u] - Gref));
       sBf[t] = __expf((float)(gb_[u] - gi_[u]));
@@ -218,6 +220,16 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
     for (int e = 0; e < EPP; ++e) sVt[(p * EPP + e) * P::VTS + r] = piece_elem<Tin>(vp_[u], e);
   }
   __syncthreads();
+  // old states alive at each token: m minus the states of the list whose death
+  // token is at or before it (a state lives while its death token is later)
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    const int j = tid + RTHR * u;
+    if (j < m) {
+      const int d = le[u].dt - c0;
+      if (d >= 0 && d < RL) atomicAdd(&sAold[d], 1);
+    }
+  }
   // compact list of the chunk's state leaders (wave 0)
   if (wv == 0) {
     int n = 0;
@@ -236,6 +248,49 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   }
   __syncthreads();
   const int nLead = sCnt[0];
+  {
+    // inclusive prefix of the death counts over the chunk's tokens
+    constexpr int TPW = (RL + RTHR - 1) / RTHR;  // tokens per thread (1)
+    static_assert(TPW == 1, "one token per thread");
+    int hv = (tid < RL) ? sAold[tid] : 0;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(hv, o, 64);
+      if (lane >= o) hv += y;
+    }
+    if (lane == 63) sWsum[wv] = hv;
+    __syncthreads();
+    int base = 0;
+    for (int w2 = 0; w2 < wv; ++w2) base += sWsum[w2];
+    if (tid < RL) sAold[tid] = m - (base + hv);
+    __syncthreads();
+  }
+  // lambda window of every token: lambda[t][Aold_t - 1 + x] for x < lw, the
+  // weights of the states that hold the chunk's own tokens.  Consecutive lanes
+  // read consecutive entries of a row; every load is issued before the stores.
+  // (The window lies past the key ring, clear of the state ring of the inter
+  // part.)
+  if (Lin && lw > 0) {
+    constexpr int WPT = RL * 32 / RTHR;
+    Tin lv[WPT];
+    const int nwin = nrow * lw;
+#pragma unroll
+    for (int u = 0; u < WPT; ++u) {
+      const int idx = tid + RTHR * u;
+      if (idx < nwin) {
+        const int t = idx / lw, x = idx - t * lw;
+        lv[u] = Lin[(size_t)(c0 + t) * C + min(max(sAold[t] - 1 + x, 0), C - 1)];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < WPT; ++u) {
+      const int idx = tid + RTHR * u;
+      if (idx < nwin) {
+        const int t = idx / lw, x = idx - t * lw;
+        sLamW[t * lws + x] = lv[u];
+      }
+    }
+  }
   // first leader of each 32-token block (the leader list is in token order)
   for (int sb = tid; sb <= RL / 32; sb += RTHR) {
     int lo = 0, hi = nLead;
@@ -381,11 +436,6 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
       for (int r = 0; r < 16; ++r) acc[NT - 1][r] += wP * f[NT - 1][r];
     }
   }
-  // old states alive at each of this wave's tokens (chronological index of
-  // the first in-chunk state at that token)
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt)
-    if (rv[nt]) sAold[tr[nt]] = cnt[nt];
   __syncthreads();  // the state ring and the lambda blocks are no longer read
 
   // The chunk's keys pass through a 2 KU-slot LDS ring, 32 tokens per block;
@@ -420,35 +470,10 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
     for (int u = 0; u < P::KU; ++u)
       if (sb0 + u < nblk) kstore(sb0 + u, kq[u]);
   };
-  // the first KU blocks are requested before the lambda window is built
+  // the first KU blocks
 #pragma unroll
   for (int u = 0; u < P::KU; ++u)
     if (u < nblk) kload(u, kq[u]);
-
-  // lambda window of every token: lambda[t][Aold_t - 1 + x] for x < lw, the
-  // weights of the states that hold the chunk's own tokens.  Consecutive lanes
-  // read consecutive entries of a row; every load is issued before the stores.
-  if (Lin && lw > 0) {
-    constexpr int WPT = RL * 32 / RTHR;
-    Tin lv[WPT];
-    const int nwin = nrow * lw;
-#pragma unroll
-    for (int u = 0; u < WPT; ++u) {
-      const int idx = tid + RTHR * u;
-      if (idx < nwin) {
-        const int t = idx / lw, x = idx - t * lw;
-        lv[u] = Lin[(size_t)(c0 + t) * C + min(max(sAold[t] - 1 + x, 0), C - 1)];
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < WPT; ++u) {
-      const int idx = tid + RTHR * u;
-      if (idx < nwin) {
-        const int t = idx / lw, x = idx - t * lw;
-        sLamW[t * lws + x] = lv[u];
-      }
-    }
-  }
 
   // ------------------------------------------------------- key-block loop
   int before[NT];  // live in-chunk leaders in the blocks before, at each tile token
