@@ -116,8 +116,8 @@ struct ScanP {
   static size_t smem_bytes(int C) {
     size_t off = DEAD_BYTES;                            // sK, sV, sP, sVV
     off += (size_t)(DK + DV) * TRS * E;                 // sKt, sVt
-    off += (size_t)SL * SL * 4;                         // sR
-    off += (size_t)2 * SWAVE * SL * 4;                  // sPart, sQ
+    off += (size_t)SL * (SL + 1) * 4;                   // sR
+    off += (size_t)SWAVE * SL * 4;                      // sPart
     off += (size_t)SL * 4 * 8;                          // float rows
     off += (size_t)SL * 4 * 3 + SL * 2;                 // int rows, int8 rows
     off = round_up(off, 8);
@@ -171,10 +171,9 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
   Tin* sKd = reinterpret_cast<Tin*>(smem);  // [NTERM][DK][TRS] decayed keys (alias)
   Tin* sKt = reinterpret_cast<Tin*>(smem + P::DEAD_BYTES);  // keys, transposed [DK][TRS]
   Tin* sVt = sKt + DK * P::TRS;            // values, transposed [DV][TRS]
-  float* sR = reinterpret_cast<float*>(sVt + DV * P::TRS);  // [SL][SL], R[p][t]
-  float* sPart = sR + SL * SL;                          // [SWAVE][SL]
-  float* sQ = sPart + SWAVE * SL;                      // [SWAVE][SL]
-  float* sGc = sQ + SWAVE * SL;  // G_t - G(chunk start), float
+  float* sR = reinterpret_cast<float*>(sVt + DV * P::TRS);  // [SL][SL+1], R[p][t] at [t][p]
+  float* sPart = sR + SL * (SL + 1);                    // [SWAVE][SL]
+  float* sGc = sPart + SWAVE * SL;  // G_t - G(chunk start), float
   float* sA = sGc + SL;        // exp(sGc[t])
   float* sAl2 = sA + SL;       // alpha_t^2
   float* sDe = sAl2 + SL;      // exp(G_end - G_t)
@@ -426,31 +425,21 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
       sa[tid] = sP[tid * (SL + 1) + tid] * sVV[tid * (SL + 1) + tid];
     }
     {
-      // wave q: partial suffix sums over s in [QS q, QS q + QS) for row t = lane
-      constexpr int QS = SL / SWAVE;
-      const int t = lane;
-      const int q = wv;
-      float part = 0.f;
-      const float gt = sGc[t];
+      // row t of R: lane l holds s = SL - 1 - l, so the suffix sum over s is a
+      // prefix sum over the lanes (DPP ladder); wave q takes rows t = q, q +
+      // SWAVE, ...  R[p][t] is stored at sR[t (SL + 1) + p].
+      const int s = SL - 1 - lane;
+      const float gs = sGc[s];
 #pragma unroll
-      for (int i = QS - 1; i >= 0; --i) {
-        const int s = QS * q + i;
-        if (s < t) part += __expf(gt - sGc[s]) * (sP[t * (SL + 1) + s] * sVV[t * (SL + 1) + s]);
-        sR[s * SL + t] = (s < t) ? part : 0.f;
-      }
-      sQ[q * SL + t] = part;
-    }
-    __syncthreads();
-    {
-      const int t = lane;
-      const int q = wv;
-      constexpr int QS = SL / SWAVE;
-      float tail = 0.f;
-      for (int q2 = q + 1; q2 < SWAVE; ++q2) tail += sQ[q2 * SL + t];
-#pragma unroll
-      for (int i = 0; i < QS; ++i) {
-        const int s = QS * q + i;
-        if (s < t) sR[s * SL + t] += tail;
+      for (int t = wv; t < SL; t += SWAVE) {
+        float x = (s < t) ? __expf(sGc[t] - gs) * (sP[t * (SL + 1) + s] * sVV[t * (SL + 1) + s]) : 0.f;
+        x += dpp_f<0x111, 0xF>(0.f, x);
+        x += dpp_f<0x112, 0xF>(0.f, x);
+        x += dpp_f<0x114, 0xF>(0.f, x);
+        x += dpp_f<0x118, 0xF>(0.f, x);
+        x += dpp_f<0x142, 0xA>(0.f, x);
+        x += dpp_f<0x143, 0xC>(0.f, x);
+        sR[t * (SL + 1) + s] = x;
       }
     }
     __syncthreads();
@@ -512,9 +501,9 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
         const int first = p + 1;  // first token scored against this state
         float ct;
         if (p < 0)
-          ct = At * c0t + sR[t];  // R[0][t]
+          ct = At * c0t + sR[t * (SL + 1)];  // R[0][t]
         else
-          ct = (t > p) ? sR[p * SL + t] : 0.f;
+          ct = (t > p) ? sR[t * (SL + 1) + p] : 0.f;
         // |S|^2 before token t: b(t+1) = alpha_{t+1}^2 (b(t) + 2 c(t) + a_t), b(first) = binit
         const float binit = (p < 0) ? sA[0] * sA[0] * b0 : 0.f;
         const int ustart = (p < 0) ? 0 : p;
