@@ -271,6 +271,8 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   // (The window lies past the key ring, clear of the state ring of the inter
   // part.)
   if (Lin && lw > 0) {
+    // (lw is a power of two)
+    const int lwl = __builtin_ctz((unsigned)lw);
     constexpr int WPT = RL * 32 / RTHR;
     Tin lv[WPT];
     const int nwin = nrow * lw;
@@ -278,7 +280,7 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
     for (int u = 0; u < WPT; ++u) {
       const int idx = tid + RTHR * u;
       if (idx < nwin) {
-        const int t = idx / lw, x = idx - t * lw;
+        const int t = idx >> lwl, x = idx & (lw - 1);
         lv[u] = Lin[(size_t)(c0 + t) * C + min(max(sAold[t] - 1 + x, 0), C - 1)];
       }
     }
@@ -286,7 +288,7 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
     for (int u = 0; u < WPT; ++u) {
       const int idx = tid + RTHR * u;
       if (idx < nwin) {
-        const int t = idx / lw, x = idx - t * lw;
+        const int t = idx >> lwl, x = idx & (lw - 1);
         sLamW[t * lws + x] = lv[u];
       }
     }
