@@ -5,6 +5,7 @@ relative, final cache states within 1e-4, token counts exact."""
 import numpy as np
 import pytest
 
+from oracle import oracle_forward
 from tests import harness as H
 from paper_2606_10650_amd.workloads import WORKLOADS, make_inputs, make_decode_tokens
 
@@ -237,3 +238,57 @@ def test_skip_readout_builds_the_same_cache():
     torch.cuda.synchronize()
     H.assert_decisions(b.cpu().numpy().reshape(2, -1), mi.cpu().numpy().reshape(2, -1), ref, "skip")
     H.assert_cache(dla.cache_export(cache), ref["cache"], 1e-4, what="skip")
+
+
+def test_prefill_full_size_sampled_heads():
+    """The 16k-token workload at its full size (B=4, H=16, T=16384, C=128, bf16),
+    in the launch configuration the benchmark times.  Three heads are checked
+    against the oracle: every decision (near ties pinned), the outputs of two
+    64-token windows (the oracle continues from its own cache up to each
+    window) and the final cache."""
+    torch = _torch()
+    dla = _dla()
+    w = WORKLOADS["cfg3"]
+    x = make_inputs(w)
+    nh = w.B * w.H
+    heads = [0, 23, nh - 1]
+    xs = {key: x[key][heads] for key in ("q", "k", "v", "lam", "g")}
+    dec = H.run_oracle(w, {key: xs[key] for key in ("k", "v", "g")}, full=False)
+    bo_s, mo_s, nb, nm = H.near_tie_overrides(dec)
+    bo = np.full((nh, w.T), -1, np.int8)
+    mo = np.full((nh, w.T), -1, np.int32)
+    bo[heads], mo[heads] = bo_s, mo_s
+    _report("prefill-full", case=w.label, near_b=nb, near_m=nm,
+            boundaries=int(dec["b"].sum()), merges=int((dec["merge"] >= 0).sum()))
+    q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+    shp = (w.B, w.H, w.T)
+    out, b, mi, _ = dla.prefill(cache, q, k, v, g, lam, tau=w.tau,
+                                boundary_override=torch.from_numpy(bo).reshape(shp).cuda(),
+                                merge_override=torch.from_numpy(mo).reshape(shp).cuda())
+    torch.cuda.synchronize()
+    H.assert_decisions(b.cpu().numpy().reshape(nh, w.T)[heads], mi.cpu().numpy().reshape(nh, w.T)[heads],
+                       dec, w.label)
+    og = out.float().cpu().numpy().reshape(nh, w.T, w.dv)[heads]
+    # oracle in pieces: no outputs outside the two windows
+    from oracle import OracleCache
+    xf = H.f64(xs, w)
+    oc = OracleCache.empty(len(heads), w.C, w.dk, w.dv)
+    windows = [(8192, 8256), (w.T - 64, w.T)]
+    t0 = 0
+    for (a, e) in windows + [(w.T, w.T)]:
+        for (s0, s1, want) in ((t0, a, False), (a, e, True)):
+            if s1 <= s0:
+                continue
+            sl = slice(s0, s1)
+            r = oracle_forward(xf["k"][:, sl], xf["v"][:, sl], xf["g"][:, sl], w.C, w.tau,
+                               q=xf["q"][:, sl], lam=xf["lam"][:, sl], want_out=want, cache=oc,
+                               b_override=np.ascontiguousarray(bo_s[:, sl]),
+                               m_override=np.ascontiguousarray(mo_s[:, sl]))
+            if want:
+                H.assert_outputs(og[:, sl], r["out"], H.TOL[w.dtype], f"{w.label} tokens {s0}..{s1}")
+        t0 = e
+    exp = dla.cache_export(cache, heads=heads)
+    H.assert_cache(exp, oc, 1e-4, heads=range(len(heads)), what=w.label)
+    assert (exp["tokens"] == w.T).all()
+    _report("prefill-full-ok", case=w.label, heads=heads)
