@@ -292,3 +292,70 @@ def test_prefill_full_size_sampled_heads():
     H.assert_cache(exp, oc, 1e-4, heads=range(len(heads)), what=w.label)
     assert (exp["tokens"] == w.T).all()
     _report("prefill-full-ok", case=w.label, heads=heads)
+
+
+def test_decode_full_size_sampled_heads():
+    """The decode workload at its full size (64 x 32 heads, C=128, d=128): a
+    32k-token prefix drawn on the device and absorbed without readout, then
+    decode steps, in the launch configuration the benchmark times.  Two heads
+    are checked against the oracle: every decision of the prefix and the
+    steps (near ties pinned), the steps' outputs and the final cache."""
+    torch = _torch()
+    dla = _dla()
+    from paper_2606_10650_amd.workloads import make_prefix_torch
+    from oracle import OracleCache
+    w = WORKLOADS["cfg5"]
+    nh = w.B * w.H
+    heads = [0, nh - 1]
+    steps = 4
+    _, k, v, g = make_prefix_torch(w, "cuda")
+    kh = k.reshape(nh, w.T, w.dk)[heads].float().cpu().numpy().astype(np.float64)
+    vh = v.reshape(nh, w.T, w.dv)[heads].float().cpu().numpy().astype(np.float64)
+    gh = g.reshape(nh, w.T)[heads].cpu().numpy().astype(np.float64)
+    dec = oracle_forward(kh, vh, gh, w.C, w.tau, full=False)
+    bo_s, mo_s, nb, nm = H.near_tie_overrides(dec)
+    _report("decode-full", case=w.label, near_b=nb, near_m=nm, boundaries=int(dec["b"].sum()),
+            merges=int((dec["merge"] >= 0).sum()))
+    bo = np.full((nh, w.T), -1, np.int8)
+    mo = np.full((nh, w.T), -1, np.int32)
+    bo[heads], mo[heads] = bo_s, mo_s
+    shp = (w.B, w.H, w.T)
+    cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+    dla.prefill(cache, None, k, v, g, None, tau=w.tau, skip_readout=True, want_exports=False,
+                boundary_override=torch.from_numpy(bo).reshape(shp).cuda(),
+                merge_override=torch.from_numpy(mo).reshape(shp).cuda())
+    torch.cuda.synchronize()
+    del k, v, g
+    torch.cuda.empty_cache()
+    # the oracle over the sampled heads' prefix, then the steps
+    oc = OracleCache.empty(len(heads), w.C, w.dk, w.dv)
+    oracle_forward(kh, vh, gh, w.C, w.tau, want_out=False, cache=oc, b_override=bo_s, m_override=mo_s)
+    x = make_decode_tokens(w, steps=steps)
+    xd = {key: x[key] for key in ("q", "k", "v", "lam", "g")}
+    xh = H.f64({key: xd[key].reshape(nh, steps, -1)[heads] if key != "g" else xd[key].reshape(nh, steps)[heads]
+                for key in xd}, w)
+    pre = oc.copy()
+    dstep = oracle_forward(xh["k"], xh["v"], xh["g"], w.C, w.tau, q=xh["q"], lam=xh["lam"], cache=pre)
+    sbo, smo, _, _ = H.near_tie_overrides(dstep)
+    ref = oracle_forward(xh["k"], xh["v"], xh["g"], w.C, w.tau, q=xh["q"], lam=xh["lam"], cache=oc,
+                         b_override=sbo, m_override=smo)
+    q, kk, vv, gg, lam = H.inputs_to_device(w, xd, w.B, w.H)
+    outs, bs, ms = [], [], []
+    for t in range(steps):
+        sb = np.full(nh, -1, np.int8)
+        sm = np.full(nh, -1, np.int32)
+        sb[heads], sm[heads] = sbo[:, t], smo[:, t]
+        o, b, mi, _ = dla.decode_step(cache, q[:, :, t].contiguous(), kk[:, :, t].contiguous(),
+                                      vv[:, :, t].contiguous(), gg[:, :, t].contiguous(),
+                                      lam[:, :, t].contiguous(),
+                                      boundary_override=torch.from_numpy(sb).reshape(w.B, w.H).cuda(),
+                                      merge_override=torch.from_numpy(sm).reshape(w.B, w.H).cuda())
+        outs.append(o.reshape(nh, 1, w.dv)[heads])
+        bs.append(b.reshape(nh, 1)[heads])
+        ms.append(mi.reshape(nh, 1)[heads])
+    torch.cuda.synchronize()
+    H.assert_decisions(torch.cat(bs, 1).cpu().numpy(), torch.cat(ms, 1).cpu().numpy(), ref, w.label)
+    H.assert_outputs(torch.cat(outs, 1).float().cpu().numpy(), ref["out"], H.TOL[w.dtype], w.label)
+    exp = dla.cache_export(cache, heads=heads)
+    H.assert_cache(exp, oc, 1e-4, heads=range(len(heads)), what=w.label)
+    _report("decode-full-ok", case=w.label, heads=heads)
