@@ -240,18 +240,21 @@ def test_skip_readout_builds_the_same_cache():
     H.assert_cache(dla.cache_export(cache), ref["cache"], 1e-4, what="skip")
 
 
-def test_prefill_full_size_sampled_heads():
-    """The 16k-token workload at its full size (B=4, H=16, T=16384, C=128, bf16),
-    in the launch configuration the benchmark times.  Three heads are checked
-    against the oracle: every decision (near ties pinned), the outputs of two
-    64-token windows (the oracle continues from its own cache up to each
-    window) and the final cache."""
+@pytest.mark.parametrize("name", ["cfg2", "cfg3", "cfg4"])
+def test_prefill_full_size_sampled_heads(name):
+    """A prefill workload at its full size (cfg3, the 16k-token workload, in the
+    launch configuration the benchmark times; cfg4 at 64k tokens and C=256 runs
+    as several pool segments).  Three heads are checked against the oracle:
+    every decision (near ties pinned), the outputs of two 64-token windows (the
+    oracle continues from its own cache up to each window) and the final
+    cache."""
     torch = _torch()
     dla = _dla()
-    w = WORKLOADS["cfg3"]
+    from oracle import OracleCache
+    w = WORKLOADS[name]
     x = make_inputs(w)
     nh = w.B * w.H
-    heads = [0, 23, nh - 1]
+    heads = [0, nh // 2 - 1, nh - 1]
     xs = {key: x[key][heads] for key in ("q", "k", "v", "lam", "g")}
     dec = H.run_oracle(w, {key: xs[key] for key in ("k", "v", "g")}, full=False)
     bo_s, mo_s, nb, nm = H.near_tie_overrides(dec)
@@ -261,6 +264,7 @@ def test_prefill_full_size_sampled_heads():
     _report("prefill-full", case=w.label, near_b=nb, near_m=nm,
             boundaries=int(dec["b"].sum()), merges=int((dec["merge"] >= 0).sum()))
     q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    del x
     cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
     shp = (w.B, w.H, w.T)
     out, b, mi, _ = dla.prefill(cache, q, k, v, g, lam, tau=w.tau,
@@ -270,13 +274,13 @@ def test_prefill_full_size_sampled_heads():
     H.assert_decisions(b.cpu().numpy().reshape(nh, w.T)[heads], mi.cpu().numpy().reshape(nh, w.T)[heads],
                        dec, w.label)
     og = out.float().cpu().numpy().reshape(nh, w.T, w.dv)[heads]
+    del q, k, v, g, lam, out
     # oracle in pieces: no outputs outside the two windows
-    from oracle import OracleCache
     xf = H.f64(xs, w)
     oc = OracleCache.empty(len(heads), w.C, w.dk, w.dv)
-    windows = [(8192, 8256), (w.T - 64, w.T)]
+    windows = [(w.T // 2, w.T // 2 + 64), (w.T - 64, w.T)]
     t0 = 0
-    for (a, e) in windows + [(w.T, w.T)]:
+    for (a, e) in windows:
         for (s0, s1, want) in ((t0, a, False), (a, e, True)):
             if s1 <= s0:
                 continue
