@@ -19,8 +19,8 @@
  * - Shapes come from the cache descriptor: batch B, heads H, capacity C, key
  *   and value head dimensions d_k, d_v.  Supported: d_k, d_v in {64, 128},
  *   1 <= C <= 1024, B*H >= 1.  dla_prefill returns DLA_ERR_UNSUPPORTED when a
- *   stage's per-workgroup working set would not fit in 160 KiB of LDS (float32
- *   inputs with d_k = 128 and C above about 900).
+ *   stage's per-workgroup working set would not fit in 160 KiB of LDS; every
+ *   shape of the supported set, in either input type, fits.
  * - Token tensors are row-major [B][H][T][d] (d fastest); log_gate is
  *   [B][H][T] float32 (the per-token log-decay g_t <= 0 of the base model:
  *   every state decays by exp(g_t) at token t, the caller owns g_t <= 0);

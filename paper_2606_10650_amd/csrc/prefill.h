@@ -200,7 +200,8 @@ hipError_t launch_prefill_prep(const PrefillArgs& a, hipStream_t s);
 hipError_t launch_prefill_scan(const PrefillArgs& a, hipStream_t s);
 hipError_t launch_prefill_update(const PrefillArgs& a, const SegPlan& p, int seg, hipStream_t s);
 hipError_t launch_prefill_readout(const PrefillArgs& a, const SegPlan& p, int seg, hipStream_t s);
-// whether the update and readout stages' working sets fit in LDS for this shape
+// whether the scan, update and readout stages' working sets fit in LDS for this
+// shape
 bool prefill_chunks_supported(const dla_cache_desc& d, dla_dtype in_dtype);
 
 // Stages in order, segment by segment; ev (nullable) receives an event before

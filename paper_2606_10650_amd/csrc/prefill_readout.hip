@@ -677,12 +677,13 @@ static hipError_t launch_readout_dims(const PrefillArgs& a, const SegPlan& p, in
 }
 
 bool prefill_update_supported(const dla_cache_desc& d, dla_dtype in_dtype);
+bool prefill_scan_supported(const dla_cache_desc& d, dla_dtype in_dtype);
 
 bool prefill_chunks_supported(const dla_cache_desc& d, dla_dtype in_dtype) {
   const bool f = in_dtype == DLA_F32;
   const int lw = d.d_k == 128 ? (f ? readout_window<128, float>(d.C) : readout_window<128, bf16_t>(d.C))
                               : (f ? readout_window<64, float>(d.C) : readout_window<64, bf16_t>(d.C));
-  return lw >= 0 && prefill_update_supported(d, in_dtype);
+  return lw >= 0 && prefill_update_supported(d, in_dtype) && prefill_scan_supported(d, in_dtype);
 }
 
 hipError_t launch_prefill_readout(const PrefillArgs& a, const SegPlan& p, int seg, hipStream_t s) {

@@ -30,6 +30,8 @@
 // which Alg. 2 merged that state into its left neighbour), from which the
 // readout stage reconstructs the chronological index of every state at every
 // token without a replay.
+#include <type_traits>
+
 #include "mfma.h"
 #include "prefill.h"
 
@@ -108,14 +110,18 @@ struct ScanP {
   static constexpr int KRS = DK + EPP;  // sK  [SL][KRS]
   static constexpr int VRS = DV + EPP;  // sV  [SL][VRS]
   static constexpr int TRS = SL + EPP;  // sKt [DK][TRS], sVt [DV][TRS] (transposed)
+  // transposed copies for 16-bit inputs; float32 inputs (twice the bytes) read
+  // the row-major copies element by element instead, to stay within LDS
+  static constexpr bool TRANS = E == 2;
   static constexpr int NTERM = E == 2 ? 3 : 1;  // bf16 terms that carry a float32 value
-  // sK, sV, sP and sVV are contiguous and dead once the tables are built; the
-  // decayed keys of the state advance (NTERM x [DK][TRS]) reuse their bytes
+  // sK, sV, sP and sVV are contiguous and dead once the tables are built; for
+  // 16-bit inputs the decayed keys of the state advance (NTERM x [DK][TRS])
+  // reuse their bytes (float32 inputs form them in the advance instead)
   static constexpr size_t DEAD_BYTES = (size_t)SL * (KRS + VRS) * E + 2 * (size_t)SL * (SL + 1) * 4;
   static_assert((size_t)NTERM * DK * TRS * E <= DEAD_BYTES, "decayed keys");
   static size_t smem_bytes(int C) {
     size_t off = DEAD_BYTES;                            // sK, sV, sP, sVV
-    off += (size_t)(DK + DV) * TRS * E;                 // sKt, sVt
+    off += TRANS ? (size_t)(DK + DV) * TRS * E : 0;     // sKt, sVt
     off += (size_t)SL * (SL + 1) * 4;                   // sR
     off += (size_t)SWAVE * SL * 4;                      // sPart
     off += (size_t)SL * 4 * 8;                          // float rows
@@ -171,7 +177,7 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
   Tin* sKd = reinterpret_cast<Tin*>(smem);  // [NTERM][DK][TRS] decayed keys (alias)
   Tin* sKt = reinterpret_cast<Tin*>(smem + P::DEAD_BYTES);  // keys, transposed [DK][TRS]
   Tin* sVt = sKt + DK * P::TRS;            // values, transposed [DV][TRS]
-  float* sR = reinterpret_cast<float*>(sVt + DV * P::TRS);  // [SL][SL+1], R[p][t] at [t][p]
+  float* sR = reinterpret_cast<float*>(P::TRANS ? sVt + DV * P::TRS : sKt);  // [SL][SL+1], R[p][t] at [t][p]
   float* sPart = sR + SL * (SL + 1);                    // [SWAVE][SL]
   float* sGc = sPart + SWAVE * SL;  // G_t - G(chunk start), float
   float* sA = sGc + SL;        // exp(sGc[t])
@@ -293,8 +299,9 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
       const u32x4s z = {0u, 0u, 0u, 0u};
       const u32x4s val = (r < nrow) ? pk[u] : z;
       *reinterpret_cast<u32x4s*>(sK + r * KRS + pc * P::EPP) = val;
+      if constexpr (P::TRANS)
 #pragma unroll
-      for (int e = 0; e < P::EPP; ++e) sKt[(pc * P::EPP + e) * P::TRS + r] = piece_elem<Tin>(val, e);
+        for (int e = 0; e < P::EPP; ++e) sKt[(pc * P::EPP + e) * P::TRS + r] = piece_elem<Tin>(val, e);
     }
 #pragma unroll
     for (int u = 0; u < V16; ++u) {
@@ -303,8 +310,9 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
       const u32x4s z = {0u, 0u, 0u, 0u};
       const u32x4s val = (r < nrow) ? pv[u] : z;
       *reinterpret_cast<u32x4s*>(sV + r * VRS + pc * P::EPP) = val;
+      if constexpr (P::TRANS)
 #pragma unroll
-      for (int e = 0; e < P::EPP; ++e) sVt[(pc * P::EPP + e) * P::TRS + r] = piece_elem<Tin>(val, e);
+        for (int e = 0; e < P::EPP; ++e) sVt[(pc * P::EPP + e) * P::TRS + r] = piece_elem<Tin>(val, e);
     }
     if (tid < SL) {
       // log-decay offsets from the chunk start; the last token's G is the
@@ -449,7 +457,7 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
     // chunk's decayed keys exp(G_end - G_s) k_s for the state advance, split
     // into NTERM terms of the input type, transposed: item (i, g) covers row i of
     // d_k and tokens 8 g .. 8 g + 7 (zero past the chunk end, where sDe = 0).
-    if (wv != 0 && wv != 4) {
+    if (P::TRANS && wv != 0 && wv != 4) {
       constexpr int NITEM = DK * (SL / 8);
       const int hw = wv < 4 ? wv - 1 : wv - 2;  // 0 .. 5
       for (int it = hw * 64 + lane; it < NITEM; it += 6 * 64) {
@@ -628,13 +636,27 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
         // with the tokens before s0 masked out of V
         const int sb0 = 16 * st + 8 * half;
         FT ka[P::NTERM];
+        if constexpr (P::TRANS) {
 #pragma unroll
-        for (int q = 0; q < P::NTERM; ++q) ka[q] = FR::load(sKd + (q * DK + 32 * band + l32) * P::TRS + sb0);
+          for (int q = 0; q < P::NTERM; ++q) ka[q] = FR::load(sKd + (q * DK + 32 * band + l32) * P::TRS + sb0);
+        } else {
+          // float32: one term, formed here from the row-major keys
+#pragma unroll
+          for (int e = 0; e < 8; ++e) ka[0][e] = sDe[sb0 + e] * sK[(sb0 + e) * KRS + 32 * band + l32];
+        }
         const bool part = 16 * st < s0;  // wave-uniform
         FT vb[NTW];
 #pragma unroll
         for (int k = 0; k < NTW; ++k) {
-          vb[k] = tok(k) ? FR::load(sVt + (32 * tj(k) + l32) * P::TRS + sb0) : FR::zero();
+          if constexpr (P::TRANS) {
+            vb[k] = tok(k) ? FR::load(sVt + (32 * tj(k) + l32) * P::TRS + sb0) : FR::zero();
+          } else {
+            vb[k] = FR::zero();
+            if (tok(k)) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) vb[k][e] = sV[(sb0 + e) * VRS + 32 * tj(k) + l32];
+            }
+          }
           if (part) {
 #pragma unroll
             for (int e = 0; e < 8; ++e)
@@ -666,6 +688,20 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
     M.n[j] = sN[j];
     M.ibar[j] = sIb[j];
   }
+}
+
+// whether the scan's LDS working set fits for this shape
+bool prefill_scan_supported(const dla_cache_desc& d, dla_dtype in_dtype) {
+  auto fits = [&](auto dk_c, auto dv_c) {
+    constexpr int DK = decltype(dk_c)::value, DV = decltype(dv_c)::value;
+    const size_t b = in_dtype == DLA_F32 ? ScanP<DK, DV, float>::smem_bytes(d.C)
+                                         : ScanP<DK, DV, bf16_t>::smem_bytes(d.C);
+    return b <= 160 * 1024;
+  };
+  using I64 = std::integral_constant<int, 64>;
+  using I128 = std::integral_constant<int, 128>;
+  if (d.d_k == 128) return d.d_v == 128 ? fits(I128{}, I128{}) : fits(I128{}, I64{});
+  return d.d_v == 128 ? fits(I64{}, I128{}) : fits(I64{}, I64{});
 }
 
 template <int DK, int DV>

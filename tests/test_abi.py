@@ -85,3 +85,23 @@ def test_missing_library_fails_loudly(tmp_path, monkeypatch):
     monkeypatch.setattr(dla, "_LIB_PATH", str(tmp_path / "nope.so"))
     with pytest.raises(RuntimeError, match="missing"):
         dla.lib()
+
+
+@pytest.mark.parametrize("dtype", [0, 1])  # DLA_F32, DLA_BF16
+def test_every_supported_shape_passes_the_prefill_shape_check(dtype):
+    """Every head dimension pair and capacity the header declares supported
+    gets past dla_prefill's shape checks (the stages' LDS working sets fit):
+    with no workspace the call stops at DLA_ERR_WORKSPACE, before any device
+    access."""
+    from paper_2606_10650_amd import dla
+    L = dla.lib()
+    p = dla.Params(0.5, 1e-6, 1e-6, 0)
+    fake = ctypes.c_void_p(0x1000)
+    for dk in (64, 128):
+        for dv in (64, 128):
+            for C in (1, 8, 128, 256, 512, 1000, 1024):
+                d = dla.CacheDesc(1, 2, C, dk, dv)
+                st = L.dla_prefill(ctypes.byref(d), fake, fake, fake, fake, fake, fake, 4096, dtype,
+                                   ctypes.byref(p), fake, dtype, None, None, None, None, None,
+                                   None, 0, None)
+                assert st == dla.DLA_ERR_WORKSPACE, (dk, dv, C, dtype, st)

@@ -105,6 +105,18 @@ def test_prefill_mixed_head_dims():
     _prefill_case(WORKLOADS["cfg2"].replace(B=2, H=1, T=500, C=7, dk=128, dv=64))
 
 
+def test_prefill_f32_head_dim_128():
+    # float32 inputs at d = 128 (the scan reads its row-major copies)
+    _prefill_case(WORKLOADS["cfg1"].replace(T=600, dk=128, dv=128))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_prefill_largest_capacity(dtype):
+    # C = 1024 with every token a boundary: merges start after 1024 tokens
+    w = WORKLOADS["cfg1" if dtype == "f32" else "cfg2"].replace(B=1, H=1, T=1100, dk=128, dv=128)
+    _prefill_case(w, C=1024, tau=0.0)
+
+
 def test_prefill_continuation():
     _prefill_case(WORKLOADS["cfg2"].replace(B=1, H=2, T=900, C=10), T_split=[1, 300, 301, 640])
     _prefill_case(WORKLOADS["cfg1_iid"].replace(T=200), T_split=[57, 128])
