@@ -292,6 +292,25 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
   for (int c0 = 0; c0 < T; c0 += SL) {
     const int nrow = min(SL, T - c0);
     // ------------------------------------------------ stage the chunk
+    // transposed copy of a 16-bit piece (8 columns of token r, r = lane): the
+    // lane pair (2i, 2i + 1) swaps halves, so each lane writes 32-bit words
+    // holding both tokens of the pair, 4 columns each
+    auto put_t = [&](Tin* dst, int pc, int r, const u32x4s& val) __attribute__((always_inline)) {
+      const bool odd = (r & 1) != 0;
+      const uint32_t s0 = odd ? val[0] : val[2], s1 = odd ? val[1] : val[3];
+      const uint32_t r0 = (uint32_t)__builtin_amdgcn_mov_dpp((int)s0, 0xB1, 0xF, 0xF, false);
+      const uint32_t r1 = (uint32_t)__builtin_amdgcn_mov_dpp((int)s1, 0xB1, 0xF, 0xF, false);
+      // even lane: columns 0..3, own token first; odd lane: columns 4..7, the
+      // partner's token (r - 1) first
+      const uint32_t m0 = odd ? val[2] : val[0], m1 = odd ? val[3] : val[1];
+      const uint32_t lo0 = odd ? r0 : m0, hi0 = odd ? m0 : r0;
+      const uint32_t lo1 = odd ? r1 : m1, hi1 = odd ? m1 : r1;
+      uint32_t* row = reinterpret_cast<uint32_t*>(dst + (pc * P::EPP + (odd ? 4 : 0)) * P::TRS + (r & ~1));
+      row[0] = __builtin_amdgcn_perm(hi0, lo0, 0x05040100u);
+      row[P::TRS / 2] = __builtin_amdgcn_perm(hi0, lo0, 0x07060302u);
+      row[P::TRS] = __builtin_amdgcn_perm(hi1, lo1, 0x05040100u);
+      row[3 * (P::TRS / 2)] = __builtin_amdgcn_perm(hi1, lo1, 0x07060302u);
+    };
 #pragma unroll
     for (int u = 0; u < K16; ++u) {
       const int pi = tid + STHR * u;
@@ -299,9 +318,7 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
       const u32x4s z = {0u, 0u, 0u, 0u};
       const u32x4s val = (r < nrow) ? pk[u] : z;
       *reinterpret_cast<u32x4s*>(sK + r * KRS + pc * P::EPP) = val;
-      if constexpr (P::TRANS)
-#pragma unroll
-        for (int e = 0; e < P::EPP; ++e) sKt[(pc * P::EPP + e) * P::TRS + r] = piece_elem<Tin>(val, e);
+      if constexpr (P::TRANS) put_t(sKt, pc, r, val);
     }
 #pragma unroll
     for (int u = 0; u < V16; ++u) {
@@ -310,9 +327,7 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
       const u32x4s z = {0u, 0u, 0u, 0u};
       const u32x4s val = (r < nrow) ? pv[u] : z;
       *reinterpret_cast<u32x4s*>(sV + r * VRS + pc * P::EPP) = val;
-      if constexpr (P::TRANS)
-#pragma unroll
-        for (int e = 0; e < P::EPP; ++e) sVt[(pc * P::EPP + e) * P::TRS + r] = piece_elem<Tin>(val, e);
+      if constexpr (P::TRANS) put_t(sVt, pc, r, val);
     }
     if (tid < SL) {
       // log-decay offsets from the chunk start; the last token's G is the
