@@ -28,7 +28,7 @@ def _report(tag, **kw):
     print(f"[{tag}] " + " ".join(f"{k}={v}" for k, v in kw.items()), flush=True)
 
 
-def _prefill_case(w, C=None, tau=None, T_split=None):
+def _prefill_case(w, C=None, tau=None, T_split=None, out_dtype=None):
     torch = _torch()
     dla = _dla()
     C = C or w.C
@@ -46,7 +46,7 @@ def _prefill_case(w, C=None, tau=None, T_split=None):
     mo_d = torch.from_numpy(mo).reshape(shp).cuda()
     if T_split is None:
         out, b, mi, sc = dla.prefill(cache, q, k, v, g, lam, tau=tau, boundary_override=bo_d,
-                                     merge_override=mo_d)
+                                     merge_override=mo_d, out_dtype=out_dtype)
     else:
         parts = []
         s0 = 0
@@ -65,8 +65,11 @@ def _prefill_case(w, C=None, tau=None, T_split=None):
                        w.label)
     serr = np.abs(sc.cpu().numpy().reshape(nh, -1) - ref["score"]).max()
     assert serr < H.DELTA_B / 10, f"score error {serr}"
-    rel = H.assert_outputs(out.float().cpu().numpy().reshape(nh, w.T, w.dv), ref["out"],
-                           H.TOL[w.dtype], w.label)
+    if out_dtype is not None:
+        assert out.dtype == out_dtype
+    # a bfloat16 input or output sets the tolerance
+    tol = H.TOL["bf16"] if (w.dtype == "bf16" or out.dtype == torch.bfloat16) else H.TOL["f32"]
+    rel = H.assert_outputs(out.float().cpu().numpy().reshape(nh, w.T, w.dv), ref["out"], tol, w.label)
     exp = dla.cache_export(cache)
     H.assert_cache(exp, ref["cache"], 1e-4, what=w.label)
     assert (exp["tokens"] == w.T).all()
@@ -117,6 +120,13 @@ def test_prefill_largest_capacity(dtype):
     _prefill_case(w, C=1024, tau=0.0)
 
 
+def test_prefill_mixed_output_types():
+    # bfloat16 inputs with float32 outputs, and float32 inputs with bfloat16 outputs
+    torch = _torch()
+    _prefill_case(WORKLOADS["cfg2"].replace(B=1, H=2, T=700, C=9), out_dtype=torch.float32)
+    _prefill_case(WORKLOADS["cfg1"].replace(T=400), out_dtype=torch.bfloat16)
+
+
 def test_prefill_continuation():
     _prefill_case(WORKLOADS["cfg2"].replace(B=1, H=2, T=900, C=10), T_split=[1, 300, 301, 640])
     _prefill_case(WORKLOADS["cfg1_iid"].replace(T=200), T_split=[57, 128])
@@ -157,8 +167,10 @@ def test_decode_steps_from_empty_match_oracle():
         H.assert_cache(dla.cache_export(cache), ref["cache"], 1e-4, what=w.label)
 
 
-def test_prefill_then_decode_continuation():
-    """prefill(T1) followed by decode steps equals the oracle over all tokens."""
+@pytest.mark.parametrize("out_f32", [False, True])
+def test_prefill_then_decode_continuation(out_f32):
+    """prefill(T1) followed by decode steps equals the oracle over all tokens
+    (bfloat16 inputs; outputs in bfloat16, or in float32)."""
     torch = _torch()
     dla = _dla()
     w = WORKLOADS["cfg2"].replace(B=1, H=2, T=420, C=8)
@@ -169,18 +181,20 @@ def test_prefill_then_decode_continuation():
     bo_d = torch.from_numpy(bo).reshape(1, 2, w.T).cuda()
     mo_d = torch.from_numpy(mo).reshape(1, 2, w.T).cuda()
     T1 = 389
+    od = torch.float32 if out_f32 else None
     cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
     o1, b1, m1, _ = dla.prefill(cache, q[:, :, :T1].contiguous(), k[:, :, :T1].contiguous(),
                                 v[:, :, :T1].contiguous(), g[:, :, :T1].contiguous(),
                                 lam[:, :, :T1].contiguous(), boundary_override=bo_d[:, :, :T1].contiguous(),
-                                merge_override=mo_d[:, :, :T1].contiguous())
+                                merge_override=mo_d[:, :, :T1].contiguous(), out_dtype=od)
     outs, bs, ms = [o1], [b1], [m1]
     for t in range(T1, w.T):
         o, b, mi, _ = dla.decode_step(cache, q[:, :, t].contiguous(), k[:, :, t].contiguous(),
                                       v[:, :, t].contiguous(), g[:, :, t].contiguous(),
                                       lam[:, :, t].contiguous(),
                                       boundary_override=bo_d[:, :, t].contiguous(),
-                                      merge_override=mo_d[:, :, t].contiguous())
+                                      merge_override=mo_d[:, :, t].contiguous(), out_dtype=od)
+        assert o.dtype == (od or torch.bfloat16)
         outs.append(o.unsqueeze(2))
         bs.append(b.unsqueeze(2))
         ms.append(mi.unsqueeze(2))
