@@ -15,14 +15,16 @@
 //     weight is a per-lane scalar applied to the chain's result.  States are
 //     streamed from the pool two per step through a 4-slot LDS ring, six
 //     states ahead in registers, with one barrier per step; each wave reads a
-//     state's operand from LDS once for all of its tiles.  The lambda weights
-//     are gathered two states ahead.
+//     state's operand from LDS once for all of its tiles.  The weights are
+//     computed once per (token, state), by the thread of that token, into a
+//     small LDS ring (the lambda entries are requested one step ahead), and
+//     each lane reads the weights of its tiles' tokens from there.
 //   * intra-chunk part: (Q K^T (.) M) V with M[t][s] = [s <= t] exp(G_t - G_s)
-//     lambda[t][slot_t(s)] over the chunk's own keys.  Each wave loads the key
-//     rows of a block of 32 tokens straight into MFMA operand registers, one
-//     block ahead, so this part has no barriers.  slot_t(s) is uniform over a
-//     block unless a live state leader starts inside it, so lambda is gathered
-//     once per (token, block) in the common case.
+//     lambda[t][slot_t(s)] over the chunk's own keys.  The keys pass through
+//     an LDS ring of 32-token blocks, KU blocks per barrier, requested one
+//     barrier ahead.  slot_t(s) is uniform over a block unless a live state
+//     leader starts inside it, so lambda is read once per (token, block) in the
+//     common case, from a window of each token's lambda row staged in LDS.
 // Workgroups are dealt to the 8 XCDs round-robin by id; the mapping puts the
 // column groups and neighbouring chunks of one head on one XCD, so the chunk's
 // queries, keys and lambda rows, and the state copies that neighbouring chunks
@@ -36,17 +38,20 @@ namespace dla {
 template <int DK, typename Tin>
 struct RO : ChunkP<DK, Tin> {
   using B = ChunkP<DK, Tin>;
-  // inter phase: state ring (two steps of two states)
+  // inter phase: state ring (two steps of two states), then the token weights
+  // of those states (float, [step parity][state of the step][RL])
   static constexpr int NSLOT = 4;
   static constexpr size_t RING_BYTES = NSLOT * (size_t)B::SLICE16 * 16;
-  static constexpr size_t INTER_BYTES = RING_BYTES;
-  // intra phase: key ring + lambda window
+  static constexpr size_t WRING_BYTES = 4 * (size_t)B::RL * 4;
+  static constexpr size_t INTER_BYTES = RING_BYTES + WRING_BYTES;
+  // intra phase: key ring, and the lambda window, which is written before the
+  // inter phase and so lies past both the key ring and the inter region
   static constexpr int KU = B::E == 2 ? 4 : 2;  // key blocks per barrier
   static constexpr int KSLOT = 2 * KU;
   static constexpr size_t KRING_BYTES = (KSLOT * (size_t)B::KBUF * B::E + 15) / 16 * 16;
+  static constexpr size_t WIN_OFF = KRING_BYTES > INTER_BYTES ? KRING_BYTES : INTER_BYTES;
   __host__ __device__ static size_t region_bytes(int lw) {
-    const size_t intra = KRING_BYTES + (size_t)B::RL * (lw > 0 ? lw + 1 : 0) * B::E;
-    return round_up(INTER_BYTES > intra ? INTER_BYTES : intra, 16);
+    return round_up(WIN_OFF + (size_t)B::RL * (lw > 0 ? lw + 1 : 0) * B::E, 16);
   }
   static size_t smem_bytes(int C, int lw) {
     size_t off = region_bytes(lw);
@@ -102,7 +107,8 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   u32x4* ring = reinterpret_cast<u32x4*>(smem);                   // NSLOT state slices
   // intra phase (same bytes)
   Tin* kring = reinterpret_cast<Tin*>(smem);                      // KSLOT x [32][KRS] keys
-  Tin* sLamW = reinterpret_cast<Tin*>(smem + P::KRING_BYTES);     // [RL][lw + 1] lambda
+  Tin* sLamW = reinterpret_cast<Tin*>(smem + P::WIN_OFF);         // [RL][lw + 1] lambda
+  float* sW = reinterpret_cast<float*>(smem + P::RING_BYTES);     // [2][2][RL] token weights
   const int lws = lw + 1;
   const size_t rgn = P::region_bytes(lw);
   Tin* sVt = reinterpret_cast<Tin*>(smem + rgn);                  // [NC][VTS] values
@@ -305,27 +311,30 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
 
   // ------------------------------------------------ inter-chunk readout
   // Step J handles states 2J and 2J+1: the registers loaded two steps earlier
-  // go to ring slots 2 (J & 1) and 2 (J & 1) + 1, the lambda weights of states
-  // 2J+2 and 2J+3 are read and the slices of states 2J+4 and 2J+5 requested,
-  // and after one barrier every wave reads the two operands from LDS.  Steps
-  // run in pairs over named register buffers (constant indexing); steps past
-  // the last state have sSf = 0.
-  // The weight of state j at token t is lambda[t][x], x = (live states up to
-  // j) - 1 (a state merged away at or before t is weighted as the live state
-  // that absorbed it).
-  int cnt[NT];  // live states up to the last state whose weight was read
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) cnt[nt] = 0;
+  // go to ring slots 2 (J & 1) and 2 (J & 1) + 1, and each thread turns the
+  // lambda entries of its own token for those two states (requested one step
+  // earlier) into weights in LDS; then the lambda entries of states 2J+2 and
+  // 2J+3 are requested and the slices of states 2J+4 and 2J+5, and after one
+  // barrier every wave reads the two operands and its tiles' weights from LDS.
+  // A slot written in step J was last read in step J-2, before the barrier of
+  // step J-1.  Steps run in pairs over named register buffers (constant
+  // indexing); steps past the last state have sSf = 0.
+  // The weight of state j at token t is lambda[t][x] exp(G_t - F_j), x = (live
+  // states up to j) - 1 (a state merged away at or before t is weighted as the
+  // live state that absorbed it).
   if (m > 0) {
-    float rf[NT];
-    const Tin* lp[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      rf[nt] = rv[nt] ? sRf[tr[nt]] : 0.f;
-      // lambda row (clamped to a valid row; a missing lambda reads the key
-      // tensor and is replaced by 1)
-      lp[nt] = Lin ? Lin + (size_t)(c0 + (rv[nt] ? tr[nt] : 0)) * C : Kin;
-    }
+    // this thread's token for the weights (threads past RL have none)
+    const bool tw_ok = tid < nrow;
+    const float rfw = tw_ok ? sRf[tid] : 0.f;
+    // lambda row of the token (a missing lambda reads the key tensor, and the
+    // value read is replaced by 1)
+    const Tin* lrow = Lin ? Lin + (size_t)(c0 + (tw_ok ? tid : 0)) * C : Kin;
+    int cw = 0;  // live states up to the last state whose lambda was requested
+    auto lam_req = [&](int j) __attribute__((always_inline)) -> Tin {
+      const int dj = sDt[min(j, C + 7)];
+      cw += (int)(j < m) & (int)(dj > c0 + tid);
+      return lrow[Lin ? max(cw - 1, 0) : 0];
+    };
     constexpr int SL16 = P::SLICE16;
     constexpr int V16 = (SL16 + RTHR - 1) / RTHR;
     struct Pre {
@@ -344,18 +353,7 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
         }
       }
     };
-    // weight of state j at each tile token: advance the live count, then gather
-    auto lam_req = [&](int j, Tin (&lv)[NT]) __attribute__((always_inline)) {
-      const int dj = sDt[min(j, C + 7)];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        cnt[nt] += (j < m && dj > c0 + tr[nt]) ? 1 : 0;
-        lv[nt] = lp[nt][Lin ? max(cnt[nt] - 1, 0) : 0];
-      }
-    };
-    Tin lamC0[NT], lamC1[NT];
-    lam_req(0, lamC0);
-    lam_req(1, lamC1);
+    Tin lam0 = lam_req(0), lam1 = lam_req(1);
     prefetch2(0, preA);
     prefetch2(2, preB);
     // The tiles are staggered: after the MFMA chain of tile k of state j comes
@@ -373,13 +371,13 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
         __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
       }
     };
-    auto sub = [&](const Tin* A, float sf, const Tin (&lc)[NT]) __attribute__((always_inline)) {
+    auto sub = [&](const Tin* A, const float* wt) __attribute__((always_inline)) {
       FT sa[KS];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) sa[ks] = FR::load(A + ((ks * 2 + half) * 32 + l32) * 8);
       float wg[NT];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) wg[nt] = (Lin ? to_f32(lc[nt]) : 1.f) * rf[nt] * sf;
+      for (int nt = 0; nt < NT; ++nt) wg[nt] = wt[tr[nt]];
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
@@ -412,22 +410,21 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
           const int pi = tid + RTHR * u;
           if (SL16 % RTHR == 0 || pi < SL16) rb[s2 * SL16 + pi] = pr.x[s2][u];
         }
-      Tin lamN0[NT], lamN1[NT];
-      lam_req(2 * J + 2, lamN0);
-      lam_req(2 * J + 3, lamN1);
+      float* wt = sW + (J & 1) * 2 * RL;
+      if (RL == RTHR || tid < RL) {
+        wt[tid] = (Lin ? to_f32(lam0) : 1.f) * rfw * sSf[2 * J];
+        wt[RL + tid] = (Lin ? to_f32(lam1) : 1.f) * rfw * sSf[2 * J + 1];
+      }
+      lam0 = lam_req(2 * J + 2);
+      lam1 = lam_req(2 * J + 3);
       __builtin_amdgcn_sched_barrier(0);
       prefetch2(2 * J + 4, pr);
       __builtin_amdgcn_sched_barrier(0);
       __syncthreads();
       const Tin* A = reinterpret_cast<const Tin*>(rb);
-      sub(A, sSf[2 * J], lamC0);
+      sub(A, wt);
       __builtin_amdgcn_sched_barrier(0);
-      sub(A + P::SLICE, sSf[2 * J + 1], lamC1);
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        lamC0[nt] = lamN0[nt];
-        lamC1[nt] = lamN1[nt];
-      }
+      sub(A + P::SLICE, wt + RL);
     };
     for (int J0 = 0; 2 * J0 < m; J0 += 2) {
       step(J0, preA);
@@ -532,7 +529,7 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
       const int nt = N0 + i;
       const int ti = tile_of<NT>(wv, nt);
       const int trn = tr[nt];
-      const int Aold = cnt[nt];
+      const int Aold = sAold[trn];  // old states alive at the token
       const Tin* lrow = Lin ? Lin + (size_t)(c0 + (rv[nt] ? trn : 0)) * C : nullptr;
       const Tin* lwin = sLamW + trn * lws;
       // weight of the state at window position x (x = live in-chunk leaders up
