@@ -16,6 +16,19 @@ namespace dla {
 
 
 
+// Every state is read or written at most once per step, and the states of all
+// heads (gigabytes) do not fit in the caches, so state traffic goes with the
+// non-temporal hint.
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 ld_stream(const float4* p) {
+  const f32x4v x = __builtin_nontemporal_load(reinterpret_cast<const f32x4v*>(p));
+  return make_float4(x[0], x[1], x[2], x[3]);
+}
+__device__ __forceinline__ void st_stream(float4* p, const float4& v) {
+  const f32x4v x = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(x, reinterpret_cast<f32x4v*>(p));
+}
+
 template <int DK, int DV>
 struct StateTile {
   static constexpr int CQ = DV / 4;      // float4 per row
@@ -91,7 +104,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     float4 vq = reinterpret_cast<const float4*>(sv)[cq];
 #pragma unroll
     for (int r = 0; r < ST::NV; ++r) {
-      Sopen[r] = src[tid + 256 * r];
+      Sopen[r] = ld_stream(src + tid + 256 * r);
       const float kr = sk[rg + ST::RG * r];
       const float4 s = Sopen[r];
       ct += kr * (s.x * vq.x + s.y * vq.y + s.z * vq.z + s.w * vq.w);
@@ -188,7 +201,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     } else {
       const float4* src = reinterpret_cast<const float4*>(states + (size_t)sP[j] * D);
 #pragma unroll
-      for (int r = 0; r < ST::NV; ++r) X[r] = src[tid + 256 * r];
+      for (int r = 0; r < ST::NV; ++r) X[r] = ld_stream(src + tid + 256 * r);
     }
     const int post = (istar >= 0 && j > istar) ? j - 1 : j;
     const float w = a.skip_readout ? 0.f : sLam[post] * __expf((float)(Gn - sF[j]));
@@ -215,7 +228,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
       } else {
         const float4* src = reinterpret_cast<const float4*>(states + (size_t)sP[j2] * D);
 #pragma unroll
-        for (int r = 0; r < ST::NV; ++r) Y[r] = src[tid + 256 * r];
+        for (int r = 0; r < ST::NV; ++r) Y[r] = ld_stream(src + tid + 256 * r);
       }
       const float w2 = a.skip_readout ? 0.f : sLam[j] * __expf((float)(Gn - sF[j2]));
       const float e = __expf((float)(sF[j2] - sF[j]));
@@ -232,7 +245,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
         s.y = e * X[r].y + Y[r].y;
         s.z = e * X[r].z + Y[r].z;
         s.w = e * X[r].w + Y[r].w;
-        dst[tid + 256 * r] = s;
+        st_stream(dst + tid + 256 * r, s);
       }
       o4[0] += w2 * z0;
       o4[1] += w2 * z1;
@@ -252,7 +265,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
         s.y = f * X[r].y + kr * vq.y;
         s.z = f * X[r].z + kr * vq.z;
         s.w = f * X[r].w + kr * vq.w;
-        dst[tid + 256 * r] = s;
+        st_stream(dst + tid + 256 * r, s);
       }
     }
   }
@@ -265,7 +278,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
 #pragma unroll
     for (int r = 0; r < ST::NV; ++r) {
       const float kr = sk[rg + ST::RG * r];
-      dst[tid + 256 * r] = make_float4(kr * vq.x, kr * vq.y, kr * vq.z, kr * vq.w);
+      st_stream(dst + tid + 256 * r, make_float4(kr * vq.x, kr * vq.y, kr * vq.z, kr * vq.w));
     }
   }
 
