@@ -218,13 +218,15 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
     }
   };
   // store a band of a state: float32 master, and its copy when obj >= 0 (the
-  // copy's 8-byte pieces at ((ib / 8 + g4) * 256 + l32 * 8 + 4 half) elements)
+  // copy's 8-byte pieces at ((ib / 8 + g4) * 256 + l32 * 8 + 4 half) elements).
+  // The stores carry the non-temporal hint (cache policy 2): the states of a
+  // call (gigabytes) are not re-read before they have left the caches.
   auto store_state = [&](const f32x16& acc16, int phys, int obj) __attribute__((always_inline)) {
     const __amdgpu_buffer_rsrc_t rs = band_rsrc(phys);
 #pragma unroll
     for (int r = 0; r < 16; ++r)
       __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc16[r]), rs,
-                                            voff_lane + (r & 3) * DV * 4, (r >> 2) * 8 * DV * 4, 0);
+                                            voff_lane + (r & 3) * DV * 4, (r >> 2) * 8 * DV * 4, 2);
     obj = __builtin_amdgcn_readfirstlane(obj);
     if (obj >= 0) {
       const __amdgpu_buffer_rsrc_t ro = buffer_rsrc(obj_slice(obj), U::CP::SLICE * E);
@@ -236,11 +238,11 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
           typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
           const bf16x4 v4 = {(__bf16)acc16[4 * g4], (__bf16)acc16[4 * g4 + 1], (__bf16)acc16[4 * g4 + 2],
                              (__bf16)acc16[4 * g4 + 3]};
-          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v4), ro, voff, soff, 0);
+          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v4), ro, voff, soff, 2);
         } else {
           const u32x4 v4 = {__float_as_uint(acc16[4 * g4]), __float_as_uint(acc16[4 * g4 + 1]),
                             __float_as_uint(acc16[4 * g4 + 2]), __float_as_uint(acc16[4 * g4 + 3])};
-          __builtin_amdgcn_raw_buffer_store_b128(v4, ro, voff, soff, 0);
+          __builtin_amdgcn_raw_buffer_store_b128(v4, ro, voff, soff, 2);
         }
       }
     }
