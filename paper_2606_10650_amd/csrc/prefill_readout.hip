@@ -226,6 +226,47 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
     for (int e = 0; e < EPP; ++e) sVt[(p * EPP + e) * P::VTS + r] = piece_elem<Tin>(vp_[u], e);
   }
   __syncthreads();
+  // The inter phase's first requests (the lambda entries of states 0 and 1 at
+  // this thread's token, and the pool slices of states 0 .. 3) go out as soon
+  // as the list tables are in LDS, so that their latency overlaps the rest of
+  // the set-up.  Thread tid forms the weights of token tid (threads past RL
+  // have none).
+  const bool tw_ok = tid < nrow;
+  const float rfw = tw_ok ? sRf[tid] : 0.f;
+  // lambda row of the token (a missing lambda reads the key tensor, and the
+  // value read is replaced by 1)
+  const Tin* lrow = Lin ? Lin + (size_t)(c0 + (tw_ok ? tid : 0)) * C : Kin;
+  int cw = 0;  // live states up to the last state whose lambda was requested
+  auto lam_req = [&](int j) __attribute__((always_inline)) -> Tin {
+    const int dj = sDt[min(j, C + 7)];
+    cw += (int)(j < m) & (int)(dj > c0 + tid);
+    return lrow[Lin ? max(cw - 1, 0) : 0];
+  };
+  constexpr int SL16 = P::SLICE16;
+  constexpr int V16 = (SL16 + RTHR - 1) / RTHR;
+  struct Pre {
+    u32x4 x[2][V16];
+  };
+  Pre preA, preB;
+  auto prefetch2 = [&](int jb, Pre& pr) __attribute__((always_inline)) {
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      const u32x4* src = reinterpret_cast<const u32x4*>(pool_slice<Tin>(
+          w.pool, h, plan.P_cap, sObj[min(jb + s2, m - 1)], cg, NCG, P::SLICE));
+#pragma unroll
+      for (int u = 0; u < V16; ++u) {
+        const int pi = tid + RTHR * u;
+        if (SL16 % RTHR == 0 || pi < SL16) pr.x[s2][u] = src[pi];
+      }
+    }
+  };
+  Tin lam0 = from_f32<Tin>(0.f), lam1 = lam0;
+  if (m > 0) {
+    lam0 = lam_req(0);
+    lam1 = lam_req(1);
+    prefetch2(0, preA);
+    prefetch2(2, preB);
+  }
   // old states alive at each token: m minus the states of the list whose death
   // token is at or before it (a state lives while its death token is later)
 #pragma unroll
@@ -323,39 +364,6 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   // states up to j) - 1 (a state merged away at or before t is weighted as the
   // live state that absorbed it).
   if (m > 0) {
-    // this thread's token for the weights (threads past RL have none)
-    const bool tw_ok = tid < nrow;
-    const float rfw = tw_ok ? sRf[tid] : 0.f;
-    // lambda row of the token (a missing lambda reads the key tensor, and the
-    // value read is replaced by 1)
-    const Tin* lrow = Lin ? Lin + (size_t)(c0 + (tw_ok ? tid : 0)) * C : Kin;
-    int cw = 0;  // live states up to the last state whose lambda was requested
-    auto lam_req = [&](int j) __attribute__((always_inline)) -> Tin {
-      const int dj = sDt[min(j, C + 7)];
-      cw += (int)(j < m) & (int)(dj > c0 + tid);
-      return lrow[Lin ? max(cw - 1, 0) : 0];
-    };
-    constexpr int SL16 = P::SLICE16;
-    constexpr int V16 = (SL16 + RTHR - 1) / RTHR;
-    struct Pre {
-      u32x4 x[2][V16];
-    };
-    Pre preA, preB;
-    auto prefetch2 = [&](int jb, Pre& pr) __attribute__((always_inline)) {
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-        const u32x4* src = reinterpret_cast<const u32x4*>(pool_slice<Tin>(
-            w.pool, h, plan.P_cap, sObj[min(jb + s2, m - 1)], cg, NCG, P::SLICE));
-#pragma unroll
-        for (int u = 0; u < V16; ++u) {
-          const int pi = tid + RTHR * u;
-          if (SL16 % RTHR == 0 || pi < SL16) pr.x[s2][u] = src[pi];
-        }
-      }
-    };
-    Tin lam0 = lam_req(0), lam1 = lam_req(1);
-    prefetch2(0, preA);
-    prefetch2(2, preB);
     // The tiles are staggered: after the MFMA chain of tile k of state j comes
     // the weighting of tile k - 1 (of state j - 1 for k = 0), so every FMA runs
     // while the matrix core works on an independent chain.

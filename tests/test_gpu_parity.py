@@ -28,13 +28,15 @@ def _report(tag, **kw):
     print(f"[{tag}] " + " ".join(f"{k}={v}" for k, v in kw.items()), flush=True)
 
 
-def _prefill_case(w, C=None, tau=None, T_split=None, out_dtype=None):
+def _prefill_case(w, C=None, tau=None, T_split=None, out_dtype=None, no_lambda=False):
     torch = _torch()
     dla = _dla()
     C = C or w.C
     tau = w.tau if tau is None else tau
     w = w.replace(C=C, tau=tau)
     x = make_inputs(w)
+    if no_lambda:
+        del x["lam"]  # every state weighted 1, on both sides
     ref = H.run_oracle(w, x)
     bo, mo, nb, nm = H.near_tie_overrides(ref)
     _report("prefill", case=w.label, near_b=nb, near_m=nm, boundaries=int(ref["b"].sum()),
@@ -120,6 +122,18 @@ def test_prefill_largest_capacity(dtype):
     _prefill_case(w, C=1024, tau=0.0)
 
 
+def test_prefill_without_lambda():
+    # no readout weights: every live state counts with weight 1
+    _prefill_case(WORKLOADS["cfg2"].replace(B=1, H=2, T=900, C=10), no_lambda=True)
+    _prefill_case(WORKLOADS["cfg1"].replace(T=500), no_lambda=True)
+
+
+def test_prefill_threshold_never_reached():
+    # only the first token opens a state; every later token joins it, so each
+    # chunk's state list holds one state
+    _prefill_case(WORKLOADS["cfg2"].replace(B=1, H=2, T=1100, C=8), tau=1e30)
+
+
 def test_prefill_mixed_output_types():
     # bfloat16 inputs with float32 outputs, and float32 inputs with bfloat16 outputs
     torch = _torch()
@@ -165,6 +179,39 @@ def test_decode_steps_from_empty_match_oracle():
         H.assert_decisions(b, mi, ref, w.label)
         H.assert_outputs(out, ref["out"], H.TOL[w.dtype], w.label)
         H.assert_cache(dla.cache_export(cache), ref["cache"], 1e-4, what=w.label)
+
+
+def test_decode_without_lambda():
+    """Decode steps from an empty cache with no readout weights (every live
+    state counts with weight 1) equal the oracle's recurrence."""
+    torch = _torch()
+    dla = _dla()
+    w = WORKLOADS["cfg2"].replace(B=1, H=2, T=150, C=6)
+    x = make_inputs(w)
+    del x["lam"]
+    ref = H.run_oracle(w, x)
+    bo, mo, _, _ = H.near_tie_overrides(ref)
+    q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    assert lam is None
+    cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+    bo_d = torch.from_numpy(bo).reshape(w.B, w.H, w.T).cuda()
+    mo_d = torch.from_numpy(mo).reshape(w.B, w.H, w.T).cuda()
+    outs, bs, ms = [], [], []
+    for t in range(w.T):
+        o, b, mi, _ = dla.decode_step(cache, q[:, :, t].contiguous(), k[:, :, t].contiguous(),
+                                      v[:, :, t].contiguous(), g[:, :, t].contiguous(), None,
+                                      boundary_override=bo_d[:, :, t].contiguous(),
+                                      merge_override=mo_d[:, :, t].contiguous())
+        outs.append(o)
+        bs.append(b)
+        ms.append(mi)
+    torch.cuda.synchronize()
+    nh = w.B * w.H
+    H.assert_decisions(torch.stack(bs, 2).cpu().numpy().reshape(nh, w.T),
+                       torch.stack(ms, 2).cpu().numpy().reshape(nh, w.T), ref, "decode, no lambda")
+    H.assert_outputs(torch.stack(outs, 2).float().cpu().numpy().reshape(nh, w.T, w.dv), ref["out"],
+                     H.TOL[w.dtype], "decode, no lambda")
+    H.assert_cache(dla.cache_export(cache), ref["cache"], 1e-4, what="decode, no lambda")
 
 
 @pytest.mark.parametrize("out_f32", [False, True])
