@@ -35,6 +35,29 @@
 
 namespace dla {
 
+// Readout weights of 1 for every chronological position, read in place of a
+// missing lambda row (C <= 1024).
+struct OnesTable {
+  uint16_t b[1024];  // bfloat16 1.0
+  float f[1024];
+};
+constexpr OnesTable make_ones() {
+  OnesTable t{};
+  for (int i = 0; i < 1024; ++i) {
+    t.b[i] = 0x3F80u;
+    t.f[i] = 1.f;
+  }
+  return t;
+}
+__device__ const OnesTable kOnes = make_ones();
+template <typename Tin>
+__device__ __forceinline__ const Tin* ones_row() {
+  if constexpr (sizeof(Tin) == 2)
+    return reinterpret_cast<const Tin*>(kOnes.b);
+  else
+    return reinterpret_cast<const Tin*>(kOnes.f);
+}
+
 template <int DK, typename Tin>
 struct RO : ChunkP<DK, Tin> {
   using B = ChunkP<DK, Tin>;
@@ -233,14 +256,27 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   // have none).
   const bool tw_ok = tid < nrow;
   const float rfw = tw_ok ? sRf[tid] : 0.f;
-  // lambda row of the token (a missing lambda reads the key tensor, and the
-  // value read is replaced by 1)
-  const Tin* lrow = Lin ? Lin + (size_t)(c0 + (tw_ok ? tid : 0)) * C : Kin;
-  int cw = 0;  // live states up to the last state whose lambda was requested
+  // lambda row of the token: a buffer over the chunk's lambda rows (wave-
+  // uniform), the token's row at byte offset lrow_off; without lambda, the
+  // ones table
+  const __amdgpu_buffer_rsrc_t lrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<Tin*>(Lin ? Lin + (size_t)c0 * C : ones_row<Tin>()), (short)0,
+      Lin ? nrow * C * P::E : 1024 * P::E, 0x00020000);
+  const int lrow_off = Lin ? (tw_ok ? tid : 0) * C * P::E : 0;
+  // live states up to the last state whose lambda was requested, minus one
+  // (states past the list read a death token of 0 from the padding, so they
+  // never count)
+  int cm1 = -1;
   auto lam_req = [&](int j) __attribute__((always_inline)) -> Tin {
-    const int dj = sDt[min(j, C + 7)];
-    cw += (int)(j < m) & (int)(dj > c0 + tid);
-    return lrow[Lin ? max(cw - 1, 0) : 0];
+    cm1 += (int)(sDt[min(j, C + 7)] > c0 + tid);
+    const int off = lrow_off + max(cm1, 0) * P::E;
+    if constexpr (P::E == 2) {
+      Tin r;
+      r.x = __builtin_amdgcn_raw_buffer_load_b16(lrs, off, 0, 0);
+      return r;
+    } else {
+      return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(lrs, off, 0, 0));
+    }
   };
   constexpr int SL16 = P::SLICE16;
   constexpr int V16 = (SL16 + RTHR - 1) / RTHR;
@@ -248,15 +284,22 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
     u32x4 x[2][V16];
   };
   Pre preA, preB;
+  // the pool slices of this head and column group: object obj at
+  // pool_h + obj * NCG * SLICE (the object index is wave-uniform, so the
+  // address is formed in scalar registers)
+  const Tin* pool_h = pool_slice<Tin>(w.pool, h, plan.P_cap, 0, cg, NCG, P::SLICE);
   auto prefetch2 = [&](int jb, Pre& pr) __attribute__((always_inline)) {
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
-      const u32x4* src = reinterpret_cast<const u32x4*>(pool_slice<Tin>(
-          w.pool, h, plan.P_cap, sObj[min(jb + s2, m - 1)], cg, NCG, P::SLICE));
+      const int obj = __builtin_amdgcn_readfirstlane(sObj[min(jb + s2, m - 1)]);
+      const __amdgpu_buffer_rsrc_t src = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<Tin*>(pool_h + (size_t)obj * (NCG * P::SLICE)), (short)0, SL16 * 16,
+          0x00020000);
 #pragma unroll
       for (int u = 0; u < V16; ++u) {
         const int pi = tid + RTHR * u;
-        if (SL16 % RTHR == 0 || pi < SL16) pr.x[s2][u] = src[pi];
+        if (SL16 % RTHR == 0 || pi < SL16)
+          pr.x[s2][u] = __builtin_amdgcn_raw_buffer_load_b128(src, pi * 16, 0, 0);
       }
     }
   };
@@ -420,8 +463,8 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
         }
       float* wt = sW + (J & 1) * 2 * RL;
       if (RL == RTHR || tid < RL) {
-        wt[tid] = (Lin ? to_f32(lam0) : 1.f) * rfw * sSf[2 * J];
-        wt[RL + tid] = (Lin ? to_f32(lam1) : 1.f) * rfw * sSf[2 * J + 1];
+        wt[tid] = to_f32(lam0) * rfw * sSf[2 * J];
+        wt[RL + tid] = to_f32(lam1) * rfw * sSf[2 * J + 1];
       }
       lam0 = lam_req(2 * J + 2);
       lam1 = lam_req(2 * J + 3);
