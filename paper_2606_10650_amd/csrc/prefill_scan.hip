@@ -240,13 +240,13 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
         for (int r = 0; r < 16; ++r) x += S[k][r] * S[k][r];
       }
     x = wave_sum(x);
-    __syncthreads();
+    // one barrier: between one call's reads of sRed and the next call's writes
+    // lie the barriers of a whole chunk
     if (lane == 0) sRed[wv] = x;
     __syncthreads();
     float b = 0.f;
 #pragma unroll
     for (int i = 0; i < SWAVE; ++i) b += sRed[i];
-    __syncthreads();
     return b;
   };
   float b0 = state_norm2();
@@ -687,7 +687,7 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
             if (tok(k)) FR::mma(S[k], ka[q], vb[k]);
       }
     }
-    b0 = state_norm2();  // contains barriers; also orders the exports below
+    b0 = state_norm2();  // (contains a barrier)
     if (tid < nrow) {
       const int t = tid;
       death[c0 + t] = sDC[t];
