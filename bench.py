@@ -49,13 +49,18 @@ def log(*a):
 
 
 def source_digest(kernel: str) -> str:
-    """sha256 over the sources of a kernel, to tell whether a counter summary
-    still describes the code being timed."""
+    """sha256 over the sources of a kernel with comments and whitespace removed,
+    to tell whether a counter summary still describes the code being timed (a
+    change to a comment leaves it valid)."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in KERNEL_SOURCES[kernel]:
-        with open(os.path.join(ROOT, "paper_2606_10650_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2606_10650_amd", "csrc", f)) as fh:
+            src = fh.read()
+        src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", " ", src)
+        h.update(" ".join(src.split()).encode())
     return h.hexdigest()
 
 

@@ -13,8 +13,8 @@
 //     state that absorbed it).  The tile S~_j^T Q^T (32 columns x 32 tokens,
 //     K = d_k) is an MFMA chain; each lane owns one token of a tile, so the
 //     weight is a per-lane scalar applied to the chain's result.  States are
-//     streamed from the pool two per step through a 4-slot LDS ring, six
-//     states ahead in registers, with one barrier per step; each wave reads a
+//     streamed from the pool two per step through a 4-slot LDS ring, up to
+//     four states ahead in registers, with one barrier per step; each wave reads a
 //     state's operand from LDS once for all of its tiles.  The weights are
 //     computed once per (token, state), by the thread of that token, into a
 //     small LDS ring (the lambda entries are requested one step ahead), and
@@ -358,8 +358,7 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   // lambda window of every token: lambda[t][Aold_t - 1 + x] for x < lw, the
   // weights of the states that hold the chunk's own tokens.  Consecutive lanes
   // read consecutive entries of a row; every load is issued before the stores.
-  // (The window lies past the key ring, clear of the state ring of the inter
-  // part.)
+  // (The window lies past both the key ring and the inter region.)
   if (Lin && lw > 0) {
     // (lw is a power of two)
     const int lwl = __builtin_ctz((unsigned)lw);
