@@ -726,13 +726,17 @@ static hipError_t launch_scan_dims(const PrefillArgs& a, const PrefillWS& w, int
     auto k = prefill_scan_kernel<DK, DV, float>;
     const size_t shm = ScanP<DK, DV, float>::smem_bytes(a.desc.C);
     if (shm > 160 * 1024) return hipErrorInvalidValue;
-    hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+    if (hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm) !=
+        hipSuccess)
+      return hipErrorInvalidValue;
     hipLaunchKernelGGL(k, dim3(nh), dim3(STHR), shm, s, a, w);
   } else {
     auto k = prefill_scan_kernel<DK, DV, bf16_t>;
     const size_t shm = ScanP<DK, DV, bf16_t>::smem_bytes(a.desc.C);
     if (shm > 160 * 1024) return hipErrorInvalidValue;
-    hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+    if (hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm) !=
+        hipSuccess)
+      return hipErrorInvalidValue;
     hipLaunchKernelGGL(k, dim3(nh), dim3(STHR), shm, s, a, w);
   }
   return hipGetLastError();
