@@ -214,6 +214,61 @@ def test_decode_without_lambda():
     H.assert_cache(dla.cache_export(cache), ref["cache"], 1e-4, what="decode, no lambda")
 
 
+def _decode_case(w, T1=0, label=None):
+    """Prefill of the first T1 tokens (none for T1 = 0), then one decode step per
+    remaining token; every decision, output and the final cache against the
+    oracle over all tokens."""
+    torch = _torch()
+    dla = _dla()
+    label = label or w.label
+    x = make_inputs(w)
+    ref = H.run_oracle(w, x)
+    bo, mo, _, _ = H.near_tie_overrides(ref)
+    q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    shp = (w.B, w.H, w.T)
+    bo_d = torch.from_numpy(bo).reshape(shp).cuda()
+    mo_d = torch.from_numpy(mo).reshape(shp).cuda()
+    cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+    outs, bs, ms = [], [], []
+    if T1 > 0:
+        sl = slice(0, T1)
+        o1, b1, m1, _ = dla.prefill(cache, q[:, :, sl].contiguous(), k[:, :, sl].contiguous(),
+                                    v[:, :, sl].contiguous(), g[:, :, sl].contiguous(),
+                                    lam[:, :, sl].contiguous(), tau=w.tau,
+                                    boundary_override=bo_d[:, :, sl].contiguous(),
+                                    merge_override=mo_d[:, :, sl].contiguous())
+        outs.append(o1)
+        bs.append(b1)
+        ms.append(m1)
+    for t in range(T1, w.T):
+        o, b, mi, _ = dla.decode_step(cache, q[:, :, t].contiguous(), k[:, :, t].contiguous(),
+                                      v[:, :, t].contiguous(), g[:, :, t].contiguous(),
+                                      lam[:, :, t].contiguous(), tau=w.tau,
+                                      boundary_override=bo_d[:, :, t].contiguous(),
+                                      merge_override=mo_d[:, :, t].contiguous())
+        outs.append(o.unsqueeze(2))
+        bs.append(b.unsqueeze(2))
+        ms.append(mi.unsqueeze(2))
+    torch.cuda.synchronize()
+    nh = w.B * w.H
+    H.assert_decisions(torch.cat(bs, 2).cpu().numpy().reshape(nh, -1),
+                       torch.cat(ms, 2).cpu().numpy().reshape(nh, -1), ref, label)
+    H.assert_outputs(torch.cat(outs, 2).float().cpu().numpy().reshape(nh, w.T, w.dv), ref["out"],
+                     H.TOL[w.dtype], label)
+    H.assert_cache(dla.cache_export(cache), ref["cache"], 1e-4, what=label)
+
+
+def test_decode_edge_shapes():
+    # mixed head dimensions
+    _decode_case(WORKLOADS["cfg2"].replace(B=1, H=2, T=120, C=5, dk=64, dv=128), label="decode dk64 dv128")
+    _decode_case(WORKLOADS["cfg2"].replace(B=2, H=1, T=90, C=4, dk=128, dv=64), label="decode dk128 dv64")
+    # C = 1: a single state absorbs every token after the first
+    _decode_case(WORKLOADS["cfg1"].replace(T=80, C=1), label="decode C=1")
+    # the largest capacity, full, with a merge at every step
+    _decode_case(WORKLOADS["cfg2"].replace(B=1, H=1, T=1040, C=1024, tau=0.0), T1=1030,
+                 label="decode C=1024")
+
+
 @pytest.mark.parametrize("out_f32", [False, True])
 def test_prefill_then_decode_continuation(out_f32):
     """prefill(T1) followed by decode steps equals the oracle over all tokens
