@@ -69,26 +69,48 @@ typedef struct {
 /* Layer parameters.  tau: boundary threshold (b_t = [I_t >= tau], Sec. 3.1);
  * eps: the epsilon of the score's denominator (eq. importance_score);
  * eps_rms: the epsilon of the RMSNorm applied to both states before scoring
- * (unit weight, over all d_k*d_v entries).  flags: DLA_SKIP_READOUT builds the
- * cache and the exports but computes no output (out may be NULL).
+ * (unit weight, over all d_k*d_v entries).
+ * flags: DLA_SKIP_READOUT builds the cache and the exports but computes no
+ * output (out may be NULL).  DLA_SERIAL_STAGES runs every stage of a prefill
+ * on the caller's stream, one after another.  Without it, a prefill with a
+ * readout and more than one chunk (512 tokens; 256 for float32 inputs) is
+ * pipelined: it splits into segments of whole chunks and runs the sequential
+ * boundary scan (Sec. 3.1-3.2), segment after segment, on a second stream
+ * that the library forks from the caller's stream and joins back into it
+ * before the call's last stage, while the caller's stream updates and reads
+ * out the segments already scanned.  Results are identical either way; only
+ * the workspace size differs (dla_prefill_workspace_size takes the flags).
+ * The second stream and its events are created on a host thread's first
+ * pipelined call on a device and kept, per thread and device, until the
+ * process ends.
  * stage_events: NULL, or DLA_PREFILL_STAGES + 1 hipEvent_t handles (created by
- * the caller) that dla_prefill records on its stream before its first stage and
- * after each stage (token frames, boundary scan, state update, readout), for
- * timing the stages; dla_decode_step ignores it.  A prefill whose state copies
- * exceed the workspace budget (see dla_prefill_workspace_size) runs the update
- * and readout stages segment by segment, alternating; the last two events then
- * follow the last update and the last readout. */
+ * the caller) that dla_prefill records before its first stage and after each
+ * stage (token frames, boundary scan, state update, readout), for timing the
+ * stages; dla_decode_step ignores it.  All are recorded on the caller's stream
+ * except, in a pipelined call, the scan's, which is recorded on the second
+ * stream after the last scan segment.  A call split into segments (pipelined,
+ * or whose state copies exceed the workspace budget, see
+ * dla_prefill_workspace_size) alternates the update and readout stages segment
+ * by segment; the last two events then follow the last update and the last
+ * readout.
+ * readout_events, n_readout_events: NULL and 0, or n_readout_events hipEvent_t
+ * handles; the readout launch of segment s is bracketed by events 2s (before)
+ * and 2s + 1 (after), recorded on the caller's stream, for s <
+ * n_readout_events / 2. */
 typedef struct {
   float tau;
   float eps;
   float eps_rms;
   uint32_t flags;
   void* const* stage_events;
+  void* const* readout_events;
+  int32_t n_readout_events;
 } dla_params;
 
 #define DLA_PREFILL_STAGES 4
 
 #define DLA_SKIP_READOUT 1u
+#define DLA_SERIAL_STAGES 2u
 
 /* Device flags kept in the cache header (read with dla_cache_flags). */
 #define DLA_FLAG_BAD_MERGE_OVERRIDE 1u
@@ -138,9 +160,20 @@ dla_status dla_cache_flags(const dla_cache_desc* desc, void* cache, uint32_t* fl
  * 512 tokens (256 for float32 inputs; the state list of every chunk), the
  * readout needs copies of the states in the input dtype: up to C per head and
  * chunk, d_k*d_v elements each.  They are bounded to 8 GiB per call: above
- * that the call is split into segments of whole chunks that reuse the space. */
+ * that the call is split into segments of whole chunks that reuse the space.
+ * A pipelined call (see dla_params) splits into four segments (fewer when it
+ * has fewer chunks, more when the budget asks for more) and needs
+ * correspondingly less; it also keeps the scan's newest state (d_k*d_v floats
+ * per head) between segments. */
 dla_status dla_prefill_workspace_size(const dla_cache_desc* desc, int32_t T, dla_dtype in_dtype,
                                       uint32_t flags, size_t* bytes);
+
+/* Number of segments that dla_prefill splits T tokens of the given input
+ * dtype and params flags into (see dla_params and dla_prefill_workspace_size),
+ * written to *nseg; 1 when T is 0.  The readout then runs as that many
+ * launches, which readout_events can bracket. */
+dla_status dla_prefill_segment_count(const dla_cache_desc* desc, int32_t T, dla_dtype in_dtype,
+                                     uint32_t flags, int32_t* nseg);
 
 /*
  * Prefill: absorb T tokens per head into the cache, in order, computing for

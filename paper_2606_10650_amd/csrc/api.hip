@@ -3,12 +3,41 @@
 // stream and never allocates device memory.
 #include <string.h>
 
+#include <vector>
+
 #include "dla_common.h"
 #include "prefill.h"
 #include "decode.h"
 
 namespace dla {
 
+// Pipelined prefills fork a second stream from the caller's.  Each host thread
+// gets its own stream and events per device, so concurrent calls from several
+// threads never share an event; they live until the process ends.
+hipError_t pipe_resources(int n, hipStream_t* side, hipEvent_t** evs) {
+  struct PerDevice {
+    hipStream_t side = nullptr;
+    std::vector<hipEvent_t> ev;
+  };
+  static thread_local std::vector<PerDevice> per;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if ((int)per.size() <= dev) per.resize(dev + 1);
+  PerDevice& pd = per[dev];
+  if (!pd.side && (e = hipStreamCreateWithFlags(&pd.side, hipStreamNonBlocking)) != hipSuccess) {
+    pd.side = nullptr;
+    return e;
+  }
+  while ((int)pd.ev.size() < n) {
+    hipEvent_t x;
+    if ((e = hipEventCreateWithFlags(&x, hipEventDisableTiming)) != hipSuccess) return e;
+    pd.ev.push_back(x);
+  }
+  *side = pd.side;
+  *evs = pd.ev.data();
+  return hipSuccess;
+}
 
 
 __global__ void cache_init_kernel(char* cache, dla_cache_desc d, size_t meta_offset,
@@ -135,7 +164,18 @@ dla_status dla_prefill_workspace_size(const dla_cache_desc* desc, int32_t T, dla
   dla_status s = check_desc(desc);
   if (s != DLA_OK) return ret(s);
   if (!bytes || T < 0 || !dtype_ok(in_dtype)) return ret(DLA_ERR_INVALID_ARG);
-  *bytes = prefill_workspace_bytes(*desc, T, in_dtype, (flags & DLA_SKIP_READOUT) == 0);
+  *bytes = prefill_workspace_bytes(*desc, T, in_dtype, (flags & DLA_SKIP_READOUT) == 0,
+                                   (flags & DLA_SERIAL_STAGES) != 0);
+  return ret(DLA_OK);
+}
+
+dla_status dla_prefill_segment_count(const dla_cache_desc* desc, int32_t T, dla_dtype in_dtype,
+                                     uint32_t flags, int32_t* nseg) {
+  dla_status s = check_desc(desc);
+  if (s != DLA_OK) return ret(s);
+  if (!nseg || T < 0 || !dtype_ok(in_dtype)) return ret(DLA_ERR_INVALID_ARG);
+  *nseg = seg_plan(*desc, T, in_dtype, (flags & DLA_SKIP_READOUT) == 0,
+                   (flags & DLA_SERIAL_STAGES) != 0).nseg;
   return ret(DLA_OK);
 }
 
@@ -156,7 +196,10 @@ dla_status dla_prefill(const dla_cache_desc* desc, void* cache, const void* q, c
   if ((int64_t)desc->B * desc->H * (int64_t)T * (desc->C > 128 ? desc->C : 128) >
       ((int64_t)1 << 40))
     return ret(DLA_ERR_UNSUPPORTED);
-  const size_t need = prefill_workspace_bytes(*desc, T, in_dtype, !skip);
+  const bool serial = (params->flags & DLA_SERIAL_STAGES) != 0;
+  if (params->n_readout_events < 0 || (params->n_readout_events > 0 && !params->readout_events))
+    return ret(DLA_ERR_INVALID_ARG);
+  const size_t need = prefill_workspace_bytes(*desc, T, in_dtype, !skip, serial);
   if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 255u))
     return ret(DLA_ERR_WORKSPACE);
   PrefillArgs a;
@@ -185,8 +228,13 @@ dla_status dla_prefill(const dla_cache_desc* desc, void* cache, const void* q, c
   a.skip_readout = skip ? 1 : 0;
   a.in_dtype = in_dtype;
   a.out_dtype = out_dtype;
+  a.serial = serial ? 1 : 0;
   a.workspace = (char*)workspace;
-  if (launch_prefill(a, (hipStream_t)stream, params->stage_events) != hipSuccess)
+  StageEvents se;
+  se.ev = params->stage_events;
+  se.rev = params->readout_events;
+  se.nrev = params->n_readout_events;
+  if (launch_prefill(a, (hipStream_t)stream, se) != hipSuccess)
     return ret(DLA_ERR_HIP);
   return ret(DLA_OK);
 }

@@ -24,6 +24,7 @@ struct PrefillArgs {
   float tau, eps, eps_rms;
   int skip_readout;
   dla_dtype in_dtype, out_dtype;
+  int serial;  // stages one after another on the caller's stream
   char* workspace;
 };
 
@@ -46,6 +47,10 @@ constexpr int RWAVE = 8;  // waves per workgroup of the readout stage (two per S
 constexpr int RTHR = 64 * RWAVE;
 constexpr int NC = 32;    // value columns per workgroup
 constexpr size_t kPoolBudget = (size_t)8 << 30;  // bytes of state copies per segment
+// Segments of a pipelined call.  The scan runs segment by segment on a second
+// stream while the first stream updates and reads out the segments already
+// scanned, so only the first segment's scan is exposed.
+constexpr int kPipeSegs = 4;
 
 // token tiles of 32 per readout wave: two for 16-bit inputs, one for float32
 // inputs (whose operands take twice the registers and LDS)
@@ -64,7 +69,15 @@ struct SegPlan {
 
 inline size_t dtype_bytes(dla_dtype t) { return t == DLA_F32 ? 4 : 2; }
 
-inline SegPlan seg_plan(const dla_cache_desc& d, int T, dla_dtype in, bool readout) {
+// Whether a call overlaps the scan with the later stages: with a readout, at
+// least two chunks, and unless the caller asked for serial stages.
+inline bool pipelined(int T, dla_dtype in, bool readout, bool serial) {
+  const int RL = chunk_len((int)(in == DLA_F32 ? 4 : 2));
+  return readout && !serial && T > RL;
+}
+
+inline SegPlan seg_plan(const dla_cache_desc& d, int T, dla_dtype in, bool readout,
+                        bool serial) {
   SegPlan p;
   const int E = (int)dtype_bytes(in);
   p.RL = chunk_len(E);
@@ -79,7 +92,9 @@ inline SegPlan seg_plan(const dla_cache_desc& d, int T, dla_dtype in, bool reado
   int fit = (int)(kPoolBudget / per_chunk);
   if (fit < 1) fit = 1;
   p.nseg = (p.nch + fit - 1) / fit;
+  if (pipelined(T, in, readout, serial) && p.nseg < kPipeSegs) p.nseg = p.nch < kPipeSegs ? p.nch : kPipeSegs;
   p.nch_seg = (p.nch + p.nseg - 1) / p.nseg;
+  p.nseg = (p.nch + p.nch_seg - 1) / p.nch_seg;  // no empty segment
   p.P_cap = d.C * p.nch_seg;
   return p;
 }
@@ -95,6 +110,10 @@ inline SegPlan seg_plan(const dla_cache_desc& d, int T, dla_dtype in, bool reado
 //          token of the states present before the call)
 //   carry  per head: int32 m, int32 pad, double F[C], int32 perm[C], int32 lead[C]
 //          (update-stage bookkeeping handed from one segment to the next)
+//   scarry per head: int32 m, int32 pad, double Ibar[C], int32 n[C], int32 lead[C],
+//          then from a 16-byte boundary float S[d_k d_v] (the scan's bookkeeping
+//          and its newest state, in accumulator order, handed from one scan
+//          segment to the next)
 //   lists  [nh][nch] chunk lists: int32 m at offset 0, then from offset 16 one
 //          ListEntry per state present at the chunk start, in chronological order
 //   pool   [nh][P_cap] state copies, each [d_v/32][d_k/16][2][32][8] elements of
@@ -113,6 +132,8 @@ struct PrefillWS {
   size_t init_stride;
   char* carry;
   size_t carry_stride;
+  char* scarry;
+  size_t scarry_stride;
   char* lists;
   size_t list_stride;
   char* pool;
@@ -120,11 +141,14 @@ struct PrefillWS {
 
 __host__ __device__ inline size_t ws_init_stride(int C) { return round_up(16 + 16 * (size_t)C, 256); }
 __host__ __device__ inline size_t ws_carry_stride(int C) { return round_up(8 + 16 * (size_t)C, 256); }
+__host__ __device__ inline size_t ws_scarry_stride(int C, int D) {
+  return round_up(round_up(16 + 16 * (size_t)C, 16) + 4 * (size_t)D, 256);
+}
 __host__ __device__ inline size_t ws_list_stride(int C) {
   return round_up(16 + sizeof(ListEntry) * (size_t)C, 256);
 }
 
-__host__ __device__ inline PrefillWS ws_layout(char* base, int nh, int T, int C, int nch) {
+__host__ __device__ inline PrefillWS ws_layout(char* base, int nh, int T, int C, int D, int nch) {
   PrefillWS w;
   size_t off = 0;
   w.Gtok = reinterpret_cast<double*>(base + off);
@@ -137,6 +161,9 @@ __host__ __device__ inline PrefillWS ws_layout(char* base, int nh, int T, int C,
   w.carry = base + off;
   w.carry_stride = ws_carry_stride(C);
   off = round_up(off + (size_t)nh * w.carry_stride, 256);
+  w.scarry = base + off;
+  w.scarry_stride = ws_scarry_stride(C, D);
+  off = round_up(off + (size_t)nh * w.scarry_stride, 256);
   w.lists = base + off;
   w.list_stride = ws_list_stride(C);
   off = round_up(off + (size_t)nh * nch * w.list_stride, 256);
@@ -144,13 +171,15 @@ __host__ __device__ inline PrefillWS ws_layout(char* base, int nh, int T, int C,
   return w;
 }
 
-inline size_t prefill_workspace_bytes(const dla_cache_desc& d, int T, dla_dtype in, bool readout) {
+inline size_t prefill_workspace_bytes(const dla_cache_desc& d, int T, dla_dtype in, bool readout,
+                                      bool serial) {
   const size_t nh = (size_t)d.B * d.H;
-  const SegPlan p = seg_plan(d, T, in, readout);
+  const SegPlan p = seg_plan(d, T, in, readout, serial);
   size_t off = round_up(nh * T * sizeof(double), 256);
   off = round_up(off + nh * T * sizeof(int32_t), 256);
   off = round_up(off + nh * ws_init_stride(d.C), 256);
   off = round_up(off + nh * ws_carry_stride(d.C), 256);
+  off = round_up(off + nh * ws_scarry_stride(d.C, d.d_k * d.d_v), 256);
   off = round_up(off + nh * (size_t)p.nch * ws_list_stride(d.C), 256);
   off += nh * (size_t)p.P_cap * d.d_k * d.d_v * dtype_bytes(in);
   return off;
@@ -192,41 +221,106 @@ __host__ __device__ inline CarryView carry_at(const PrefillWS& w, int h, int C) 
   return v;
 }
 
+struct ScarryView {
+  int32_t* m;
+  double* ibar;
+  int32_t* n;
+  int32_t* lead;
+  float* S;
+};
+
+__host__ __device__ inline ScarryView scarry_at(const PrefillWS& w, int h, int C) {
+  char* p = w.scarry + (size_t)h * w.scarry_stride;
+  ScarryView v;
+  v.m = reinterpret_cast<int32_t*>(p);
+  v.ibar = reinterpret_cast<double*>(p + 16);
+  v.n = reinterpret_cast<int32_t*>(p + 16 + 8 * (size_t)C);
+  v.lead = v.n + C;
+  v.S = reinterpret_cast<float*>(p + round_up(16 + 16 * (size_t)C, 16));
+  return v;
+}
+
 __host__ __device__ inline char* list_at(const PrefillWS& w, int h, int c, int nch) {
   return w.lists + ((size_t)h * nch + c) * w.list_stride;
 }
 
 hipError_t launch_prefill_prep(const PrefillArgs& a, hipStream_t s);
-hipError_t launch_prefill_scan(const PrefillArgs& a, hipStream_t s);
+// the scan over tokens [tb, te) (chunk-aligned); a segment after the first
+// resumes from the scan carry that the previous one left in the workspace
+hipError_t launch_prefill_scan(const PrefillArgs& a, int tb, int te, hipStream_t s);
 hipError_t launch_prefill_update(const PrefillArgs& a, const SegPlan& p, int seg, hipStream_t s);
 hipError_t launch_prefill_readout(const PrefillArgs& a, const SegPlan& p, int seg, hipStream_t s);
 // whether the scan, update and readout stages' working sets fit in LDS for this
 // shape
 bool prefill_chunks_supported(const dla_cache_desc& d, dla_dtype in_dtype);
 
-// Stages in order, segment by segment; ev (nullable) receives an event before
-// the first stage and after the token frames, the scan, the state updates and
-// the readouts.  With one segment the four intervals time the four stages
-// exactly; with several, updates and readouts alternate and the last two
-// events follow the last update and the last readout.
-inline hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s, void* const* ev) {
-  const SegPlan p = seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout);
-  auto rec = [&](int i) -> hipError_t {
-    if (ev && hipEventRecord((hipEvent_t)ev[i], s) != hipSuccess) return hipErrorInvalidValue;
+// The second stream of a pipelined call on the current device, and n events
+// for ordering the two streams (owned by the library, one set per host thread
+// and device; created on first use).
+hipError_t pipe_resources(int n, hipStream_t* side, hipEvent_t** evs);
+
+// Event hooks of a call: ev (nullable) receives an event before the first
+// stage and after the token frames, the scan, the state updates and the
+// readouts; rev (nullable, nrev entries) receives one event before and one
+// after each segment's readout launch, for segments s < nrev / 2.
+struct StageEvents {
+  void* const* ev;
+  void* const* rev;
+  int nrev;
+};
+
+// Stages in order.  Serial: frames, the whole scan, then update and readout
+// segment by segment, all on s.  Pipelined: the scan segments run on a second
+// stream, forked from s after the token frames, and segment k's update and
+// readout on s wait for segment k's scan; s waits for the whole scan before
+// its last update, so the call joins on s.
+inline hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s, const StageEvents& se) {
+  const bool pipe = pipelined(a.T, a.in_dtype, !a.skip_readout, a.serial != 0);
+  const SegPlan p = seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout, a.serial != 0);
+  auto rec = [&](int i, hipStream_t st) -> hipError_t {
+    if (se.ev && hipEventRecord((hipEvent_t)se.ev[i], st) != hipSuccess) return hipErrorInvalidValue;
+    return hipSuccess;
+  };
+  auto rrec = [&](int seg, int end) -> hipError_t {
+    if (se.rev && 2 * seg + 1 < se.nrev &&
+        hipEventRecord((hipEvent_t)se.rev[2 * seg + end], s) != hipSuccess)
+      return hipErrorInvalidValue;
     return hipSuccess;
   };
   hipError_t e;
-  if ((e = rec(0)) != hipSuccess) return e;
+  if ((e = rec(0, s)) != hipSuccess) return e;
   if ((e = launch_prefill_prep(a, s)) != hipSuccess) return e;
-  if ((e = rec(1)) != hipSuccess) return e;
-  if ((e = launch_prefill_scan(a, s)) != hipSuccess) return e;
-  if ((e = rec(2)) != hipSuccess) return e;
-  for (int seg = 0; seg < p.nseg; ++seg) {
-    if ((e = launch_prefill_update(a, p, seg, s)) != hipSuccess) return e;
-    if (seg == p.nseg - 1 && (e = rec(3)) != hipSuccess) return e;
-    if (!a.skip_readout && (e = launch_prefill_readout(a, p, seg, s)) != hipSuccess) return e;
+  if ((e = rec(1, s)) != hipSuccess) return e;
+  hipStream_t side = s;
+  hipEvent_t* pev = nullptr;
+  if (pipe) {
+    // event 0 forks the side stream after the frames; event 1 + k marks the
+    // end of scan segment k
+    if ((e = pipe_resources(p.nseg + 1, &side, &pev)) != hipSuccess) return e;
+    if ((e = hipEventRecord(pev[0], s)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(side, pev[0], 0)) != hipSuccess) return e;
+    for (int seg = 0; seg < p.nseg; ++seg) {
+      const int tb = seg * p.nch_seg * p.RL;
+      const int te = (seg + 1 == p.nseg) ? a.T : (seg + 1) * p.nch_seg * p.RL;
+      if ((e = launch_prefill_scan(a, tb, te, side)) != hipSuccess) return e;
+      if ((e = hipEventRecord(pev[1 + seg], side)) != hipSuccess) return e;
+    }
+    if ((e = rec(2, side)) != hipSuccess) return e;
+  } else {
+    if ((e = launch_prefill_scan(a, 0, a.T, s)) != hipSuccess) return e;
+    if ((e = rec(2, s)) != hipSuccess) return e;
   }
-  return rec(4);
+  for (int seg = 0; seg < p.nseg; ++seg) {
+    if (pipe && (e = hipStreamWaitEvent(s, pev[1 + seg], 0)) != hipSuccess) return e;
+    if ((e = launch_prefill_update(a, p, seg, s)) != hipSuccess) return e;
+    if (seg == p.nseg - 1 && (e = rec(3, s)) != hipSuccess) return e;
+    if (!a.skip_readout) {
+      if ((e = rrec(seg, 0)) != hipSuccess) return e;
+      if ((e = launch_prefill_readout(a, p, seg, s)) != hipSuccess) return e;
+      if ((e = rrec(seg, 1)) != hipSuccess) return e;
+    }
+  }
+  return rec(4, s);
 }
 
 }  // namespace dla

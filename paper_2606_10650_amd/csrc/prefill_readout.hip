@@ -697,7 +697,7 @@ static int readout_window(int C) {
 template <int DK, int DV, typename Tin>
 static hipError_t launch_readout_t(const PrefillArgs& a, const SegPlan& p, int seg, hipStream_t s) {
   const int nh = a.desc.B * a.desc.H;
-  PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C, p.nch);
+  PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C, a.desc.d_k * a.desc.d_v, p.nch);
   const int cs = seg * p.nch_seg;
   const int nchs = (p.nch < cs + p.nch_seg ? p.nch : cs + p.nch_seg) - cs;
   const long long grid = (long long)round_up(nh, 8) * nchs * (DV / NC);

@@ -84,8 +84,8 @@ __global__ __launch_bounds__(256) void prefill_prep_kernel(PrefillArgs a, Prefil
 
 hipError_t launch_prefill_prep(const PrefillArgs& a, hipStream_t s) {
   const int nh = a.desc.B * a.desc.H;
-  PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C,
-                          seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout).nch);
+  PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C, a.desc.d_k * a.desc.d_v,
+                          seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout, a.serial != 0).nch);
   hipLaunchKernelGGL(prefill_prep_kernel, dim3(nh), dim3(256), 0, s, a, w);
   return hipGetLastError();
 }
@@ -144,7 +144,8 @@ __device__ __forceinline__ float score_f(float a, float b, float c, float D, flo
 }
 
 template <int DK, int DV, typename Tin>
-__global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, PrefillWS w) {
+__global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, PrefillWS w, int tb,
+                                                            int te) {
   using FR = Frag<Tin>;
   using FT = typename FR::T;
   using P = ScanP<DK, DV, Tin>;
@@ -201,13 +202,25 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
 
   Meta M = meta_at(a.cache + a.meta_offset + (size_t)h * a.meta_stride, C);
   InitView iv = init_at(w, h, C);
-  const int m0 = min(max(*M.m, 0), C);
-  for (int j = tid; j < C; j += STHR) {
-    sIb[j] = M.ibar[j];
-    sN[j] = M.n[j];
-    sLead[j] = j - m0;
+  ScarryView sv = scarry_at(w, h, C);
+  // states present before the call (copied from the cache by stage 1)
+  const int m0 = *iv.m0;
+  if (tb == 0) {
+    for (int j = tid; j < C; j += STHR) {
+      sIb[j] = M.ibar[j];
+      sN[j] = M.n[j];
+      sLead[j] = j - m0;
+    }
+    if (tid == 0) sMisc[0] = m0;
+  } else {
+    // resume where the previous segment stopped
+    for (int j = tid; j < C; j += STHR) {
+      sIb[j] = sv.ibar[j];
+      sN[j] = sv.n[j];
+      sLead[j] = sv.lead[j];
+    }
+    if (tid == 0) sMisc[0] = *sv.m;
   }
-  if (tid == 0) sMisc[0] = m0;
 
   // newest state at the start of the call, true (decayed) values, as MFMA
   // accumulators: S[k] is the wave's tile wv + SWAVE k (rows 32 band.. of d_k,
@@ -219,7 +232,14 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
 #pragma unroll
   for (int k = 0; k < NTW; ++k) S[k] = zero16();
   const double G0 = *M.G;
-  if (m0 > 0) {
+  if (tb > 0) {
+#pragma unroll
+    for (int k = 0; k < NTW; ++k)
+      if (tok(k)) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) S[k][r] = sv.S[((size_t)(wv + SWAVE * k) * 16 + r) * 64 + lane];
+      }
+  } else if (m0 > 0) {
     const float* src = reinterpret_cast<const float*>(a.cache + a.states_offset) +
                        ((size_t)h * C + min(max(M.perm[m0 - 1], 0), C - 1)) * D;
     const float f = (float)exp(G0 - M.F[m0 - 1]);
@@ -285,11 +305,11 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
       mpre = (a.m_ovr && tid < nr) ? a.m_ovr[tok0 + c0n + tid] : -1;
     }
   };
-  prefetch(0);
-  double Gprev = G0;
+  prefetch(tb);
+  double Gprev = tb > 0 ? Gtok[tb - 1] : G0;
   const float tau = a.tau;
 
-  for (int c0 = 0; c0 < T; c0 += SL) {
+  for (int c0 = tb; c0 < te; c0 += SL) {
     const int nrow = min(SL, T - c0);
     // ------------------------------------------------ stage the chunk
     // transposed copy of a 16-bit piece (8 columns of token r, r = lane): the
@@ -352,7 +372,7 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
     }
     __syncthreads();
     const double Gnext = sGlast[0];  // G after the chunk's last token
-    if (c0 + SL < T) prefetch(c0 + SL);
+    if (c0 + SL < te) prefetch(c0 + SL);
 
     // ------------------------------------------------ Gram products and the carry term
     {
@@ -699,9 +719,24 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
   }
   __syncthreads();
   const int mfin = sMisc[0];
-  for (int j = tid; j < mfin; j += STHR) {
-    M.n[j] = sN[j];
-    M.ibar[j] = sIb[j];
+  if (te == T) {
+    for (int j = tid; j < mfin; j += STHR) {
+      M.n[j] = sN[j];
+      M.ibar[j] = sIb[j];
+    }
+  } else {
+    for (int j = tid; j < mfin; j += STHR) {
+      sv.ibar[j] = sIb[j];
+      sv.n[j] = sN[j];
+      sv.lead[j] = sLead[j];
+    }
+    if (tid == 0) *sv.m = mfin;
+#pragma unroll
+    for (int k = 0; k < NTW; ++k)
+      if (tok(k)) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sv.S[((size_t)(wv + SWAVE * k) * 16 + r) * 64 + lane] = S[k][r];
+      }
   }
 }
 
@@ -720,8 +755,8 @@ bool prefill_scan_supported(const dla_cache_desc& d, dla_dtype in_dtype) {
 }
 
 template <int DK, int DV>
-static hipError_t launch_scan_dims(const PrefillArgs& a, const PrefillWS& w, int nh,
-                                   hipStream_t s) {
+static hipError_t launch_scan_dims(const PrefillArgs& a, const PrefillWS& w, int nh, int tb,
+                                   int te, hipStream_t s) {
   if (a.in_dtype == DLA_F32) {
     auto k = prefill_scan_kernel<DK, DV, float>;
     const size_t shm = ScanP<DK, DV, float>::smem_bytes(a.desc.C);
@@ -729,7 +764,7 @@ static hipError_t launch_scan_dims(const PrefillArgs& a, const PrefillWS& w, int
     if (hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm) !=
         hipSuccess)
       return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k, dim3(nh), dim3(STHR), shm, s, a, w);
+    hipLaunchKernelGGL(k, dim3(nh), dim3(STHR), shm, s, a, w, tb, te);
   } else {
     auto k = prefill_scan_kernel<DK, DV, bf16_t>;
     const size_t shm = ScanP<DK, DV, bf16_t>::smem_bytes(a.desc.C);
@@ -737,20 +772,21 @@ static hipError_t launch_scan_dims(const PrefillArgs& a, const PrefillWS& w, int
     if (hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm) !=
         hipSuccess)
       return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k, dim3(nh), dim3(STHR), shm, s, a, w);
+    hipLaunchKernelGGL(k, dim3(nh), dim3(STHR), shm, s, a, w, tb, te);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_prefill_scan(const PrefillArgs& a, hipStream_t s) {
+hipError_t launch_prefill_scan(const PrefillArgs& a, int tb, int te, hipStream_t s) {
   const int nh = a.desc.B * a.desc.H;
-  PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C,
-                          seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout).nch);
   const int dk = a.desc.d_k, dv = a.desc.d_v;
-  if (dk == 128 && dv == 128) return launch_scan_dims<128, 128>(a, w, nh, s);
-  if (dk == 64 && dv == 64) return launch_scan_dims<64, 64>(a, w, nh, s);
-  if (dk == 128 && dv == 64) return launch_scan_dims<128, 64>(a, w, nh, s);
-  return launch_scan_dims<64, 128>(a, w, nh, s);
+  PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C, dk * dv,
+                          seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout, a.serial != 0).nch);
+  if (tb < 0 || te > a.T || tb >= te || tb % SL != 0) return hipErrorInvalidValue;
+  if (dk == 128 && dv == 128) return launch_scan_dims<128, 128>(a, w, nh, tb, te, s);
+  if (dk == 64 && dv == 64) return launch_scan_dims<64, 64>(a, w, nh, tb, te, s);
+  if (dk == 128 && dv == 64) return launch_scan_dims<128, 64>(a, w, nh, tb, te, s);
+  return launch_scan_dims<64, 128>(a, w, nh, tb, te, s);
 }
 
 }  // namespace dla

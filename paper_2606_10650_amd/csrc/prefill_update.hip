@@ -687,7 +687,7 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
 template <int DK, int DV, typename Tin>
 static hipError_t launch_update_t(const PrefillArgs& a, const SegPlan& p, int seg, hipStream_t s) {
   const int nh = a.desc.B * a.desc.H;
-  PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C, p.nch);
+  PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C, a.desc.d_k * a.desc.d_v, p.nch);
   const int grid = (int)round_up(nh, 8) * (DV / NC);
   const size_t shm = update_smem_bytes<DK, Tin>(a.desc.C);
   if (shm > 160 * 1024) return hipErrorInvalidValue;

@@ -20,11 +20,12 @@ DLA_OK, DLA_ERR_INVALID_ARG, DLA_ERR_UNSUPPORTED, DLA_ERR_CACHE_MISMATCH, DLA_ER
     DLA_ERR_WORKSPACE = range(6)
 DLA_F32, DLA_BF16 = 0, 1
 DLA_SKIP_READOUT = 1
+DLA_SERIAL_STAGES = 2
 DLA_FLAG_BAD_MERGE_OVERRIDE = 1
 
 EXPORTED = ("dla_cache_layout_of", "dla_state_cache_alloc", "dla_cache_flags",
-            "dla_prefill_workspace_size", "dla_prefill", "dla_decode_step", "dla_status_string",
-            "dla_get_last_error")
+            "dla_prefill_workspace_size", "dla_prefill_segment_count", "dla_prefill",
+            "dla_decode_step", "dla_status_string", "dla_get_last_error")
 
 
 class CacheDesc(ctypes.Structure):
@@ -34,7 +35,8 @@ class CacheDesc(ctypes.Structure):
 
 class Params(ctypes.Structure):
     _fields_ = [("tau", ctypes.c_float), ("eps", ctypes.c_float), ("eps_rms", ctypes.c_float),
-                ("flags", ctypes.c_uint32), ("stage_events", ctypes.c_void_p)]
+                ("flags", ctypes.c_uint32), ("stage_events", ctypes.c_void_p),
+                ("readout_events", ctypes.c_void_p), ("n_readout_events", ctypes.c_int32)]
 
 
 PREFILL_STAGES = ("frames", "scan", "update", "readout")
@@ -68,6 +70,8 @@ def lib():
                                       P]
         L.dla_prefill_workspace_size.argtypes = [ctypes.POINTER(CacheDesc), ctypes.c_int32, I,
                                                  ctypes.c_uint32, ctypes.POINTER(ctypes.c_size_t)]
+        L.dla_prefill_segment_count.argtypes = [ctypes.POINTER(CacheDesc), ctypes.c_int32, I,
+                                                ctypes.c_uint32, ctypes.POINTER(ctypes.c_int32)]
         L.dla_prefill.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, ctypes.c_int32, I,
                                   ctypes.POINTER(Params), P, I, P, P, P, P, P, P, ctypes.c_size_t, P]
         L.dla_decode_step.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, I,
@@ -76,8 +80,8 @@ def lib():
         L.dla_status_string.restype = ctypes.c_char_p
         L.dla_get_last_error.argtypes = []
         for name in ("dla_cache_layout_of", "dla_state_cache_alloc", "dla_cache_flags",
-                     "dla_prefill_workspace_size", "dla_prefill", "dla_decode_step",
-                     "dla_get_last_error"):
+                     "dla_prefill_workspace_size", "dla_prefill_segment_count", "dla_prefill",
+                     "dla_decode_step", "dla_get_last_error"):
             getattr(L, name).restype = I
         _lib = L
     return _lib
@@ -161,35 +165,65 @@ def cache_flags(cache: StateCache) -> int:
     return int(f.value)
 
 
-def workspace_bytes(cache: StateCache, T: int, dtype=None, skip_readout: bool = False) -> int:
+def _flags(skip_readout: bool, serial: bool) -> int:
+    return (DLA_SKIP_READOUT if skip_readout else 0) | (DLA_SERIAL_STAGES if serial else 0)
+
+
+def workspace_bytes(cache: StateCache, T: int, dtype=None, skip_readout: bool = False,
+                    serial: bool = False) -> int:
     """Prefill workspace for T tokens of input dtype (torch dtype, default bf16)."""
     code = DLA_BF16 if dtype is None else _dtype_code(dtype)
     n = ctypes.c_size_t(0)
     _check(lib().dla_prefill_workspace_size(ctypes.byref(cache.desc), int(T), code,
-                                            DLA_SKIP_READOUT if skip_readout else 0,
+                                            _flags(skip_readout, serial),
                                             ctypes.byref(n)), "dla_prefill_workspace_size")
     return int(n.value)
 
 
-def _params(tau, eps, eps_rms, skip_readout, stage_events=None):
-    p = Params(float(tau), float(eps), float(eps_rms), DLA_SKIP_READOUT if skip_readout else 0,
-               None)
+def prefill_segments(cache: StateCache, T: int, dtype=None, skip_readout: bool = False,
+                     serial: bool = False) -> int:
+    """Segments (readout launches) of a prefill of T tokens."""
+    code = DLA_BF16 if dtype is None else _dtype_code(dtype)
+    n = ctypes.c_int32(0)
+    _check(lib().dla_prefill_segment_count(ctypes.byref(cache.desc), int(T), code,
+                                           _flags(skip_readout, serial), ctypes.byref(n)),
+           "dla_prefill_segment_count")
+    return int(n.value)
+
+
+def _event_array(events):
+    # torch.cuda.Event objects (enable_timing=True)
+    return (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
+
+
+def _params(tau, eps, eps_rms, skip_readout, serial=False, stage_events=None,
+            readout_events=None):
+    p = Params(float(tau), float(eps), float(eps_rms), _flags(skip_readout, serial), None, None, 0)
+    keep = []
     if stage_events is not None:
-        # torch.cuda.Event objects (enable_timing=True); keep the array alive in p
         assert len(stage_events) == len(PREFILL_STAGES) + 1
-        arr = (ctypes.c_void_p * len(stage_events))(*[e.cuda_event for e in stage_events])
-        p._events_keepalive = arr
+        arr = _event_array(stage_events)
+        keep.append(arr)
         p.stage_events = ctypes.cast(arr, ctypes.c_void_p)
+    if readout_events:
+        arr = _event_array(readout_events)
+        keep.append(arr)
+        p.readout_events = ctypes.cast(arr, ctypes.c_void_p)
+        p.n_readout_events = len(readout_events)
+    p._events_keepalive = keep  # the arrays must outlive the call
     return p
 
 
 def prefill(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5, eps: float = 1e-6,
             eps_rms: float = 1e-6, out=None, out_dtype=None, skip_readout: bool = False,
             boundary=None, merge_idx=None, score=None, boundary_override=None,
-            merge_override=None, workspace=None, want_exports: bool = True, stage_events=None):
+            merge_override=None, workspace=None, want_exports: bool = True, stage_events=None,
+            serial: bool = False, readout_events=None):
     """Absorb T tokens per head.  q, k: [B, H, T, d_k]; v: [B, H, T, d_v]; g:
-    [B, H, T] float32; lam: [B, H, T, C] or None.  Returns (out, boundary,
-    merge_idx, score); exports not requested are None."""
+    [B, H, T] float32; lam: [B, H, T, C] or None.  serial: run the stages one
+    after another on the current stream (otherwise the scan of long inputs is
+    overlapped with the later stages on a second stream).  Returns (out,
+    boundary, merge_idx, score); exports not requested are None."""
     torch = _torch()
     B, H, C = cache.B, cache.H, cache.C
     T = k.shape[2]
@@ -212,12 +246,12 @@ def prefill(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5, eps: f
                                                                         device=dev)
         score = score if score is not None else torch.empty((B, H, T), dtype=torch.float32,
                                                             device=dev)
-    wsb = workspace_bytes(cache, T, k.dtype, skip_readout)
+    wsb = workspace_bytes(cache, T, k.dtype, skip_readout, serial)
     if workspace is None or workspace.numel() < wsb:
         workspace = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
-    for e in stage_events or ():
+    for e in list(stage_events or ()) + list(readout_events or ()):
         e.record()   # make sure the event exists before the library records it
-    p = _params(tau, eps, eps_rms, skip_readout, stage_events)
+    p = _params(tau, eps, eps_rms, skip_readout, serial, stage_events, readout_events)
     st = lib().dla_prefill(ctypes.byref(cache.desc), _ptr(cache.buf), _ptr(q), _ptr(k), _ptr(v),
                            _ptr(g), _ptr(lam), int(T), _dtype_code(k.dtype), ctypes.byref(p),
                            _ptr(out), _dtype_code(out.dtype) if out is not None else DLA_F32,

@@ -368,6 +368,76 @@ def test_skip_readout_builds_the_same_cache():
     H.assert_cache(dla.cache_export(cache), ref["cache"], 1e-4, what="skip")
 
 
+def _run_modes(w, x, T_split=None):
+    """Prefill the same inputs twice, pipelined and serial (optionally as two
+    calls split at T_split), and return both runs' outputs, exports, caches
+    and the pipelined run's readout-launch event count."""
+    torch = _torch()
+    dla = _dla()
+    q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    cuts = [0, w.T] if T_split is None else [0, T_split, w.T]
+    res = {}
+    for serial in (False, True):
+        cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+        outs = []
+        for a, b in zip(cuts[:-1], cuts[1:]):
+            sl = lambda t: t[:, :, a:b].contiguous()
+            rev = None
+            if not serial:
+                rev = [torch.cuda.Event(enable_timing=True) for _ in range(16)]
+            o, bd, mi, sc = dla.prefill(cache, sl(q), sl(k), sl(v), sl(g), sl(lam), tau=w.tau,
+                                        serial=serial, readout_events=rev)
+            torch.cuda.synchronize()
+            outs.append((o.cpu(), bd.cpu(), mi.cpu(), sc.cpu()))
+            if rev is not None:
+                # every readout launch of the call is bracketed by a pair of events
+                nch = -(-(b - a) // (512 if w.dtype == "bf16" else 256))
+                per = -(-nch // min(nch, 4))
+                for i in range(-(-nch // per)):
+                    assert rev[2 * i].elapsed_time(rev[2 * i + 1]) > 0.0
+        res[serial] = (outs, dla.cache_export(cache))
+    return res
+
+
+@pytest.mark.parametrize("case", ["bf16_ragged", "bf16_three_chunks", "f32", "continuation",
+                                  "bf16_16k"])
+def test_pipelined_prefill_matches_serial(case):
+    """The pipelined prefill (scan segments on a second stream, resuming from
+    the scan carry) gives bit-identical outputs, exports and cache to the serial
+    one: ragged last chunk, fewer chunks than segments, float32 inputs (256-token
+    chunks), a continuation on a non-empty cache, and the 16k-token shape."""
+    if case == "bf16_ragged":
+        w, cut = WORKLOADS["cfg3"].replace(B=1, H=3, T=2600, C=24, span_mean=200.0), None
+    elif case == "bf16_three_chunks":
+        w, cut = WORKLOADS["cfg2"].replace(B=1, H=2, T=1100, C=12), None
+    elif case == "f32":
+        w, cut = WORKLOADS["cfg1"].replace(T=1000), None
+    elif case == "continuation":
+        w, cut = WORKLOADS["cfg2"].replace(B=1, H=2, T=2900, C=16), 1100
+    else:
+        w, cut = WORKLOADS["cfg3"].replace(B=1, H=4), None
+    _report("pipe-vs-serial", case=case, T=w.T, C=w.C, dtype=w.dtype)
+    x = make_inputs(w)
+    res = _run_modes(w, x, cut)
+    (op, cp), (os_, cs) = res[False], res[True]
+    for a, b in zip(op, os_):
+        for ta, tb in zip(a, b):
+            assert torch_equal_bits(ta, tb), case
+    for key in cp:
+        assert np.array_equal(cp[key], cs[key]), (case, key)
+    # the inputs open states after the first token, so the scan carry matters
+    assert int(os_[-1][1].sum()) > 1
+
+
+def torch_equal_bits(a, b):
+    torch = _torch()
+    if a.dtype in (torch.bfloat16, torch.float16):
+        return torch.equal(a.view(torch.int16), b.view(torch.int16))
+    if a.dtype == torch.float32:
+        return torch.equal(a.view(torch.int32), b.view(torch.int32))
+    return torch.equal(a, b)
+
+
 @pytest.mark.parametrize("name", ["cfg2", "cfg3", "cfg4"])
 def test_prefill_full_size_sampled_heads(name):
     """A prefill workload at its full size (cfg3, the 16k-token workload, in the
