@@ -250,7 +250,8 @@ def prefill(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5, eps: f
     if workspace is None or workspace.numel() < wsb:
         workspace = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
     for e in list(stage_events or ()) + list(readout_events or ()):
-        e.record()   # make sure the event exists before the library records it
+        if not e.cuda_event:
+            e.record()   # torch creates an event on its first record
     p = _params(tau, eps, eps_rms, skip_readout, serial, stage_events, readout_events)
     st = lib().dla_prefill(ctypes.byref(cache.desc), _ptr(cache.buf), _ptr(q), _ptr(k), _ptr(v),
                            _ptr(g), _ptr(lam), int(T), _dtype_code(k.dtype), ctypes.byref(p),
