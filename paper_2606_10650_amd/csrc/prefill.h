@@ -47,10 +47,9 @@ constexpr int RWAVE = 8;  // waves per workgroup of the readout stage (two per S
 constexpr int RTHR = 64 * RWAVE;
 constexpr int NC = 32;    // value columns per workgroup
 constexpr size_t kPoolBudget = (size_t)8 << 30;  // bytes of state copies per segment
-// Segments of a pipelined call.  The scan runs segment by segment on a second
-// stream while the first stream updates and reads out the segments already
-// scanned, so only the first segment's scan is exposed.
-constexpr int kPipeSegs = 4;
+// A pipelined call runs the scan segment by segment on a second stream while
+// the first stream updates and reads out the segments already scanned, so only
+// the first segment's scan is exposed; its segments grow as a ramp (seg_range).
 
 // token tiles of 32 per readout wave: two for 16-bit inputs, one for float32
 // inputs (whose operands take twice the registers and LDS)
@@ -62,10 +61,38 @@ __host__ __device__ constexpr int chunk_len(int elem_bytes) {
 struct SegPlan {
   int RL;       // tokens per chunk
   int nch;      // chunks in the call
-  int nch_seg;  // chunks per segment
+  int nch_seg;  // chunks per segment (the largest segment of a ramp)
   int nseg;     // segments
   int P_cap;    // pool objects per head (0 without a readout)
+  int first;    // 0: segments of nch_seg chunks; else a ramp starting at `first`
+  int fit;      // largest segment of a ramp (pool budget)
 };
+
+// Segment sizes of a ramp: segment k takes first * 2^k chunks (at most fit),
+// or everything left when that is at most twice as much.  The scan of a
+// segment then takes about as long as the update and readout of the one
+// before it, which costs about twice the scan's time per chunk, so the
+// caller's stream never waits for the scan after the first, short, segment.
+__host__ __device__ inline int ramp_size(int first, int fit, int k, int rem) {
+  int sz = first;
+  for (int i = 0; i < k && sz < fit; ++i) sz *= 2;
+  sz = sz < fit ? sz : fit;
+  int n = rem <= 2 * sz ? rem : sz;
+  return n < fit ? n : fit;
+}
+
+// chunks [cs, ce) of segment seg
+__host__ __device__ inline void seg_range(const SegPlan& p, int seg, int* cs, int* ce) {
+  if (p.first == 0) {
+    *cs = seg * p.nch_seg;
+    *ce = p.nch < *cs + p.nch_seg ? p.nch : *cs + p.nch_seg;
+    return;
+  }
+  int b = 0;
+  for (int k = 0; k < seg; ++k) b += ramp_size(p.first, p.fit, k, p.nch - b);
+  *cs = b;
+  *ce = b + ramp_size(p.first, p.fit, seg, p.nch - b);
+}
 
 inline size_t dtype_bytes(dla_dtype t) { return t == DLA_F32 ? 4 : 2; }
 
@@ -82,6 +109,8 @@ inline SegPlan seg_plan(const dla_cache_desc& d, int T, dla_dtype in, bool reado
   const int E = (int)dtype_bytes(in);
   p.RL = chunk_len(E);
   p.nch = T > 0 ? (T + p.RL - 1) / p.RL : 0;
+  p.first = 0;
+  p.fit = 0;
   if (!readout || p.nch == 0) {
     p.nch_seg = p.nch > 0 ? p.nch : 1;
     p.nseg = 1;
@@ -91,10 +120,21 @@ inline SegPlan seg_plan(const dla_cache_desc& d, int T, dla_dtype in, bool reado
   const size_t per_chunk = (size_t)d.B * d.H * d.C * d.d_k * d.d_v * E;
   int fit = (int)(kPoolBudget / per_chunk);
   if (fit < 1) fit = 1;
-  p.nseg = (p.nch + fit - 1) / fit;
-  if (pipelined(T, in, readout, serial) && p.nseg < kPipeSegs) p.nseg = p.nch < kPipeSegs ? p.nch : kPipeSegs;
-  p.nch_seg = (p.nch + p.nseg - 1) / p.nseg;
-  p.nseg = (p.nch + p.nch_seg - 1) / p.nch_seg;  // no empty segment
+  if (pipelined(T, in, readout, serial)) {
+    p.first = p.nch / 16 > 1 ? p.nch / 16 : 1;
+    p.fit = fit;
+    p.nseg = 0;
+    p.nch_seg = 0;
+    for (int b = 0; b < p.nch; ++p.nseg) {
+      const int n = ramp_size(p.first, fit, p.nseg, p.nch - b);
+      p.nch_seg = n > p.nch_seg ? n : p.nch_seg;
+      b += n;
+    }
+  } else {
+    p.nseg = (p.nch + fit - 1) / fit;
+    p.nch_seg = (p.nch + p.nseg - 1) / p.nseg;
+    p.nseg = (p.nch + p.nch_seg - 1) / p.nch_seg;  // no empty segment
+  }
   p.P_cap = d.C * p.nch_seg;
   return p;
 }
@@ -300,8 +340,10 @@ inline hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s, const Stag
     if ((e = hipEventRecord(pev[0], s)) != hipSuccess) return e;
     if ((e = hipStreamWaitEvent(side, pev[0], 0)) != hipSuccess) return e;
     for (int seg = 0; seg < p.nseg; ++seg) {
-      const int tb = seg * p.nch_seg * p.RL;
-      const int te = (seg + 1 == p.nseg) ? a.T : (seg + 1) * p.nch_seg * p.RL;
+      int cs, ce;
+      seg_range(p, seg, &cs, &ce);
+      const int tb = cs * p.RL;
+      const int te = (seg + 1 == p.nseg) ? a.T : ce * p.RL;
       if ((e = launch_prefill_scan(a, tb, te, side)) != hipSuccess) return e;
       if ((e = hipEventRecord(pev[1 + seg], side)) != hipSuccess) return e;
     }

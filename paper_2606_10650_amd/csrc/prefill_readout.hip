@@ -108,8 +108,9 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   constexpr int RL = P::RL;
   constexpr int EPP = P::EPP;
   const int nh = a.desc.B * a.desc.H;
-  const int cs = seg * plan.nch_seg;
-  const int nchs = min(plan.nch, cs + plan.nch_seg) - cs;
+  int cs, ce;
+  seg_range(plan, seg, &cs, &ce);
+  const int nchs = ce - cs;
   // id -> (XCD x, i); i -> (head group, chunk, column group), column group fastest
   const int bid = blockIdx.x;
   const int i = bid >> 3;
@@ -698,8 +699,9 @@ template <int DK, int DV, typename Tin>
 static hipError_t launch_readout_t(const PrefillArgs& a, const SegPlan& p, int seg, hipStream_t s) {
   const int nh = a.desc.B * a.desc.H;
   PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C, a.desc.d_k * a.desc.d_v, p.nch);
-  const int cs = seg * p.nch_seg;
-  const int nchs = (p.nch < cs + p.nch_seg ? p.nch : cs + p.nch_seg) - cs;
+  int cs, ce;
+  seg_range(p, seg, &cs, &ce);
+  const int nchs = ce - cs;
   const long long grid = (long long)round_up(nh, 8) * nchs * (DV / NC);
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
   const int lw = readout_window<DK, Tin>(a.desc.C);

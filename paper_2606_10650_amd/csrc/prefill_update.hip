@@ -96,8 +96,8 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
   const int l32 = lane & 31;
   const int C = a.desc.C;
   const int T = a.T;
-  const int cs = seg * plan.nch_seg;
-  const int ce = min(plan.nch, cs + plan.nch_seg);
+  int cs, ce;
+  seg_range(plan, seg, &cs, &ce);
   const bool last_seg = seg == plan.nseg - 1;
   const bool copies = plan.P_cap > 0;  // pool objects for a readout stage
 

@@ -105,3 +105,28 @@ def test_every_supported_shape_passes_the_prefill_shape_check(dtype):
                                    ctypes.byref(p), fake, dtype, None, None, None, None, None,
                                    None, 0, None)
                 assert st == dla.DLA_ERR_WORKSPACE, (dk, dv, C, dtype, st)
+
+
+def test_prefill_segment_counts():
+    """Segment plan (host only): a pipelined prefill of the 16k-token workload
+    runs as a ramp of four segments; serial stages keep one segment while the
+    state copies fit the pool budget; a call of one chunk is never split."""
+    from paper_2606_10650_amd import dla
+    L = dla.lib()
+
+    def count(B, H, C, d, T, dtype, flags):
+        desc = dla.CacheDesc(B, H, C, d, d)
+        n = ctypes.c_int32(0)
+        assert L.dla_prefill_segment_count(ctypes.byref(desc), T, dtype, flags,
+                                           ctypes.byref(n)) == dla.DLA_OK
+        return n.value
+
+    assert count(4, 16, 128, 128, 16384, dla.DLA_BF16, 0) == 4
+    assert count(4, 16, 128, 128, 16384, dla.DLA_BF16, dla.DLA_SERIAL_STAGES) == 1
+    # 64k tokens at C = 256: the pool budget splits even the serial call
+    assert count(1, 32, 256, 128, 65536, dla.DLA_BF16, dla.DLA_SERIAL_STAGES) == 4
+    assert count(1, 32, 256, 128, 65536, dla.DLA_BF16, 0) >= 4
+    assert count(1, 2, 16, 128, 512, dla.DLA_BF16, 0) == 1
+    assert count(1, 2, 16, 128, 1100, dla.DLA_BF16, 0) == 2
+    assert count(1, 2, 16, 128, 0, dla.DLA_BF16, 0) == 1
+    assert count(1, 2, 16, 128, 1100, dla.DLA_BF16, dla.DLA_SKIP_READOUT) == 1

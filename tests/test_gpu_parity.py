@@ -391,9 +391,7 @@ def _run_modes(w, x, T_split=None):
             outs.append((o.cpu(), bd.cpu(), mi.cpu(), sc.cpu()))
             if rev is not None:
                 # every readout launch of the call is bracketed by a pair of events
-                nch = -(-(b - a) // (512 if w.dtype == "bf16" else 256))
-                per = -(-nch // min(nch, 4))
-                for i in range(-(-nch // per)):
+                for i in range(dla.prefill_segments(cache, b - a, k.dtype)):
                     assert rev[2 * i].elapsed_time(rev[2 * i + 1]) > 0.0
         res[serial] = (outs, dla.cache_export(cache))
     return res
