@@ -68,14 +68,15 @@ struct SegPlan {
   int fit;      // largest segment of a ramp (pool budget)
 };
 
-// Segment sizes of a ramp: segment k takes first * 2^k chunks (at most fit),
-// or everything left when that is at most twice as much.  The scan of a
-// segment then takes about as long as the update and readout of the one
-// before it, which costs about twice the scan's time per chunk, so the
-// caller's stream never waits for the scan after the first, short, segment.
+// Segment sizes of a ramp: each segment is half again as long as the one
+// before (first, then growing, at most fit), and a segment takes everything
+// left when that is at most twice its size.  The update and readout of a
+// segment cost about twice the scan's time per chunk, so while they run the
+// scan of the next, longer segment finishes, and the caller's stream rarely
+// waits for the scan after the first, short, segment.
 __host__ __device__ inline int ramp_size(int first, int fit, int k, int rem) {
   int sz = first;
-  for (int i = 0; i < k && sz < fit; ++i) sz *= 2;
+  for (int i = 0; i < k && sz < fit; ++i) sz += (sz + 1) / 2;
   sz = sz < fit ? sz : fit;
   int n = rem <= 2 * sz ? rem : sz;
   return n < fit ? n : fit;

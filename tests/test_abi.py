@@ -109,7 +109,7 @@ def test_every_supported_shape_passes_the_prefill_shape_check(dtype):
 
 def test_prefill_segment_counts():
     """Segment plan (host only): a pipelined prefill of the 16k-token workload
-    runs as a ramp of four segments; serial stages keep one segment while the
+    runs as a ramp of five segments; serial stages keep one segment while the
     state copies fit the pool budget; a call of one chunk is never split."""
     from paper_2606_10650_amd import dla
     L = dla.lib()
@@ -121,7 +121,7 @@ def test_prefill_segment_counts():
                                            ctypes.byref(n)) == dla.DLA_OK
         return n.value
 
-    assert count(4, 16, 128, 128, 16384, dla.DLA_BF16, 0) == 4
+    assert count(4, 16, 128, 128, 16384, dla.DLA_BF16, 0) == 5   # 2, 3, 5, 8, 14 chunks
     assert count(4, 16, 128, 128, 16384, dla.DLA_BF16, dla.DLA_SERIAL_STAGES) == 1
     # 64k tokens at C = 256: the pool budget splits even the serial call
     assert count(1, 32, 256, 128, 65536, dla.DLA_BF16, dla.DLA_SERIAL_STAGES) == 4
