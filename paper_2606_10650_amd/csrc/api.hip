@@ -14,25 +14,32 @@ namespace dla {
 // Pipelined prefills fork a second stream from the caller's.  Each host thread
 // gets its own stream and events per device, so concurrent calls from several
 // threads never share an event; they live until the process ends.
-hipError_t pipe_resources(int n, hipStream_t* side, hipEvent_t** evs) {
+hipError_t pipe_resources(hipStream_t caller, int n, hipStream_t* side, hipEvent_t** evs) {
   struct PerDevice {
     hipStream_t side = nullptr;
     std::vector<hipEvent_t> ev;
   };
   static thread_local std::vector<PerDevice> per;
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
+  // the device of the caller's stream (the current device for the null
+  // stream); the second stream and the events are made on it
+  int dev = 0, cur = 0;
+  hipError_t e = hipStreamGetDevice(caller, &dev);
   if (e != hipSuccess) return e;
+  if (dev < 0) return hipErrorInvalidDevice;
   if ((int)per.size() <= dev) per.resize(dev + 1);
   PerDevice& pd = per[dev];
-  if (!pd.side && (e = hipStreamCreateWithFlags(&pd.side, hipStreamNonBlocking)) != hipSuccess) {
-    pd.side = nullptr;
-    return e;
-  }
-  while ((int)pd.ev.size() < n) {
-    hipEvent_t x;
-    if ((e = hipEventCreateWithFlags(&x, hipEventDisableTiming)) != hipSuccess) return e;
-    pd.ev.push_back(x);
+  if (!pd.side || (int)pd.ev.size() < n) {
+    if ((e = hipGetDevice(&cur)) != hipSuccess) return e;
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    if (!pd.side && (e = hipStreamCreateWithFlags(&pd.side, hipStreamNonBlocking)) != hipSuccess)
+      pd.side = nullptr;
+    while (e == hipSuccess && (int)pd.ev.size() < n) {
+      hipEvent_t x;
+      if ((e = hipEventCreateWithFlags(&x, hipEventDisableTiming)) == hipSuccess) pd.ev.push_back(x);
+    }
+    const hipError_t r = (cur != dev) ? hipSetDevice(cur) : hipSuccess;
+    if (e != hipSuccess) return e;
+    if (r != hipSuccess) return r;
   }
   *side = pd.side;
   *evs = pd.ev.data();

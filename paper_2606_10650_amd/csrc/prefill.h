@@ -295,10 +295,10 @@ hipError_t launch_prefill_readout(const PrefillArgs& a, const SegPlan& p, int se
 // shape
 bool prefill_chunks_supported(const dla_cache_desc& d, dla_dtype in_dtype);
 
-// The second stream of a pipelined call on the current device, and n events
-// for ordering the two streams (owned by the library, one set per host thread
-// and device; created on first use).
-hipError_t pipe_resources(int n, hipStream_t* side, hipEvent_t** evs);
+// The second stream of a pipelined call on the device of the caller's stream,
+// and n events for ordering the two streams (owned by the library, one set per
+// host thread and device; created on first use).
+hipError_t pipe_resources(hipStream_t caller, int n, hipStream_t* side, hipEvent_t** evs);
 
 // Event hooks of a call: ev (nullable) receives an event before the first
 // stage and after the token frames, the scan, the state updates and the
@@ -337,7 +337,7 @@ inline hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s, const Stag
   if (pipe) {
     // event 0 forks the side stream after the frames; event 1 + k marks the
     // end of scan segment k
-    if ((e = pipe_resources(p.nseg + 1, &side, &pev)) != hipSuccess) return e;
+    if ((e = pipe_resources(s, p.nseg + 1, &side, &pev)) != hipSuccess) return e;
     if ((e = hipEventRecord(pev[0], s)) != hipSuccess) return e;
     if ((e = hipStreamWaitEvent(side, pev[0], 0)) != hipSuccess) return e;
     for (int seg = 0; seg < p.nseg; ++seg) {

@@ -427,6 +427,65 @@ def test_pipelined_prefill_matches_serial(case):
     assert int(os_[-1][1].sum()) > 1
 
 
+def test_pipelined_prefill_on_user_streams_and_threads():
+    """A pipelined prefill enqueued on a stream the caller created, and two
+    pipelined prefills on separate caches from two host threads at once (each
+    thread has its own second stream and events), match the same prefill on
+    the default stream bit for bit."""
+    import threading
+    torch = _torch()
+    dla = _dla()
+    w = WORKLOADS["cfg2"].replace(B=1, H=2, T=2100, C=12)
+    x = make_inputs(w)
+    q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    assert dla.prefill_segments(dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv), w.T, k.dtype) > 1
+
+    def run():
+        cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+        o, b, m, sc = dla.prefill(cache, q, k, v, g, lam, tau=w.tau)
+        return cache, o, b, m, sc
+
+    ref = run()
+    torch.cuda.synchronize()
+    ref_cache = dla.cache_export(ref[0])
+
+    def check(res, what):
+        for ta, tb in zip(res[1:], ref[1:]):
+            assert torch_equal_bits(ta.cpu(), tb.cpu()), what
+        ce = dla.cache_export(res[0])
+        for key in ce:
+            assert np.array_equal(ce[key], ref_cache[key]), (what, key)
+
+    st = torch.cuda.Stream()
+    st.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(st):
+        res = run()
+    st.synchronize()
+    check(res, "user stream")
+
+    out = [None, None]
+    err = []
+
+    def worker(i):
+        try:
+            s2 = torch.cuda.Stream()
+            s2.wait_stream(torch.cuda.default_stream())
+            with torch.cuda.stream(s2):
+                out[i] = run()
+            s2.synchronize()
+        except Exception as e:  # reported below, on the main thread
+            err.append(e)
+
+    ths = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+    for t in ths:
+        t.start()
+    for t in ths:
+        t.join(timeout=120)
+    assert not err, err
+    for i in range(2):
+        check(out[i], f"thread {i}")
+
+
 def torch_equal_bits(a, b):
     torch = _torch()
     if a.dtype in (torch.bfloat16, torch.float16):
