@@ -61,6 +61,20 @@ def test_host_side_errors():
     st = L.dla_prefill(ctypes.byref(d), fake, fake, fake, fake, fake, None, 10, 1, ctypes.byref(p),
                        fake, 1, None, None, None, None, None, fake, 16, None)
     assert st == dla.DLA_ERR_WORKSPACE
+    # readout events: a negative count, or a count without the array
+    for n_ev, arr in ((-1, None), (4, None)):
+        pe = dla.Params(0.5, 1e-6, 1e-6, 0, None, arr, n_ev)
+        st = L.dla_prefill(ctypes.byref(d), fake, fake, fake, fake, fake, None, 10, 1,
+                           ctypes.byref(pe), fake, 1, None, None, None, None, None, fake, 1 << 30,
+                           None)
+        assert st == dla.DLA_ERR_INVALID_ARG, n_ev
+    # the serial flag needs a larger workspace than the pipelined default
+    wp, wsr = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    d16 = dla.CacheDesc(4, 16, 128, 128, 128)
+    assert L.dla_prefill_workspace_size(ctypes.byref(d16), 16384, 1, 0, ctypes.byref(wp)) == 0
+    assert L.dla_prefill_workspace_size(ctypes.byref(d16), 16384, 1, dla.DLA_SERIAL_STAGES,
+                                        ctypes.byref(wsr)) == 0
+    assert wsr.value > wp.value
     # bad dtype
     st = L.dla_prefill(ctypes.byref(d), fake, fake, fake, fake, fake, None, 10, 7, ctypes.byref(p),
                        fake, 1, None, None, None, None, None, fake, 1 << 30, None)
