@@ -66,6 +66,7 @@ struct SegPlan {
   int P_cap;    // pool objects per head (0 without a readout)
   int first;    // 0: segments of nch_seg chunks; else a ramp starting at `first`
   int fit;      // largest segment of a ramp (pool budget)
+  int shared;   // 1: one pool for the whole call, objects numbered across segments
 };
 
 // Segment sizes of a ramp: each segment is half again as long as the one
@@ -112,6 +113,7 @@ inline SegPlan seg_plan(const dla_cache_desc& d, int T, dla_dtype in, bool reado
   p.nch = T > 0 ? (T + p.RL - 1) / p.RL : 0;
   p.first = 0;
   p.fit = 0;
+  p.shared = 0;
   if (!readout || p.nch == 0) {
     p.nch_seg = p.nch > 0 ? p.nch : 1;
     p.nseg = 1;
@@ -136,7 +138,10 @@ inline SegPlan seg_plan(const dla_cache_desc& d, int T, dla_dtype in, bool reado
     p.nch_seg = (p.nch + p.nseg - 1) / p.nseg;
     p.nseg = (p.nch + p.nch_seg - 1) / p.nch_seg;  // no empty segment
   }
-  p.P_cap = d.C * p.nch_seg;
+  // a pipelined call whose copies all fit the budget keeps one pool, so that
+  // no segment starts with copies of the states already present
+  p.shared = (p.first > 0 && p.nch <= fit) ? 1 : 0;
+  p.P_cap = d.C * (p.shared ? p.nch : p.nch_seg);
   return p;
 }
 
@@ -149,8 +154,9 @@ inline SegPlan seg_plan(const dla_cache_desc& d, int T, dla_dtype in, bool reado
 //   init   per head: int32 m0, int32 pad, double G0, double F0[C], int32 perm0[C],
 //          int32 death0[C] (the cache's metadata before the call, and the death
 //          token of the states present before the call)
-//   carry  per head: int32 m, int32 pad, double F[C], int32 perm[C], int32 lead[C]
-//          (update-stage bookkeeping handed from one segment to the next)
+//   carry  per head: int32 m, int32 next_obj, double F[C], int32 perm[C],
+//          int32 lead[C], int32 obj[C] (update-stage bookkeeping handed from one
+//          segment to the next; next_obj and obj only with a shared pool)
 //   scarry per head: int32 m, int32 pad, double Ibar[C], int32 n[C], int32 lead[C],
 //          then from a 16-byte boundary float S[d_k d_v] (the scan's bookkeeping
 //          and its newest state, in accumulator order, handed from one scan
@@ -181,7 +187,7 @@ struct PrefillWS {
 };
 
 __host__ __device__ inline size_t ws_init_stride(int C) { return round_up(16 + 16 * (size_t)C, 256); }
-__host__ __device__ inline size_t ws_carry_stride(int C) { return round_up(8 + 16 * (size_t)C, 256); }
+__host__ __device__ inline size_t ws_carry_stride(int C) { return round_up(8 + 20 * (size_t)C, 256); }
 __host__ __device__ inline size_t ws_scarry_stride(int C, int D) {
   return round_up(round_up(16 + 16 * (size_t)C, 16) + 4 * (size_t)D, 256);
 }
@@ -247,18 +253,22 @@ __host__ __device__ inline InitView init_at(const PrefillWS& w, int h, int C) {
 
 struct CarryView {
   int32_t* m;
+  int32_t* next_obj;
   double* F;
   int32_t* perm;
   int32_t* lead;
+  int32_t* obj;
 };
 
 __host__ __device__ inline CarryView carry_at(const PrefillWS& w, int h, int C) {
   char* p = w.carry + (size_t)h * w.carry_stride;
   CarryView v;
   v.m = reinterpret_cast<int32_t*>(p);
+  v.next_obj = v.m + 1;
   v.F = reinterpret_cast<double*>(p + 8);
   v.perm = reinterpret_cast<int32_t*>(p + 8 + 8 * (size_t)C);
   v.lead = v.perm + C;
+  v.obj = v.lead + C;
   return v;
 }
 

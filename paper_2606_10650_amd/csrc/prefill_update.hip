@@ -146,10 +146,13 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
       sPerm[j] = min(max(cv.perm[j], 0), C - 1);
       sF[j] = cv.F[j];
       sLead[j] = cv.lead[j];
-      sObj[j] = j;
+      sObj[j] = plan.shared ? min(max(cv.obj[j], 0), plan.P_cap - 1) : j;
     }
   }
-  int next_obj = m;
+  // with a shared pool, a later segment continues the object numbering and
+  // its states already have copies (made by the chunk before the segment)
+  int next_obj = (plan.shared && seg > 0) ? min(max(*cv.next_obj, 0), plan.P_cap) : m;
+  const bool fresh = !(plan.shared && seg > 0);
 
   float* states = reinterpret_cast<float*>(a.cache + a.states_offset) + (size_t)h * C * D;
   const double* Gtok = w.Gtok + (size_t)h * T;
@@ -162,7 +165,7 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
 
   // copies of the states present at the segment start
   __syncthreads();
-  if (copies) {
+  if (copies && fresh) {
     for (int j = 0; j < m; ++j) {
       const float* src = states + (size_t)sPerm[j] * D + cg * NC;
       Tin* dst = obj_slice(j);
@@ -253,9 +256,9 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
     const int nrow = min(RL, T - c0);
     const int c1 = c0 + nrow;
     const double Gend = Gtok[c1 - 1];
-    // copies of this chunk's rebuilt states are read by the next chunk of the
-    // segment only
-    const bool make_obj = copies && c + 1 < ce;
+    // copies of this chunk's rebuilt states are read by the next chunk: of the
+    // segment only, or of the call with a shared pool
+    const bool make_obj = copies && c + 1 < (plan.shared ? plan.nch : ce);
     __syncthreads();
     for (int i = tid; i < RL; i += NTHR) sDeath[i] = (i < nrow) ? death[c0 + i] : -1;
     for (int j = tid; j < m; j += NTHR) {
@@ -678,8 +681,12 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
         cv.perm[j] = sPerm[j];
         cv.F[j] = sF[j];
         cv.lead[j] = sLead[j];
+        cv.obj[j] = sObj[j];
       }
-      if (tid == 0) *cv.m = m;
+      if (tid == 0) {
+        *cv.m = m;
+        *cv.next_obj = next_obj;
+      }
     }
   }
 }

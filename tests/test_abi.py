@@ -68,13 +68,14 @@ def test_host_side_errors():
                            ctypes.byref(pe), fake, 1, None, None, None, None, None, fake, 1 << 30,
                            None)
         assert st == dla.DLA_ERR_INVALID_ARG, n_ev
-    # the serial flag needs a larger workspace than the pipelined default
+    # a pipelined call needs no more workspace than a serial one (the same pool
+    # when every state copy fits the budget, plus the scan carry)
     wp, wsr = ctypes.c_size_t(0), ctypes.c_size_t(0)
     d16 = dla.CacheDesc(4, 16, 128, 128, 128)
     assert L.dla_prefill_workspace_size(ctypes.byref(d16), 16384, 1, 0, ctypes.byref(wp)) == 0
     assert L.dla_prefill_workspace_size(ctypes.byref(d16), 16384, 1, dla.DLA_SERIAL_STAGES,
                                         ctypes.byref(wsr)) == 0
-    assert wsr.value > wp.value
+    assert wp.value >= wsr.value and wp.value - wsr.value < (1 << 24)
     # bad dtype
     st = L.dla_prefill(ctypes.byref(d), fake, fake, fake, fake, fake, None, 10, 7, ctypes.byref(p),
                        fake, 1, None, None, None, None, None, fake, 1 << 30, None)
