@@ -162,8 +162,9 @@ dla_status dla_cache_flags(const dla_cache_desc* desc, void* cache, uint32_t* fl
  * chunk, d_k*d_v elements each.  They are bounded to 8 GiB per call: above
  * that the call is split into segments of whole chunks that reuse the space.
  * A pipelined call (see dla_params) splits into segments that grow by half
- * from one sixteenth of the chunks (2, 3, 5, 8 and 14 chunks at 16384 tokens),
- * none larger than the budget allows, and needs correspondingly less; it also
+ * from one sixteenth of the chunks (2, 3, 5, 8 and 14 chunks at 16384 tokens).
+ * Its segments share one pool when all its copies fit the budget; otherwise
+ * none is larger than the budget allows and each reuses the space.  It also
  * keeps the scan's newest state (d_k*d_v floats per head) between segments. */
 dla_status dla_prefill_workspace_size(const dla_cache_desc* desc, int32_t T, dla_dtype in_dtype,
                                       uint32_t flags, size_t* bytes);
