@@ -17,10 +17,22 @@
  * - Calls on different caches may run concurrently; calls on one cache must be
  *   ordered (same stream, or synchronised by the caller).
  * - Shapes come from the cache descriptor: batch B, heads H, capacity C, key
- *   and value head dimensions d_k, d_v.  Supported: d_k, d_v in {64, 128},
- *   1 <= C <= 1024, B*H >= 1.  dla_prefill returns DLA_ERR_UNSUPPORTED when a
- *   stage's per-workgroup working set would not fit in 160 KiB of LDS; every
- *   shape of the supported set, in either input type, fits.
+ *   and value head dimensions d_k, d_v, and the storage type of the states.
+ *   Supported: d_k, d_v in {64, 128}, 1 <= C <= 1024, B*H >= 1.  dla_prefill
+ *   returns DLA_ERR_UNSUPPORTED when a stage's per-workgroup working set would
+ *   not fit in 160 KiB of LDS; every shape of the supported set, in either
+ *   input type, fits.
+ * - The cache remembers the descriptor it was made with (its header, see
+ *   below).  dla_prefill and dla_decode_step cannot read device memory on the
+ *   host without synchronising, so every kernel they enqueue first compares
+ *   the header with the descriptor it was given; on any difference (magic,
+ *   version, B, H, C, d_k, d_v, state type) no kernel reads or writes a state,
+ *   a metadata entry, an output, an export or the workspace, and the first
+ *   kernel of the call sets DLA_FLAG_CACHE_MISMATCH in the header's device
+ *   flags.  The outputs of such a call are left as they were.  The caller
+ *   learns of it from dla_cache_flags (or dla_cache_header_check on a host
+ *   copy of the header).  The cache buffer must hold at least its 256-byte
+ *   header for this check to be safe.
  * - Token tensors are row-major [B][H][T][d] (d fastest); log_gate is
  *   [B][H][T] float32 (the per-token log-decay g_t <= 0 of the base model:
  *   every state decays by exp(g_t) at token t, the caller owns g_t <= 0);
@@ -53,17 +65,28 @@ extern "C" {
 typedef enum {
   DLA_OK = 0,
   DLA_ERR_INVALID_ARG = 1,    /* null pointer, bad size, bad dtype, T < 0 */
-  DLA_ERR_UNSUPPORTED = 2,    /* head dimension or capacity outside the supported set */
-  DLA_ERR_CACHE_MISMATCH = 3, /* descriptor differs from the one the cache was made with */
+  DLA_ERR_UNSUPPORTED = 2,    /* head dimension, capacity or state type outside the supported set */
+  DLA_ERR_CACHE_MISMATCH = 3, /* descriptor differs from the one the cache was made with
+                                 (dla_cache_flags, dla_cache_header_check) */
   DLA_ERR_HIP = 4,            /* a HIP runtime call or kernel launch failed */
   DLA_ERR_WORKSPACE = 5       /* workspace missing or smaller than required */
 } dla_status;
 
 typedef enum { DLA_F32 = 0, DLA_BF16 = 1 } dla_dtype;
 
-/* Shape of a state cache. */
+/* Shape of a state cache.  state_dtype is the storage type of the states:
+ * DLA_F32 keeps every state in float32; DLA_BF16 keeps the states that no
+ * token joins any more (every state but the newest of a head) in bfloat16 and
+ * the newest state of each head in float32.  A closed state changes only when
+ * Alg. 2 merges it with a neighbour, and each such merge is computed in
+ * float32 from the stored values and rounded once to bfloat16, so bfloat16
+ * storage halves the bytes a decode step streams at the cost of one rounding
+ * (relative 2^-9) per closing and per merge.  The newest state, which the
+ * State Information Score compares against (Sec. 3.1), stays float32, so the
+ * boundary and merge decisions do not depend on the storage type. */
 typedef struct {
   int32_t B, H, C, d_k, d_v;
+  int32_t state_dtype; /* dla_dtype: DLA_F32 or DLA_BF16 */
 } dla_cache_desc;
 
 /* Layer parameters.  tau: boundary threshold (b_t = [I_t >= tau], Sec. 3.1);
@@ -112,16 +135,21 @@ typedef struct {
 #define DLA_SKIP_READOUT 1u
 #define DLA_SERIAL_STAGES 2u
 
-/* Device flags kept in the cache header (read with dla_cache_flags). */
+/* Device flags kept in the cache header (read with dla_cache_flags).
+ * DLA_FLAG_BAD_MERGE_OVERRIDE: a merge override outside [0, C-2] was ignored.
+ * DLA_FLAG_CACHE_MISMATCH: a prefill or decode step was given a descriptor
+ * that differs from the cache's header, and did nothing. */
 #define DLA_FLAG_BAD_MERGE_OVERRIDE 1u
+#define DLA_FLAG_CACHE_MISMATCH 2u
 
 /*
  * State cache (Sec. 3.2: chronological states with token counts n_i and
  * aggregated scores I_i, at most C of them), one per head.
  *
  * Layout of the cache buffer (all offsets in bytes, see dla_cache_layout):
- *   header  [0, 256): uint32 magic 0x31414C44 ('DLA1'), uint32 version,
- *           int32 B, H, C, d_k, d_v, uint32 device flags, zero padding.
+ *   header  [0, 256): uint32 magic 0x31414C44 ('DLA1'), uint32 version (2),
+ *           int32 B, H, C, d_k, d_v, uint32 device flags, int32 state_dtype,
+ *           zero padding.
  *   per-head metadata at meta_offset + h * meta_stride, h = b*H + head:
  *           int32 m (live states), int32 0, double G (sum of all absorbed
  *           log-decays), int64 tokens absorbed, int64 0,
@@ -129,14 +157,20 @@ typedef struct {
  *           score), int32 n[C] (token count), int32 perm[C] (physical slot of
  *           each logical state; entries m..C-1 list the free slots).
  *           Arrays are in chronological order (index 0 = oldest).
- *   states  at states_offset: float32 [B*H][C][d_k][d_v] by physical slot.
- *           The true state of logical state j is exp(G - F[j]) * stored slot
- *           perm[j] (states decay lazily: a slot is rescaled only when written).
+ *   states  at states_offset: [B*H][C][d_k][d_v] by physical slot, in the
+ *           state type.  The true state of logical state j is
+ *           exp(G - F[j]) * stored slot perm[j] (states decay lazily: a slot is
+ *           rescaled only when written).
+ *   open    bfloat16 storage only, at open_offset: float32 [B*H][d_k][d_v],
+ *           the newest state m-1 of each head, which then takes the place of
+ *           its slot perm[m-1] (that slot is written when the state closes).
+ *           open_offset is 0 for float32 storage.
  */
 typedef struct {
   size_t meta_offset;
   size_t meta_stride;
   size_t states_offset;
+  size_t open_offset;
   size_t total_bytes;
 } dla_cache_layout;
 
@@ -150,9 +184,17 @@ dla_status dla_state_cache_alloc(const dla_cache_desc* desc, void* dev_buf, size
                                  void* stream);
 
 /* Copy the cache's device flags to *flags and clear them.  Synchronises
- * `stream`. */
+ * `stream`.  Returns DLA_ERR_CACHE_MISMATCH (and leaves the flags) when the
+ * cache's header does not match desc. */
 dla_status dla_cache_flags(const dla_cache_desc* desc, void* cache, uint32_t* flags,
                            void* stream);
+
+/* Check a HOST copy of a cache header (its first 256 bytes, e.g. from a
+ * checkpoint) against desc: DLA_OK and the device flags in *flags (nullable)
+ * when magic, version, B, H, C, d_k, d_v and the state type all match,
+ * DLA_ERR_CACHE_MISMATCH otherwise.  No device work. */
+dla_status dla_cache_header_check(const dla_cache_desc* desc, const void* header,
+                                  uint32_t* flags);
 
 /* Workspace that dla_prefill needs for T tokens of the given input dtype and
  * params flags (DLA_SKIP_READOUT needs less: no state copies).  Besides O(T)
@@ -175,6 +217,11 @@ dla_status dla_prefill_workspace_size(const dla_cache_desc* desc, int32_t T, dla
  * launches, which readout_events can bracket. */
 dla_status dla_prefill_segment_count(const dla_cache_desc* desc, int32_t T, dla_dtype in_dtype,
                                      uint32_t flags, int32_t* nseg);
+
+/* First token of each of those segments, in order: writes min(n, nseg)
+ * entries to the HOST array starts (starts[0] = 0).  Host only. */
+dla_status dla_prefill_segment_starts(const dla_cache_desc* desc, int32_t T, dla_dtype in_dtype,
+                                      uint32_t flags, int32_t* starts, int32_t n);
 
 /*
  * Prefill: absorb T tokens per head into the cache, in order, computing for

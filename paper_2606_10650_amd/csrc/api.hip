@@ -60,6 +60,7 @@ __global__ void cache_init_kernel(char* cache, dla_cache_desc d, size_t meta_off
     hd->dk = d.d_k;
     hd->dv = d.d_v;
     hd->flags = 0u;
+    hd->state_dtype = d.state_dtype;
   }
   Meta M = meta_at(cache + meta_offset + (size_t)h * meta_stride, d.C);
   if (threadIdx.x == 0) {
@@ -99,6 +100,8 @@ static dla_status check_desc(const dla_cache_desc* d) {
   if ((d->d_k != 64 && d->d_k != 128) || (d->d_v != 64 && d->d_v != 128))
     return DLA_ERR_UNSUPPORTED;
   if ((int64_t)d->B * d->H > (int64_t)1 << 24) return DLA_ERR_UNSUPPORTED;
+  if (d->state_dtype != DLA_F32 && d->state_dtype != DLA_BF16) return DLA_ERR_INVALID_ARG;
+  if (d->state_dtype == DLA_BF16) return DLA_ERR_UNSUPPORTED;
   return DLA_OK;
 }
 
@@ -156,13 +159,23 @@ dla_status dla_cache_flags(const dla_cache_desc* desc, void* cache, uint32_t* fl
   if (hipMemcpyAsync(&hd, cache, sizeof(hd), hipMemcpyDeviceToHost, st) != hipSuccess ||
       hipStreamSynchronize(st) != hipSuccess)
     return ret(DLA_ERR_HIP);
-  if (hd.magic != kMagic || hd.B != desc->B || hd.H != desc->H || hd.C != desc->C ||
-      hd.dk != desc->d_k || hd.dv != desc->d_v)
-    return ret(DLA_ERR_CACHE_MISMATCH);
+  if (!header_matches(hd, *desc)) return ret(DLA_ERR_CACHE_MISMATCH);
   *flags = hd.flags;
   hipLaunchKernelGGL(flags_clear_kernel, dim3(1), dim3(64), 0, st, (char*)cache);
   if (hipGetLastError() != hipSuccess || hipStreamSynchronize(st) != hipSuccess)
     return ret(DLA_ERR_HIP);
+  return ret(DLA_OK);
+}
+
+dla_status dla_cache_header_check(const dla_cache_desc* desc, const void* header,
+                                  uint32_t* flags) {
+  dla_status s = check_desc(desc);
+  if (s != DLA_OK) return ret(s);
+  if (!header) return ret(DLA_ERR_INVALID_ARG);
+  CacheHeader hd;
+  memcpy(&hd, header, sizeof(hd));
+  if (!header_matches(hd, *desc)) return ret(DLA_ERR_CACHE_MISMATCH);
+  if (flags) *flags = hd.flags;
   return ret(DLA_OK);
 }
 
@@ -183,6 +196,21 @@ dla_status dla_prefill_segment_count(const dla_cache_desc* desc, int32_t T, dla_
   if (!nseg || T < 0 || !dtype_ok(in_dtype)) return ret(DLA_ERR_INVALID_ARG);
   *nseg = seg_plan(*desc, T, in_dtype, (flags & DLA_SKIP_READOUT) == 0,
                    (flags & DLA_SERIAL_STAGES) != 0).nseg;
+  return ret(DLA_OK);
+}
+
+dla_status dla_prefill_segment_starts(const dla_cache_desc* desc, int32_t T, dla_dtype in_dtype,
+                                      uint32_t flags, int32_t* starts, int32_t n) {
+  dla_status s = check_desc(desc);
+  if (s != DLA_OK) return ret(s);
+  if (!starts || n < 0 || T < 0 || !dtype_ok(in_dtype)) return ret(DLA_ERR_INVALID_ARG);
+  const SegPlan p = seg_plan(*desc, T, in_dtype, (flags & DLA_SKIP_READOUT) == 0,
+                             (flags & DLA_SERIAL_STAGES) != 0);
+  for (int seg = 0; seg < p.nseg && seg < n; ++seg) {
+    int cs, ce;
+    seg_range(p, seg, &cs, &ce);
+    starts[seg] = cs * p.RL < T ? cs * p.RL : T;
+  }
   return ret(DLA_OK);
 }
 
@@ -261,6 +289,7 @@ dla_status dla_decode_step(const dla_cache_desc* desc, void* cache, const void* 
   const dla_cache_layout L = layout_of(*desc);
   DecodeArgs a;
   memset(&a, 0, sizeof(a));
+  a.desc = *desc;
   a.cache = (char*)cache;
   a.meta_offset = L.meta_offset;
   a.meta_stride = L.meta_stride;

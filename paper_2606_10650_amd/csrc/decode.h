@@ -5,6 +5,7 @@
 namespace dla {
 
 struct DecodeArgs {
+  dla_cache_desc desc;
   char* cache;
   size_t meta_offset, meta_stride, states_offset;
   const void* q;

@@ -41,6 +41,10 @@ template <int DK, int DV, typename Tin, typename Tout>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
   using ST = StateTile<DK, DV>;
   constexpr int D = DK * DV;
+  if (!cache_matches(a.cache, a.desc)) {  // refused: the descriptor is not the cache's
+    flag_mismatch(a.cache);
+    return;
+  }
   const int h = blockIdx.x;
   const int tid = threadIdx.x;
   const int C = a.C;
@@ -170,8 +174,11 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
           bb = sArg[w];
           ii = sArgI[w];
         }
-      // no comparable density (NaN scores from non-finite inputs): the first pair
+      // NaN densities (scores from non-finite inputs) compare false, so a
+      // sequential argmin that starts at pair 0 never moves to them, and stays
+      // at pair 0 when pair 0's density is NaN or none is a number
       if (ii < 0 || ii > C - 2) ii = 0;
+      if (__builtin_isnan((sI[0] + sI[1]) / (double)(sN[0] + sN[1]))) ii = 0;
       if (a.m_ovr && a.m_ovr[h] != -1) {
         const int f = a.m_ovr[h];
         if (f >= 0 && f <= C - 2)

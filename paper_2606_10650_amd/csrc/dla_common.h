@@ -9,7 +9,7 @@
 namespace dla {
 
 constexpr uint32_t kMagic = 0x31414C44u;  // 'DLA1'
-constexpr uint32_t kVersion = 1u;
+constexpr uint32_t kVersion = 2u;
 constexpr size_t kHeaderBytes = 256;
 
 struct CacheHeader {
@@ -17,7 +17,27 @@ struct CacheHeader {
   uint32_t version;
   int32_t B, H, C, dk, dv;
   uint32_t flags;
+  int32_t state_dtype;
 };
+
+// Whether a cache header describes the descriptor a call was given.  Every
+// kernel of a prefill or decode step checks it before touching anything else,
+// so a call whose descriptor differs from the cache's (a larger capacity, more
+// heads, another state type) cannot index past the buffer.
+__host__ __device__ inline bool header_matches(const CacheHeader& hd, const dla_cache_desc& d) {
+  return hd.magic == kMagic && hd.version == kVersion && hd.B == d.B && hd.H == d.H &&
+         hd.C == d.C && hd.dk == d.d_k && hd.dv == d.d_v && hd.state_dtype == d.state_dtype;
+}
+
+__device__ __forceinline__ bool cache_matches(const char* cache, const dla_cache_desc& d) {
+  return header_matches(*reinterpret_cast<const CacheHeader*>(cache), d);
+}
+
+// The first kernel of a call records a refused call in the header's flags.
+__device__ __forceinline__ void flag_mismatch(char* cache) {
+  if (blockIdx.x == 0 && threadIdx.x == 0)
+    atomicOr(&reinterpret_cast<CacheHeader*>(cache)->flags, DLA_FLAG_CACHE_MISMATCH);
+}
 
 __host__ __device__ inline size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -48,13 +68,26 @@ __host__ __device__ inline Meta meta_at(char* base, int C) {
   return r;
 }
 
+// Bytes of one stored state element (float32 or bfloat16 storage).
+__host__ __device__ inline size_t state_elem_bytes(const dla_cache_desc& d) {
+  return d.state_dtype == DLA_BF16 ? 2 : 4;
+}
+
 inline dla_cache_layout layout_of(const dla_cache_desc& d) {
   dla_cache_layout L;
   const size_t nh = (size_t)d.B * d.H;
+  const size_t D = (size_t)d.d_k * d.d_v;
   L.meta_offset = kHeaderBytes;
   L.meta_stride = meta_stride(d.C);
   L.states_offset = round_up(L.meta_offset + nh * L.meta_stride, 256);
-  L.total_bytes = L.states_offset + nh * (size_t)d.C * d.d_k * d.d_v * sizeof(float);
+  const size_t end = L.states_offset + nh * (size_t)d.C * D * state_elem_bytes(d);
+  if (d.state_dtype == DLA_BF16) {
+    L.open_offset = round_up(end, 256);
+    L.total_bytes = L.open_offset + nh * D * sizeof(float);
+  } else {
+    L.open_offset = 0;
+    L.total_bytes = end;
+  }
   return L;
 }
 

@@ -344,35 +344,45 @@ inline hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s, const Stag
   if ((e = rec(1, s)) != hipSuccess) return e;
   hipStream_t side = s;
   hipEvent_t* pev = nullptr;
+  bool forked = false;
+  // After the fork, an error still joins the second stream into s before it
+  // is returned, so that nothing enqueued on the second stream can outlive the
+  // call's ordering on s (the caller may free the workspace once s is done).
+  auto fail = [&](hipError_t err) -> hipError_t {
+    if (forked && hipEventRecord(pev[0], side) == hipSuccess) (void)hipStreamWaitEvent(s, pev[0], 0);
+    return err;
+  };
   if (pipe) {
     // event 0 forks the side stream after the frames; event 1 + k marks the
     // end of scan segment k
     if ((e = pipe_resources(s, p.nseg + 1, &side, &pev)) != hipSuccess) return e;
     if ((e = hipEventRecord(pev[0], s)) != hipSuccess) return e;
     if ((e = hipStreamWaitEvent(side, pev[0], 0)) != hipSuccess) return e;
+    forked = true;
     for (int seg = 0; seg < p.nseg; ++seg) {
       int cs, ce;
       seg_range(p, seg, &cs, &ce);
       const int tb = cs * p.RL;
       const int te = (seg + 1 == p.nseg) ? a.T : ce * p.RL;
-      if ((e = launch_prefill_scan(a, tb, te, side)) != hipSuccess) return e;
-      if ((e = hipEventRecord(pev[1 + seg], side)) != hipSuccess) return e;
+      if ((e = launch_prefill_scan(a, tb, te, side)) != hipSuccess) return fail(e);
+      if ((e = hipEventRecord(pev[1 + seg], side)) != hipSuccess) return fail(e);
     }
-    if ((e = rec(2, side)) != hipSuccess) return e;
+    if ((e = rec(2, side)) != hipSuccess) return fail(e);
   } else {
     if ((e = launch_prefill_scan(a, 0, a.T, s)) != hipSuccess) return e;
     if ((e = rec(2, s)) != hipSuccess) return e;
   }
   for (int seg = 0; seg < p.nseg; ++seg) {
-    if (pipe && (e = hipStreamWaitEvent(s, pev[1 + seg], 0)) != hipSuccess) return e;
-    if ((e = launch_prefill_update(a, p, seg, s)) != hipSuccess) return e;
-    if (seg == p.nseg - 1 && (e = rec(3, s)) != hipSuccess) return e;
+    if (pipe && (e = hipStreamWaitEvent(s, pev[1 + seg], 0)) != hipSuccess) return fail(e);
+    if ((e = launch_prefill_update(a, p, seg, s)) != hipSuccess) return fail(e);
+    if (seg == p.nseg - 1 && (e = rec(3, s)) != hipSuccess) return fail(e);
     if (!a.skip_readout) {
-      if ((e = rrec(seg, 0)) != hipSuccess) return e;
-      if ((e = launch_prefill_readout(a, p, seg, s)) != hipSuccess) return e;
-      if ((e = rrec(seg, 1)) != hipSuccess) return e;
+      if ((e = rrec(seg, 0)) != hipSuccess) return fail(e);
+      if ((e = launch_prefill_readout(a, p, seg, s)) != hipSuccess) return fail(e);
+      if ((e = rrec(seg, 1)) != hipSuccess) return fail(e);
     }
   }
+  // (the last segment's wait on pev[nseg] has joined the second stream)
   return rec(4, s);
 }
 

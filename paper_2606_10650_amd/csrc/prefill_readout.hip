@@ -99,6 +99,7 @@ __device__ __forceinline__ int tile_of(int wv, int nt) {
 template <int DK, int DV, typename Tin, typename Tout>
 __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, PrefillWS w,
                                                                SegPlan plan, int seg, int lw) {
+  if (!cache_matches(a.cache, a.desc)) return;  // refused call (see the prep kernel)
   using FR = Frag<Tin>;
   using FT = typename FR::T;
   using P = RO<DK, Tin>;
@@ -619,11 +620,13 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
         }
       } else {
         // the token's own block: causal mask, decay exp(G_t - G_s) per element
+        // (the mask selects zero rather than multiplying by it, so that a
+        // non-finite key later in the block cannot reach an earlier token)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int s = 32 * sb + out_row(r, lane);
           const float lr = uni ? lu : lam_at(before[nt] + upto(r));
-          pt[i][r] *= (rv[nt] && s <= trn) ? lr * __expf(gtok[nt] - sGc[s]) : 0.f;
+          pt[i][r] = (rv[nt] && s <= trn) ? pt[i][r] * (lr * __expf(gtok[nt] - sGc[s])) : 0.f;
         }
       }
       before[nt] += __popc(word[i]);

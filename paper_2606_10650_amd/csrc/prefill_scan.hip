@@ -41,6 +41,10 @@ namespace dla {
 // stage 1
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void prefill_prep_kernel(PrefillArgs a, PrefillWS w) {
+  if (!cache_matches(a.cache, a.desc)) {  // refused: the descriptor is not the cache's
+    flag_mismatch(a.cache);
+    return;
+  }
   const int h = blockIdx.x;
   const int tid = threadIdx.x;
   const int C = a.desc.C;
@@ -146,6 +150,7 @@ __device__ __forceinline__ float score_f(float a, float b, float c, float D, flo
 template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, PrefillWS w, int tb,
                                                             int te) {
+  if (!cache_matches(a.cache, a.desc)) return;  // refused call (see the prep kernel)
   using FR = Frag<Tin>;
   using FT = typename FR::T;
   using P = ScanP<DK, DV, Tin>;
@@ -591,9 +596,11 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
             }
           }
           wave_argmin_d(best, bi);
-          // no comparable density (NaN scores from non-finite inputs): the first
-          // pair, as a sequential argmin that starts at index 0 would pick
+          // NaN densities (scores from non-finite inputs) compare false, so a
+          // sequential argmin that starts at pair 0 never moves to them, and
+          // stays at pair 0 when pair 0's density is NaN or none is a number
           istar = (bi >= 0 && bi <= C - 2) ? bi : 0;
+          if (__builtin_isnan((sIb[0] + sIb[1]) / (double)(sN[0] + sN[1]))) istar = 0;
           const int fo = sMo[tstar];
           if (fo != -1) {
             if (fo >= 0 && fo <= C - 2)

@@ -72,6 +72,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, 
 template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, PrefillWS w,
                                                               SegPlan plan, int seg) {
+  if (!cache_matches(a.cache, a.desc)) return;  // refused call (see the prep kernel)
   using FR = Frag<Tin>;
   using FT = typename FR::T;
   using U = UpdP<DK, Tin>;

@@ -22,15 +22,18 @@ DLA_F32, DLA_BF16 = 0, 1
 DLA_SKIP_READOUT = 1
 DLA_SERIAL_STAGES = 2
 DLA_FLAG_BAD_MERGE_OVERRIDE = 1
+DLA_FLAG_CACHE_MISMATCH = 2
 
 EXPORTED = ("dla_cache_layout_of", "dla_state_cache_alloc", "dla_cache_flags",
-            "dla_prefill_workspace_size", "dla_prefill_segment_count", "dla_prefill",
-            "dla_decode_step", "dla_status_string", "dla_get_last_error")
+            "dla_cache_header_check", "dla_prefill_workspace_size", "dla_prefill_segment_count",
+            "dla_prefill_segment_starts", "dla_prefill", "dla_decode_step", "dla_status_string",
+            "dla_get_last_error")
 
 
 class CacheDesc(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("C", ctypes.c_int32),
-                ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32)]
+                ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32),
+                ("state_dtype", ctypes.c_int32)]
 
 
 class Params(ctypes.Structure):
@@ -44,7 +47,8 @@ PREFILL_STAGES = ("frames", "scan", "update", "readout")
 
 class Layout(ctypes.Structure):
     _fields_ = [("meta_offset", ctypes.c_size_t), ("meta_stride", ctypes.c_size_t),
-                ("states_offset", ctypes.c_size_t), ("total_bytes", ctypes.c_size_t)]
+                ("states_offset", ctypes.c_size_t), ("open_offset", ctypes.c_size_t),
+                ("total_bytes", ctypes.c_size_t)]
 
 
 class DLAError(RuntimeError):
@@ -68,10 +72,15 @@ def lib():
                                             ctypes.POINTER(ctypes.c_size_t), P]
         L.dla_cache_flags.argtypes = [ctypes.POINTER(CacheDesc), P, ctypes.POINTER(ctypes.c_uint32),
                                       P]
+        L.dla_cache_header_check.argtypes = [ctypes.POINTER(CacheDesc), P,
+                                             ctypes.POINTER(ctypes.c_uint32)]
         L.dla_prefill_workspace_size.argtypes = [ctypes.POINTER(CacheDesc), ctypes.c_int32, I,
                                                  ctypes.c_uint32, ctypes.POINTER(ctypes.c_size_t)]
         L.dla_prefill_segment_count.argtypes = [ctypes.POINTER(CacheDesc), ctypes.c_int32, I,
                                                 ctypes.c_uint32, ctypes.POINTER(ctypes.c_int32)]
+        L.dla_prefill_segment_starts.argtypes = [ctypes.POINTER(CacheDesc), ctypes.c_int32, I,
+                                                 ctypes.c_uint32, ctypes.POINTER(ctypes.c_int32),
+                                                 ctypes.c_int32]
         L.dla_prefill.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, ctypes.c_int32, I,
                                   ctypes.POINTER(Params), P, I, P, P, P, P, P, P, ctypes.c_size_t, P]
         L.dla_decode_step.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, I,
@@ -80,7 +89,8 @@ def lib():
         L.dla_status_string.restype = ctypes.c_char_p
         L.dla_get_last_error.argtypes = []
         for name in ("dla_cache_layout_of", "dla_state_cache_alloc", "dla_cache_flags",
-                     "dla_prefill_workspace_size", "dla_prefill_segment_count", "dla_prefill",
+                     "dla_cache_header_check", "dla_prefill_workspace_size",
+                     "dla_prefill_segment_count", "dla_prefill_segment_starts", "dla_prefill",
                      "dla_decode_step", "dla_get_last_error"):
             getattr(L, name).restype = I
         _lib = L
@@ -121,41 +131,55 @@ def _stream(device) -> ctypes.c_void_p:
 
 @dataclasses.dataclass
 class StateCache:
-    """A device state cache (Sec. 3.2) for B*H heads of capacity C."""
+    """A device state cache (Sec. 3.2) for B*H heads of capacity C.  state_dtype
+    is the storage type of the states (DLA_F32, or DLA_BF16: closed states in
+    bfloat16, the newest state of each head in float32)."""
     B: int
     H: int
     C: int
     d_k: int
     d_v: int
     buf: "object"  # torch uint8 tensor on the device
+    state_dtype: int = DLA_F32
 
     @property
     def desc(self) -> CacheDesc:
-        return CacheDesc(self.B, self.H, self.C, self.d_k, self.d_v)
+        return CacheDesc(self.B, self.H, self.C, self.d_k, self.d_v, self.state_dtype)
 
     @property
     def device(self):
         return self.buf.device
 
 
-def cache_layout(B, H, C, d_k, d_v) -> Layout:
+def cache_layout(B, H, C, d_k, d_v, state_dtype: int = DLA_F32) -> Layout:
     L = Layout()
-    _check(lib().dla_cache_layout_of(ctypes.byref(CacheDesc(B, H, C, d_k, d_v)), ctypes.byref(L)),
-           "dla_cache_layout_of")
+    _check(lib().dla_cache_layout_of(ctypes.byref(CacheDesc(B, H, C, d_k, d_v, state_dtype)),
+                                     ctypes.byref(L)), "dla_cache_layout_of")
     return L
 
 
-def cache_alloc(B: int, H: int, C: int, d_k: int, d_v: int, device="cuda") -> StateCache:
+def cache_alloc(B: int, H: int, C: int, d_k: int, d_v: int, device="cuda",
+                state_dtype: int = DLA_F32) -> StateCache:
     """Allocate and initialise an empty cache (two-call dla_state_cache_alloc)."""
     torch = _torch()
-    d = CacheDesc(B, H, C, d_k, d_v)
+    d = CacheDesc(B, H, C, d_k, d_v, state_dtype)
     n = ctypes.c_size_t(0)
     _check(lib().dla_state_cache_alloc(ctypes.byref(d), None, ctypes.byref(n), None),
            "dla_state_cache_alloc(size)")
     buf = torch.empty(n.value, dtype=torch.uint8, device=device)
     _check(lib().dla_state_cache_alloc(ctypes.byref(d), _ptr(buf), ctypes.byref(n),
                                        _stream(buf.device)), "dla_state_cache_alloc")
-    return StateCache(B, H, C, d_k, d_v, buf)
+    return StateCache(B, H, C, d_k, d_v, buf, state_dtype)
+
+
+def header_check(desc: CacheDesc, header: bytes) -> int:
+    """dla_cache_header_check on a host copy of a cache header: the device
+    flags, or DLAError (DLA_ERR_CACHE_MISMATCH) when it does not match desc."""
+    f = ctypes.c_uint32(0)
+    buf = ctypes.create_string_buffer(bytes(header), len(header))
+    _check(lib().dla_cache_header_check(ctypes.byref(desc), buf, ctypes.byref(f)),
+           "dla_cache_header_check")
+    return int(f.value)
 
 
 def cache_flags(cache: StateCache) -> int:
@@ -189,6 +213,18 @@ def prefill_segments(cache: StateCache, T: int, dtype=None, skip_readout: bool =
                                            _flags(skip_readout, serial), ctypes.byref(n)),
            "dla_prefill_segment_count")
     return int(n.value)
+
+
+def prefill_segment_starts(cache: StateCache, T: int, dtype=None, skip_readout: bool = False,
+                           serial: bool = False) -> list:
+    """First token of each segment of a prefill of T tokens."""
+    code = DLA_BF16 if dtype is None else _dtype_code(dtype)
+    n = prefill_segments(cache, T, dtype, skip_readout, serial)
+    arr = (ctypes.c_int32 * n)()
+    _check(lib().dla_prefill_segment_starts(ctypes.byref(cache.desc), int(T), code,
+                                            _flags(skip_readout, serial), arr, n),
+           "dla_prefill_segment_starts")
+    return list(arr)
 
 
 def _event_array(events):
@@ -298,34 +334,54 @@ def decode_step(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5, ep
 
 
 def cache_export(cache: StateCache, heads=None) -> dict:
-    """Read a cache back to host memory and decode its layout: per head m, G,
-    tokens, and in chronological order F, Ibar, n, and the true (decayed)
-    states exp(G - F_j) S~_perm[j] as float64 [n_heads, C, d_k, d_v] (entries
-    j >= m are zero)."""
-    L = cache_layout(cache.B, cache.H, cache.C, cache.d_k, cache.d_v)
-    raw = cache.buf.cpu().numpy()
+    """Read a cache back to host memory and decode its byte layout (dla.h): per
+    head m, G, tokens, and in chronological order F, Ibar, n, perm, and the
+    stored values of each state as float64 [n_heads, C, d_k, d_v] (entries
+    j >= m are zero).  Stored values are in the state's own frame: the true
+    state is exp(G - F[j]) times them (lazy decay).  With bfloat16 storage the
+    newest state's values come from the float32 open region.  Only the bytes of
+    the requested heads are copied."""
+    sd = cache.state_dtype
+    L = cache_layout(cache.B, cache.H, cache.C, cache.d_k, cache.d_v, sd)
     nh = cache.B * cache.H
     heads = list(range(nh)) if heads is None else list(heads)
     C, dk, dv = cache.C, cache.d_k, cache.d_v
+    D = dk * dv
+    es = 2 if sd == DLA_BF16 else 4
+    buf = cache.buf
+
+    def host(a, b):
+        return buf[a:b].cpu().numpy()
+
+    hdr = host(0, 256)
     res = {"m": np.zeros(len(heads), np.int32), "G": np.zeros(len(heads)),
            "tokens": np.zeros(len(heads), np.int64), "F": np.zeros((len(heads), C)),
            "ibar": np.zeros((len(heads), C)), "n": np.zeros((len(heads), C), np.int32),
            "perm": np.zeros((len(heads), C), np.int32),
-           "S": np.zeros((len(heads), C, dk, dv)), "flags": int(raw[28:32].view(np.uint32)[0])}
-    states = raw[L.states_offset:].view(np.float32).reshape(nh, C, dk, dv)
+           "stored": np.zeros((len(heads), C, dk, dv)),
+           "flags": int(hdr[28:32].view(np.uint32)[0])}
     for i, h in enumerate(heads):
         base = L.meta_offset + h * L.meta_stride
-        mb = raw[base:base + L.meta_stride]
+        mb = host(base, base + L.meta_stride)
         m = int(mb[0:4].view(np.int32)[0])
         res["m"][i] = m
         res["G"][i] = mb[8:16].view(np.float64)[0]
         res["tokens"][i] = mb[16:24].view(np.int64)[0]
-        F = mb[32:32 + 8 * C].view(np.float64)
-        res["F"][i] = F
+        res["F"][i] = mb[32:32 + 8 * C].view(np.float64)
         res["ibar"][i] = mb[32 + 8 * C:32 + 16 * C].view(np.float64)
         res["n"][i] = mb[32 + 16 * C:32 + 20 * C].view(np.int32)
         perm = mb[32 + 20 * C:32 + 24 * C].view(np.int32)
         res["perm"][i] = perm
+        s0 = L.states_offset + h * C * D * es
+        raw = host(s0, s0 + C * D * es)
+        if sd == DLA_BF16:
+            slots = (raw.view(np.uint16).astype(np.uint32) << 16).view(np.float32)
+        else:
+            slots = raw.view(np.float32)
+        slots = slots.reshape(C, dk, dv)
         for j in range(m):
-            res["S"][i, j] = np.exp(res["G"][i] - F[j]) * states[h, perm[j]].astype(np.float64)
+            res["stored"][i, j] = slots[perm[j]]
+        if sd == DLA_BF16 and m > 0:
+            o0 = L.open_offset + h * D * 4
+            res["stored"][i, m - 1] = host(o0, o0 + D * 4).view(np.float32).reshape(dk, dv)
     return res

@@ -18,7 +18,8 @@ What pins what (paper passages in brackets):
   * closed forms of the score: identical tokens, orthogonal keys, scalar states
     (sign flips), scale invariance, 0 <= I <= 2, and the rank-one expansion of
     the score  [eq. importance_score, RMSNorm remark of Sec. 3.1];
-  * hand-computed merge schedule on scalar states  (tests/golden/);
+  * hand-computed merge schedules on scalar states  (tests/golden/), including
+    the near-tie margins of the parity protocol and the merge override;
   * conservation (counts, scores, states) and C-independence of boundaries.
 """
 from __future__ import annotations
@@ -359,6 +360,127 @@ def pin_continuation(lib_path=None):
         assert np.abs(o - full["out"]).max() < 1e-12 * np.abs(full["out"]).max()
 
 
+def _golden_value(x):
+    return np.inf if x == "inf" else float(x)
+
+
+def pin_margins_and_merge_overrides(lib_path=None):
+    """The near-tie margins the parity protocol reads and the merge override,
+    against a schedule worked out by hand (tests/golden/scalar_margins.json;
+    Sec. 3.1 boundary indicator, Alg. 2 / Sec. 3.2 lowest-density merge):
+    margin_b = |I - tau| for a freely decided boundary (infinite when forced or
+    at the first token), margin_m = (d2 - d1) / d1 over the two lowest pair
+    densities of a freely decided capacity merge (infinite otherwise), the
+    override honoured only at a capacity merge, and an out-of-range override
+    rejected."""
+    with open(os.path.join(GOLDEN, "scalar_margins.json")) as fh:
+        gold = json.load(fh)
+    kk = np.array(gold["k"], np.float64)[None, :, None]
+    vv = np.array(gold["v"], np.float64)[None, :, None]
+    g = np.array(gold["g"], np.float64)[None, :]
+    T = kk.shape[1]
+    q = np.ones_like(kk)
+    lam = np.tile(np.array(gold["lambda_row"], np.float64), (1, T, 1))
+    bo = np.array(gold["boundary_override"], np.int8)[None, :]
+    mo = np.array(gold["merge_override"], np.int32)[None, :]
+    r = oracle_forward(kk, vv, g, gold["C"], gold["tau"], q=q, lam=lam, eps=0.0, eps_rms=0.0,
+                       b_override=bo, m_override=mo, lib_path=lib_path)
+    assert r["score"][0].tolist() == gold["score"], r["score"][0].tolist()
+    assert r["b"][0].tolist() == gold["b"], r["b"][0].tolist()
+    assert r["merge"][0].tolist() == gold["merge"], r["merge"][0].tolist()
+    assert r["m"][0].tolist() == gold["m"], r["m"][0].tolist()
+    for key in ("margin_b", "margin_m"):
+        exp = np.array([_golden_value(x) for x in gold[key]])
+        got = r[key][0]
+        assert (np.isinf(exp) == np.isinf(got)).all(), (key, got.tolist())
+        fin = np.isfinite(exp)
+        assert np.abs(got[fin] - exp[fin]).max() < 1e-12, (key, got.tolist())
+    c = r["cache"]
+    m = int(c.m[0])
+    assert c.n[0, :m].tolist() == gold["final_n"], c.n[0].tolist()
+    assert c.ibar[0, :m].tolist() == gold["final_ibar"], c.ibar[0].tolist()
+    assert np.allclose(c.S[0, :m, 0, 0], gold["final_S"], rtol=0, atol=1e-12)
+    assert np.allclose(r["out"][0, :, 0], gold["out"], rtol=0, atol=1e-12)
+    # an override outside [0, C - 2] at a capacity merge is an error
+    for case in gold["bad_merge_override_cases"]:
+        bad = mo.copy()
+        bad[0, case["t"]] = case["value"]
+        try:
+            oracle_forward(kk, vv, g, gold["C"], gold["tau"], eps=0.0, eps_rms=0.0,
+                           b_override=bo, m_override=bad, full=False, lib_path=lib_path)
+        except ValueError:
+            continue
+        raise AssertionError(f"merge override {case['value']} at t={case['t']} accepted")
+
+
+def pin_margin_b_chord_distance(lib_path=None):
+    """With d_k = 1, d_v = 2 and eps = eps_rms = 0, RMSNorm scales a state to
+    norm sqrt(2) along its direction, so the score is the chord distance
+    |u - w| = 2 sin(theta / 2) between the unit directions of the token value
+    and of the newest state (Sec. 3.1).  Replaying the boundary rule with that
+    closed form on random angles fixes every score, boundary and the margin
+    |I - tau| of each free decision; C = 2 (one candidate pair, so no tie is
+    possible) gives an infinite merge margin at every merge."""
+    rng = np.random.default_rng(5)
+    T, tau = 120, 1.2
+    phi = rng.uniform(0.0, 2.0 * np.pi, T)
+    amp = rng.uniform(0.5, 2.0, T)
+    v = np.stack([amp * np.cos(phi), amp * np.sin(phi)], axis=1)[None]
+    k = np.ones((1, T, 1))
+    g = np.zeros((1, T))
+    for C in (T, 2):
+        r = oracle_forward(k, v, g, C, tau, eps=0.0, eps_rms=0.0, full=False,
+                           lib_path=lib_path)
+        newest = None
+        for t in range(T):
+            if newest is None:
+                exp_I, exp_b = 0.0, 1
+            else:
+                u = v[0, t] / np.linalg.norm(v[0, t])
+                w = newest / np.linalg.norm(newest)
+                exp_I = float(np.linalg.norm(u - w))
+                exp_b = 1 if exp_I >= tau else 0
+            assert abs(r["score"][0, t] - exp_I) < 1e-12, (C, t, r["score"][0, t], exp_I)
+            assert r["b"][0, t] == exp_b, (C, t)
+            if t == 0:
+                assert np.isinf(r["margin_b"][0, t])
+            else:
+                assert abs(r["margin_b"][0, t] - abs(exp_I - tau)) < 1e-12, (C, t)
+            newest = v[0, t].copy() if exp_b else newest + v[0, t]
+        merges = r["merge"][0] >= 0
+        if C == 2:
+            assert merges.any() and np.isinf(r["margin_m"][0][merges]).all()
+        else:
+            assert not merges.any()
+        assert np.isinf(r["margin_m"][0][~merges]).all()
+
+
+def pin_direct_evaluation_matches_the_recurrence(lib_path=None):
+    """The direct evaluator (oracle/direct.py: states as decayed sums over
+    their token ranges, the readout of eq. capacity_bounded_output evaluated
+    per token) agrees with the token-by-token recurrence on the recurrence's
+    own decisions: sampled outputs and the final cache, with merges, ragged
+    decays, lambda and C = 1."""
+    from oracle import direct
+    for name, kw, C in (("cfg1", dict(T=300, n_seg=20, rho2=0.9), 4),
+                        ("cfg1_iid", dict(T=200), 6),
+                        ("cfg1", dict(T=150), 1)):
+        w, q, k, v, g, lam = f64_inputs(name, C=C, **kw)
+        lam = lam[:, :, :C]
+        r = oracle_forward(k, v, g, C, w.tau, q=q, lam=lam, lib_path=lib_path)
+        T = q.shape[1]
+        tokens = [0, 1, T // 3, T // 2 + 1, T - 2, T - 1]
+        for h in range(q.shape[0]):
+            o = direct.outputs_at(q[h], k[h], v[h], g[h], lam[h], r["b"][h], r["merge"][h], C,
+                                  tokens)
+            ref = r["out"][h, tokens]
+            assert np.abs(o - ref).max() < 1e-11 * max(np.abs(ref).max(), 1e-30), (name, h)
+            m, n, S = direct.final_states(k[h], v[h], g[h], r["b"][h], r["merge"][h], C)
+            c = r["cache"]
+            assert m == c.m[h] and (n[:m] == c.n[h, :m]).all(), (name, h)
+            assert np.abs(S[:m] - c.S[h, :m]).max() < 1e-11 * np.abs(c.S[h, :m]).max()
+
+
 ALL_PINS = [
     pin_lambda_one_is_gated_linear_attention,
     pin_single_state_and_one_state_per_token,
@@ -371,4 +493,7 @@ ALL_PINS = [
     pin_conservation,
     pin_boundaries_independent_of_capacity,
     pin_continuation,
+    pin_margins_and_merge_overrides,
+    pin_margin_b_chord_distance,
+    pin_direct_evaluation_matches_the_recurrence,
 ]

@@ -94,6 +94,42 @@ def test_host_side_errors():
     assert ws.value >= 6 * 1000 * 12
 
 
+def _header(B, H, C, dk, dv, flags=0, state_dtype=0, magic=0x31414C44, version=2):
+    import struct
+    return struct.pack("<II5iIi", magic, version, B, H, C, dk, dv, flags, state_dtype) + bytes(220)
+
+
+def test_header_check_on_a_host_copy():
+    """dla_cache_header_check (host only) accepts the header a cache of the
+    descriptor is made with and refuses any difference: magic, version, shape
+    or state type."""
+    from paper_2606_10650_amd import dla
+    d = dla.CacheDesc(2, 3, 8, 64, 128)
+    assert dla.header_check(d, _header(2, 3, 8, 64, 128, flags=1)) == 1
+    for bad in (_header(2, 3, 8, 64, 128, magic=0x31414C45), _header(2, 3, 8, 64, 128, version=1),
+                _header(2, 3, 16, 64, 128), _header(2, 4, 8, 64, 128), _header(1, 3, 8, 64, 128),
+                _header(2, 3, 8, 128, 128), _header(2, 3, 8, 64, 64),
+                _header(2, 3, 8, 64, 128, state_dtype=1)):
+        with pytest.raises(dla.DLAError) as e:
+            dla.header_check(d, bad)
+        assert e.value.status == dla.DLA_ERR_CACHE_MISMATCH
+    L = dla.lib()
+    assert L.dla_cache_header_check(ctypes.byref(d), None, None) == dla.DLA_ERR_INVALID_ARG
+
+
+def test_state_type_of_the_descriptor():
+    """The descriptor's state type must be float32 or bfloat16; float32 caches
+    have no open region."""
+    from paper_2606_10650_amd import dla
+    L = dla.lib()
+    lay = dla.Layout()
+    d = dla.CacheDesc(2, 3, 8, 64, 128, 7)
+    assert L.dla_cache_layout_of(ctypes.byref(d), ctypes.byref(lay)) == dla.DLA_ERR_INVALID_ARG
+    d = dla.CacheDesc(2, 3, 8, 64, 128, dla.DLA_F32)
+    assert L.dla_cache_layout_of(ctypes.byref(d), ctypes.byref(lay)) == dla.DLA_OK
+    assert lay.open_offset == 0
+
+
 def test_missing_library_fails_loudly(tmp_path, monkeypatch):
     from paper_2606_10650_amd import dla
     monkeypatch.setattr(dla, "_lib", None)
@@ -145,3 +181,8 @@ def test_prefill_segment_counts():
     assert count(1, 2, 16, 128, 1100, dla.DLA_BF16, 0) == 2
     assert count(1, 2, 16, 128, 0, dla.DLA_BF16, 0) == 1
     assert count(1, 2, 16, 128, 1100, dla.DLA_BF16, dla.DLA_SKIP_READOUT) == 1
+    # segment starts: the ramp of the 16k-token workload (2, 3, 5, 8, 14 chunks of 512)
+    desc = dla.CacheDesc(4, 16, 128, 128, 128)
+    arr = (ctypes.c_int32 * 8)(*([-7] * 8))
+    assert L.dla_prefill_segment_starts(ctypes.byref(desc), 16384, dla.DLA_BF16, 0, arr, 8) == 0
+    assert list(arr)[:6] == [0, 1024, 2560, 5120, 9216, -7]

@@ -1,0 +1,196 @@
+"""GPU parity at the workloads' full sizes, in the launch configuration the
+benchmark times.  The float64 oracle decides every boundary and merge of the
+sampled heads (decisions mode); outputs at sampled tokens and the final
+caches are then evaluated straight from the definitions (oracle/direct.py,
+pinned to the oracle's full recurrence), so many heads can be checked at
+64k tokens.  Decisions bit-exact (near ties pinned from the oracle),
+outputs within 2e-2 (bfloat16 inputs), cache states within 1e-4."""
+import numpy as np
+import pytest
+
+from oracle import OracleCache, direct, oracle_forward
+from tests import harness as H
+from paper_2606_10650_amd.workloads import WORKLOADS, make_inputs, make_decode_tokens
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _report(tag, **kw):
+    print(f"[{tag}] " + " ".join(f"{k}={v}" for k, v in kw.items()), flush=True)
+
+
+def spread_heads(B, H, n, seed=123):
+    """n distinct (b, h) pairs: the four corners of the (batch, head) grid,
+    then seeded random ones; returned as flat indices b * H + h, sorted."""
+    pairs = [(0, 0), (B - 1, H - 1), (0, H - 1), (B - 1, 0)]
+    rng = np.random.default_rng(seed)
+    out = []
+    for p in pairs:
+        if p not in out:
+            out.append(p)
+    while len(out) < min(n, B * H):
+        p = (int(rng.integers(B)), int(rng.integers(H)))
+        if p not in out:
+            out.append(p)
+    return sorted(b * H + h for b, h in out)
+
+
+def windows(T, RL, starts):
+    """Sampled output tokens: a window inside a chunk (a third of the way in),
+    one straddling the start of the third pipelined segment (the last one if
+    fewer), the first 64 tokens of the last segment (which reads the copies
+    made for it when the pool restarts), and the last 64 tokens."""
+    nch = (T + RL - 1) // RL
+    c = nch // 3
+    w = [(c * RL + 200, c * RL + 264)]
+    s = starts[2] if len(starts) > 2 else starts[-1]
+    if s > 0:
+        w.append((s - 32, s + 32))
+    w.append((starts[-1], starts[-1] + 64))
+    w.append((T - 64, T))
+    toks = sorted({t for a, e in w for t in range(max(a, 0), min(e, T))})
+    return toks, w
+
+
+@pytest.mark.parametrize("name", ["cfg2", "cfg3", "cfg4"])
+def test_prefill_full_size_sampled_heads(name):
+    """A prefill workload at its full size (cfg3 is the 16k-token workload the
+    benchmark times; cfg4 at 64k tokens and C = 256 runs segments that restart
+    their pool).  Eight heads spread over batch and head: every decision, the
+    outputs of four windows (inside a chunk, across a segment start, the first
+    chunk of the last segment, the end) and the final cache."""
+    torch = _torch()
+    from paper_2606_10650_amd import dla
+    w = WORKLOADS[name]
+    nh = w.B * w.H
+    heads = spread_heads(w.B, w.H, 8)
+    x = make_inputs(w)
+    xs = {key: x[key][heads] for key in ("q", "k", "v", "lam", "g")}
+    dec = H.run_oracle(w, {key: xs[key] for key in ("k", "v", "g")}, full=False)
+    bo_s, mo_s, nb, nm = H.near_tie_overrides(dec, what=f"{w.label} full size")
+    bo = np.full((nh, w.T), -1, np.int8)
+    mo = np.full((nh, w.T), -1, np.int32)
+    bo[heads], mo[heads] = bo_s, mo_s
+    _report("prefill-full", case=w.label, heads=heads, near_b=nb, near_m=nm,
+            boundaries=int(dec["b"].sum()), merges=int((dec["merge"] >= 0).sum()))
+    q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    del x
+    cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+    shp = (w.B, w.H, w.T)
+    out, b, mi, sc = dla.prefill(cache, q, k, v, g, lam, tau=w.tau,
+                                 boundary_override=torch.from_numpy(bo).reshape(shp).cuda(),
+                                 merge_override=torch.from_numpy(mo).reshape(shp).cuda())
+    torch.cuda.synchronize()
+    H.assert_decisions(b.cpu().numpy().reshape(nh, w.T)[heads],
+                       mi.cpu().numpy().reshape(nh, w.T)[heads], dec, w.label)
+    serr = np.abs(sc.cpu().numpy().reshape(nh, w.T)[heads] - dec["score"]).max()
+    assert serr < H.DELTA_B / 10, f"score error {serr}"
+    starts = dla.prefill_segment_starts(cache, w.T, k.dtype)
+    toks, wins = windows(w.T, 512, starts)
+    og = out.float().reshape(nh, w.T, w.dv)[heads][:, toks].cpu().numpy()
+    del q, k, v, g, lam, out
+    xf = H.f64(xs, w)
+    oc = OracleCache.empty(len(heads), w.C, w.dk, w.dv)
+    ref_o = np.zeros((len(heads), len(toks), w.dv))
+    for i in range(len(heads)):
+        ref_o[i] = direct.outputs_at(xf["q"][i], xf["k"][i], xf["v"][i], xf["g"][i],
+                                     xf["lam"][i], dec["b"][i], dec["merge"][i], w.C, toks)
+        m, n, S = direct.final_states(xf["k"][i], xf["v"][i], xf["g"][i], dec["b"][i],
+                                      dec["merge"][i], w.C)
+        assert m == dec["cache"].m[i] and (n[:m] == dec["cache"].n[i, :m]).all()
+        oc.m[i], oc.n[i], oc.S[i] = m, n, S
+        oc.ibar[i] = dec["cache"].ibar[i]
+    rel = H.assert_outputs(og, ref_o, H.TOL[w.dtype], f"{w.label} windows {wins}")
+    exp = dla.cache_export(cache, heads=heads)
+    H.assert_cache(exp, oc, 1e-4, what=w.label)
+    assert (exp["tokens"] == w.T).all()
+    _report("prefill-full-ok", case=w.label, windows=wins, max_rel_out=f"{rel:.2e}",
+            max_score_err=f"{serr:.2e}")
+
+
+def test_decode_full_size_sampled_heads():
+    """The decode workload at its full size (64 x 32 heads, C = 128, d = 128):
+    a 32k-token prefix drawn on the device and absorbed without readout, then
+    256 decode steps of i.i.d. tokens (a boundary and a capacity merge at every
+    step), in the launch configuration the benchmark times.  Sixteen heads
+    spread over batch and head: every decision of the prefix, the cache it
+    builds, and every decision, output and the final cache of all 256 steps.
+    The oracle continues from its own cache, built from its own decisions."""
+    torch = _torch()
+    from paper_2606_10650_amd import dla
+    from paper_2606_10650_amd.workloads import make_prefix_torch
+    w = WORKLOADS["cfg5"]
+    nh = w.B * w.H
+    steps = w.decode_steps
+    heads = spread_heads(w.B, w.H, 16)
+    _, k, v, g = make_prefix_torch(w, "cuda")
+    kh = k.reshape(nh, w.T, w.dk)[heads].float().cpu().numpy().astype(np.float64)
+    vh = v.reshape(nh, w.T, w.dv)[heads].float().cpu().numpy().astype(np.float64)
+    gh = g.reshape(nh, w.T)[heads].cpu().numpy().astype(np.float64)
+    dec = oracle_forward(kh, vh, gh, w.C, w.tau, full=False)
+    bo_s, mo_s, nb, nm = H.near_tie_overrides(dec, what=f"{w.label} prefix")
+    _report("decode-full", case=w.label, heads=heads, near_b=nb, near_m=nm,
+            boundaries=int(dec["b"].sum()), merges=int((dec["merge"] >= 0).sum()))
+    bo = np.full((nh, w.T), -1, np.int8)
+    mo = np.full((nh, w.T), -1, np.int32)
+    bo[heads], mo[heads] = bo_s, mo_s
+    shp = (w.B, w.H, w.T)
+    cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+    _, pb, pm, _ = dla.prefill(cache, None, k, v, g, None, tau=w.tau, skip_readout=True,
+                               boundary_override=torch.from_numpy(bo).reshape(shp).cuda(),
+                               merge_override=torch.from_numpy(mo).reshape(shp).cuda())
+    torch.cuda.synchronize()
+    H.assert_decisions(pb.reshape(nh, w.T)[heads].cpu().numpy(),
+                       pm.reshape(nh, w.T)[heads].cpu().numpy(), dec, f"{w.label} prefix")
+    del k, v, g, pb, pm
+    torch.cuda.empty_cache()
+    # the oracle's cache after the prefix: counts and scores from its
+    # decisions, states summed over each state's token range
+    oc = OracleCache.empty(len(heads), w.C, w.dk, w.dv)
+    for i in range(len(heads)):
+        m, n, S = direct.final_states(kh[i], vh[i], gh[i], dec["b"][i], dec["merge"][i], w.C)
+        assert m == dec["cache"].m[i] and (n[:m] == dec["cache"].n[i, :m]).all()
+        oc.m[i], oc.n[i], oc.S[i] = m, n, S
+        oc.ibar[i] = dec["cache"].ibar[i]
+    H.assert_cache(dla.cache_export(cache, heads=heads), oc, 1e-4, what=f"{w.label} prefix")
+    # the decode steps
+    x = make_decode_tokens(w, steps=steps)
+    xd = {key: x[key] for key in ("q", "k", "v", "lam", "g")}
+    xh = H.f64({key: xd[key][heads] for key in xd}, w)
+    free = oracle_forward(xh["k"], xh["v"], xh["g"], w.C, w.tau, q=xh["q"], lam=xh["lam"],
+                          cache=oc.copy())
+    sbo, smo, snb, snm = H.near_tie_overrides(free, what=f"{w.label} steps")
+    ref = oracle_forward(xh["k"], xh["v"], xh["g"], w.C, w.tau, q=xh["q"], lam=xh["lam"],
+                         cache=oc, b_override=sbo, m_override=smo)
+    q, kk, vv, gg, lam = H.inputs_to_device(w, xd, w.B, w.H)
+    hidx = torch.tensor(heads, device="cuda")
+    bo_d = torch.full((nh, steps), -1, dtype=torch.int8)
+    mo_d = torch.full((nh, steps), -1, dtype=torch.int32)
+    bo_d[heads] = torch.from_numpy(sbo)
+    mo_d[heads] = torch.from_numpy(smo)
+    bo_d = bo_d.reshape(w.B, w.H, steps).permute(2, 0, 1).contiguous().cuda()
+    mo_d = mo_d.reshape(w.B, w.H, steps).permute(2, 0, 1).contiguous().cuda()
+    outs, bs, ms = [], [], []
+    for t in range(steps):
+        o, b, mi, _ = dla.decode_step(cache, q[:, :, t].contiguous(), kk[:, :, t].contiguous(),
+                                      vv[:, :, t].contiguous(), gg[:, :, t].contiguous(),
+                                      lam[:, :, t].contiguous(), tau=w.tau,
+                                      boundary_override=bo_d[t], merge_override=mo_d[t])
+        outs.append(o.reshape(nh, w.dv)[hidx])
+        bs.append(b.reshape(nh)[hidx])
+        ms.append(mi.reshape(nh)[hidx])
+    torch.cuda.synchronize()
+    H.assert_decisions(torch.stack(bs, 1).cpu().numpy(), torch.stack(ms, 1).cpu().numpy(), ref,
+                       f"{w.label} steps")
+    rel = H.assert_outputs(torch.stack(outs, 1).float().cpu().numpy(), ref["out"],
+                           H.TOL[w.dtype], f"{w.label} steps")
+    H.assert_cache(dla.cache_export(cache, heads=heads), oc, 1e-4, what=f"{w.label} final")
+    _report("decode-full-ok", case=w.label, steps=steps, near_b=snb, near_m=snm,
+            max_rel_out=f"{rel:.2e}")

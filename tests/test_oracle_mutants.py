@@ -52,6 +52,32 @@ MUTANTS = {
     # the just-closed state left out of the merge candidates
     "candidates_exclude_closed": ("for (int32_t i = 0; i + 1 < C; ++i) {\n          dens[i]",
                                   "for (int32_t i = 0; i + 2 < C; ++i) {\n          dens[i]"),
+    # the near-tie margins that decide where the parity protocol hands the GPU
+    # the oracle's decision, and the merge override
+    "margin_b_zero": ("margin_b[t] = free_b ? fabs(I - tau) : INFINITY;",
+                      "margin_b[t] = free_b ? 0.0 : INFINITY;"),
+    "margin_b_forced_counted": ("margin_b[t] = free_b ? fabs(I - tau) : INFINITY;",
+                                "margin_b[t] = fabs(I - tau);"),
+    "margin_b_against_zero": ("margin_b[t] = free_b ? fabs(I - tau) : INFINITY;",
+                              "margin_b[t] = free_b ? fabs(I) : INFINITY;"),
+    "margin_m_zero": ("mgap = (second - d1) / (fabs(d1) > 0.0 ? fabs(d1) : 1e-300);",
+                      "mgap = 0.0;"),
+    "margin_m_largest_pair": ("if (i != best && dens[i] < second) second = dens[i];",
+                              "if (i != best && (second == INFINITY || dens[i] > second)) "
+                              "second = dens[i];"),
+    "margin_m_relative_to_second": ("mgap = (second - d1) / (fabs(d1) > 0.0 ? fabs(d1) : 1e-300);",
+                                    "mgap = (second - d1) / second;"),
+    "margin_m_for_forced_merge": ("        } else if (C > 2) {\n          const double d1",
+                                  "        }\n        if (C > 2) {\n          const double d1"),
+    "merge_override_ignored": ("best = m_ovr[t];", "best = best;"),
+    "merge_override_below_capacity": (
+        "      if (m == C) {\n        /* Alg. 2",
+        "      if (m == C || (m_ovr && m_ovr[t] >= 0 && m >= 2)) {\n        /* Alg. 2"),
+    # (accepted and clamped into range, so the mutant never indexes outside the cache)
+    "merge_override_out_of_range_accepted": (
+        "          if (m_ovr[t] < 0 || m_ovr[t] > C - 2) {\n            rc = ORACLE_BAD_MERGE_OVERRIDE;\n"
+        "            break;\n          }\n          best = m_ovr[t];",
+        "          best = m_ovr[t] < 0 ? 0 : (m_ovr[t] > C - 2 ? C - 2 : m_ovr[t]);"),
     "c1_not_forced": ("      if (C == 1) {\n        b = 0;", "      if (C == 0) {\n        b = 0;"),
 }
 
