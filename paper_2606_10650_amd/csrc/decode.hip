@@ -226,7 +226,12 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     o4[3] += w * y3;
 
     if (j == istar) {
-      // merged pair: frame of the later state, S~ = exp(F_{i+1} - F_i) S~_i + S~_{i+1}
+      // merged pair, stored in this step's frame Gn:
+      //   S~ = exp(Gn - F_i) S~_i + exp(Gn - F_{i+1}) S~_{i+1}.
+      // Gn is at least as recent as either frame, so both factors are <= 1.
+      // (The frame of the later state is not always the more recent one: the
+      // left state may have been rewritten by a merge after its neighbour was
+      // last written, and rebasing to the older frame can overflow.)
       const int j2 = j + 1;
       float4 Y[ST::NV];
       if (j2 == m - 1) {
@@ -237,8 +242,9 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
 #pragma unroll
         for (int r = 0; r < ST::NV; ++r) Y[r] = ld_stream(src + tid + 256 * r);
       }
-      const float w2 = a.skip_readout ? 0.f : sLam[j] * __expf((float)(Gn - sF[j2]));
-      const float e = __expf((float)(sF[j2] - sF[j]));
+      const float e2 = __expf((float)(Gn - sF[j2]));
+      const float w2 = a.skip_readout ? 0.f : sLam[j] * e2;
+      const float e1 = __expf((float)(Gn - sF[j]));
       float z0 = 0.f, z1 = 0.f, z2 = 0.f, z3 = 0.f;
       float4* dst = reinterpret_cast<float4*>(states + (size_t)sP[j] * D);
 #pragma unroll
@@ -248,10 +254,10 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
         z2 += qr[r] * Y[r].z;
         z3 += qr[r] * Y[r].w;
         float4 s;
-        s.x = e * X[r].x + Y[r].x;
-        s.y = e * X[r].y + Y[r].y;
-        s.z = e * X[r].z + Y[r].z;
-        s.w = e * X[r].w + Y[r].w;
+        s.x = e1 * X[r].x + e2 * Y[r].x;
+        s.y = e1 * X[r].y + e2 * Y[r].y;
+        s.z = e1 * X[r].z + e2 * Y[r].z;
+        s.w = e1 * X[r].w + e2 * Y[r].w;
         st_stream(dst + tid + 256 * r, s);
       }
       o4[0] += w2 * z0;
@@ -323,7 +329,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
       // merge istar, istar+1; shift later states down; freed slot goes to perm[m-1]
       for (int j = tid; j < C; j += 256) {
         if (j == istar) {
-          M.F[j] = sF[j + 1];
+          M.F[j] = Gn;
           M.n[j] = sN[j] + sN[j + 1];
           M.ibar[j] = sI[j] + sI[j + 1];
         } else if (j > istar && j < m - 1) {

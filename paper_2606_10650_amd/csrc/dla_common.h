@@ -238,7 +238,9 @@ __device__ __forceinline__ double info_score(double a, double b, double c, doubl
   const double rs2 = a / D + eps_rms;
   const double rS2 = b / D + eps_rms;
   const double num = a / rs2 + b / rS2 - 2.0 * c / sqrt(rs2 * rS2);
-  return sqrt(num > 0.0 ? num : 0.0) / (sqrt(b / rS2) + eps);
+  // rounding can take num a little below 0; a NaN (non-finite inputs) passes
+  // through, as the score of the definition would be NaN
+  return sqrt(num < 0.0 ? 0.0 : num) / (sqrt(b / rS2) + eps);
 }
 
 }  // namespace dla

@@ -144,7 +144,9 @@ __device__ __forceinline__ float score_f(float a, float b, float c, float D, flo
   const float rs2 = a / D + eps_rms;
   const float rS2 = b / D + eps_rms;
   const float num = a / rs2 + b / rS2 - 2.f * c * rsqrtf(rs2 * rS2);
-  return sqrtf(fmaxf(num, 0.f)) / (sqrtf(b / rS2) + eps);
+  // rounding can take num a little below 0; a NaN (non-finite inputs) passes
+  // through, as the score of the definition would be NaN
+  return sqrtf(num < 0.f ? 0.f : num) / (sqrtf(b / rS2) + eps);
 }
 
 template <int DK, int DV, typename Tin>

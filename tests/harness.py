@@ -59,12 +59,14 @@ def run_oracle(w, x, C=None, tau=None, full=True, cache=None, b_override=None, m
                           full=full, cache=cache, b_override=b_override, m_override=m_override)
 
 
-def near_tie_overrides(ref, b_override=None, m_override=None, what=""):
+def near_tie_overrides(ref, b_override=None, m_override=None, what="", max_frac=None):
     """Overrides that pin the oracle's decision wherever it is a near tie.
 
     The number of pinned decisions is bounded: at most INJECT_FRAC of the
     decisions the oracle took freely (boundaries with a finite margin_b,
-    capacity merges with a finite margin_m), and at least one is allowed.  A
+    capacity merges with a finite margin_m), and at least one is allowed;
+    max_frac replaces INJECT_FRAC for a workload whose structure makes near
+    ties common (the caller states why).  A
     margin that came out wrong (zero, say) would pin every decision and leave
     the kernels' own decision logic untested; the bound makes that fail."""
     bo = np.full(ref["b"].shape, -1, np.int8) if b_override is None else b_override.copy()
@@ -75,7 +77,7 @@ def near_tie_overrides(ref, b_override=None, m_override=None, what=""):
     mo[nm] = ref["merge"][nm]
     free = int(np.isfinite(ref["margin_b"]).sum() + np.isfinite(ref["margin_m"]).sum())
     n_inj = int(nb.sum() + nm.sum())
-    limit = max(1, int(INJECT_FRAC * free))
+    limit = max(1, int((INJECT_FRAC if max_frac is None else max_frac) * free))
     assert n_inj <= limit, (f"{what}: {n_inj} near-tie decisions pinned from the oracle "
                             f"({int(nb.sum())} boundaries, {int(nm.sum())} merges) out of "
                             f"{free} free decisions; at most {limit} allowed")

@@ -166,7 +166,13 @@ def test_decode_full_size_sampled_heads():
     xh = H.f64({key: xd[key][heads] for key in xd}, w)
     free = oracle_forward(xh["k"], xh["v"], xh["g"], w.C, w.tau, q=xh["q"], lam=xh["lam"],
                           cache=oc.copy())
-    sbo, smo, snb, snm = H.near_tie_overrides(free, what=f"{w.label} steps")
+    # Every step opens a state for an i.i.d. token, whose score against the
+    # newest state sits at sqrt(2) up to O(1 / sqrt(d_k d_v)); when Alg. 2 then
+    # picks between pairs of such single-token states their densities differ
+    # by a few 1e-6 relative, so about 3% of these merges are near ties
+    # (measured: 132 of the 4096 merges over 16 heads x 256 steps).  The bound
+    # is 5% of the free decisions here instead of 0.5%.
+    sbo, smo, snb, snm = H.near_tie_overrides(free, what=f"{w.label} steps", max_frac=0.05)
     ref = oracle_forward(xh["k"], xh["v"], xh["g"], w.C, w.tau, q=xh["q"], lam=xh["lam"],
                          cache=oc, b_override=sbo, m_override=smo)
     q, kk, vv, gg, lam = H.inputs_to_device(w, xd, w.B, w.H)
@@ -187,10 +193,16 @@ def test_decode_full_size_sampled_heads():
         bs.append(b.reshape(nh)[hidx])
         ms.append(mi.reshape(nh)[hidx])
     torch.cuda.synchronize()
-    H.assert_decisions(torch.stack(bs, 1).cpu().numpy(), torch.stack(ms, 1).cpu().numpy(), ref,
-                       f"{w.label} steps")
-    rel = H.assert_outputs(torch.stack(outs, 1).float().cpu().numpy(), ref["out"],
-                           H.TOL[w.dtype], f"{w.label} steps")
+    gb, gm = torch.stack(bs, 1).cpu().numpy(), torch.stack(ms, 1).cpu().numpy()
+    H.assert_decisions(gb, gm, ref, f"{w.label} steps")
+    go = torch.stack(outs, 1).float().cpu().numpy()
+    bad = np.argwhere(~np.isfinite(ref["out"]).all(-1))
+    assert len(bad) == 0, f"oracle outputs not finite at (head, step) {bad[:8].tolist()}"
+    bad = np.argwhere(~np.isfinite(go).all(-1))
+    assert len(bad) == 0, (f"GPU outputs not finite at (head, step) {bad[:8].tolist()} of "
+                           f"{len(bad)}; merges there {[int(gm[i, t]) for i, t in bad[:8]]}, "
+                           f"non-finite entries {int((~np.isfinite(go[tuple(bad[0])])).sum())}")
+    rel = H.assert_outputs(go, ref["out"], H.TOL[w.dtype], f"{w.label} steps")
     H.assert_cache(dla.cache_export(cache, heads=heads), oc, 1e-4, what=f"{w.label} final")
     _report("decode-full-ok", case=w.label, steps=steps, near_b=snb, near_m=snm,
             max_rel_out=f"{rel:.2e}")

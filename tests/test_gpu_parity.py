@@ -269,6 +269,17 @@ def test_decode_edge_shapes():
                  label="decode C=1024")
 
 
+def test_decode_merges_states_of_far_apart_frames():
+    """Regression: a decode-step merge whose left state was rewritten more
+    recently than its right neighbour.  The merged state was rebased to the
+    right state's (older) frame with a factor exp(F_right - F_left) > 1, which
+    overflows once the frames lie more than ~88 nats apart.  Steep decay
+    (g ~ U(-0.2, 0)) over a 2400-token prefill spreads the frames by hundreds
+    of nats; tau = 0 then merges at every decode step."""
+    _decode_case(WORKLOADS["cfg2"].replace(B=1, H=2, T=2600, C=16, g_lo=-0.2, tau=0.0), T1=2400,
+                 label="decode merges, far-apart frames")
+
+
 @pytest.mark.parametrize("out_f32", [False, True])
 def test_prefill_then_decode_continuation(out_f32):
     """prefill(T1) followed by decode steps equals the oracle over all tokens
