@@ -246,6 +246,29 @@ dla_status dla_prefill(const dla_cache_desc* desc, void* cache, const void* q, c
                        void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * dla_prefill for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same arguments, results and errors as dla_prefill, without the workspace.
+ * Its workspace is a static device array of DLA_STATIC_SCRATCH_BYTES that the
+ * library holds on every device it runs on until the process ends; nothing is
+ * allocated by the call.  The stages always run serially on `stream` (no
+ * second stream or event is created; DLA_SERIAL_STAGES is implied).  A call
+ * whose workspace (dla_prefill_workspace_size with DLA_SERIAL_STAGES) exceeds
+ * DLA_STATIC_SCRATCH_BYTES returns DLA_ERR_WORKSPACE and enqueues nothing.
+ * Every call on a device shares that device's array, and no part of it needs
+ * clearing between calls: calls that overlap on one device race (order them on
+ * one stream).
+ */
+#define DLA_STATIC_SCRATCH_BYTES ((size_t)128 << 20)
+dla_status dla_prefill_static(const dla_cache_desc* desc, void* cache, const void* q,
+                              const void* k, const void* v, const float* log_gate,
+                              const void* lambda, int32_t T, dla_dtype in_dtype,
+                              const dla_params* params, void* out, dla_dtype out_dtype,
+                              int8_t* boundary, int32_t* merge_idx, float* score,
+                              const int8_t* boundary_override, const int32_t* merge_override,
+                              void* stream);
+
+/*
  * Decode step: absorb one token per head (the prefill semantics with T = 1),
  * streaming every live state once.  q, k: [B][H][d_k]; v, out: [B][H][d_v];
  * log_gate: [B][H]; lambda: [B][H][C] (nullable); exports and overrides:

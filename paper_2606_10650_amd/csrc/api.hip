@@ -3,6 +3,7 @@
 // stream and never allocates device memory.
 #include <string.h>
 
+#include <mutex>
 #include <vector>
 
 #include "dla_common.h"
@@ -46,6 +47,37 @@ hipError_t pipe_resources(hipStream_t caller, int n, hipStream_t* side, hipEvent
   return hipSuccess;
 }
 
+
+// Workspace of dla_prefill_static: a file-scope device array, one copy per
+// device the library runs on, kept until the process ends.  Host code never
+// passes the array's name to a kernel (on the host it is only a stand-in for
+// the symbol): the device address of this device's copy comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+static __device__ __align__(256) char scratch[DLA_STATIC_SCRATCH_BYTES];
+
+hipError_t static_scratch(hipStream_t caller, void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0, cur = 0;
+  hipError_t e = hipStreamGetDevice(caller, &dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    if ((e = hipGetDevice(&cur)) != hipSuccess) return e;
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    const hipError_t r = (cur != dev) ? hipSetDevice(cur) : hipSuccess;
+    if (e != hipSuccess) return e;
+    if (r != hipSuccess) return r;
+    if (!p || ((uintptr_t)p & 255u)) return hipErrorInvalidValue;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
+}
 
 __global__ void cache_init_kernel(char* cache, dla_cache_desc d, size_t meta_offset,
                                   size_t meta_stride) {
@@ -214,12 +246,17 @@ dla_status dla_prefill_segment_starts(const dla_cache_desc* desc, int32_t T, dla
   return ret(DLA_OK);
 }
 
-dla_status dla_prefill(const dla_cache_desc* desc, void* cache, const void* q, const void* k,
-                       const void* v, const float* log_gate, const void* lambda, int32_t T,
-                       dla_dtype in_dtype, const dla_params* params, void* out,
-                       dla_dtype out_dtype, int8_t* boundary, int32_t* merge_idx, float* score,
-                       const int8_t* boundary_override, const int32_t* merge_override,
-                       void* workspace, size_t workspace_bytes, void* stream) {
+// The body of dla_prefill and dla_prefill_static.  static_ws: the workspace
+// is this device's static scratch (stages forced serial, so that no stream or
+// event is ever created; the workspace arguments are ignored).
+static dla_status prefill_impl(const dla_cache_desc* desc, void* cache, const void* q,
+                               const void* k, const void* v, const float* log_gate,
+                               const void* lambda, int32_t T, dla_dtype in_dtype,
+                               const dla_params* params, void* out, dla_dtype out_dtype,
+                               int8_t* boundary, int32_t* merge_idx, float* score,
+                               const int8_t* boundary_override, const int32_t* merge_override,
+                               void* workspace, size_t workspace_bytes, void* stream,
+                               bool static_ws) {
   dla_status s = check_desc(desc);
   if (s != DLA_OK) return ret(s);
   if (!params || T < 0 || !dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return ret(DLA_ERR_INVALID_ARG);
@@ -231,10 +268,15 @@ dla_status dla_prefill(const dla_cache_desc* desc, void* cache, const void* q, c
   if ((int64_t)desc->B * desc->H * (int64_t)T * (desc->C > 128 ? desc->C : 128) >
       ((int64_t)1 << 40))
     return ret(DLA_ERR_UNSUPPORTED);
-  const bool serial = (params->flags & DLA_SERIAL_STAGES) != 0;
+  const bool serial = static_ws || (params->flags & DLA_SERIAL_STAGES) != 0;
   if (params->n_readout_events < 0 || (params->n_readout_events > 0 && !params->readout_events))
     return ret(DLA_ERR_INVALID_ARG);
   const size_t need = prefill_workspace_bytes(*desc, T, in_dtype, !skip, serial);
+  if (static_ws) {
+    if (need > DLA_STATIC_SCRATCH_BYTES) return ret(DLA_ERR_WORKSPACE);
+    if (static_scratch((hipStream_t)stream, &workspace) != hipSuccess) return ret(DLA_ERR_HIP);
+    workspace_bytes = DLA_STATIC_SCRATCH_BYTES;
+  }
   if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 255u))
     return ret(DLA_ERR_WORKSPACE);
   PrefillArgs a;
@@ -272,6 +314,29 @@ dla_status dla_prefill(const dla_cache_desc* desc, void* cache, const void* q, c
   if (launch_prefill(a, (hipStream_t)stream, se) != hipSuccess)
     return ret(DLA_ERR_HIP);
   return ret(DLA_OK);
+}
+
+dla_status dla_prefill(const dla_cache_desc* desc, void* cache, const void* q, const void* k,
+                       const void* v, const float* log_gate, const void* lambda, int32_t T,
+                       dla_dtype in_dtype, const dla_params* params, void* out,
+                       dla_dtype out_dtype, int8_t* boundary, int32_t* merge_idx, float* score,
+                       const int8_t* boundary_override, const int32_t* merge_override,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+  return prefill_impl(desc, cache, q, k, v, log_gate, lambda, T, in_dtype, params, out, out_dtype,
+                      boundary, merge_idx, score, boundary_override, merge_override, workspace,
+                      workspace_bytes, stream, false);
+}
+
+dla_status dla_prefill_static(const dla_cache_desc* desc, void* cache, const void* q,
+                              const void* k, const void* v, const float* log_gate,
+                              const void* lambda, int32_t T, dla_dtype in_dtype,
+                              const dla_params* params, void* out, dla_dtype out_dtype,
+                              int8_t* boundary, int32_t* merge_idx, float* score,
+                              const int8_t* boundary_override, const int32_t* merge_override,
+                              void* stream) {
+  return prefill_impl(desc, cache, q, k, v, log_gate, lambda, T, in_dtype, params, out, out_dtype,
+                      boundary, merge_idx, score, boundary_override, merge_override, nullptr, 0,
+                      stream, true);
 }
 
 dla_status dla_decode_step(const dla_cache_desc* desc, void* cache, const void* q, const void* k,

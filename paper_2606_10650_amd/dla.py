@@ -26,8 +26,9 @@ DLA_FLAG_CACHE_MISMATCH = 2
 
 EXPORTED = ("dla_cache_layout_of", "dla_state_cache_alloc", "dla_cache_flags",
             "dla_cache_header_check", "dla_prefill_workspace_size", "dla_prefill_segment_count",
-            "dla_prefill_segment_starts", "dla_prefill", "dla_decode_step", "dla_status_string",
-            "dla_get_last_error")
+            "dla_prefill_segment_starts", "dla_prefill", "dla_prefill_static", "dla_decode_step",
+            "dla_status_string", "dla_get_last_error")
+STATIC_SCRATCH_BYTES = 128 << 20   # DLA_STATIC_SCRATCH_BYTES
 
 
 class CacheDesc(ctypes.Structure):
@@ -83,6 +84,9 @@ def lib():
                                                  ctypes.c_int32]
         L.dla_prefill.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, ctypes.c_int32, I,
                                   ctypes.POINTER(Params), P, I, P, P, P, P, P, P, ctypes.c_size_t, P]
+        L.dla_prefill_static.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P,
+                                         ctypes.c_int32, I, ctypes.POINTER(Params), P, I, P, P, P,
+                                         P, P, P]
         L.dla_decode_step.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, I,
                                       ctypes.POINTER(Params), P, I, P, P, P, P, P, P]
         L.dla_status_string.argtypes = [I]
@@ -91,7 +95,7 @@ def lib():
         for name in ("dla_cache_layout_of", "dla_state_cache_alloc", "dla_cache_flags",
                      "dla_cache_header_check", "dla_prefill_workspace_size",
                      "dla_prefill_segment_count", "dla_prefill_segment_starts", "dla_prefill",
-                     "dla_decode_step", "dla_get_last_error"):
+                     "dla_prefill_static", "dla_decode_step", "dla_get_last_error"):
             getattr(L, name).restype = I
         _lib = L
     return _lib
@@ -296,6 +300,32 @@ def prefill(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5, eps: f
                            _ptr(merge_override), _ptr(workspace), workspace.numel(),
                            _stream(dev))
     _check(st, "dla_prefill")
+    return out, boundary, merge_idx, score
+
+
+def prefill_static(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5,
+                   eps: float = 1e-6, eps_rms: float = 1e-6, out, boundary=None, merge_idx=None,
+                   score=None, boundary_override=None, merge_override=None,
+                   skip_readout: bool = False):
+    """dla_prefill_static: prefill with the library's static device scratch as
+    workspace (stages serial).  Allocates nothing: the caller passes the output
+    and any export buffers.  Shapes as prefill."""
+    B, H, C = cache.B, cache.H, cache.C
+    T = k.shape[2]
+    dev = cache.device
+    assert k.shape == (B, H, T, cache.d_k) and v.shape == (B, H, T, cache.d_v)
+    assert g.shape == (B, H, T)
+    for t in (q, k, v, g, lam, out, boundary, merge_idx, score, boundary_override,
+              merge_override):
+        assert t is None or (t.is_contiguous() and t.device == dev)
+    p = _params(tau, eps, eps_rms, skip_readout, serial=True)
+    st = lib().dla_prefill_static(ctypes.byref(cache.desc), _ptr(cache.buf), _ptr(q), _ptr(k),
+                                  _ptr(v), _ptr(g), _ptr(lam), int(T), _dtype_code(k.dtype),
+                                  ctypes.byref(p), _ptr(out),
+                                  _dtype_code(out.dtype) if out is not None else DLA_F32,
+                                  _ptr(boundary), _ptr(merge_idx), _ptr(score),
+                                  _ptr(boundary_override), _ptr(merge_override), _stream(dev))
+    _check(st, "dla_prefill_static")
     return out, boundary, merge_idx, score
 
 
