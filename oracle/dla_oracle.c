@@ -103,15 +103,17 @@ static int run_head(int64_t T, int32_t C, int32_t dk, int32_t dv, const double* 
                     double tau, double eps, double eps_rms, const int8_t* b_ovr,
                     const int32_t* m_ovr, int32_t full, double* out, int8_t* b_out,
                     int32_t* merge_out, double* score_out, int32_t* m_out, double* margin_b,
-                    double* margin_m, int32_t* cache_m, int64_t* n, double* ibar, double* S) {
+                    double* margin_m, double* mag_out, int32_t* cache_m, int64_t* n,
+                    double* ibar, double* S) {
   const int64_t D = (int64_t)dk * dv;
-  double* s = (double*)malloc(sizeof(double) * D * 3);
+  double* s = (double*)malloc(sizeof(double) * (D * 3 + dv));
   double* dens = (double*)malloc(sizeof(double) * (C > 1 ? C : 1));
   if (!s || !dens) {
     free(s);
     free(dens);
     return ORACLE_NOMEM;
   }
+  double* y = s + 3 * D;
   double* ns = s + D;
   double* nS = s + 2 * D;
   int32_t m = *cache_m;
@@ -197,17 +199,24 @@ static int run_head(int64_t T, int32_t C, int32_t dk, int32_t dv, const double* 
     }
 
     if (out) {
+      /* o_t = sum_j lambda_{t,j} S_j^T q_t, one term y_j = S_j^T q_t per state.
+       * mag_t = sum_j |lambda_{t,j}| ||S_j||_F ||q_t|| bounds the sizes of the
+       * terms the sum adds up (||y_j|| <= ||S_j||_F ||q_t||); it is the scale
+       * against which a perturbation of the stored states is measured. */
       double* ot = out + t * dv;
       const double* qt = q + t * dk;
+      double mag = 0.0;
       for (int32_t c = 0; c < dv; ++c) ot[c] = 0.0;
       for (int32_t j = 0; j < m; ++j) {
         const double lj = lam ? lam[t * C + j] : 1.0;
         const double* Sj = S + (int64_t)j * D;
-        for (int32_t a = 0; a < dk; ++a) {
-          const double w = lj * qt[a];
-          for (int32_t c = 0; c < dv; ++c) ot[c] += w * Sj[a * dv + c];
-        }
+        for (int32_t c = 0; c < dv; ++c) y[c] = 0.0;
+        for (int32_t a = 0; a < dk; ++a)
+          for (int32_t c = 0; c < dv; ++c) y[c] += qt[a] * Sj[a * dv + c];
+        for (int32_t c = 0; c < dv; ++c) ot[c] += lj * y[c];
+        if (mag_out) mag += fabs(lj) * frob(Sj, D);
       }
+      if (mag_out) mag_out[t] = mag * frob(qt, dk);
     }
     if (b_out) b_out[t] = (int8_t)b;
     if (merge_out) merge_out[t] = merged;
@@ -228,7 +237,8 @@ static int run_head(int64_t T, int32_t C, int32_t dk, int32_t dv, const double* 
  * Layouts (row-major): q, k [n_heads][T][dk]; v [n_heads][T][dv]; g [n_heads][T];
  * lam [n_heads][T][C] or NULL; overrides [n_heads][T] or NULL (-1 = free);
  * outputs out [n_heads][T][dv]; b_out, merge_out, score_out, m_out, margin_b,
- * margin_m [n_heads][T]; each output may be NULL.
+ * margin_m, mag_out [n_heads][T]; each output may be NULL (mag_out is written
+ * only with out).
  *
  * The cache is read and written: cache_m [n_heads], cache_n and cache_ibar
  * [n_heads][C], cache_S [n_heads][C][dk][dv] -- chronological order, true
@@ -243,8 +253,8 @@ int dla_oracle_forward(int64_t n_heads, int64_t T, int32_t C, int32_t dk, int32_
                        const double* lam, double tau, double eps, double eps_rms,
                        const int8_t* b_ovr, const int32_t* m_ovr, int32_t full, double* out,
                        int8_t* b_out, int32_t* merge_out, double* score_out, int32_t* m_out,
-                       double* margin_b, double* margin_m, int32_t* cache_m, int64_t* cache_n,
-                       double* cache_ibar, double* cache_S) {
+                       double* margin_b, double* margin_m, double* mag_out, int32_t* cache_m,
+                       int64_t* cache_n, double* cache_ibar, double* cache_S) {
   if (n_heads < 0 || T < 0 || C < 1 || dk < 1 || dv < 1 || !k || !v || !g || !cache_m ||
       !cache_n || !cache_ibar || !cache_S)
     return ORACLE_BAD_ARG;
@@ -260,7 +270,8 @@ int dla_oracle_forward(int64_t n_heads, int64_t T, int32_t C, int32_t dk, int32_
                      b_out ? b_out + tok : NULL, merge_out ? merge_out + tok : NULL,
                      score_out ? score_out + tok : NULL, m_out ? m_out + tok : NULL,
                      margin_b ? margin_b + tok : NULL, margin_m ? margin_m + tok : NULL,
-                     cache_m + h, cache_n + h * C, cache_ibar + h * C, cache_S + h * C * D);
+                     mag_out ? mag_out + tok : NULL, cache_m + h, cache_n + h * C,
+                     cache_ibar + h * C, cache_S + h * C * D);
     if (r != ORACLE_OK) {
 #pragma omp critical
       rc = r;

@@ -42,7 +42,7 @@ def _load(path: Optional[str] = None):
     lib.dla_oracle_forward.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
                                        ctypes.c_int32, ctypes.c_int32, P, P, P, P, P,
                                        ctypes.c_double, ctypes.c_double, ctypes.c_double, P, P,
-                                       ctypes.c_int32, P, P, P, P, P, P, P, P, P, P, P]
+                                       ctypes.c_int32, P, P, P, P, P, P, P, P, P, P, P, P]
     lib.dla_oracle_threads.restype = ctypes.c_int
     if path is None:
         _lib = lib
@@ -80,8 +80,9 @@ def oracle_forward(k, v, g, C: int, tau: float, *, q=None, lam=None, eps: float 
                    lib_path: Optional[str] = None):
     """Run the oracle on float64 inputs shaped [n_heads, T, d] (g: [n_heads, T],
     lam: [n_heads, T, C]).  Returns a dict with out, b, merge, score, m,
-    margin_b, margin_m and the final cache.  The cache argument is updated in
-    place when given."""
+    margin_b, margin_m, mag (sum over states of |lambda| ||S_j||_F ||q||, which
+    bounds the sizes of the readout's terms; with out) and the final cache.  The cache argument is
+    updated in place when given."""
     k = np.ascontiguousarray(k, np.float64)
     v = np.ascontiguousarray(v, np.float64)
     g = np.ascontiguousarray(g, np.float64)
@@ -103,6 +104,7 @@ def oracle_forward(k, v, g, C: int, tau: float, *, q=None, lam=None, eps: float 
         "m": np.zeros((nh, T), np.int32),
         "margin_b": np.zeros((nh, T)),
         "margin_m": np.zeros((nh, T)),
+        "mag": np.zeros((nh, T)) if want_out else None,
     }
     bo = None if b_override is None else np.ascontiguousarray(b_override, np.int8)
     mo = None if m_override is None else np.ascontiguousarray(m_override, np.int32)
@@ -110,7 +112,7 @@ def oracle_forward(k, v, g, C: int, tau: float, *, q=None, lam=None, eps: float 
     rc = lib.dla_oracle_forward(nh, T, C, dk, dv, _p(q), _p(k), _p(v), _p(g), _p(lam), tau, eps,
                                 eps_rms, _p(bo), _p(mo), 1 if full else 0, _p(res["out"]),
                                 _p(res["b"]), _p(res["merge"]), _p(res["score"]), _p(res["m"]),
-                                _p(res["margin_b"]), _p(res["margin_m"]), _p(cache.m),
+                                _p(res["margin_b"]), _p(res["margin_m"]), _p(res["mag"]), _p(cache.m),
                                 _p(cache.n), _p(cache.ibar), _p(cache.S))
     if rc != 0:
         raise ValueError(f"oracle error {rc}")

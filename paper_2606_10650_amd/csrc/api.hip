@@ -133,7 +133,6 @@ static dla_status check_desc(const dla_cache_desc* d) {
     return DLA_ERR_UNSUPPORTED;
   if ((int64_t)d->B * d->H > (int64_t)1 << 24) return DLA_ERR_UNSUPPORTED;
   if (d->state_dtype != DLA_F32 && d->state_dtype != DLA_BF16) return DLA_ERR_INVALID_ARG;
-  if (d->state_dtype == DLA_BF16) return DLA_ERR_UNSUPPORTED;
   return DLA_OK;
 }
 
@@ -287,6 +286,7 @@ static dla_status prefill_impl(const dla_cache_desc* desc, void* cache, const vo
   a.meta_offset = L.meta_offset;
   a.meta_stride = L.meta_stride;
   a.states_offset = L.states_offset;
+  a.open_offset = L.open_offset;
   a.q = q;
   a.k = k;
   a.v = v;
@@ -359,6 +359,8 @@ dla_status dla_decode_step(const dla_cache_desc* desc, void* cache, const void* 
   a.meta_offset = L.meta_offset;
   a.meta_stride = L.meta_stride;
   a.states_offset = L.states_offset;
+  a.open_offset = L.open_offset;
+  a.nsplit = decode_splits(desc->B * desc->H, desc->C);
   a.q = q;
   a.k = k;
   a.v = v;
@@ -370,7 +372,6 @@ dla_status dla_decode_step(const dla_cache_desc* desc, void* cache, const void* 
   a.score_out = score;
   a.b_ovr = boundary_override;
   a.m_ovr = merge_override;
-  a.C = desc->C;
   a.tau = params->tau;
   a.eps = params->eps;
   a.eps_rms = params->eps_rms;

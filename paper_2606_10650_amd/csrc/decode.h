@@ -7,7 +7,8 @@ namespace dla {
 struct DecodeArgs {
   dla_cache_desc desc;
   char* cache;
-  size_t meta_offset, meta_stride, states_offset;
+  size_t meta_offset, meta_stride, states_offset, open_offset;
+  int nsplit;  // workgroups per head (1 .. kMaxSplit)
   const void* q;
   const void* k;
   const void* v;
@@ -19,12 +20,13 @@ struct DecodeArgs {
   float* score_out;
   const int8_t* b_ovr;
   const int32_t* m_ovr;
-  int C;
   float tau, eps, eps_rms;
   int skip_readout;
 };
 
 hipError_t launch_decode(const DecodeArgs& a, int nheads, int dk, int dv, dla_dtype in,
                          dla_dtype out, hipStream_t s);
+// workgroups per head for nheads heads of capacity C
+int decode_splits(int nheads, int C);
 
 }  // namespace dla

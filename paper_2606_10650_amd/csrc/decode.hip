@@ -1,53 +1,101 @@
 // Decode step of the DLA layer: one token per head against a resident cache.
 //
-// One 256-thread workgroup per head.  The step is bound by HBM bandwidth: every
-// live state (d_k x d_v float32) is streamed once for the readout
-// o = sum_j lambda_j q^T S_j (eq. capacity_bounded_output), and at most two
-// states are written (the accumulated newest state, or the merged pair of
-// Alg. 2 and the new state).  States decay lazily: a slot stores S~ with the
-// true state exp(G - F_j) S~, so untouched states are never rewritten.
+// The step is bound by HBM bandwidth: every live state (d_k x d_v) is streamed
+// once for the readout o = sum_j lambda_j q^T S_j (eq. capacity_bounded_output),
+// and at most three states are written (the merged pair of Alg. 2, the state
+// that closes when a new one opens, and the new or accumulated newest state).
+// States decay lazily: a slot stores S~ with the true state exp(G - F_j) S~, so
+// untouched states are never rewritten.
 //
-// Thread mapping inside a state: float4 index tid + 256 r of the row-major
-// d_k x d_v array, i.e. thread tid owns the 4 columns 4*(tid % (d_v/4)) .. +3
-// of the rows (tid / (d_v/4)) + r * (256 / (d_v/4)).  Loads are fully coalesced.
+// Storage: float32 slots, or bfloat16 slots for the closed states with the
+// newest state of each head in a float32 open region.  The decisions read only
+// the newest state, the counts and the aggregated scores, so they do not depend
+// on the storage type.
+//
+// Work split: NS workgroups of 256 threads per head (NS = 1 when there are
+// enough heads to fill the chip).  Each takes the step's decisions (identical
+// arithmetic on identical data, so every workgroup of a head reaches the same
+// ones) and streams one contiguous range of the pre-merge states, the merged
+// pair never split between two ranges; it writes its partial output to a small
+// area in the head's metadata and counts itself in with one atomic add.  The
+// last workgroup to arrive (no workgroup ever waits for another) sums the
+// partials in split order, writes the output and the newest state, and updates
+// the metadata: by then every workgroup has read what it needed.
+//
+// Thread mapping inside a state: element group tid + 256 r (4 consecutive
+// elements) of the row-major d_k x d_v array, i.e. thread tid owns the 4
+// columns 4*(tid % (d_v/4)) .. +3 of the rows (tid / (d_v/4)) + r * (256 /
+// (d_v/4)).  Loads are coalesced (16 bytes per lane for float32 storage, 8 for
+// bfloat16).
 #include "decode.h"
 
 namespace dla {
-
-
 
 // Every state is read or written at most once per step, and the states of all
 // heads (gigabytes) do not fit in the caches, so state traffic goes with the
 // non-temporal hint.
 typedef float f32x4v __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ float4 ld_stream(const float4* p) {
-  const f32x4v x = __builtin_nontemporal_load(reinterpret_cast<const f32x4v*>(p));
+typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float4 ld_group(const float* base, int g, bool stream) {
+  const f32x4v* p = reinterpret_cast<const f32x4v*>(base) + g;
+  const f32x4v x = stream ? __builtin_nontemporal_load(p) : *p;
   return make_float4(x[0], x[1], x[2], x[3]);
 }
-__device__ __forceinline__ void st_stream(float4* p, const float4& v) {
+__device__ __forceinline__ float4 ld_group(const bf16_t* base, int g, bool stream) {
+  const u32x2v* p = reinterpret_cast<const u32x2v*>(base) + g;
+  const u32x2v x = stream ? __builtin_nontemporal_load(p) : *p;
+  return make_float4(__uint_as_float(x[0] << 16), __uint_as_float(x[0] & 0xFFFF0000u),
+                     __uint_as_float(x[1] << 16), __uint_as_float(x[1] & 0xFFFF0000u));
+}
+__device__ __forceinline__ void st_group(float* base, int g, const float4& v) {
   const f32x4v x = {v.x, v.y, v.z, v.w};
-  __builtin_nontemporal_store(x, reinterpret_cast<f32x4v*>(p));
+  __builtin_nontemporal_store(x, reinterpret_cast<f32x4v*>(base) + g);
+}
+__device__ __forceinline__ void st_group(bf16_t* base, int g, const float4& v) {
+  // round to nearest even, as the pool copies and the outputs are rounded
+  const uint32_t lo0 = from_f32<bf16_t>(v.x).x, hi0 = from_f32<bf16_t>(v.y).x;
+  const uint32_t lo1 = from_f32<bf16_t>(v.z).x, hi1 = from_f32<bf16_t>(v.w).x;
+  const u32x2v x = {lo0 | (hi0 << 16), lo1 | (hi1 << 16)};
+  __builtin_nontemporal_store(x, reinterpret_cast<u32x2v*>(base) + g);
 }
 
 template <int DK, int DV>
 struct StateTile {
-  static constexpr int CQ = DV / 4;      // float4 per row
+  static constexpr int CQ = DV / 4;      // 4-element groups per row
   static constexpr int RG = 256 / CQ;    // row groups
   static constexpr int RPT = DK / RG;    // rows per thread
-  static constexpr int NV = RPT;         // float4 per thread
+  static constexpr int NV = RPT;         // groups per thread
 };
 
-template <int DK, int DV, typename Tin, typename Tout>
+// States [j0, j1) of split sp out of ns, over the m pre-merge states; a
+// boundary that would fall between the merged pair (istar, istar + 1) moves one
+// state on, so both sit in one range.
+__device__ __forceinline__ void split_range(int m, int ns, int sp, int istar, int* j0, int* j1) {
+  const int per = (m + ns - 1) / ns;
+  int a0 = min(m, sp * per), a1 = min(m, (sp + 1) * per);
+  if (istar >= 0) {
+    if (a0 == istar + 1) ++a0;
+    if (a1 == istar + 1) ++a1;
+  }
+  *j0 = a0;
+  *j1 = a1;
+}
+
+template <int DK, int DV, typename Tin, typename Tout, typename TS>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
   using ST = StateTile<DK, DV>;
   constexpr int D = DK * DV;
+  constexpr bool SB = sizeof(TS) == 2;  // bfloat16 closed states, float32 open region
   if (!cache_matches(a.cache, a.desc)) {  // refused: the descriptor is not the cache's
     flag_mismatch(a.cache);
     return;
   }
-  const int h = blockIdx.x;
+  const int ns = a.nsplit;
+  const int h = blockIdx.x / ns;
+  const int sp = blockIdx.x % ns;
   const int tid = threadIdx.x;
-  const int C = a.C;
+  const int C = a.desc.C;
   const int cq = tid % ST::CQ;
   const int rg = tid / ST::CQ;
 
@@ -88,7 +136,10 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
   __syncthreads();
 
   const double Gn = G0 + (double)a.g[h];
-  float* states = reinterpret_cast<float*>(a.cache + a.states_offset) + (size_t)h * C * D;
+  TS* states = reinterpret_cast<TS*>(a.cache + a.states_offset) + (size_t)h * C * D;
+  float* open = SB ? reinterpret_cast<float*>(a.cache + a.open_offset) + (size_t)h * D : nullptr;
+  // the newest state's storage: its slot, or the open region
+  float* newest = SB ? open : reinterpret_cast<float*>(states) + (size_t)(m > 0 ? sP[m - 1] : 0) * D;
 
   // |k|^2, |v|^2, q.k
   float kk = 0.f, vv = 0.f, qk = 0.f;
@@ -100,15 +151,15 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     for (int i = tid; i < DV; i += 64) vv += sv[i] * sv[i];
   }
 
-  // newest state in registers, and the two scalars b = |S~|^2, c = k^T S~ v
+  // newest state in registers, and the two scalars b = |S~|^2, c = k^T S~ v;
+  // every workgroup of a head reads it, so with several it is read cacheable
   float4 Sopen[ST::NV];
   float ct = 0.f, bt = 0.f;
   if (m > 0) {
-    const float4* src = reinterpret_cast<const float4*>(states + (size_t)sP[m - 1] * D);
-    float4 vq = reinterpret_cast<const float4*>(sv)[cq];
+    const float4 vq = reinterpret_cast<const float4*>(sv)[cq];
 #pragma unroll
     for (int r = 0; r < ST::NV; ++r) {
-      Sopen[r] = ld_stream(src + tid + 256 * r);
+      Sopen[r] = ld_group(newest, tid + 256 * r, ns == 1);
       const float kr = sk[rg + ST::RG * r];
       const float4 s = Sopen[r];
       ct += kr * (s.x * vq.x + s.y * vq.y + s.z * vq.z + s.w * vq.w);
@@ -183,7 +234,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
         const int f = a.m_ovr[h];
         if (f >= 0 && f <= C - 2)
           ii = f;
-        else
+        else if (sp == 0)
           atomicOr(&reinterpret_cast<CacheHeader*>(a.cache)->flags, DLA_FLAG_BAD_MERGE_OVERRIDE);
       }
       sDec[1] = ii;
@@ -193,22 +244,24 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
   }
   const int m_post = b ? (istar >= 0 ? m : m + 1) : m;
 
-  // stream every live state: readout partials and the state writes
+  // stream this workgroup's states: readout partials and the state writes
   float o4[4] = {0.f, 0.f, 0.f, 0.f};
   float qr[ST::NV];
 #pragma unroll
   for (int r = 0; r < ST::NV; ++r) qr[r] = sq[rg + ST::RG * r];
+  int j0, j1;
+  split_range(m, ns, sp, istar, &j0, &j1);
 
-  for (int j = 0; j < m; ++j) {
+  for (int j = j0; j < j1; ++j) {
     const bool is_open = (j == m - 1);
     float4 X[ST::NV];
     if (is_open) {
 #pragma unroll
       for (int r = 0; r < ST::NV; ++r) X[r] = Sopen[r];
     } else {
-      const float4* src = reinterpret_cast<const float4*>(states + (size_t)sP[j] * D);
+      const TS* src = states + (size_t)sP[j] * D;
 #pragma unroll
-      for (int r = 0; r < ST::NV; ++r) X[r] = ld_stream(src + tid + 256 * r);
+      for (int r = 0; r < ST::NV; ++r) X[r] = ld_group(src, tid + 256 * r, true);
     }
     const int post = (istar >= 0 && j > istar) ? j - 1 : j;
     const float w = a.skip_readout ? 0.f : sLam[post] * __expf((float)(Gn - sF[j]));
@@ -238,15 +291,15 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
 #pragma unroll
         for (int r = 0; r < ST::NV; ++r) Y[r] = Sopen[r];
       } else {
-        const float4* src = reinterpret_cast<const float4*>(states + (size_t)sP[j2] * D);
+        const TS* src = states + (size_t)sP[j2] * D;
 #pragma unroll
-        for (int r = 0; r < ST::NV; ++r) Y[r] = ld_stream(src + tid + 256 * r);
+        for (int r = 0; r < ST::NV; ++r) Y[r] = ld_group(src, tid + 256 * r, true);
       }
       const float e2 = __expf((float)(Gn - sF[j2]));
       const float w2 = a.skip_readout ? 0.f : sLam[j] * e2;
       const float e1 = __expf((float)(Gn - sF[j]));
       float z0 = 0.f, z1 = 0.f, z2 = 0.f, z3 = 0.f;
-      float4* dst = reinterpret_cast<float4*>(states + (size_t)sP[j] * D);
+      TS* dst = states + (size_t)sP[j] * D;
 #pragma unroll
       for (int r = 0; r < ST::NV; ++r) {
         z0 += qr[r] * Y[r].x;
@@ -258,55 +311,87 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
         s.y = e1 * X[r].y + e2 * Y[r].y;
         s.z = e1 * X[r].z + e2 * Y[r].z;
         s.w = e1 * X[r].w + e2 * Y[r].w;
-        st_stream(dst + tid + 256 * r, s);
+        st_group(dst, tid + 256 * r, s);
       }
       o4[0] += w2 * z0;
       o4[1] += w2 * z1;
       o4[2] += w2 * z2;
       o4[3] += w2 * z3;
       ++j;  // the pair is done
-    } else if (is_open && !b) {
-      // accumulate: S~' = exp(Gn - F) S~ + k v^T in frame Gn
-      const float f = __expf((float)(Gn - sF[j]));
-      const float4 vq = reinterpret_cast<const float4*>(sv)[cq];
-      float4* dst = reinterpret_cast<float4*>(states + (size_t)sP[j] * D);
+    } else if (SB && is_open && b) {
+      // the newest state closes: its bfloat16 copy goes to its slot, in its
+      // own frame (a merge with its left neighbour is handled above)
+      TS* dst = states + (size_t)sP[j] * D;
 #pragma unroll
-      for (int r = 0; r < ST::NV; ++r) {
-        const float kr = sk[rg + ST::RG * r];
-        float4 s;
-        s.x = f * X[r].x + kr * vq.x;
-        s.y = f * X[r].y + kr * vq.y;
-        s.z = f * X[r].z + kr * vq.z;
-        s.w = f * X[r].w + kr * vq.w;
-        st_stream(dst + tid + 256 * r, s);
-      }
+      for (int r = 0; r < ST::NV; ++r) st_group(dst, tid + 256 * r, X[r]);
     }
   }
 
-  // new state k v^T (frame Gn) in the slot freed by the merge or the first free slot
-  if (b) {
-    const int phys = (istar >= 0) ? sP[istar + 1] : sP[m];
-    const float4 vq = reinterpret_cast<const float4*>(sv)[cq];
-    float4* dst = reinterpret_cast<float4*>(states + (size_t)phys * D);
-#pragma unroll
-    for (int r = 0; r < ST::NV; ++r) {
-      const float kr = sk[rg + ST::RG * r];
-      st_stream(dst + tid + 256 * r, make_float4(kr * vq.x, kr * vq.y, kr * vq.z, kr * vq.w));
-    }
-  }
-
-  // the new token's own contribution lambda_{m'-1} (q.k) v, then reduce the partials
+  // the workgroup's partial output
   if (!a.skip_readout) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) sOut[rg][4 * cq + c] = o4[c];
-    __syncthreads();
-    if (tid < DV) {
-      float acc = 0.f;
+  }
+  __syncthreads();
+  float acc = 0.f;
+  if (!a.skip_readout && tid < DV) {
 #pragma unroll
-      for (int g2 = 0; g2 < ST::RG; ++g2) acc += sOut[g2][tid];
-      acc += sLam[m_post - 1] * qk2 * sv[tid];
-      static_cast<Tout*>(a.out)[(size_t)h * DV + tid] = from_f32<Tout>(acc);
+    for (int g2 = 0; g2 < ST::RG; ++g2) acc += sOut[g2][tid];
+  }
+  if (ns > 1) {
+    // hand the partial to the last workgroup of the head to arrive
+    float* part = decode_partials(mbase, C) + (size_t)sp * DV;
+    if (!a.skip_readout && tid < DV) part[tid] = acc;
+    __threadfence();
+    __syncthreads();
+    if (tid == 0) {
+      const int prev = atomicAdd(reinterpret_cast<int32_t*>(mbase + 4), 1);
+      sDec[2] = (prev == ns - 1) ? 1 : 0;
     }
+    __syncthreads();
+    if (!sDec[2]) return;
+    __threadfence();
+    if (!a.skip_readout && tid < DV) {
+      const float* all = decode_partials(mbase, C);
+      acc = 0.f;
+      for (int s2 = 0; s2 < ns; ++s2) acc += all[(size_t)s2 * DV + tid];
+    }
+  }
+
+  // ---------------------------------------------- the last (or only) workgroup
+  // the newest state: accumulated (b = 0), or the new state k v^T in frame Gn
+  // (its slot is the one the merge freed, or the first free slot; with
+  // bfloat16 storage it lives in the open region)
+  {
+    float* dst;
+    if (SB)
+      dst = open;
+    else if (!b)
+      dst = reinterpret_cast<float*>(states) + (size_t)sP[m - 1] * D;
+    else
+      dst = reinterpret_cast<float*>(states) + (size_t)((istar >= 0) ? sP[istar + 1] : sP[m]) * D;
+    const float f = b ? 0.f : __expf((float)(Gn - sF[m - 1]));
+    const float4 vq = reinterpret_cast<const float4*>(sv)[cq];
+#pragma unroll
+    for (int r = 0; r < ST::NV; ++r) {
+      const float kr = sk[rg + ST::RG * r];
+      float4 s;
+      if (b) {
+        s = make_float4(kr * vq.x, kr * vq.y, kr * vq.z, kr * vq.w);
+      } else {
+        s.x = f * Sopen[r].x + kr * vq.x;
+        s.y = f * Sopen[r].y + kr * vq.y;
+        s.z = f * Sopen[r].z + kr * vq.z;
+        s.w = f * Sopen[r].w + kr * vq.w;
+      }
+      st_group(dst, tid + 256 * r, s);
+    }
+  }
+
+  // the new token's own contribution lambda_{m'-1} (q.k) v
+  if (!a.skip_readout && tid < DV) {
+    acc += sLam[m_post - 1] * qk2 * sv[tid];
+    static_cast<Tout*>(a.out)[(size_t)h * DV + tid] = from_f32<Tout>(acc);
   }
 
   // exports
@@ -314,10 +399,10 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     if (a.b_out) a.b_out[h] = (int8_t)b;
     if (a.merge_out) a.merge_out[h] = istar;
     if (a.score_out) a.score_out[h] = (float)I;
+    if (ns > 1) *reinterpret_cast<int32_t*>(mbase + 4) = 0;  // ready for the next step
   }
 
   // metadata update (chronological arrays, parallel over slots)
-  __syncthreads();
   if (!b) {
     if (tid == 0) {
       M.F[m - 1] = Gn;
@@ -358,28 +443,46 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
   }
 }
 
-template <int DK, int DV>
+// Workgroups per head: enough for about four per compute unit over all heads,
+// at most kMaxSplit, and at least two states per workgroup.
+int decode_splits(int nheads, int C) {
+  int ns = (1024 + nheads - 1) / nheads;
+  ns = ns < kMaxSplit ? ns : kMaxSplit;
+  const int byc = C / 2 > 1 ? C / 2 : 1;
+  ns = ns < byc ? ns : byc;
+  return ns > 1 ? ns : 1;
+}
+
+template <int DK, int DV, typename TS>
 static hipError_t launch_decode_dims(const DecodeArgs& a, int nheads, dla_dtype in, dla_dtype out,
                                      hipStream_t s) {
-  const size_t shm = (size_t)a.C * (8 + 8 + 4 + 4 + 4);
+  const size_t shm = (size_t)a.desc.C * (8 + 8 + 4 + 4 + 4);
+  const dim3 grid((unsigned)(nheads * a.nsplit));
   if (in == DLA_F32 && out == DLA_F32)
-    hipLaunchKernelGGL((decode_kernel<DK, DV, float, float>), dim3(nheads), dim3(256), shm, s, a);
+    hipLaunchKernelGGL((decode_kernel<DK, DV, float, float, TS>), grid, dim3(256), shm, s, a);
   else if (in == DLA_F32 && out == DLA_BF16)
-    hipLaunchKernelGGL((decode_kernel<DK, DV, float, bf16_t>), dim3(nheads), dim3(256), shm, s, a);
+    hipLaunchKernelGGL((decode_kernel<DK, DV, float, bf16_t, TS>), grid, dim3(256), shm, s, a);
   else if (in == DLA_BF16 && out == DLA_F32)
-    hipLaunchKernelGGL((decode_kernel<DK, DV, bf16_t, float>), dim3(nheads), dim3(256), shm, s, a);
+    hipLaunchKernelGGL((decode_kernel<DK, DV, bf16_t, float, TS>), grid, dim3(256), shm, s, a);
   else
-    hipLaunchKernelGGL((decode_kernel<DK, DV, bf16_t, bf16_t>), dim3(nheads), dim3(256), shm, s,
-                       a);
+    hipLaunchKernelGGL((decode_kernel<DK, DV, bf16_t, bf16_t, TS>), grid, dim3(256), shm, s, a);
   return hipGetLastError();
+}
+
+template <int DK, int DV>
+static hipError_t launch_decode_st(const DecodeArgs& a, int nheads, dla_dtype in, dla_dtype out,
+                                   hipStream_t s) {
+  if (a.desc.state_dtype == DLA_BF16) return launch_decode_dims<DK, DV, bf16_t>(a, nheads, in, out, s);
+  return launch_decode_dims<DK, DV, float>(a, nheads, in, out, s);
 }
 
 hipError_t launch_decode(const DecodeArgs& a, int nheads, int dk, int dv, dla_dtype in,
                          dla_dtype out, hipStream_t s) {
-  if (dk == 128 && dv == 128) return launch_decode_dims<128, 128>(a, nheads, in, out, s);
-  if (dk == 64 && dv == 64) return launch_decode_dims<64, 64>(a, nheads, in, out, s);
-  if (dk == 128 && dv == 64) return launch_decode_dims<128, 64>(a, nheads, in, out, s);
-  return launch_decode_dims<64, 128>(a, nheads, in, out, s);
+  if (a.nsplit < 1 || a.nsplit > kMaxSplit) return hipErrorInvalidValue;
+  if (dk == 128 && dv == 128) return launch_decode_st<128, 128>(a, nheads, in, out, s);
+  if (dk == 64 && dv == 64) return launch_decode_st<64, 64>(a, nheads, in, out, s);
+  if (dk == 128 && dv == 64) return launch_decode_st<128, 64>(a, nheads, in, out, s);
+  return launch_decode_st<64, 128>(a, nheads, in, out, s);
 }
 
 }  // namespace dla

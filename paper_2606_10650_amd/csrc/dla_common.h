@@ -41,8 +41,21 @@ __device__ __forceinline__ void flag_mismatch(char* cache) {
 
 __host__ __device__ inline size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-__host__ __device__ inline size_t meta_stride(int C) {
-  return round_up(32 + 24 * (size_t)C, 256);
+// Workgroups per head of a decode step at most; each leaves a partial output
+// of d_v floats in the head's metadata (see decode.hip).
+constexpr int kMaxSplit = 16;
+
+__host__ __device__ inline size_t meta_partials_offset(int C) {
+  return round_up(32 + 24 * (size_t)C, 64);
+}
+
+__host__ __device__ inline size_t meta_stride(int C, int dv) {
+  return round_up(meta_partials_offset(C) + (size_t)kMaxSplit * dv * sizeof(float), 256);
+}
+
+// the decode step's partial outputs of one head: float [kMaxSplit][d_v]
+__device__ __forceinline__ float* decode_partials(char* meta, int C) {
+  return reinterpret_cast<float*>(meta + meta_partials_offset(C));
 }
 
 // Per-head metadata (chronological arrays).  See dla.h for the byte layout.
@@ -78,7 +91,7 @@ inline dla_cache_layout layout_of(const dla_cache_desc& d) {
   const size_t nh = (size_t)d.B * d.H;
   const size_t D = (size_t)d.d_k * d.d_v;
   L.meta_offset = kHeaderBytes;
-  L.meta_stride = meta_stride(d.C);
+  L.meta_stride = meta_stride(d.C, d.d_v);
   L.states_offset = round_up(L.meta_offset + nh * L.meta_stride, 256);
   const size_t end = L.states_offset + nh * (size_t)d.C * D * state_elem_bytes(d);
   if (d.state_dtype == DLA_BF16) {

@@ -8,7 +8,7 @@ namespace dla {
 struct PrefillArgs {
   dla_cache_desc desc;
   char* cache;
-  size_t meta_offset, meta_stride, states_offset;
+  size_t meta_offset, meta_stride, states_offset, open_offset;
   const void* q;
   const void* k;
   const void* v;

@@ -247,8 +247,12 @@ __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, Prefi
         for (int r = 0; r < 16; ++r) S[k][r] = sv.S[((size_t)(wv + SWAVE * k) * 16 + r) * 64 + lane];
       }
   } else if (m0 > 0) {
-    const float* src = reinterpret_cast<const float*>(a.cache + a.states_offset) +
-                       ((size_t)h * C + min(max(M.perm[m0 - 1], 0), C - 1)) * D;
+    // the newest state: its float32 slot, or the open region with bfloat16 storage
+    const float* src =
+        a.desc.state_dtype == DLA_BF16
+            ? reinterpret_cast<const float*>(a.cache + a.open_offset) + (size_t)h * D
+            : reinterpret_cast<const float*>(a.cache + a.states_offset) +
+                  ((size_t)h * C + min(max(M.perm[m0 - 1], 0), C - 1)) * D;
     const float f = (float)exp(G0 - M.F[m0 - 1]);
 #pragma unroll
     for (int k = 0; k < NTW; ++k)

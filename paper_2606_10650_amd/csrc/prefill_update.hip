@@ -69,7 +69,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, 
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
 }
 
-template <int DK, int DV, typename Tin>
+template <int DK, int DV, typename Tin, typename TS>
 __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, PrefillWS w,
                                                               SegPlan plan, int seg) {
   if (!cache_matches(a.cache, a.desc)) return;  // refused call (see the prep kernel)
@@ -155,7 +155,12 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
   int next_obj = (plan.shared && seg > 0) ? min(max(*cv.next_obj, 0), plan.P_cap) : m;
   const bool fresh = !(plan.shared && seg > 0);
 
-  float* states = reinterpret_cast<float*>(a.cache + a.states_offset) + (size_t)h * C * D;
+  // masters: float32 slots, or bfloat16 slots for closed states with the
+  // newest state of the head in the float32 open region
+  constexpr bool SB = sizeof(TS) == 2;
+  constexpr int ES = (int)sizeof(TS);
+  TS* states = reinterpret_cast<TS*>(a.cache + a.states_offset) + (size_t)h * C * D;
+  float* open = SB ? reinterpret_cast<float*>(a.cache + a.open_offset) + (size_t)h * D : nullptr;
   const double* Gtok = w.Gtok + (size_t)h * T;
   const int32_t* death = w.death + (size_t)h * T;
   const Tin* Kin = static_cast<const Tin*>(a.k) + (size_t)h * T * DK;
@@ -168,13 +173,18 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
   __syncthreads();
   if (copies && fresh) {
     for (int j = 0; j < m; ++j) {
-      const float* src = states + (size_t)sPerm[j] * D + cg * NC;
+      const bool from_open = SB && j == m - 1;  // (wave-uniform)
+      const TS* src = states + (size_t)sPerm[j] * D + cg * NC;
+      const float* srco = from_open ? open + cg * NC : nullptr;
       Tin* dst = obj_slice(j);
       const int c = tid & 31;
       for (int kg = tid >> 5; kg < DK / 8; kg += NTHR / 32) {
         float x[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] = src[(size_t)(8 * kg + e) * DV + c];
+        for (int e = 0; e < 8; ++e) {
+          const size_t idx = (size_t)(8 * kg + e) * DV + c;
+          x[e] = from_open ? srco[idx] : to_f32(src[idx]);
+        }
         Tin* d8 = dst + kg * 256 + c * 8;
 #pragma unroll
         for (int e = 0; e < 8; ++e) d8[e] = from_f32<Tin>(x[e]);
@@ -187,32 +197,47 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
   const int band = wv % NBAND;
   const int ib = 32 * band;
   const int set = wv / NBAND;
-  // Band accesses of a float32 master go through a buffer resource based at the
-  // band's first element: lane offset (4 half d_v + l32) * 4 bytes, element r
-  // at row 8 (r / 4) + r % 4 further (the 8 (r / 4) rows in the scalar offset)
-  const int voff_lane = (4 * half * DV + l32) * 4;
+  // Band accesses of a master go through a buffer resource based at the band's
+  // first element: lane offset (4 half d_v + l32) elements, element r at row
+  // 8 (r / 4) + r % 4 further (the 8 (r / 4) rows in the scalar offset)
   // (slot and object numbers are wave-uniform: read them into scalars so the
   // resources live in scalar registers)
   auto band_rsrc = [&](int phys) __attribute__((always_inline)) {
     phys = __builtin_amdgcn_readfirstlane(phys);
-    return buffer_rsrc(states + (size_t)phys * D + (size_t)ib * DV + cg * NC, 32 * DV * 4);
+    return buffer_rsrc(states + (size_t)phys * D + (size_t)ib * DV + cg * NC, 32 * DV * ES);
   };
-  // decayed old states j = ja..jb (float32 masters) added to a band accumulator,
-  // two states' loads in flight at a time
-  auto add_old = [&](f32x16& acc16, int ja, int jb, double Gend) __attribute__((always_inline)) {
-    for (int j = ja; j <= jb; j += 2) {
-      const bool two = j + 1 <= jb;
-      const __amdgpu_buffer_rsrc_t r0 = band_rsrc(sPerm[j]);
-      const __amdgpu_buffer_rsrc_t r1 = band_rsrc(sPerm[two ? j + 1 : j]);
-      float x[16], y[16];
+  auto open_rsrc = [&]() __attribute__((always_inline)) {
+    return buffer_rsrc(open + (size_t)ib * DV + cg * NC, 32 * DV * 4);
+  };
+  // a band of master j of the states present at the chunk start (the newest of
+  // them, j = m - 1, is in the open region with bfloat16 storage)
+  auto load_band = [&](int j, float (&x)[16]) __attribute__((always_inline)) {
+    if (SB && j == m - 1) {
+      const __amdgpu_buffer_rsrc_t r0 = open_rsrc();
 #pragma unroll
       for (int r = 0; r < 16; ++r)
         x[r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-                                             r0, voff_lane + (r & 3) * DV * 4, (r >> 2) * 8 * DV * 4, 0));
+            r0, (4 * half * DV + l32 + (r & 3) * DV) * 4, (r >> 2) * 8 * DV * 4, 0));
+    } else {
+      const __amdgpu_buffer_rsrc_t r0 = band_rsrc(sPerm[j]);
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        y[r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-                                             r1, voff_lane + (r & 3) * DV * 4, (r >> 2) * 8 * DV * 4, 0));
+      for (int r = 0; r < 16; ++r) {
+        const int vo = (4 * half * DV + l32 + (r & 3) * DV) * ES, so = (r >> 2) * 8 * DV * ES;
+        if constexpr (ES == 4)
+          x[r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r0, vo, so, 0));
+        else
+          x[r] = __uint_as_float((uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r0, vo, so, 0) << 16);
+      }
+    }
+  };
+  // decayed old states j = ja..jb added to a band accumulator, two states'
+  // loads in flight at a time
+  auto add_old = [&](f32x16& acc16, int ja, int jb, double Gend) __attribute__((always_inline)) {
+    for (int j = ja; j <= jb; j += 2) {
+      const bool two = j + 1 <= jb;
+      float x[16], y[16];
+      load_band(j, x);
+      load_band(two ? j + 1 : j, y);
       const float f0 = __expf((float)(Gend - sF[j]));
       const float f1 = two ? __expf((float)(Gend - sF[j + 1])) : 0.f;
 #pragma unroll
@@ -221,16 +246,32 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
       for (int r = 0; r < 16; ++r) acc16[r] += f1 * y[r];
     }
   };
-  // store a band of a state: float32 master, and its copy when obj >= 0 (the
-  // copy's 8-byte pieces at ((ib / 8 + g4) * 256 + l32 * 8 + 4 half) elements).
-  // The stores carry the non-temporal hint (cache policy 2): the states of a
-  // call (gigabytes) are not re-read before they have left the caches.
-  auto store_state = [&](const f32x16& acc16, int phys, int obj) __attribute__((always_inline)) {
-    const __amdgpu_buffer_rsrc_t rs = band_rsrc(phys);
+  // store a band of a state: the master (in the open region for the newest
+  // state after the chunk with bfloat16 storage), and its copy when obj >= 0
+  // (the copy's 8-byte pieces at ((ib / 8 + g4) * 256 + l32 * 8 + 4 half)
+  // elements).  The stores carry the non-temporal hint (cache policy 2): the
+  // states of a call (gigabytes) are not re-read before they have left the
+  // caches.
+  auto store_state = [&](const f32x16& acc16, int phys, int obj, bool to_open)
+      __attribute__((always_inline)) {
+    if (SB && to_open) {
+      const __amdgpu_buffer_rsrc_t rs = open_rsrc();
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc16[r]), rs,
-                                            voff_lane + (r & 3) * DV * 4, (r >> 2) * 8 * DV * 4, 2);
+      for (int r = 0; r < 16; ++r)
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc16[r]), rs,
+                                              (4 * half * DV + l32 + (r & 3) * DV) * 4,
+                                              (r >> 2) * 8 * DV * 4, 2);
+    } else {
+      const __amdgpu_buffer_rsrc_t rs = band_rsrc(phys);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int vo = (4 * half * DV + l32 + (r & 3) * DV) * ES, so = (r >> 2) * 8 * DV * ES;
+        if constexpr (ES == 4)
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc16[r]), rs, vo, so, 2);
+        else
+          __builtin_amdgcn_raw_buffer_store_b16(from_f32<bf16_t>(acc16[r]).x, rs, vo, so, 2);
+      }
+    }
     obj = __builtin_amdgcn_readfirstlane(obj);
     if (obj >= 0) {
       const __amdgpu_buffer_rsrc_t ro = buffer_rsrc(obj_slice(obj), U::CP::SLICE * E);
@@ -355,6 +396,10 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
           ld_[u] = sLead[ja_[u]];
           ph_[u] = sPerm[ja_[u]];
           ch_[u] = (jb_[u] > ja_[u] || r1_[u] >= r0_[u]) ? 1 : 0;
+          // with bfloat16 storage the newest state at the chunk start lives
+          // in the open region: when it closes untouched, it is written to
+          // its slot (rebuilt from itself)
+          if (SB && ja_[u] == m - 1 && e != ne - 1) ch_[u] = 1;
         } else {
           ja_[u] = -1;
           jb_[u] = -2;
@@ -455,7 +500,7 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
       if (i < ncont)
         acc = u16;
       else
-        store_state(u16, ePhys[e], eObj[e]);
+        store_state(u16, ePhys[e], eObj[e], e == ne - 1);
     }
     __syncthreads();
 
@@ -568,7 +613,7 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
           if (rc == inR)
             xacc = acc;
           else
-            store_state(acc, ePhys[rc], eObj[rc]);
+            store_state(acc, ePhys[rc], eObj[rc], rc == ne - 1);
           acc = zero16();
           ++rc;
           if (rc >= ne) break;
@@ -625,7 +670,7 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
           acc[4 * r4 + 3] += x.w;
         }
       }
-      store_state(acc, ePhys[outR], eObj[outR]);
+      store_state(acc, ePhys[outR], eObj[outR], outR == ne - 1);
     }
     __syncthreads();
 
@@ -692,14 +737,14 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
   }
 }
 
-template <int DK, int DV, typename Tin>
+template <int DK, int DV, typename Tin, typename TS>
 static hipError_t launch_update_t(const PrefillArgs& a, const SegPlan& p, int seg, hipStream_t s) {
   const int nh = a.desc.B * a.desc.H;
   PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C, a.desc.d_k * a.desc.d_v, p.nch);
   const int grid = (int)round_up(nh, 8) * (DV / NC);
   const size_t shm = update_smem_bytes<DK, Tin>(a.desc.C);
   if (shm > 160 * 1024) return hipErrorInvalidValue;
-  auto k = prefill_update_kernel<DK, DV, Tin>;
+  auto k = prefill_update_kernel<DK, DV, Tin, TS>;
   if (hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm) !=
       hipSuccess)
     return hipErrorInvalidValue;
@@ -710,8 +755,12 @@ static hipError_t launch_update_t(const PrefillArgs& a, const SegPlan& p, int se
 template <int DK, int DV>
 static hipError_t launch_update_dims(const PrefillArgs& a, const SegPlan& p, int seg,
                                      hipStream_t s) {
-  if (a.in_dtype == DLA_F32) return launch_update_t<DK, DV, float>(a, p, seg, s);
-  return launch_update_t<DK, DV, bf16_t>(a, p, seg, s);
+  const bool sb = a.desc.state_dtype == DLA_BF16;
+  if (a.in_dtype == DLA_F32)
+    return sb ? launch_update_t<DK, DV, float, bf16_t>(a, p, seg, s)
+              : launch_update_t<DK, DV, float, float>(a, p, seg, s);
+  return sb ? launch_update_t<DK, DV, bf16_t, bf16_t>(a, p, seg, s)
+            : launch_update_t<DK, DV, bf16_t, float>(a, p, seg, s);
 }
 
 bool prefill_update_supported(const dla_cache_desc& d, dla_dtype in_dtype) {

@@ -18,6 +18,24 @@ from paper_2606_10650_amd.workloads import to_f64
 DELTA_B = 1e-4   # |I - tau| below this is a near tie (GPU score error is ~1e-6)
 DELTA_M = 1e-5   # relative density gap below this is a near tie
 TOL = {"f32": 1e-4, "bf16": 2e-2}
+# final cache states, relative Frobenius error per state: float32 storage, and
+# bfloat16 storage of the closed states (unit roundoff 2^-8 per rounding, one
+# rounding when a state closes and one per merge or rebuild it goes through,
+# independent errors adding in quadrature)
+STATE_TOL = {False: 1e-4, True: 2e-2}
+
+
+def state_mag_tol(bf16_states: bool, dk: int) -> float:
+    """Outputs over bfloat16-stored states: each state S_j carries rounding
+    errors of relative size up to u = 2^-8 per element (one rounding when it
+    closes, one per merge or rebuild).  An error matrix E of that size moves
+    the state's readout term E^T q by about u ||S_j||_F ||q|| / sqrt(d_k) when
+    q is not aligned with it -- independently of the term S_j^T q itself,
+    which is small when q is nearly orthogonal to a low-rank state.  So the
+    output may move by u / sqrt(d_k) times the oracle's mag = sum_j
+    |lambda_j| ||S_j||_F ||q||; a factor 4 covers the tail (a CPU emulation of
+    the rounding schedule on the decode workload peaks at 1.15)."""
+    return 4.0 * 2.0 ** -8 / np.sqrt(dk) if bf16_states else 0.0
 INJECT_FRAC = 0.005  # pinned near ties allowed, as a fraction of free decisions
 INJECTIONS = []      # every call's counts, for the session report
 
@@ -96,14 +114,21 @@ def assert_decisions(gpu_b, gpu_m, ref, what=""):
                            f"{gm[tuple(bad[0])]} ref {ref['merge'][tuple(bad[0])]}")
 
 
-def assert_outputs(o_gpu, o_ref, tol, what=""):
-    """||o_gpu - o_ref|| <= tol * max(||o_ref_t||, rms_t ||o_ref_t||) per token."""
+def assert_outputs(o_gpu, o_ref, tol, what="", mag=None, mag_tol=0.0):
+    """||o_gpu - o_ref|| <= tol * max(||o_ref_t||, rms_t ||o_ref_t||)
+    (+ mag_tol * mag_t, the oracle's sum of the readout terms' sizes, for
+    bfloat16-stored states) per token."""
     og = np.asarray(o_gpu, np.float64).reshape(o_ref.shape)
     err = np.linalg.norm(og - o_ref, axis=-1)
     nrm = np.linalg.norm(o_ref, axis=-1)
     rms = np.sqrt((nrm ** 2).mean(axis=-1, keepdims=True))
-    ratio = err / (tol * np.maximum(nrm, rms))
+    extra = 0.0 if mag is None else mag_tol * np.asarray(mag).reshape(nrm.shape)
+    ratio = err / (tol * np.maximum(nrm, rms) + extra)
     worst = np.unravel_index(np.argmax(ratio), ratio.shape)
+    rel = (err / np.maximum(nrm, rms)).ravel()
+    print(f"[outputs] {what}: relative error max {rel.max():.3e} p99.9 "
+          f"{np.quantile(rel, 0.999):.3e} p99 {np.quantile(rel, 0.99):.3e} "
+          f"median {np.median(rel):.3e}", flush=True)
     assert ratio.max() <= 1.0, (f"{what}: output error {err[worst]:.3e} at {worst} exceeds "
                                 f"{tol} x {max(nrm[worst], rms[worst[0], 0]):.3e}")
     return float((err / np.maximum(nrm, rms)).max())
@@ -134,8 +159,11 @@ def oracle_cache_from(exp, dk, dv):
 
 
 def assert_cache(exp, ref_cache: OracleCache, tol, heads=None, what=""):
+    """Counts and state counts exact, aggregated scores to 1e-5, states to tol
+    relative per state; returns the largest relative state error."""
     heads = range(len(exp["m"])) if heads is None else heads
     S = true_states(exp)
+    worst = 0.0
     for i, h in enumerate(heads):
         m = int(ref_cache.m[h])
         assert exp["m"][i] == m, f"{what}: head {h} m {exp['m'][i]} vs {m}"
@@ -145,5 +173,12 @@ def assert_cache(exp, ref_cache: OracleCache, tol, heads=None, what=""):
         for j in range(m):
             Sr = ref_cache.S[h, j]
             e = np.linalg.norm(S[i, j] - Sr)
+            if e > tol * max(np.linalg.norm(Sr), 1e-30):
+                errs = [np.linalg.norm(S[i, jj] - ref_cache.S[h, jj]) /
+                        max(np.linalg.norm(ref_cache.S[h, jj]), 1e-30) for jj in range(m)]
+                print(f"[cache] {what}: head {h} state errors {np.round(errs, 5).tolist()}")
             assert e <= tol * max(np.linalg.norm(Sr), 1e-30), \
                 f"{what}: head {h} state {j} rel err {e / np.linalg.norm(Sr):.3e}"
+            worst = max(worst, e / max(np.linalg.norm(Sr), 1e-30))
+    print(f"[cache] {what}: largest relative state error {worst:.3e}", flush=True)
+    return worst

@@ -93,6 +93,22 @@ def brute_outputs(q, k, v, g, lam, hist):
     return out
 
 
+def brute_term_magnitudes(q, k, v, g, lam, hist):
+    """sum_j |lam[t, j]| ||S_j(t)||_F ||q_t||, S_j(t) = sum over the slot's
+    members of exp(G_t - G_s) k_s v_s^T."""
+    G = cum_gate(g)
+    T = q.shape[0]
+    mag = np.zeros(T)
+    for t in range(T):
+        for j, members in enumerate(hist[t]):
+            s = np.array(members)
+            Sj = (k[s] * np.exp(G[t] - G[s])[:, None]).T @ v[s]
+            lj = 1.0 if lam is None else lam[t, j]
+            mag[t] += abs(lj) * np.linalg.norm(Sj)
+        mag[t] *= np.linalg.norm(q[t])
+    return mag
+
+
 def rms_sq_norm(x2, D, eps_rms):
     """||N(X)||^2 for ||X||^2 = x2 under RMSNorm over D entries."""
     return x2 / (x2 / D + eps_rms)
@@ -146,6 +162,13 @@ def pin_single_state_and_one_state_per_token(lib_path=None):
                                lam=lam[h:h + 1, :, :C], lib_path=lib_path)
             ref = lam[h, :, :1] * base
             assert np.abs(r["out"][0] - ref).max() < 1e-12 * np.abs(ref).max(), (C, tau)
+            # a single state, the gated state P_t: |lam_0| ||P_t||_F ||q_t||
+            G = cum_gate(g[h])
+            P = [(k[h, :t + 1] * np.exp(G[t] - G[:t + 1])[:, None]).T @ v[h, :t + 1]
+                 for t in range(T)]
+            ref_mag = np.array([abs(lam[h, t, 0]) * np.linalg.norm(P[t]) * np.linalg.norm(q[h, t])
+                                for t in range(T)])
+            assert np.abs(r["mag"][0] - ref_mag).max() < 1e-12 * ref_mag.max(), (C, tau)
             assert r["b"][0, 0] == 1 and r["b"][0, 1:].sum() == 0
         r = oracle_forward(k[h:h + 1], v[h:h + 1], g[h:h + 1], T, 0.0, q=q[h:h + 1],
                            lam=lam[h:h + 1], lib_path=lib_path)
@@ -170,6 +193,11 @@ def pin_brute_force_membership(lib_path=None):
             out = brute_outputs(q[h], k[h], v[h], g[h], lam[h], hist)
             err = np.abs(out - r["out"][h]).max() / np.abs(out).max()
             assert err < 1e-11, f"{name} C={C}: brute-force output rel err {err}"
+            # the scale of the readout's terms: sum_j |lambda_{t,j}| ||S_j||_F ||q_t||
+            mag = brute_term_magnitudes(q[h], k[h], v[h], g[h], lam[h], hist)
+            merr = np.abs(mag - r["mag"][h]).max() / mag.max()
+            assert merr < 1e-11, f"{name} C={C}: term magnitudes rel err {merr}"
+            assert (r["mag"][h] >= np.linalg.norm(r["out"][h], axis=-1) * (1 - 1e-12)).all()
             # independent scalar Alg. 2 on membership lists
             prev = []
             for t in range(len(b)):

@@ -28,7 +28,9 @@ def _report(tag, **kw):
     print(f"[{tag}] " + " ".join(f"{k}={v}" for k, v in kw.items()), flush=True)
 
 
-def _prefill_case(w, C=None, tau=None, T_split=None, out_dtype=None, no_lambda=False):
+def _prefill_case(w, C=None, tau=None, T_split=None, out_dtype=None, no_lambda=False,
+                  state_dtype=0):
+    """state_dtype: DLA_F32 (0) or DLA_BF16 (1) storage of the cache's states."""
     torch = _torch()
     dla = _dla()
     C = C or w.C
@@ -42,7 +44,7 @@ def _prefill_case(w, C=None, tau=None, T_split=None, out_dtype=None, no_lambda=F
     _report("prefill", case=w.label, near_b=nb, near_m=nm, boundaries=int(ref["b"].sum()),
             merges=int((ref["merge"] >= 0).sum()))
     q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
-    cache = dla.cache_alloc(w.B, w.H, C, w.dk, w.dv)
+    cache = dla.cache_alloc(w.B, w.H, C, w.dk, w.dv, state_dtype=state_dtype)
     shp = (w.B, w.H, w.T)
     bo_d = torch.from_numpy(bo).reshape(shp).cuda()
     mo_d = torch.from_numpy(mo).reshape(shp).cuda()
@@ -69,13 +71,16 @@ def _prefill_case(w, C=None, tau=None, T_split=None, out_dtype=None, no_lambda=F
     assert serr < H.DELTA_B / 10, f"score error {serr}"
     if out_dtype is not None:
         assert out.dtype == out_dtype
-    # a bfloat16 input or output sets the tolerance
-    tol = H.TOL["bf16"] if (w.dtype == "bf16" or out.dtype == torch.bfloat16) else H.TOL["f32"]
-    rel = H.assert_outputs(out.float().cpu().numpy().reshape(nh, w.T, w.dv), ref["out"], tol, w.label)
+    # a bfloat16 input, output or state storage sets the tolerance
+    sb = state_dtype == dla.DLA_BF16
+    tol = H.TOL["bf16"] if (w.dtype == "bf16" or out.dtype == torch.bfloat16 or sb) else H.TOL["f32"]
+    rel = H.assert_outputs(out.float().cpu().numpy().reshape(nh, w.T, w.dv), ref["out"], tol,
+                           w.label, mag=ref["mag"], mag_tol=H.state_mag_tol(sb, w.dk))
     exp = dla.cache_export(cache)
-    H.assert_cache(exp, ref["cache"], 1e-4, what=w.label)
+    srel = H.assert_cache(exp, ref["cache"], H.STATE_TOL[sb], what=w.label)
     assert (exp["tokens"] == w.T).all()
-    _report("prefill-ok", case=w.label, max_score_err=f"{serr:.2e}", max_rel_out=f"{rel:.2e}")
+    _report("prefill-ok", case=w.label, state="bf16" if sb else "f32", max_score_err=f"{serr:.2e}",
+            max_rel_out=f"{rel:.2e}", max_rel_state=f"{srel:.2e}")
 
 
 def test_prefill_cfg1():
@@ -214,13 +219,14 @@ def test_decode_without_lambda():
     H.assert_cache(dla.cache_export(cache), ref["cache"], 1e-4, what="decode, no lambda")
 
 
-def _decode_case(w, T1=0, label=None):
+def _decode_case(w, T1=0, label=None, state_dtype=0):
     """Prefill of the first T1 tokens (none for T1 = 0), then one decode step per
     remaining token; every decision, output and the final cache against the
-    oracle over all tokens."""
+    oracle over all tokens.  state_dtype: storage of the cache's states."""
     torch = _torch()
     dla = _dla()
     label = label or w.label
+    sb = state_dtype == dla.DLA_BF16
     x = make_inputs(w)
     ref = H.run_oracle(w, x)
     bo, mo, _, _ = H.near_tie_overrides(ref, what=label)
@@ -228,7 +234,7 @@ def _decode_case(w, T1=0, label=None):
     shp = (w.B, w.H, w.T)
     bo_d = torch.from_numpy(bo).reshape(shp).cuda()
     mo_d = torch.from_numpy(mo).reshape(shp).cuda()
-    cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+    cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv, state_dtype=state_dtype)
     outs, bs, ms = [], [], []
     if T1 > 0:
         sl = slice(0, T1)
@@ -253,9 +259,12 @@ def _decode_case(w, T1=0, label=None):
     nh = w.B * w.H
     H.assert_decisions(torch.cat(bs, 2).cpu().numpy().reshape(nh, -1),
                        torch.cat(ms, 2).cpu().numpy().reshape(nh, -1), ref, label)
-    H.assert_outputs(torch.cat(outs, 2).float().cpu().numpy().reshape(nh, w.T, w.dv), ref["out"],
-                     H.TOL[w.dtype], label)
-    H.assert_cache(dla.cache_export(cache), ref["cache"], 1e-4, what=label)
+    rel = H.assert_outputs(torch.cat(outs, 2).float().cpu().numpy().reshape(nh, w.T, w.dv),
+                           ref["out"], H.TOL["bf16" if sb else w.dtype], label, mag=ref["mag"],
+                           mag_tol=H.state_mag_tol(sb, w.dk))
+    srel = H.assert_cache(dla.cache_export(cache), ref["cache"], H.STATE_TOL[sb], what=label)
+    _report("decode-ok", case=label, state="bf16" if sb else "f32", max_rel_out=f"{rel:.2e}",
+            max_rel_state=f"{srel:.2e}")
 
 
 def test_decode_edge_shapes():
@@ -267,6 +276,45 @@ def test_decode_edge_shapes():
     # the largest capacity, full, with a merge at every step
     _decode_case(WORKLOADS["cfg2"].replace(B=1, H=1, T=1040, C=1024, tau=0.0), T1=1030,
                  label="decode C=1024")
+
+
+@pytest.mark.parametrize("case", ["bf16_ragged", "spans_bursts", "f32_inputs", "continuation",
+                                  "capacity_one", "threshold_zero"])
+def test_prefill_bf16_state_storage(case):
+    """bfloat16 storage of the closed states (the newest state stays float32):
+    decisions bit-exact, outputs and final cache states within the bfloat16
+    tolerance."""
+    bf = 1  # DLA_BF16
+    if case == "bf16_ragged":
+        _prefill_case(WORKLOADS["cfg2"].replace(B=1, H=4, T=1000, C=12), state_dtype=bf)
+    elif case == "spans_bursts":
+        _prefill_case(WORKLOADS["cfg3"].replace(B=1, H=3, T=2600, C=24, span_mean=200.0),
+                      state_dtype=bf)
+    elif case == "f32_inputs":
+        _prefill_case(WORKLOADS["cfg1"].replace(T=600), state_dtype=bf)
+    elif case == "continuation":
+        _prefill_case(WORKLOADS["cfg2"].replace(B=1, H=2, T=2900, C=16), T_split=[1, 700, 701, 1600],
+                      state_dtype=bf)
+    elif case == "capacity_one":
+        _prefill_case(WORKLOADS["cfg2"].replace(B=1, H=2, T=1100), C=1, state_dtype=bf)
+    else:
+        _prefill_case(WORKLOADS["cfg2"].replace(B=1, H=2, T=700), C=64, tau=0.0, state_dtype=bf)
+
+
+def test_decode_bf16_state_storage():
+    """Decode with bfloat16 storage: from an empty cache (several workgroups
+    per head), after a prefill, at C = 1, with steep decay and a merge at every
+    step, and at the largest capacity."""
+    bf = 1  # DLA_BF16
+    _decode_case(WORKLOADS["cfg2"].replace(B=1, H=2, T=200, C=6), label="decode bf16 empty",
+                 state_dtype=bf)
+    _decode_case(WORKLOADS["cfg2"].replace(B=1, H=2, T=1300, C=12), T1=1100,
+                 label="decode bf16 after prefill", state_dtype=bf)
+    _decode_case(WORKLOADS["cfg1"].replace(T=80, C=1), label="decode bf16 C=1", state_dtype=bf)
+    _decode_case(WORKLOADS["cfg2"].replace(B=1, H=2, T=2600, C=16, g_lo=-0.2, tau=0.0), T1=2400,
+                 label="decode bf16 far-apart frames", state_dtype=bf)
+    _decode_case(WORKLOADS["cfg2"].replace(B=1, H=1, T=1040, C=1024, tau=0.0), T1=1030,
+                 label="decode bf16 C=1024", state_dtype=bf)
 
 
 def test_decode_merges_states_of_far_apart_frames():

@@ -43,7 +43,7 @@ MUTANTS = {
                            "      if (m > 0)\n"
                            "        for (int64_t i = 0; i < D; ++i) S[(int64_t)(m - 1) * D + i] += s[i];\n"
                            "      memcpy(S + (int64_t)m * D, s, sizeof(double) * D);"),
-    "readout_transposed": ("ot[c] += w * Sj[a * dv + c];", "ot[c] += w * Sj[c * dk + a];"),
+    "readout_transposed": ("y[c] += qt[a] * Sj[a * dv + c];", "y[c] += qt[a] * Sj[c * dk + a];"),
     "lambda_recency_index": ("lam[t * C + j]", "lam[t * C + (m - 1 - j)]"),
     "readout_skips_newest": ("for (int32_t j = 0; j < m; ++j) {\n        const double lj",
                              "for (int32_t j = 0; j + 1 < m; ++j) {\n        const double lj"),
@@ -78,6 +78,10 @@ MUTANTS = {
         "          if (m_ovr[t] < 0 || m_ovr[t] > C - 2) {\n            rc = ORACLE_BAD_MERGE_OVERRIDE;\n"
         "            break;\n          }\n          best = m_ovr[t];",
         "          best = m_ovr[t] < 0 ? 0 : (m_ovr[t] > C - 2 ? C - 2 : m_ovr[t]);"),
+    # the size of the readout's terms (the rounding scale of stored states)
+    "magnitude_signed_lambda": ("mag += fabs(lj) * frob(Sj, D);", "mag += lj * frob(Sj, D);"),
+    "magnitude_last_state_only": ("mag += fabs(lj) * frob(Sj, D);", "mag = fabs(lj) * frob(Sj, D);"),
+    "magnitude_without_query": ("mag_out[t] = mag * frob(qt, dk);", "mag_out[t] = mag;"),
     "c1_not_forced": ("      if (C == 1) {\n        b = 0;", "      if (C == 0) {\n        b = 0;"),
 }
 
