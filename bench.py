@@ -4,21 +4,23 @@
 One step = one prefill of the 16k-token workload from an empty cache (B=4,
 H=16, T=16384, d_k=d_v=128, C=128, tau=0.5, bf16 inputs, float32 states,
 long stable spans alternating with short i.i.d. bursts): token frames, the
-boundary scan with the capacity schedule, and the readout + state update --
+boundary scan with the capacity schedule, the state update and the readout --
 every step of the hot path.  `value` is prefill tokens/s (B*T tokens per step)
 with all inputs resident in HBM.
 
 Also reported on the same line:
-  * roofline of the dominant kernel (the readout) from HIP events that the
-    library records around each of its launches in the timed steps (the
-    prefill is pipelined: the scan runs on a second stream, segment by
-    segment, beside the update and readout of the segments already scanned);
-    the stage breakdown comes from three more steps run with serial stages;
+  * roofline of the dominant kernel (the readout), from HIP events that the
+    library records around each of its launches in the timed steps, and of
+    the whole call (the method's FLOPs over the step time); fractions against
+    the data-sheet peaks and against the peaks measured on this device by the
+    library's measurement kernels (dla_peak.h);
+  * the other prefill workloads (4k tokens at C = 64, 64k tokens at C = 256);
   * the decode step at C = 128 on full caches built from a 32k-token prefix
-    (B=64, H=32): mean and median microseconds per step over 256 steps, with
-    its HBM roofline;
-  * cpu_baseline: the float64 oracle on a bounded sample of the prefill
-    workload, timed on the host cores.
+    (B=64, H=32), with float32 and with bfloat16 storage of the closed
+    states, and on few heads (B=1, H=32: several workgroups per head);
+  * cache and workspace bytes;
+  * cpu_baseline: the float64 oracle on bounded samples (a prefill of one
+    sequence, and decode steps on a few heads of the GPU-built cache).
 
     python bench.py [--steps K] [--warmup W] [--gpus 1]
 """
@@ -36,8 +38,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "DLA layer fwd tokens/sec (prefill) + decode-step µs; % of HBM/MFMA roofline"
-PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
-PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (data sheet)
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (data sheet)
 PROFILES = os.path.join(ROOT, "profiles")
 # sources whose kernels the counter summaries describe
 KERNEL_SOURCES = {
@@ -99,7 +101,47 @@ def copy_probe(args, torch):
     print(json.dumps({"copy_probe_bytes": n, "launches": 5}), flush=True)
 
 
-def prefill_bench(args, torch, dla, W):
+def measured_peaks(torch, dla):
+    """Dense bfloat16 MFMA rate and HBM read bandwidth of this device, from the
+    library's measurement kernels: the best of three runs each."""
+    blocks, iters = 2048, 4096
+    sink = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    dla.peak_mfma_bf16(blocks, 64, sink)   # warm-up
+    best = 1e30
+    for _ in range(3):
+        ev[0].record()
+        dla.peak_mfma_bf16(blocks, iters, sink)
+        ev[1].record()
+        torch.cuda.synchronize()
+        best = min(best, ev[0].elapsed_time(ev[1]))
+    tflops = blocks * 16.0 * iters * 32768 / (best * 1e-3) / 1e12
+    buf = torch.empty(4 << 30, dtype=torch.uint8, device="cuda")
+    buf.fill_(1)
+    rb = 8192
+    rsink = torch.empty(rb * 256, dtype=torch.float32, device="cuda")
+    dla.peak_hbm_read(buf, rb, rsink)
+    best = 1e30
+    for _ in range(3):
+        ev[0].record()
+        dla.peak_hbm_read(buf, rb, rsink)
+        ev[1].record()
+        torch.cuda.synchronize()
+        best = min(best, ev[0].elapsed_time(ev[1]))
+    gbs = buf.numel() / (best * 1e-3) / 1e9
+    del buf
+    torch.cuda.empty_cache()
+    return {"mfma_bf16_tflops": round(tflops, 1), "hbm_read_gbs": round(gbs, 1),
+            "how": ("dla_peak_mfma_bf16: 2048 workgroups x 4 waves x 4 independent chains of "
+                    "v_mfma_f32_32x32x16_bf16; dla_peak_hbm_read: one read of 4 GiB with 16-byte "
+                    "non-temporal loads; best of 3")}
+
+
+def frac(achieved, peak):
+    return round(achieved / peak, 4)
+
+
+def prefill_bench(args, torch, dla, W, steps, warmup, with_events=True, serial_steps=3):
     from paper_2606_10650_amd.workloads import make_inputs
     t0 = time.time()
     x = make_inputs(W)
@@ -120,9 +162,9 @@ def prefill_bench(args, torch, dla, W):
     g = torch.from_numpy(x["g"]).reshape(B, H, T).cuda()
     del x
     cache = dla.cache_alloc(B, H, W.C, W.dk, W.dv)
-    ws = torch.empty(max(dla.workspace_bytes(cache, T, k.dtype),
-                         dla.workspace_bytes(cache, T, k.dtype, serial=True)),
-                     dtype=torch.uint8, device="cuda")
+    ws_pipe = dla.workspace_bytes(cache, T, k.dtype)
+    ws_serial = dla.workspace_bytes(cache, T, k.dtype, serial=True)
+    ws = torch.empty(max(ws_pipe, ws_serial), dtype=torch.uint8, device="cuda")
     out = torch.empty((B, H, T, W.dv), dtype=k.dtype, device="cuda")
     bnd = torch.empty((B, H, T), dtype=torch.int8, device="cuda")
     mrg = torch.empty((B, H, T), dtype=torch.int32, device="cuda")
@@ -140,101 +182,117 @@ def prefill_bench(args, torch, dla, W):
                     score=scr, workspace=ws, stage_events=events, readout_events=rev,
                     serial=serial)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
     # the timed steps: the pipelined prefill, with every readout launch
     # bracketed by a pair of events on the stream it runs on
     nseg = dla.prefill_segments(cache, T, k.dtype)
     revs = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * nseg)]
-            for _ in range(args.steps)]
+            for _ in range(steps)] if with_events else [None] * steps
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
-    for e in [start, stop] + [e for r in revs for e in r]:
+    for e in [start, stop] + [e for r in revs if r for e in r]:
         e.record()   # created here, outside the timed region
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     start.record()
-    for i in range(args.steps):
+    for i in range(steps):
         step(rev=revs[i])
     stop.record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    ms = (t1 - t0) * 1e3 / args.steps
-    log(f"[bench] prefill wall clock {ms:.3f} ms/step, "
-        f"events {start.elapsed_time(stop) / args.steps:.3f} ms/step")
-    ro_launch = np.array([[r[2 * j].elapsed_time(r[2 * j + 1]) for j in range(nseg)] for r in revs])
-    ro_ms = float(ro_launch.sum(axis=1).mean())   # readout time per step, all launches
-    # stage breakdown: the same step with the stages one after another
-    ns = len(dla.PREFILL_STAGES)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(ns + 1)] for _ in range(3)]
-    for e in evs:
-        step(events=e, serial=True)
-    torch.cuda.synchronize()
-    stages = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(ns)] for e in evs])
-    st_ms = stages.mean(axis=0)
-
-    # algorithmic work of the readout kernel, from this run's exports: the sum
-    # over tokens of 2 m_t d_k d_v (the readout over the m_t live states)
+    ms = (t1 - t0) * 1e3 / steps
+    log(f"[bench] {W.name} prefill wall clock {ms:.3f} ms/step, "
+        f"events {start.elapsed_time(stop) / steps:.3f} ms/step")
+    res = {"ms_per_step": ms, "value": B * T / (ms * 1e-3), "workspace_bytes": ws_pipe,
+           "cache_bytes": nbytes}
+    # algorithmic work from this run's exports: per token and head 2 m_t d_k d_v
+    # (the readout over the m_t live states) + 4 d_k d_v (accumulate and score)
     b = bnd.cpu().numpy().reshape(B * H, T).astype(np.int64)
     mm = (mrg.cpu().numpy().reshape(B * H, T) >= 0).astype(np.int64)
     m_t = np.cumsum(b, axis=1) - np.cumsum(mm, axis=1)
-    flops = 2.0 * W.dk * W.dv * m_t.sum()
-    flops_cap = 2.0 * W.dk * W.dv * W.C * m_t.size
-    achieved = flops / (ro_ms * 1e-3) / 1e12
-    return {
-        "ms_per_step": ms,
-        "value": B * T / (ms * 1e-3),
-        "stages_ms_serial": dict(zip(dla.PREFILL_STAGES, [round(float(s), 4) for s in st_ms])),
-        "roofline": {"kernel": "prefill_readout_kernel", "bound": "mfma",
-                     "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": counter_traffic("prefill_readout_kernel", W.name),
-                     "launches_per_step": nseg,
-                     "launch_ms_mean": round(float(ro_launch.mean()), 4),
-                     "flops_per_launch": flops / nseg,
-                     "flops_per_launch_at_m_eq_C": flops_cap / nseg},
-        "decisions": {"boundaries": int(b.sum()), "merges": int(mm.sum()),
-                      "mean_live_states": round(float(m_t.mean()), 2)},
-    }
+    d2 = float(W.dk * W.dv)
+    flops_ro = 2.0 * d2 * m_t.sum()
+    flops_call = flops_ro + 4.0 * d2 * m_t.size
+    flops_call_cap = (2.0 * W.C + 4.0) * d2 * m_t.size
+    res["decisions"] = {"boundaries": int(b.sum()), "merges": int(mm.sum()),
+                        "mean_live_states": round(float(m_t.mean()), 2)}
+    call = flops_call / (ms * 1e-3) / 1e12
+    res["roofline_call"] = {
+        "bound": "mfma", "achieved": round(call, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+        "frac": frac(call, PEAK_BF16_TFLOPS),
+        "frac_at_m_eq_C": frac(flops_call_cap / (ms * 1e-3) / 1e12, PEAK_BF16_TFLOPS),
+        "flops_per_step": flops_call, "flops_per_step_at_m_eq_C": flops_call_cap}
+    if with_events:
+        ro_launch = np.array([[r[2 * j].elapsed_time(r[2 * j + 1]) for j in range(nseg)]
+                              for r in revs])
+        ro_ms = float(ro_launch.sum(axis=1).mean())   # readout time per step, all launches
+        achieved = flops_ro / (ro_ms * 1e-3) / 1e12
+        res["roofline"] = {"kernel": "prefill_readout_kernel", "bound": "mfma",
+                           "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                           "unit": "TFLOP/s", "frac": frac(achieved, PEAK_BF16_TFLOPS),
+                           "traffic": counter_traffic("prefill_readout_kernel", W.name),
+                           "launches_per_step": nseg,
+                           "launch_ms_mean": round(float(ro_launch.mean()), 4),
+                           "readout_ms_per_step": round(ro_ms, 4),
+                           "flops_per_launch": flops_ro / nseg,
+                           "flops_per_launch_at_m_eq_C": 2.0 * d2 * W.C * m_t.size / nseg}
+    if serial_steps:
+        # stage breakdown: the same step with the stages one after another
+        ns = len(dla.PREFILL_STAGES)
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(ns + 1)]
+               for _ in range(serial_steps)]
+        for e in evs:
+            step(events=e, serial=True)
+        torch.cuda.synchronize()
+        stages = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(ns)] for e in evs])
+        res["stages_ms_serial"] = dict(zip(dla.PREFILL_STAGES,
+                                           [round(float(s), 4) for s in stages.mean(axis=0)]))
+    del q, k, v, lam, g, out, ws, cache
+    torch.cuda.empty_cache()
+    return res
 
 
-def decode_bench(args, torch, dla, W):
-    from paper_2606_10650_amd.workloads import make_decode_tokens, make_prefix_torch
+def decode_bytes(W, m_live, state_dtype_bf16):
+    """HBM bytes of one decode step per head on a full cache with a boundary
+    and a merge: every live state read once; the merged pair written, with
+    bfloat16 storage also the state that closes, and the new newest state;
+    the token vectors, lambda row and output."""
+    D = W.dk * W.dv
+    if state_dtype_bf16:
+        rd = (m_live - 1) * D * 2 + D * 4
+        wr = 2 * D * 2 + D * 4
+    else:
+        rd = m_live * D * 4
+        wr = 2 * D * 4
+    return rd + wr + (2 * W.dk + W.dv + W.C + W.dv) * 2
+
+
+def decode_bench(args, torch, dla, W, steps, state_dtype, label):
+    from paper_2606_10650_amd.workloads import make_decode_tokens_torch, make_prefix_torch
     t0 = time.time()
     _, k, v, g = make_prefix_torch(W, "cuda")
     torch.cuda.synchronize()
-    log(f"[bench] decode prefix {W.label} drawn on device in {time.time() - t0:.1f}s")
-    cache = dla.cache_alloc(W.B, W.H, W.C, W.dk, W.dv)
-    t0 = time.time()
+    cache = dla.cache_alloc(W.B, W.H, W.C, W.dk, W.dv, state_dtype=state_dtype)
     dla.prefill(cache, None, k, v, g, None, tau=W.tau, skip_readout=True, want_exports=False)
     torch.cuda.synchronize()
-    log(f"[bench] decode prefix absorbed in {time.time() - t0:.1f}s")
+    log(f"[bench] {label}: prefix drawn and absorbed in {time.time() - t0:.1f}s")
     del k, v, g
     torch.cuda.empty_cache()
-    steps = args.decode_steps
-    x = make_decode_tokens(W, steps=steps + 2)
-
-    def dev(a, shape):
-        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).reshape(shape).cuda()
-
-    nh = W.B * W.H
-    q = dev(x["q"], (W.B, W.H, steps + 2, W.dk)).permute(2, 0, 1, 3).contiguous()
-    kk = dev(x["k"], (W.B, W.H, steps + 2, W.dk)).permute(2, 0, 1, 3).contiguous()
-    vv = dev(x["v"], (W.B, W.H, steps + 2, W.dv)).permute(2, 0, 1, 3).contiguous()
-    lam = dev(x["lam"], (W.B, W.H, steps + 2, W.C)).permute(2, 0, 1, 3).contiguous()
-    gg = torch.from_numpy(x["g"]).reshape(W.B, W.H, steps + 2).permute(2, 0, 1).contiguous().cuda()
+    q, kk, vv, gg, lam = make_decode_tokens_torch(W, steps + 2, "cuda")
     out = torch.empty((W.B, W.H, W.dv), dtype=torch.bfloat16, device="cuda")
     bnd = torch.empty((steps, W.B, W.H), dtype=torch.int8, device="cuda")
     mrg = torch.empty((steps, W.B, W.H), dtype=torch.int32, device="cuda")
-    m_before = dla.cache_export(cache, heads=[0])["m"][0]
-    # warm-up on a copy of the cache, then 256 timed steps on the prefix cache
-    warm = dla.StateCache(W.B, W.H, W.C, W.dk, W.dv, cache.buf.clone())
+    m_before = int(dla.cache_export(cache, heads=[0])["m"][0])
+    # warm-up on a copy of the cache, then the timed steps on the prefix cache
+    warm = dla.StateCache(W.B, W.H, W.C, W.dk, W.dv, cache.buf.clone(), state_dtype)
     for i in range(2):
         dla.decode_step(warm, q[i], kk[i], vv[i], gg[i], lam[i], tau=W.tau, out=out,
                         want_exports=False)
     torch.cuda.synchronize()
     del warm
+    torch.cuda.empty_cache()
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     evs[0].record()
     for i in range(steps):
@@ -245,25 +303,32 @@ def decode_bench(args, torch, dla, W):
     us = np.array([evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(steps)])
     nb = int(bnd.sum().item())
     nm = int((mrg >= 0).sum().item())
-    # HBM bytes per step: every live state read once (float32), plus the written
-    # states (merged pair and new state, or the accumulated newest state), plus
-    # the token vectors, lambda row and output
-    m_live = W.C  # full caches
-    per_head = m_live * W.dk * W.dv * 4 + 2 * W.dk * W.dv * 4 + (2 * W.dk + W.dv + W.C + W.dv) * 2
-    bytes_step = per_head * nh
+    nh = W.B * W.H
+    sb = state_dtype == dla.DLA_BF16
+    bytes_step = decode_bytes(W, W.C, sb) * nh
     ach = bytes_step / (np.mean(us) * 1e-6) / 1e9
-    return {
-        "config": {"workload": f"decode {W.B}x{W.H} heads, C={W.C}, d={W.dk}, prefix {W.T} tokens",
-                   "B": W.B, "H": W.H, "C": W.C, "prefix_tokens": W.T, "steps": steps},
+    res = {
+        "config": {"workload": (f"decode {W.B}x{W.H} heads, C={W.C}, d={W.dk}, prefix {W.T} "
+                                f"tokens, {'bf16' if sb else 'f32'} state storage"),
+                   "B": W.B, "H": W.H, "C": W.C, "prefix_tokens": W.T, "steps": steps,
+                   "state_dtype": "bf16" if sb else "f32"},
         "us_per_step_mean": round(float(np.mean(us)), 2),
         "us_per_step_p50": round(float(np.median(us)), 2),
-        "live_states_before": int(m_before),
+        "live_states_before": m_before,
         "boundaries": nb, "merges": nm,
+        "cache_bytes": cache.buf.numel(),
         "roofline": {"kernel": "decode_kernel", "bound": "hbm", "achieved": round(ach, 1),
-                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
-                     "traffic": counter_traffic("decode_kernel", W.name),
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": frac(ach, PEAK_HBM_GBS),
+                     "traffic": (counter_traffic("decode_kernel", W.name) if not sb else
+                                 counter_traffic("decode_kernel", W.name + "_bf16")),
                      "bytes_per_launch": bytes_step},
     }
+    if args.decode_cpu_heads and W.B * W.H > 1000 and not sb:
+        res["_cache"] = cache   # for the CPU baseline of the decode step
+    else:
+        del cache
+    torch.cuda.empty_cache()
+    return res
 
 
 def cpu_baseline(args, W):
@@ -285,6 +350,38 @@ def cpu_baseline(args, W):
                        f"(all heads of a token together), comparable with value / B")}
 
 
+def cpu_decode_baseline(args, torch, dla, W, cache):
+    """The float64 oracle's decode step from the GPU-built cache of a few heads
+    (copied to the host), timed on the host cores: microseconds per step for
+    all B*H heads, scaled from the sample (heads are independent)."""
+    from oracle import OracleCache, oracle_forward, oracle_threads
+    from paper_2606_10650_amd.workloads import make_decode_tokens_torch
+    nh = W.B * W.H
+    heads = list(range(args.decode_cpu_heads))
+    steps = args.decode_cpu_steps
+    exp = dla.cache_export(cache, heads=heads)
+    # the oracle's cache: true states exp(G - F_j) times the stored values
+    oc = OracleCache.empty(len(heads), W.C, W.dk, W.dv)
+    for i in range(len(heads)):
+        m = int(exp["m"][i])
+        oc.m[i], oc.n[i], oc.ibar[i] = m, exp["n"][i], exp["ibar"][i]
+        oc.S[i, :m] = np.exp(exp["G"][i] - exp["F"][i, :m])[:, None, None] * exp["stored"][i, :m]
+    q, k, v, g, lam = make_decode_tokens_torch(W, steps, "cpu")
+
+    def host(t):
+        t = t.reshape(steps, nh, -1)[:, heads].float().numpy().astype(np.float64)
+        return np.ascontiguousarray(np.transpose(t, (1, 0, 2)))
+    xq, xk, xv, xl, xg = host(q), host(k), host(v), host(lam), host(g)[..., 0]
+    t0 = time.perf_counter()
+    oracle_forward(xk, xv, xg, W.C, W.tau, q=xq, lam=xl, cache=oc)
+    dt = time.perf_counter() - t0
+    us_all = dt / steps * 1e6 * nh / len(heads)
+    return {"us_per_step": round(us_all, 1), "unit": "us/step (all heads)",
+            "cores": oracle_threads(), "kind": "oracle",
+            "sample": (f"float64 oracle, {steps} decode steps of {len(heads)} of the {nh} heads "
+                       f"from the GPU-built cache ({dt:.1f} s), scaled to all heads")}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -292,9 +389,14 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="cfg3")
     ap.add_argument("--decode-steps", type=int, default=256)
+    ap.add_argument("--other-steps", type=int, default=5)
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-others", action="store_true")
+    ap.add_argument("--no-peaks", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=16384)
+    ap.add_argument("--decode-cpu-heads", type=int, default=16)
+    ap.add_argument("--decode-cpu-steps", type=int, default=16)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -310,7 +412,7 @@ def main():
     from paper_2606_10650_amd import dla
     from paper_2606_10650_amd.workloads import WORKLOADS
     W = WORKLOADS[args.workload]
-    pre = prefill_bench(args, torch, dla, W)
+    pre = prefill_bench(args, torch, dla, W, args.steps, args.warmup)
     log(f"[bench] prefill {pre['ms_per_step']:.3f} ms/step, serial stages {pre['stages_ms_serial']}")
     res = {
         "metric": METRIC,
@@ -333,12 +435,53 @@ def main():
         "stages_ms_serial": pre["stages_ms_serial"],
         "decisions": pre["decisions"],
         "roofline": pre["roofline"],
+        "roofline_call": pre["roofline_call"],
+        "memory": {"cache_bytes": pre["cache_bytes"], "workspace_bytes": pre["workspace_bytes"]},
     }
+    if not args.no_peaks:
+        pk = measured_peaks(torch, dla)
+        res["peaks_measured"] = pk
+        for key in ("roofline", "roofline_call"):
+            res[key]["frac_measured_peak"] = frac(res[key]["achieved"], pk["mfma_bf16_tflops"])
+        log(f"[bench] measured peaks {pk}")
+    if not args.no_others:
+        others = {}
+        for name in ("cfg2", "cfg4"):
+            Wo = WORKLOADS[name]
+            r = prefill_bench(args, torch, dla, Wo, args.other_steps, 1, serial_steps=0)
+            others[name] = {
+                "workload": (f"prefill {name}: B={Wo.B} H={Wo.H} T={Wo.T} d={Wo.dk} C={Wo.C} "
+                             f"bf16, {Wo.structure}"),
+                "ms_per_step": round(r["ms_per_step"], 4), "tokens_per_s": round(r["value"], 1),
+                "roofline_readout_frac": r["roofline"]["frac"],
+                "roofline_call_frac": r["roofline_call"]["frac"],
+                "roofline_call_frac_at_m_eq_C": r["roofline_call"]["frac_at_m_eq_C"],
+                "workspace_bytes": r["workspace_bytes"], "decisions": r["decisions"]}
+        res["prefill_workloads"] = others
+    cache5 = None
     if not args.no_decode:
-        res["decode"] = decode_bench(args, torch, dla, WORKLOADS["cfg5"])
-        log(f"[bench] decode {res['decode']['us_per_step_mean']} us/step")
+        W5 = WORKLOADS["cfg5"]
+        dec = {}
+        for sd, tag in ((dla.DLA_F32, "f32"), (dla.DLA_BF16, "bf16")):
+            d = decode_bench(args, torch, dla, W5, args.decode_steps, sd, f"decode {tag}")
+            cache5 = d.pop("_cache", cache5)
+            dec[tag] = d
+            log(f"[bench] decode ({tag} states) {d['us_per_step_mean']} us/step")
+        res["decode"] = dec["f32"]
+        res["decode_bf16_states"] = dec["bf16"]
+        few = W5.replace(B=1, T=8192)
+        d = decode_bench(args, torch, dla, few, 64, dla.DLA_F32, "decode few heads")
+        res["decode_few_heads"] = d
+        log(f"[bench] decode (1x32 heads) {d['us_per_step_mean']} us/step")
+        if pk := res.get("peaks_measured"):
+            for key in ("decode", "decode_bf16_states", "decode_few_heads"):
+                res[key]["roofline"]["frac_measured_peak"] = frac(res[key]["roofline"]["achieved"],
+                                                                  pk["hbm_read_gbs"])
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(args, W)
+        if cache5 is not None:
+            res["cpu_baseline"]["decode"] = cpu_decode_baseline(args, torch, dla,
+                                                                WORKLOADS["cfg5"], cache5)
     print(json.dumps(res), flush=True)
 
 

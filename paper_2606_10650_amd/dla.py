@@ -27,7 +27,7 @@ DLA_FLAG_CACHE_MISMATCH = 2
 EXPORTED = ("dla_cache_layout_of", "dla_state_cache_alloc", "dla_cache_flags",
             "dla_cache_header_check", "dla_prefill_workspace_size", "dla_prefill_segment_count",
             "dla_prefill_segment_starts", "dla_prefill", "dla_prefill_static", "dla_decode_step",
-            "dla_status_string", "dla_get_last_error")
+            "dla_status_string", "dla_get_last_error", "dla_peak_mfma_bf16", "dla_peak_hbm_read")
 STATIC_SCRATCH_BYTES = 128 << 20   # DLA_STATIC_SCRATCH_BYTES
 
 
@@ -89,13 +89,16 @@ def lib():
                                          P, P, P]
         L.dla_decode_step.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, I,
                                       ctypes.POINTER(Params), P, I, P, P, P, P, P, P]
+        L.dla_peak_mfma_bf16.argtypes = [ctypes.c_int32, ctypes.c_int32, P, P]
+        L.dla_peak_hbm_read.argtypes = [P, ctypes.c_size_t, ctypes.c_int32, P, P]
         L.dla_status_string.argtypes = [I]
         L.dla_status_string.restype = ctypes.c_char_p
         L.dla_get_last_error.argtypes = []
         for name in ("dla_cache_layout_of", "dla_state_cache_alloc", "dla_cache_flags",
                      "dla_cache_header_check", "dla_prefill_workspace_size",
                      "dla_prefill_segment_count", "dla_prefill_segment_starts", "dla_prefill",
-                     "dla_prefill_static", "dla_decode_step", "dla_get_last_error"):
+                     "dla_prefill_static", "dla_decode_step", "dla_get_last_error",
+                     "dla_peak_mfma_bf16", "dla_peak_hbm_read"):
             getattr(L, name).restype = I
         _lib = L
     return _lib
@@ -415,3 +418,19 @@ def cache_export(cache: StateCache, heads=None) -> dict:
             o0 = L.open_offset + h * D * 4
             res["stored"][i, m - 1] = host(o0, o0 + D * 4).view(np.float32).reshape(dk, dv)
     return res
+
+
+def peak_mfma_bf16(blocks: int, iters: int, sink) -> None:
+    """Enqueue the dense bfloat16 MFMA rate kernel (blocks * 16 * iters * 32768
+    operations); sink: a float32 device tensor of blocks * 256 elements."""
+    assert sink.numel() >= blocks * 256
+    _check(lib().dla_peak_mfma_bf16(int(blocks), int(iters), _ptr(sink), _stream(sink.device)),
+           "dla_peak_mfma_bf16")
+
+
+def peak_hbm_read(buf, blocks: int, sink) -> None:
+    """Enqueue one read of the device buffer buf (bytes a multiple of 4096)."""
+    assert sink.numel() >= blocks * 256
+    nbytes = buf.numel() * buf.element_size()
+    _check(lib().dla_peak_hbm_read(_ptr(buf), nbytes, int(blocks), _ptr(sink),
+                                   _stream(sink.device)), "dla_peak_hbm_read")

@@ -265,7 +265,9 @@ def make_decode_tokens(w: Workload, steps: Optional[int] = None, heads: Optional
     out["lam"] = np.empty((n, steps, w.C), sdt)
     seg = np.arange(steps, dtype=np.int64)
     rho2 = np.zeros(steps)
-    for i, (b, h) in enumerate(heads):
+
+    def one(i):
+        b, h = heads[i]
         k, v, q, g = _head_tokens(w, b, h, seg, rho2, t0=w.T)
         out["k"][i] = store(k, w.dtype)
         out["v"][i] = store(v, w.dtype)
@@ -273,6 +275,8 @@ def make_decode_tokens(w: Workload, steps: Optional[int] = None, heads: Optional
         out["g"][i] = g.astype(np.float32)
         out["lam"][i] = store(1.0 + 0.5 * (to_f64(out["q"][i], w.dtype) @ lambda_weights(w, h).T),
                               w.dtype)
+
+    _parallel(one, n)
     out["heads"] = list(heads)
     return out
 
@@ -309,3 +313,28 @@ def make_prefix_torch(w: Workload, device, with_q: bool = False):
             qq = torch.randn((w.H, w.T, w.dk), generator=gen, device=device)
             q[b] = (qq / qq.norm(dim=-1, keepdim=True)).to(tdt)
     return q, k, v, g
+
+
+def make_decode_tokens_torch(w: Workload, steps: int, device):
+    """Device-side draw of i.i.d. decode tokens (rho2 = 0) with the recipe of
+    make_decode_tokens, from torch's generator seeded with w.seed: q, k
+    normalised, v ~ N(0, I), g ~ U(g_lo, 0), lambda = 1 + 0.5 (w_j . q) with the
+    per-head projection of lambda_weights, computed from the stored query.
+    Values differ from make_decode_tokens' numpy streams.  Returns tensors laid
+    out [steps, B, H, *] (one contiguous slice per step): q, k [.., d_k], v
+    [.., d_v], lam [.., C] in the storage dtype, g [steps, B, H] float32."""
+    import torch
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(w.seed) * 1000003 + 29)
+    shp = (steps, w.B, w.H)
+    q = torch.randn(shp + (w.dk,), generator=gen, device=device)
+    q = (q / q.norm(dim=-1, keepdim=True)).to(tdt)
+    k = torch.randn(shp + (w.dk,), generator=gen, device=device)
+    k = (k / k.norm(dim=-1, keepdim=True)).to(tdt)
+    v = torch.randn(shp + (w.dv,), generator=gen, device=device).to(tdt)
+    g = torch.rand(shp, generator=gen, device=device) * w.g_lo
+    Wt = torch.from_numpy(np.stack([lambda_weights(w, h).T for h in range(w.H)])).to(
+        device=device, dtype=torch.float32).contiguous()          # [H, d_k, C]
+    lam = 1.0 + 0.5 * torch.matmul(q.float().unsqueeze(-2), Wt).squeeze(-2)
+    return q, k, v, g.contiguous(), lam.to(tdt).contiguous()

@@ -13,14 +13,20 @@ HEADER = os.path.join(ROOT, "include", "dla.h")
 
 
 def _declared():
-    src = open(HEADER).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(dla_[a-z_]+)\s*\(", src)))
+    """Entry points declared by every header under include/."""
+    names = set()
+    for f in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if f.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", f)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names |= set(re.findall(r"\b(dla_[a-z0-9_]+)\s*\(", src))
+    return sorted(names)
 
 
 def test_header_compiles_as_c(tmp_path):
     c = tmp_path / "t.c"
-    c.write_text('#include "dla.h"\nint main(void){dla_cache_desc d={1,1,1,64,64};(void)d;return 0;}\n')
+    c.write_text('#include "dla.h"\n#include "dla_peak.h"\n'
+                 'int main(void){dla_cache_desc d={1,1,1,64,64,DLA_BF16};(void)d;return 0;}\n')
     subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"),
                     "-fsyntax-only", str(c)], check=True)
 

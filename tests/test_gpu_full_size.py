@@ -10,7 +10,7 @@ import pytest
 
 from oracle import OracleCache, direct, oracle_forward
 from tests import harness as H
-from paper_2606_10650_amd.workloads import WORKLOADS, make_inputs, make_decode_tokens
+from paper_2606_10650_amd.workloads import WORKLOADS, make_inputs, make_decode_tokens_torch
 
 pytestmark = pytest.mark.gpu
 
@@ -165,10 +165,14 @@ def test_decode_full_size_sampled_heads(state):
         oc.ibar[i] = dec["cache"].ibar[i]
     H.assert_cache(dla.cache_export(cache, heads=heads), oc, H.STATE_TOL[sb],
                    what=f"{w.label} prefix")
-    # the decode steps
-    x = make_decode_tokens(w, steps=steps)
-    xd = {key: x[key] for key in ("q", "k", "v", "lam", "g")}
-    xh = H.f64({key: xd[key][heads] for key in xd}, w)
+    # the decode steps: tokens drawn on the device, the sampled heads' values
+    # read back as the kernels see them
+    dq, dk_, dv_, dg, dl = make_decode_tokens_torch(w, steps, "cuda")
+
+    def host(t):   # [steps, B, H, *] -> the sampled heads [n, steps, *], float64
+        t = t.reshape(steps, nh, -1)[:, heads].float().cpu().numpy().astype(np.float64)
+        return np.ascontiguousarray(np.transpose(t, (1, 0, 2)))
+    xh = {"q": host(dq), "k": host(dk_), "v": host(dv_), "lam": host(dl), "g": host(dg)[..., 0]}
     free = oracle_forward(xh["k"], xh["v"], xh["g"], w.C, w.tau, q=xh["q"], lam=xh["lam"],
                           cache=oc.copy())
     # Every step opens a state for an i.i.d. token, whose score against the
@@ -181,7 +185,6 @@ def test_decode_full_size_sampled_heads(state):
                                               max_frac=0.05)
     ref = oracle_forward(xh["k"], xh["v"], xh["g"], w.C, w.tau, q=xh["q"], lam=xh["lam"],
                          cache=oc, b_override=sbo, m_override=smo)
-    q, kk, vv, gg, lam = H.inputs_to_device(w, xd, w.B, w.H)
     hidx = torch.tensor(heads, device="cuda")
     bo_d = torch.full((nh, steps), -1, dtype=torch.int8)
     mo_d = torch.full((nh, steps), -1, dtype=torch.int32)
@@ -191,9 +194,7 @@ def test_decode_full_size_sampled_heads(state):
     mo_d = mo_d.reshape(w.B, w.H, steps).permute(2, 0, 1).contiguous().cuda()
     outs, bs, ms = [], [], []
     for t in range(steps):
-        o, b, mi, _ = dla.decode_step(cache, q[:, :, t].contiguous(), kk[:, :, t].contiguous(),
-                                      vv[:, :, t].contiguous(), gg[:, :, t].contiguous(),
-                                      lam[:, :, t].contiguous(), tau=w.tau,
+        o, b, mi, _ = dla.decode_step(cache, dq[t], dk_[t], dv_[t], dg[t], dl[t], tau=w.tau,
                                       boundary_override=bo_d[t], merge_override=mo_d[t])
         outs.append(o.reshape(nh, w.dv)[hidx])
         bs.append(b.reshape(nh)[hidx])
