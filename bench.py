@@ -294,11 +294,21 @@ def decode_bench(args, torch, dla, W, steps, state_dtype, label):
     del warm
     torch.cuda.empty_cache()
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    for e in evs:
+        e.record()   # created here, outside the timed region
+    torch.cuda.synchronize()
+    # The stream is held by a short device-side sleep while the steps are
+    # enqueued, so that the events time the kernels and not the host's
+    # enqueueing (a step on few heads takes less time on the device than the
+    # Python call that enqueues it); the wall clock is reported beside.
+    torch.cuda._sleep(int(2e6) * (1 + steps // 8))
+    t0 = time.perf_counter()
     evs[0].record()
     for i in range(steps):
         dla.decode_step(cache, q[i + 2], kk[i + 2], vv[i + 2], gg[i + 2], lam[i + 2], tau=W.tau,
                         out=out, boundary=bnd[i], merge_idx=mrg[i], score=None)
         evs[i + 1].record()
+    t_enq = time.perf_counter() - t0
     torch.cuda.synchronize()
     us = np.array([evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(steps)])
     nb = int(bnd.sum().item())
@@ -314,6 +324,7 @@ def decode_bench(args, torch, dla, W, steps, state_dtype, label):
                    "state_dtype": "bf16" if sb else "f32"},
         "us_per_step_mean": round(float(np.mean(us)), 2),
         "us_per_step_p50": round(float(np.median(us)), 2),
+        "us_per_step_host_enqueue": round(t_enq / steps * 1e6, 2),
         "live_states_before": m_before,
         "boundaries": nb, "merges": nm,
         "cache_bytes": cache.buf.numel(),
@@ -395,8 +406,8 @@ def main():
     ap.add_argument("--no-peaks", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=16384)
-    ap.add_argument("--decode-cpu-heads", type=int, default=16)
-    ap.add_argument("--decode-cpu-steps", type=int, default=16)
+    ap.add_argument("--decode-cpu-heads", type=int, default=128)
+    ap.add_argument("--decode-cpu-steps", type=int, default=64)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()

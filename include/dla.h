@@ -151,14 +151,14 @@ typedef struct {
  *           int32 B, H, C, d_k, d_v, uint32 device flags, int32 state_dtype,
  *           zero padding.
  *   per-head metadata at meta_offset + h * meta_stride, h = b*H + head:
- *           int32 m (live states), int32 decode arrival count (0 between
- *           calls), double G (sum of all absorbed log-decays), int64 tokens
- *           absorbed, int64 0,
+ *           int32 m (live states), int32 0, double G (sum of all absorbed
+ *           log-decays), int64 tokens absorbed, int64 0,
  *           double F[C] (frame of each live state), double Ibar[C] (aggregated
  *           score), int32 n[C] (token count), int32 perm[C] (physical slot of
  *           each logical state; entries m..C-1 list the free slots),
- *           then from a 64-byte boundary float [16][d_v]: scratch for the
- *           partial outputs of a decode step split over several workgroups.
+ *           then from a 64-byte boundary 64 bytes and float [16][d_v]:
+ *           scratch for the decisions and the partial outputs of a decode step
+ *           split over several workgroups.
  *           Arrays are in chronological order (index 0 = oldest).
  *   states  at states_offset: [B*H][C][d_k][d_v] by physical slot, in the
  *           state type.  The true state of logical state j is
@@ -274,9 +274,9 @@ dla_status dla_prefill_static(const dla_cache_desc* desc, void* cache, const voi
 /*
  * Decode step: absorb one token per head (the prefill semantics with T = 1),
  * streaming every live state once.  With few heads the step splits each head's
- * states over up to 16 workgroups, which meet in the scratch area of the
- * head's metadata (the sum of their partial outputs is taken in a fixed order,
- * so results are deterministic).  q, k: [B][H][d_k]; v, out: [B][H][d_v];
+ * states over up to 16 workgroups, which leave partial outputs in the scratch
+ * area of the head's metadata; a second kernel on the same stream sums them in
+ * a fixed order (results are deterministic) and ends the step.  q, k: [B][H][d_k]; v, out: [B][H][d_v];
  * log_gate: [B][H]; lambda: [B][H][C] (nullable); exports and overrides:
  * [B][H] (nullable).  Needs no workspace.
  */

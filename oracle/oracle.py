@@ -76,12 +76,13 @@ def _p(a):
 
 def oracle_forward(k, v, g, C: int, tau: float, *, q=None, lam=None, eps: float = 1e-6,
                    eps_rms: float = 1e-6, b_override=None, m_override=None, full: bool = True,
-                   want_out: bool = True, cache: Optional[OracleCache] = None,
-                   lib_path: Optional[str] = None):
+                   want_out: bool = True, want_mag: bool = False,
+                   cache: Optional[OracleCache] = None, lib_path: Optional[str] = None):
     """Run the oracle on float64 inputs shaped [n_heads, T, d] (g: [n_heads, T],
     lam: [n_heads, T, C]).  Returns a dict with out, b, merge, score, m,
-    margin_b, margin_m, mag (sum over states of |lambda| ||S_j||_F ||q||, which
-    bounds the sizes of the readout's terms; with out) and the final cache.  The cache argument is
+    margin_b, margin_m, mag (with want_mag: the sum over states of |lambda|
+    ||S_j||_F ||q||, which bounds the sizes of the readout's terms; with out)
+    and the final cache.  The cache argument is
     updated in place when given."""
     k = np.ascontiguousarray(k, np.float64)
     v = np.ascontiguousarray(v, np.float64)
@@ -104,7 +105,7 @@ def oracle_forward(k, v, g, C: int, tau: float, *, q=None, lam=None, eps: float 
         "m": np.zeros((nh, T), np.int32),
         "margin_b": np.zeros((nh, T)),
         "margin_m": np.zeros((nh, T)),
-        "mag": np.zeros((nh, T)) if want_out else None,
+        "mag": np.zeros((nh, T)) if (want_out and want_mag) else None,
     }
     bo = None if b_override is None else np.ascontiguousarray(b_override, np.int8)
     mo = None if m_override is None else np.ascontiguousarray(m_override, np.int32)

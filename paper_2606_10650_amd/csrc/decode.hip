@@ -12,15 +12,17 @@
 // the newest state, the counts and the aggregated scores, so they do not depend
 // on the storage type.
 //
-// Work split: NS workgroups of 256 threads per head (NS = 1 when there are
-// enough heads to fill the chip).  Each takes the step's decisions (identical
-// arithmetic on identical data, so every workgroup of a head reaches the same
-// ones) and streams one contiguous range of the pre-merge states, the merged
-// pair never split between two ranges; it writes its partial output to a small
-// area in the head's metadata and counts itself in with one atomic add.  The
-// last workgroup to arrive (no workgroup ever waits for another) sums the
+// Work split: one workgroup of 256 threads per head when there are enough heads
+// to fill the chip.  With few heads, NS workgroups per head: each takes the
+// step's decisions (identical arithmetic on identical data, so every workgroup
+// of a head reaches the same ones) and streams one contiguous range of the
+// pre-merge states, the merged pair never split between two ranges, leaving
+// its partial output (and, for the first, the decisions) in a small area of
+// the head's metadata; a second kernel, one workgroup per head, then sums the
 // partials in split order, writes the output and the newest state, and updates
-// the metadata: by then every workgroup has read what it needed.
+// the metadata.  The kernel boundary orders the two: no workgroup waits for
+// another, and no device-scope fence is needed (one per workgroup, with the L2
+// write-back it implies, made the split step 2.4 times slower).
 //
 // Thread mapping inside a state: element group tid + 256 r (4 consecutive
 // elements) of the row-major d_k x d_v array, i.e. thread tid owns the 4
@@ -37,14 +39,27 @@ namespace dla {
 typedef float f32x4v __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
 
-__device__ __forceinline__ float4 ld_group(const float* base, int g, bool stream) {
+// NT: with the non-temporal hint.  (A template parameter, not a run-time
+// choice: a select between a hinted and a plain load of one address is folded
+// into one load without the hint.)
+template <bool NT>
+__device__ __forceinline__ float4 ld_group(const float* base, int g) {
   const f32x4v* p = reinterpret_cast<const f32x4v*>(base) + g;
-  const f32x4v x = stream ? __builtin_nontemporal_load(p) : *p;
+  f32x4v x;
+  if constexpr (NT)
+    x = __builtin_nontemporal_load(p);
+  else
+    x = *p;
   return make_float4(x[0], x[1], x[2], x[3]);
 }
-__device__ __forceinline__ float4 ld_group(const bf16_t* base, int g, bool stream) {
+template <bool NT>
+__device__ __forceinline__ float4 ld_group(const bf16_t* base, int g) {
   const u32x2v* p = reinterpret_cast<const u32x2v*>(base) + g;
-  const u32x2v x = stream ? __builtin_nontemporal_load(p) : *p;
+  u32x2v x;
+  if constexpr (NT)
+    x = __builtin_nontemporal_load(p);
+  else
+    x = *p;
   return make_float4(__uint_as_float(x[0] << 16), __uint_as_float(x[0] & 0xFFFF0000u),
                      __uint_as_float(x[1] << 16), __uint_as_float(x[1] & 0xFFFF0000u));
 }
@@ -82,7 +97,117 @@ __device__ __forceinline__ void split_range(int m, int ns, int sp, int istar, in
   *j1 = a1;
 }
 
-template <int DK, int DV, typename Tin, typename Tout, typename TS>
+// The decisions of a split step, handed to the finishing kernel.
+struct DecodeRecord {
+  int32_t b, istar;
+  double I;
+};
+
+// The end of a step for head h, by one workgroup: the newest state
+// (accumulated, or the new state k v^T in frame Gn, in the slot the merge
+// freed or the first free slot; with bfloat16 storage in the open region),
+// the output acc + lambda_{m'-1} (q.k) v, the exports and the metadata.
+// open_at(r) gives the thread's r-th group of the newest state before the
+// step (needed only when b = 0).
+template <int DK, int DV, typename Tout, typename TS, typename OpenAt>
+__device__ __forceinline__ void finish_step(const DecodeArgs& a, int h, int m, int b, int istar,
+                                            double I, double Gn, float acc, float qk2,
+                                            const float* sk, const float* sv, const double* sF,
+                                            const double* sI, const int32_t* sN,
+                                            const int32_t* sP, const float* sLam, Meta M,
+                                            TS* states, float* open, OpenAt open_at) {
+  using ST = StateTile<DK, DV>;
+  constexpr int D = DK * DV;
+  constexpr bool SB = sizeof(TS) == 2;
+  const int tid = threadIdx.x;
+  const int cq = tid % ST::CQ;
+  const int rg = tid / ST::CQ;
+  const int C = a.desc.C;
+  const int m_post = b ? (istar >= 0 ? m : m + 1) : m;
+  {
+    float* dst;
+    if (SB)
+      dst = open;
+    else if (!b)
+      dst = reinterpret_cast<float*>(states) + (size_t)sP[m - 1] * D;
+    else
+      dst = reinterpret_cast<float*>(states) + (size_t)((istar >= 0) ? sP[istar + 1] : sP[m]) * D;
+    const float4 vq = reinterpret_cast<const float4*>(sv)[cq];
+    if (b) {
+#pragma unroll
+      for (int r = 0; r < ST::NV; ++r) {
+        const float kr = sk[rg + ST::RG * r];
+        st_group(dst, tid + 256 * r, make_float4(kr * vq.x, kr * vq.y, kr * vq.z, kr * vq.w));
+      }
+    } else {
+      const float f = __expf((float)(Gn - sF[m - 1]));
+#pragma unroll
+      for (int r = 0; r < ST::NV; ++r) {
+        const float kr = sk[rg + ST::RG * r];
+        const float4 o = open_at(r);
+        float4 s;
+        s.x = f * o.x + kr * vq.x;
+        s.y = f * o.y + kr * vq.y;
+        s.z = f * o.z + kr * vq.z;
+        s.w = f * o.w + kr * vq.w;
+        st_group(dst, tid + 256 * r, s);
+      }
+    }
+  }
+  // the new token's own contribution lambda_{m'-1} (q.k) v
+  if (!a.skip_readout && tid < DV) {
+    acc += sLam[m_post - 1] * qk2 * sv[tid];
+    static_cast<Tout*>(a.out)[(size_t)h * DV + tid] = from_f32<Tout>(acc);
+  }
+  if (tid == 0) {
+    if (a.b_out) a.b_out[h] = (int8_t)b;
+    if (a.merge_out) a.merge_out[h] = istar;
+    if (a.score_out) a.score_out[h] = (float)I;
+  }
+  // metadata update (chronological arrays, parallel over slots)
+  if (!b) {
+    if (tid == 0) {
+      M.F[m - 1] = Gn;
+      M.n[m - 1] = sN[m - 1] + 1;
+      M.ibar[m - 1] = sI[m - 1] + I;
+    }
+  } else {
+    if (istar >= 0) {
+      // merge istar, istar+1; shift later states down; freed slot goes to perm[m-1]
+      for (int j = tid; j < C; j += 256) {
+        if (j == istar) {
+          M.F[j] = Gn;
+          M.n[j] = sN[j] + sN[j + 1];
+          M.ibar[j] = sI[j] + sI[j + 1];
+        } else if (j > istar && j < m - 1) {
+          M.F[j] = sF[j + 1];
+          M.n[j] = sN[j + 1];
+          M.ibar[j] = sI[j + 1];
+          M.perm[j] = sP[j + 1];
+        } else if (j == m - 1) {
+          // the new state takes the freed slot
+          M.perm[j] = sP[istar + 1];
+          M.F[j] = Gn;
+          M.n[j] = 1;
+          M.ibar[j] = I;
+        }
+      }
+    } else if (tid == 0) {
+      M.F[m] = Gn;
+      M.n[m] = 1;
+      M.ibar[m] = I;
+    }
+    if (tid == 0) *M.m = m_post;
+  }
+  if (tid == 0) {
+    *M.G = Gn;
+    *M.tokens += 1;
+  }
+}
+
+// SPLIT: one of NS workgroups of a head (partials to the metadata's scratch;
+// decode_finish_kernel ends the step); otherwise the whole step of a head.
+template <int DK, int DV, typename Tin, typename Tout, typename TS, bool SPLIT>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
   using ST = StateTile<DK, DV>;
   constexpr int D = DK * DV;
@@ -91,7 +216,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     flag_mismatch(a.cache);
     return;
   }
-  const int ns = a.nsplit;
+  const int ns = SPLIT ? a.nsplit : 1;
   const int h = blockIdx.x / ns;
   const int sp = blockIdx.x % ns;
   const int tid = threadIdx.x;
@@ -152,14 +277,14 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
   }
 
   // newest state in registers, and the two scalars b = |S~|^2, c = k^T S~ v;
-  // every workgroup of a head reads it, so with several it is read cacheable
+  // every workgroup of a split head reads it, so there it is read cacheable
   float4 Sopen[ST::NV];
   float ct = 0.f, bt = 0.f;
   if (m > 0) {
     const float4 vq = reinterpret_cast<const float4*>(sv)[cq];
 #pragma unroll
     for (int r = 0; r < ST::NV; ++r) {
-      Sopen[r] = ld_group(newest, tid + 256 * r, ns == 1);
+      Sopen[r] = ld_group<!SPLIT>(newest, tid + 256 * r);
       const float kr = sk[rg + ST::RG * r];
       const float4 s = Sopen[r];
       ct += kr * (s.x * vq.x + s.y * vq.y + s.z * vq.z + s.w * vq.w);
@@ -261,7 +386,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     } else {
       const TS* src = states + (size_t)sP[j] * D;
 #pragma unroll
-      for (int r = 0; r < ST::NV; ++r) X[r] = ld_group(src, tid + 256 * r, true);
+      for (int r = 0; r < ST::NV; ++r) X[r] = ld_group<true>(src, tid + 256 * r);
     }
     const int post = (istar >= 0 && j > istar) ? j - 1 : j;
     const float w = a.skip_readout ? 0.f : sLam[post] * __expf((float)(Gn - sF[j]));
@@ -293,7 +418,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
       } else {
         const TS* src = states + (size_t)sP[j2] * D;
 #pragma unroll
-        for (int r = 0; r < ST::NV; ++r) Y[r] = ld_group(src, tid + 256 * r, true);
+        for (int r = 0; r < ST::NV; ++r) Y[r] = ld_group<true>(src, tid + 256 * r);
       }
       const float e2 = __expf((float)(Gn - sF[j2]));
       const float w2 = a.skip_readout ? 0.f : sLam[j] * e2;
@@ -338,109 +463,77 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
 #pragma unroll
     for (int g2 = 0; g2 < ST::RG; ++g2) acc += sOut[g2][tid];
   }
-  if (ns > 1) {
-    // hand the partial to the last workgroup of the head to arrive
-    float* part = decode_partials(mbase, C) + (size_t)sp * DV;
-    if (!a.skip_readout && tid < DV) part[tid] = acc;
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) {
-      const int prev = atomicAdd(reinterpret_cast<int32_t*>(mbase + 4), 1);
-      sDec[2] = (prev == ns - 1) ? 1 : 0;
-    }
-    __syncthreads();
-    if (!sDec[2]) return;
-    __threadfence();
-    if (!a.skip_readout && tid < DV) {
-      const float* all = decode_partials(mbase, C);
-      acc = 0.f;
-      for (int s2 = 0; s2 < ns; ++s2) acc += all[(size_t)s2 * DV + tid];
-    }
-  }
-
-  // ---------------------------------------------- the last (or only) workgroup
-  // the newest state: accumulated (b = 0), or the new state k v^T in frame Gn
-  // (its slot is the one the merge freed, or the first free slot; with
-  // bfloat16 storage it lives in the open region)
-  {
-    float* dst;
-    if (SB)
-      dst = open;
-    else if (!b)
-      dst = reinterpret_cast<float*>(states) + (size_t)sP[m - 1] * D;
-    else
-      dst = reinterpret_cast<float*>(states) + (size_t)((istar >= 0) ? sP[istar + 1] : sP[m]) * D;
-    const float f = b ? 0.f : __expf((float)(Gn - sF[m - 1]));
-    const float4 vq = reinterpret_cast<const float4*>(sv)[cq];
-#pragma unroll
-    for (int r = 0; r < ST::NV; ++r) {
-      const float kr = sk[rg + ST::RG * r];
-      float4 s;
-      if (b) {
-        s = make_float4(kr * vq.x, kr * vq.y, kr * vq.z, kr * vq.w);
-      } else {
-        s.x = f * Sopen[r].x + kr * vq.x;
-        s.y = f * Sopen[r].y + kr * vq.y;
-        s.z = f * Sopen[r].z + kr * vq.z;
-        s.w = f * Sopen[r].w + kr * vq.w;
-      }
-      st_group(dst, tid + 256 * r, s);
-    }
-  }
-
-  // the new token's own contribution lambda_{m'-1} (q.k) v
-  if (!a.skip_readout && tid < DV) {
-    acc += sLam[m_post - 1] * qk2 * sv[tid];
-    static_cast<Tout*>(a.out)[(size_t)h * DV + tid] = from_f32<Tout>(acc);
-  }
-
-  // exports
-  if (tid == 0) {
-    if (a.b_out) a.b_out[h] = (int8_t)b;
-    if (a.merge_out) a.merge_out[h] = istar;
-    if (a.score_out) a.score_out[h] = (float)I;
-    if (ns > 1) *reinterpret_cast<int32_t*>(mbase + 4) = 0;  // ready for the next step
-  }
-
-  // metadata update (chronological arrays, parallel over slots)
-  if (!b) {
-    if (tid == 0) {
-      M.F[m - 1] = Gn;
-      M.n[m - 1] = sN[m - 1] + 1;
-      M.ibar[m - 1] = sI[m - 1] + I;
+  if constexpr (SPLIT) {
+    // for the finishing kernel: the partial, and (first workgroup) the decisions
+    if (!a.skip_readout && tid < DV) decode_partials(mbase, C)[(size_t)sp * DV + tid] = acc;
+    if (sp == 0 && tid == 0) {
+      DecodeRecord* rec = reinterpret_cast<DecodeRecord*>(decode_record(mbase, C));
+      rec->b = b;
+      rec->istar = istar;
+      rec->I = I;
     }
   } else {
-    if (istar >= 0) {
-      // merge istar, istar+1; shift later states down; freed slot goes to perm[m-1]
-      for (int j = tid; j < C; j += 256) {
-        if (j == istar) {
-          M.F[j] = Gn;
-          M.n[j] = sN[j] + sN[j + 1];
-          M.ibar[j] = sI[j] + sI[j + 1];
-        } else if (j > istar && j < m - 1) {
-          M.F[j] = sF[j + 1];
-          M.n[j] = sN[j + 1];
-          M.ibar[j] = sI[j + 1];
-          M.perm[j] = sP[j + 1];
-        } else if (j == m - 1) {
-          // the new state takes the freed slot
-          M.perm[j] = sP[istar + 1];
-          M.F[j] = Gn;
-          M.n[j] = 1;
-          M.ibar[j] = I;
-        }
-      }
-    } else if (tid == 0) {
-      M.F[m] = Gn;
-      M.n[m] = 1;
-      M.ibar[m] = I;
-    }
-    if (tid == 0) *M.m = m_post;
+    finish_step<DK, DV, Tout, TS>(a, h, m, b, istar, I, Gn, acc, qk2, sk, sv, sF, sI, sN, sP, sLam,
+                                  M, states, open, [&](int r) { return Sopen[r]; });
   }
-  if (tid == 0) {
-    *M.G = Gn;
-    *M.tokens += 1;
+}
+
+// The end of a split step, one workgroup per head: the partials of the NS
+// workgroups summed in split order, then finish_step.
+template <int DK, int DV, typename Tin, typename Tout, typename TS>
+__global__ __launch_bounds__(256) void decode_finish_kernel(DecodeArgs a) {
+  constexpr int D = DK * DV;
+  constexpr bool SB = sizeof(TS) == 2;
+  if (!cache_matches(a.cache, a.desc)) return;  // refused call (see decode_kernel)
+  const int h = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int C = a.desc.C;
+  const int ns = a.nsplit;
+  extern __shared__ double smem[];
+  double* sF = smem;                                    // [C]
+  double* sI = sF + C;                                  // [C]
+  int32_t* sN = reinterpret_cast<int32_t*>(sI + C);     // [C]
+  int32_t* sP = sN + C;                                 // [C]
+  float* sLam = reinterpret_cast<float*>(sP + C);       // [C]
+  __shared__ float sk[DK], sv[DV];
+  __shared__ float red[8];
+  const Tin* q = static_cast<const Tin*>(a.q) + (size_t)h * DK;
+  const Tin* k = static_cast<const Tin*>(a.k) + (size_t)h * DK;
+  const Tin* v = static_cast<const Tin*>(a.v) + (size_t)h * DV;
+  float qk = 0.f;
+  for (int i = tid; i < DK; i += 256) {
+    sk[i] = to_f32(k[i]);
+    if (!a.skip_readout) qk += to_f32(q[i]) * sk[i];
   }
+  for (int i = tid; i < DV; i += 256) sv[i] = to_f32(v[i]);
+  char* mbase = a.cache + a.meta_offset + (size_t)h * a.meta_stride;
+  Meta M = meta_at(mbase, C);
+  const int m = min(max(*M.m, 0), C);
+  const double Gn = *M.G + (double)a.g[h];
+  for (int j = tid; j < C; j += 256) {
+    sF[j] = M.F[j];
+    sI[j] = M.ibar[j];
+    sN[j] = M.n[j];
+    sP[j] = min(max(M.perm[j], 0), C - 1);
+    sLam[j] = a.lam ? to_f32(static_cast<const Tin*>(a.lam)[(size_t)h * C + j]) : 1.f;
+  }
+  const DecodeRecord rec = *reinterpret_cast<const DecodeRecord*>(decode_record(mbase, C));
+  float dummy = 0.f;
+  block_sum2_256(qk, dummy, red);   // (its barriers also publish the LDS tables)
+  float acc = 0.f;
+  if (!a.skip_readout && tid < DV) {
+    const float* part = decode_partials(mbase, C);
+    for (int s2 = 0; s2 < ns; ++s2) acc += part[(size_t)s2 * DV + tid];
+  }
+  TS* states = reinterpret_cast<TS*>(a.cache + a.states_offset) + (size_t)h * C * D;
+  float* open = SB ? reinterpret_cast<float*>(a.cache + a.open_offset) + (size_t)h * D : nullptr;
+  const float* newest =
+      SB ? open : reinterpret_cast<const float*>(states) + (size_t)(m > 0 ? sP[m - 1] : 0) * D;
+  const int b = min(max(rec.b, 0), 1);
+  const int istar = (b && m == C) ? min(max(rec.istar, 0), C - 2) : -1;
+  finish_step<DK, DV, Tout, TS>(a, h, m, b, istar, rec.I, Gn, acc, qk, sk, sv, sF, sI, sN, sP,
+                                sLam, M, states, open,
+                                [&](int r) { return ld_group<true>(newest, threadIdx.x + 256 * r); });
 }
 
 // Workgroups per head: enough for about four per compute unit over all heads,
@@ -453,20 +546,30 @@ int decode_splits(int nheads, int C) {
   return ns > 1 ? ns : 1;
 }
 
+template <int DK, int DV, typename Tin, typename Tout, typename TS>
+static hipError_t launch_decode_t(const DecodeArgs& a, int nheads, hipStream_t s) {
+  const size_t shm = (size_t)a.desc.C * (8 + 8 + 4 + 4 + 4);
+  if (a.nsplit == 1) {
+    hipLaunchKernelGGL((decode_kernel<DK, DV, Tin, Tout, TS, false>), dim3((unsigned)nheads),
+                       dim3(256), shm, s, a);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL((decode_kernel<DK, DV, Tin, Tout, TS, true>),
+                     dim3((unsigned)(nheads * a.nsplit)), dim3(256), shm, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((decode_finish_kernel<DK, DV, Tin, Tout, TS>), dim3((unsigned)nheads),
+                     dim3(256), shm, s, a);
+  return hipGetLastError();
+}
+
 template <int DK, int DV, typename TS>
 static hipError_t launch_decode_dims(const DecodeArgs& a, int nheads, dla_dtype in, dla_dtype out,
                                      hipStream_t s) {
-  const size_t shm = (size_t)a.desc.C * (8 + 8 + 4 + 4 + 4);
-  const dim3 grid((unsigned)(nheads * a.nsplit));
-  if (in == DLA_F32 && out == DLA_F32)
-    hipLaunchKernelGGL((decode_kernel<DK, DV, float, float, TS>), grid, dim3(256), shm, s, a);
-  else if (in == DLA_F32 && out == DLA_BF16)
-    hipLaunchKernelGGL((decode_kernel<DK, DV, float, bf16_t, TS>), grid, dim3(256), shm, s, a);
-  else if (in == DLA_BF16 && out == DLA_F32)
-    hipLaunchKernelGGL((decode_kernel<DK, DV, bf16_t, float, TS>), grid, dim3(256), shm, s, a);
-  else
-    hipLaunchKernelGGL((decode_kernel<DK, DV, bf16_t, bf16_t, TS>), grid, dim3(256), shm, s, a);
-  return hipGetLastError();
+  if (in == DLA_F32 && out == DLA_F32) return launch_decode_t<DK, DV, float, float, TS>(a, nheads, s);
+  if (in == DLA_F32 && out == DLA_BF16) return launch_decode_t<DK, DV, float, bf16_t, TS>(a, nheads, s);
+  if (in == DLA_BF16 && out == DLA_F32) return launch_decode_t<DK, DV, bf16_t, float, TS>(a, nheads, s);
+  return launch_decode_t<DK, DV, bf16_t, bf16_t, TS>(a, nheads, s);
 }
 
 template <int DK, int DV>

@@ -45,17 +45,21 @@ __host__ __device__ inline size_t round_up(size_t x, size_t a) { return (x + a -
 // of d_v floats in the head's metadata (see decode.hip).
 constexpr int kMaxSplit = 16;
 
-__host__ __device__ inline size_t meta_partials_offset(int C) {
+// Scratch of a split decode step in each head's metadata: the decisions
+// (64 bytes reserved), then the partial outputs float [kMaxSplit][d_v].
+__host__ __device__ inline size_t meta_record_offset(int C) {
   return round_up(32 + 24 * (size_t)C, 64);
 }
 
 __host__ __device__ inline size_t meta_stride(int C, int dv) {
-  return round_up(meta_partials_offset(C) + (size_t)kMaxSplit * dv * sizeof(float), 256);
+  return round_up(meta_record_offset(C) + 64 + (size_t)kMaxSplit * dv * sizeof(float), 256);
 }
 
-// the decode step's partial outputs of one head: float [kMaxSplit][d_v]
+__device__ __forceinline__ char* decode_record(char* meta, int C) {
+  return meta + meta_record_offset(C);
+}
 __device__ __forceinline__ float* decode_partials(char* meta, int C) {
-  return reinterpret_cast<float*>(meta + meta_partials_offset(C));
+  return reinterpret_cast<float*>(meta + meta_record_offset(C) + 64);
 }
 
 // Per-head metadata (chronological arrays).  See dla.h for the byte layout.

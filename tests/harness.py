@@ -74,7 +74,8 @@ def run_oracle(w, x, C=None, tau=None, full=True, cache=None, b_override=None, m
     xf = f64(x, w)
     return oracle_forward(xf["k"], xf["v"], xf["g"], C or w.C, w.tau if tau is None else tau,
                           q=xf.get("q") if full else None, lam=xf.get("lam") if full else None,
-                          full=full, cache=cache, b_override=b_override, m_override=m_override)
+                          full=full, cache=cache, b_override=b_override, m_override=m_override,
+                          want_mag=full)
 
 
 def near_tie_overrides(ref, b_override=None, m_override=None, what="", max_frac=None):

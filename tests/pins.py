@@ -159,7 +159,7 @@ def pin_single_state_and_one_state_per_token(lib_path=None):
         base = gated_linear_attention(q[h], k[h], v[h], g[h])
         for C, tau in ((1, 0.5), (5, np.inf)):
             r = oracle_forward(k[h:h + 1], v[h:h + 1], g[h:h + 1], C, tau, q=q[h:h + 1],
-                               lam=lam[h:h + 1, :, :C], lib_path=lib_path)
+                               lam=lam[h:h + 1, :, :C], want_mag=True, lib_path=lib_path)
             ref = lam[h, :, :1] * base
             assert np.abs(r["out"][0] - ref).max() < 1e-12 * np.abs(ref).max(), (C, tau)
             # a single state, the gated state P_t: |lam_0| ||P_t||_F ||q_t||
@@ -186,7 +186,7 @@ def pin_brute_force_membership(lib_path=None):
                         ("cfg1", dict(T=64, dk=4, dv=6, n_seg=9), 2),
                         ("cfg1", dict(T=80, dk=6, dv=4, n_seg=20, rho2=0.9), 5)):
         w, q, k, v, g, lam = f64_inputs(name, C=C, **kw)
-        r = oracle_forward(k, v, g, C, w.tau, q=q, lam=lam, lib_path=lib_path)
+        r = oracle_forward(k, v, g, C, w.tau, q=q, lam=lam, want_mag=True, lib_path=lib_path)
         for h in range(q.shape[0]):
             b, merge, score = r["b"][h], r["merge"][h], r["score"][h]
             hist = replay_membership(b, merge, C)

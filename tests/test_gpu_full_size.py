@@ -184,7 +184,7 @@ def test_decode_full_size_sampled_heads(state):
     sbo, smo, snb, snm = H.near_tie_overrides(free, what=f"{w.label} steps ({state} states)",
                                               max_frac=0.05)
     ref = oracle_forward(xh["k"], xh["v"], xh["g"], w.C, w.tau, q=xh["q"], lam=xh["lam"],
-                         cache=oc, b_override=sbo, m_override=smo)
+                         cache=oc, b_override=sbo, m_override=smo, want_mag=True)
     hidx = torch.tensor(heads, device="cuda")
     bo_d = torch.full((nh, steps), -1, dtype=torch.int8)
     mo_d = torch.full((nh, steps), -1, dtype=torch.int32)
