@@ -19,6 +19,9 @@ Also reported on the same line:
     (B=64, H=32), with float32 and with bfloat16 storage of the closed
     states, and on few heads (B=1, H=32: several workgroups per head);
   * cache and workspace bytes;
+  * a sweep of a Mamba-2-shaped layer under DLA and under fixed merging
+    policies (single state, every-K blocking, log-linear buckets) on the same
+    kernels: prefill tokens/s and memory over batch size and context length;
   * cpu_baseline: the float64 oracle on bounded samples (a prefill of one
     sequence, and decode steps on a few heads of the GPU-built cache).
 
@@ -342,6 +345,93 @@ def decode_bench(args, torch, dla, W, steps, state_dtype, label):
     return res
 
 
+def policy_sweep(args, torch, dla):
+    """Prefill throughput and memory of one Mamba-2-shaped layer (48 heads, state
+    size d_k = 128, head dimension d_v = 64, bf16 inputs, float32 states) under
+    DLA (C = 30, tau = 0.6) and under fixed policies on the same kernels, driven
+    through the override path: a single state (the base model), every-64-token
+    blocking with C = 30, and log-linear buckets (C = ceil(log2 T) + 1).  The
+    two sweeps of the paper's efficiency study (Sec. 4.3): batch size at 128
+    tokens, and context length at batch 1.  Inputs: segments of geometric length
+    (mean 64 tokens).  Memory is what the layer holds besides its inputs and
+    outputs: the state cache and the prefill workspace."""
+    from paper_2606_10650_amd import policies as P
+    from paper_2606_10650_amd.workloads import Workload, make_prefix_torch
+    base = Workload("mamba2_layer", 1, 48, 128, 128, 64, 30, 0.6, "bf16", -0.05, 7, "geom",
+                    mean_len=64)
+    points = [("batch", B, 128) for B in (1, 16, 64, 256)] + \
+             [("context", 1, T) for T in (1024, 4096, 16384, 65536)]
+    rows = []
+    # bring the device out of its idle clocks before the first (smallest) point
+    a = torch.randn(4096, 4096, device="cuda", dtype=torch.bfloat16)
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < 0.3:
+        for _ in range(20):
+            a = (a @ a).clamp_(-1, 1)
+        torch.cuda.synchronize()
+    del a
+    for sweep, B, T in points:
+        W = base.replace(B=B, T=T)
+        q, k, v, g, lam = make_prefix_torch(W, "cuda", with_lambda=True)
+        for pol in ("single_state", "every_k", "log_linear", "dla"):
+            C, b, m = P.schedule(pol, T, C_dla=W.C, K=64)
+            shp = (B, W.H, T)
+            bo = None if b is None else torch.from_numpy(b).cuda().expand(shp).contiguous()
+            mo = None if m is None else torch.from_numpy(m).cuda().expand(shp).contiguous()
+            lamC = lam[..., :C].contiguous()
+            cache = dla.cache_alloc(B, W.H, C, W.dk, W.dv)
+            wsb = dla.workspace_bytes(cache, T, k.dtype)
+            ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+            out = torch.empty((B, W.H, T, W.dv), dtype=k.dtype, device="cuda")
+            bnd = torch.empty(shp, dtype=torch.int8, device="cuda")
+            mrg = torch.empty(shp, dtype=torch.int32, device="cuda")
+
+            def step(e0=None, e1=None):
+                dla.cache_reset(cache)
+                if e0 is not None:
+                    e0.record()
+                dla.prefill(cache, q, k, v, g, lamC, tau=W.tau, out=out, boundary=bnd,
+                            merge_idx=mrg, boundary_override=bo, merge_override=mo, workspace=ws)
+                if e1 is not None:
+                    e1.record()
+
+            for _ in range(3):
+                step()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            step()
+            torch.cuda.synchronize()
+            n = int(min(200, max(args.sweep_steps, 0.05 / max(time.perf_counter() - t0, 1e-6))))
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in range(n)]
+            for e in evs:
+                step(*e)
+            torch.cuda.synchronize()
+            ms = float(np.mean([a.elapsed_time(z) for a, z in evs]))
+            bb = bnd.cpu().numpy().reshape(-1, T).astype(np.int64)
+            mm = (mrg.cpu().numpy().reshape(-1, T) >= 0).astype(np.int64)
+            live = np.cumsum(bb, axis=1) - np.cumsum(mm, axis=1)
+            io = sum(t.numel() * t.element_size() for t in (q, k, v, g, lamC, out))
+            rows.append({"sweep": sweep, "B": B, "T": T, "policy": pol, "C": C,
+                         "ms": round(ms, 4), "tokens_per_s": round(B * T / (ms * 1e-3), 1),
+                         "cache_MB": round(cache.buf.numel() / 2**20, 3),
+                         "workspace_MB": round(wsb / 2**20, 3),
+                         "io_MB": round(io / 2**20, 3),
+                         "boundaries": int(bb.sum()), "merges": int(mm.sum()),
+                         "mean_live_states": round(float(live.mean()), 2), "steps_timed": n})
+            log(f"[sweep] {sweep} B={B} T={T} {pol} C={C}: {ms:.4f} ms, "
+                f"{rows[-1]['tokens_per_s']:.0f} tok/s, cache {rows[-1]['cache_MB']} MB, "
+                f"workspace {rows[-1]['workspace_MB']} MB, live {rows[-1]['mean_live_states']}")
+            del cache, ws, out, bnd, mrg, bo, mo, lamC
+        del q, k, v, g, lam
+        torch.cuda.empty_cache()
+    return {"layer": ("Mamba-2-780M-shaped layer: H=48, d_k=128, d_v=64, bf16 inputs, f32 "
+                      "states, geometric segments (mean 64); DLA C=30 tau=0.6; every_k K=64 "
+                      "C=30; log_linear C=ceil(log2 T)+1; single_state C=1"),
+            "timing": "HIP events around each prefill call (cache reset outside), mean",
+            "rows": rows}
+
+
 def cpu_baseline(args, W):
     from oracle import oracle_forward, oracle_threads
     from paper_2606_10650_amd.workloads import make_inputs, to_f64
@@ -405,6 +495,8 @@ def main():
     ap.add_argument("--no-others", action="store_true")
     ap.add_argument("--no-peaks", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--sweep-steps", type=int, default=3)
     ap.add_argument("--cpu-tokens", type=int, default=16384)
     ap.add_argument("--decode-cpu-heads", type=int, default=128)
     ap.add_argument("--decode-cpu-steps", type=int, default=64)
@@ -488,6 +580,8 @@ def main():
             for key in ("decode", "decode_bf16_states", "decode_few_heads"):
                 res[key]["roofline"]["frac_measured_peak"] = frac(res[key]["roofline"]["achieved"],
                                                                   pk["hbm_read_gbs"])
+    if not args.no_sweep:
+        res["policy_sweep"] = policy_sweep(args, torch, dla)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(args, W)
         if cache5 is not None:

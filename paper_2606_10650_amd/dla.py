@@ -179,6 +179,13 @@ def cache_alloc(B: int, H: int, C: int, d_k: int, d_v: int, device="cuda",
     return StateCache(B, H, C, d_k, d_v, buf, state_dtype)
 
 
+def cache_reset(cache: StateCache) -> None:
+    """Empty an allocated cache in place (dla_state_cache_alloc on its buffer)."""
+    n = ctypes.c_size_t(cache.buf.numel())
+    _check(lib().dla_state_cache_alloc(ctypes.byref(cache.desc), _ptr(cache.buf), ctypes.byref(n),
+                                       _stream(cache.device)), "dla_state_cache_alloc")
+
+
 def header_check(desc: CacheDesc, header: bytes) -> int:
     """dla_cache_header_check on a host copy of a cache header: the device
     flags, or DLAError (DLA_ERR_CACHE_MISMATCH) when it does not match desc."""

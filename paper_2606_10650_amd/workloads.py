@@ -281,12 +281,14 @@ def make_decode_tokens(w: Workload, steps: Optional[int] = None, heads: Optional
     return out
 
 
-def make_prefix_torch(w: Workload, device, with_q: bool = False):
-    """Device-side draw of a prefill workload's k, v, g (and q) with the same
-    recipe as make_inputs, from torch's generator seeded with w.seed: for
-    prefixes too large to draw on the host (B*H*T in the billions).  Values
+def make_prefix_torch(w: Workload, device, with_q: bool = False, with_lambda: bool = False):
+    """Device-side draw of a prefill workload's k, v, g (and q, lambda) with
+    the same recipe as make_inputs, from torch's generator seeded with w.seed:
+    for prefixes too large to draw on the host (B*H*T in the billions).  Values
     differ from make_inputs' numpy streams; the segment plan is the same.
-    Returns bf16/f32 tensors [B, H, T, d] and g [B, H, T] float32."""
+    Returns bf16/f32 tensors q, k [B, H, T, d_k], v [B, H, T, d_v], g [B, H, T]
+    float32, and with with_lambda (which implies with_q) lam [B, H, T, C]."""
+    with_q = with_q or with_lambda
     import torch
     tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     gen = torch.Generator(device=device)
@@ -312,7 +314,14 @@ def make_prefix_torch(w: Workload, device, with_q: bool = False):
         if with_q:
             qq = torch.randn((w.H, w.T, w.dk), generator=gen, device=device)
             q[b] = (qq / qq.norm(dim=-1, keepdim=True)).to(tdt)
-    return q, k, v, g
+    if not with_lambda:
+        return q, k, v, g
+    Wt = torch.from_numpy(np.stack([lambda_weights(w, h).T for h in range(w.H)])).to(
+        device=device, dtype=torch.float32).contiguous()          # [H, d_k, C]
+    lam = torch.empty((w.B, w.H, w.T, w.C), dtype=tdt, device=device)
+    for b in range(w.B):
+        lam[b] = (1.0 + 0.5 * torch.matmul(q[b].float(), Wt)).to(tdt)
+    return q, k, v, g, lam
 
 
 def make_decode_tokens_torch(w: Workload, steps: int, device):
