@@ -61,11 +61,25 @@ __device__ __forceinline__ const Tin* ones_row() {
 template <int DK, typename Tin>
 struct RO : ChunkP<DK, Tin> {
   using B = ChunkP<DK, Tin>;
-  // inter phase: state ring (two steps of two states), then the token weights
-  // of those states (float, [step parity][state of the step][RL])
-  static constexpr int NSLOT = 4;
+  // 16-bit operands of the next state are read from LDS into registers while
+  // the MFMA chains of the current state run (float32 operands take twice the
+  // registers and are read at the start of their own state)
+  static constexpr bool PREF = B::E == 2;
+  static constexpr int PF = PREF ? 1 : 0;
+  // inter phase: state ring of NPAIR steps of two states (four for 16-bit
+  // inputs, two for float32 inputs, whose slices are twice the size); a
+  // step's slices are requested LEAD steps ahead
+  static constexpr int NPAIR = B::E == 2 ? 4 : 2;
+  static constexpr int NSLOT = 2 * NPAIR;
+  static constexpr int LEAD = NPAIR - 1;
+  // then the lambda ring: NLAM states x waves x 64 lanes, one dword per lane
+  // (a 16-bit entry lands zero-extended); lane l holds the entry of the token
+  // of tile l / 32, column l % 32.  A step's entries are requested LAM_D steps
+  // ahead.
+  static constexpr int LAM_D = LEAD - PF;
+  static constexpr int NLAM = 2 * (LAM_D + 1);
   static constexpr size_t RING_BYTES = NSLOT * (size_t)B::SLICE16 * 16;
-  static constexpr size_t WRING_BYTES = 4 * (size_t)B::RL * 4;
+  static constexpr size_t WRING_BYTES = (size_t)NLAM * RWAVE * 64 * 4;
   static constexpr size_t INTER_BYTES = RING_BYTES + WRING_BYTES;
   // intra phase: key ring, and the lambda window, which is written before the
   // inter phase and so lies past both the key ring and the inter region
@@ -133,7 +147,6 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   // intra phase (same bytes)
   Tin* kring = reinterpret_cast<Tin*>(smem);                      // KSLOT x [32][KRS] keys
   Tin* sLamW = reinterpret_cast<Tin*>(smem + P::WIN_OFF);         // [RL][lw + 1] lambda
-  float* sW = reinterpret_cast<float*>(smem + P::RING_BYTES);     // [2][2][RL] token weights
   const int lws = lw + 1;
   const size_t rgn = P::region_bytes(lw);
   Tin* sVt = reinterpret_cast<Tin*>(smem + rgn);                  // [NC][VTS] values
@@ -251,46 +264,53 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
     for (int e = 0; e < EPP; ++e) sVt[(p * EPP + e) * P::VTS + r] = piece_elem<Tin>(vp_[u], e);
   }
   __syncthreads();
-  // The inter phase's first requests (the lambda entries of states 0 and 1 at
-  // this thread's token, and the pool slices of states 0 .. 3) go out as soon
-  // as the list tables are in LDS, so that their latency overlaps the rest of
-  // the set-up.  Thread tid forms the weights of token tid (threads past RL
-  // have none).
-  const bool tw_ok = tid < nrow;
-  const float rfw = tw_ok ? sRf[tid] : 0.f;
-  // lambda row of the token: a buffer over the chunk's lambda rows (wave-
-  // uniform), the token's row at byte offset lrow_off; without lambda, the
-  // ones table
+  // The inter phase's first requests (the lambda entries of states 0 .. 5 at
+  // the lane's tokens, and the pool slices of states 0 .. 5) go out as soon as
+  // the list tables are in LDS, so that their latency overlaps the rest of the
+  // set-up.  Each lane forms the weights of its own tile tokens.
+  // lambda rows: a buffer over the chunk's lambda rows (wave-uniform), the
+  // row of tile token nt at byte offset loff[nt]; without lambda, the ones table
   const __amdgpu_buffer_rsrc_t lrs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<Tin*>(Lin ? Lin + (size_t)c0 * C : ones_row<Tin>()), (short)0,
       Lin ? nrow * C * P::E : 1024 * P::E, 0x00020000);
-  const int lrow_off = Lin ? (tw_ok ? tid : 0) * C * P::E : 0;
-  // live states up to the last state whose lambda was requested, minus one
-  // (states past the list read a death token of 0 from the padding, so they
-  // never count)
-  int cm1 = -1;
-  auto lam_req = [&](int j) __attribute__((always_inline)) -> Tin {
-    cm1 += (int)(sDt[min(j, C + 7)] > c0 + tid);
-    const int off = lrow_off + max(cm1, 0) * P::E;
-    if constexpr (P::E == 2) {
-      Tin r;
-      r.x = __builtin_amdgcn_raw_buffer_load_b16(lrs, off, 0, 0);
-      return r;
-    } else {
-      return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(lrs, off, 0, 0));
-    }
+  // The lane's lambda token: the token of tile min(l / 32, NT - 1), column
+  // l % 32; its row at byte offset loff.  cm: live states up to the last state
+  // whose entry was requested, minus one (states past the list read a death
+  // token of 0 from the padding, so they never count).
+  const int ltile = min(half, NT - 1);
+  const int ltok = 32 * tile_of<NT>(wv, ltile) + l32;
+  const int loff = Lin ? (ltok < nrow ? ltok : 0) * C * P::E : 0;
+  const int ltokc = c0 + ltok;
+  int cm = -1;
+  // Lambda entries of state j, requested in state order straight into the
+  // wave's slot of the LDS lambda ring (a wave reads back only what its own
+  // request wrote).
+  char* sLam = reinterpret_cast<char*>(smem) + P::RING_BYTES;
+  auto lam_slot = [&](int j) __attribute__((always_inline)) -> char* {
+    return sLam + (size_t)((j % P::NLAM) * RWAVE + wv) * 64 * 4;
+  };
+  auto lam_dt = [&](int j) __attribute__((always_inline)) -> int { return sDt[min(j, C + 7)]; };
+  // (dt: the death token of state j, lam_dt(j))
+  auto lam_dma = [&](int j, int dt) __attribute__((always_inline)) {
+    cm += (int)(dt > ltokc);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        lrs, (__attribute__((address_space(3))) void*)lam_slot(j), P::E,
+        loff + max(cm, 0) * P::E, 0, 0, 0);
+  };
+  // the entry of state j at the lane's token of tile nt
+  auto lam_get = [&](int j, int nt) __attribute__((always_inline)) -> float {
+    return to_f32(*reinterpret_cast<const Tin*>(lam_slot(j) + (32 * nt + l32) * 4));
   };
   constexpr int SL16 = P::SLICE16;
   constexpr int V16 = (SL16 + RTHR - 1) / RTHR;
-  struct Pre {
-    u32x4 x[2][V16];
-  };
-  Pre preA, preB;
+  constexpr int LEAD = P::LEAD;  // steps between a slice's request and its chains
   // the pool slices of this head and column group: object obj at
   // pool_h + obj * NCG * SLICE (the object index is wave-uniform, so the
   // address is formed in scalar registers)
   const Tin* pool_h = pool_slice<Tin>(w.pool, h, plan.P_cap, 0, cg, NCG, P::SLICE);
-  auto prefetch2 = [&](int jb, Pre& pr) __attribute__((always_inline)) {
+  // slices of states jb, jb + 1 into ring pair pr, straight from memory into
+  // LDS (each lane's 16 bytes land at the wave's base plus 16 bytes per lane)
+  auto dma2 = [&](int jb, int pr) __attribute__((always_inline)) {
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
       const int obj = __builtin_amdgcn_readfirstlane(sObj[min(jb + s2, m - 1)]);
@@ -300,17 +320,19 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
 #pragma unroll
       for (int u = 0; u < V16; ++u) {
         const int pi = tid + RTHR * u;
+        // (SL16 is a multiple of 64, so the test is uniform over a wave)
         if (SL16 % RTHR == 0 || pi < SL16)
-          pr.x[s2][u] = __builtin_amdgcn_raw_buffer_load_b128(src, pi * 16, 0, 0);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              src, (__attribute__((address_space(3))) void*)(ring + (pr * 2 + s2) * SL16 + (pi - lane)),
+              16, pi * 16, 0, 0, 0);
       }
     }
   };
-  Tin lam0 = from_f32<Tin>(0.f), lam1 = lam0;
   if (m > 0) {
-    lam0 = lam_req(0);
-    lam1 = lam_req(1);
-    prefetch2(0, preA);
-    prefetch2(2, preB);
+#pragma unroll
+    for (int j = 0; j < 2 * P::LAM_D; ++j) lam_dma(j, lam_dt(j));
+#pragma unroll
+    for (int J = 0; J < LEAD; ++J) dma2(2 * J, J);
   }
   // old states alive at each token: m minus the states of the list whose death
   // token is at or before it (a state lives while its death token is later)
@@ -395,15 +417,16 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   }
 
   // ------------------------------------------------ inter-chunk readout
-  // Step J handles states 2J and 2J+1: the registers loaded two steps earlier
-  // go to ring slots 2 (J & 1) and 2 (J & 1) + 1, and each thread turns the
-  // lambda entries of its own token for those two states (requested one step
-  // earlier) into weights in LDS; then the lambda entries of states 2J+2 and
-  // 2J+3 are requested and the slices of states 2J+4 and 2J+5, and after one
-  // barrier every wave reads the two operands and its tiles' weights from LDS.
-  // A slot written in step J was last read in step J-2, before the barrier of
-  // step J-1.  Steps run in pairs over named register buffers (constant
-  // indexing); steps past the last state have sSf = 0.
+  // Ring pair p of the LDS holds states 2J and 2J+1 for every step J = p mod 3.
+  // Step J starts with a barrier and runs the MFMA chains of states 2J and
+  // 2J+1 with their operands in registers; meanwhile the operand of the state
+  // after each is read from LDS (for 16-bit inputs), and the slices of states
+  // 2J+4 and 2J+5, loaded into registers three steps earlier, are stored into
+  // pair (J+2) % 3, whose last reader was step J-1 (before this barrier), and
+  // the registers reloaded with states 2J+10 and 2J+11.  A state's slices are
+  // thus written two steps before its chains run.  Each lane forms the weights
+  // of its own tokens from lambda entries requested six states ahead, so no
+  // step waits on a load.  Steps past the last state have sSf = 0.
   // The weight of state j at token t is lambda[t][x] exp(G_t - F_j), x = (live
   // states up to j) - 1 (a state merged away at or before t is weighted as the
   // live state that absorbed it).
@@ -413,8 +436,12 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
     // while the matrix core works on an independent chain.
     f32x16 f[NT];
     float wP = 0.f;  // weight of the last tile's pending chain result
+    float rf[NT];    // exp(G_t - G_ref) of the lane's tile tokens
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) f[nt] = zero16();
+    for (int nt = 0; nt < NT; ++nt) {
+      f[nt] = zero16();
+      rf[nt] = rv[nt] ? sRf[tr[nt]] : 0.f;
+    }
     // sched_group_barrier masks: 0x008 MFMA, 0x002 VALU, 0x100 LDS read
     auto interleave = [&]() __attribute__((always_inline)) {
 #pragma unroll
@@ -423,13 +450,26 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
         __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
       }
     };
-    auto sub = [&](const Tin* A, const float* wt) __attribute__((always_inline)) {
-      FT sa[KS];
+    // a wave's operand of the state slice at A
+    auto opload = [&](const Tin* A, FT (&sa)[KS]) __attribute__((always_inline)) {
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) sa[ks] = FR::load(A + ((ks * 2 + half) * 32 + l32) * 8);
-      float wg[NT];
+    };
+    // The chains of state j with operand sa (slice Ac).  With PREF the operand
+    // of the state after j (slice An) is read into sn meanwhile.  mid() runs
+    // between the chains of the first and the second tile.
+    auto sub = [&](int j, FT (&sa)[KS], const Tin* Ac, const Tin* An, FT (&sn)[KS],
+                   auto&& mid) __attribute__((always_inline)) {
+      // LDS reads first; their values are needed only after the first chain
+      const float sf = sSf[j];
+      float lv[NT];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) wg[nt] = wt[tr[nt]];
+      for (int nt = 0; nt < NT; ++nt) lv[nt] = lam_get(j, nt);
+      if constexpr (P::PREF)
+        opload(An, sn);
+      else
+        opload(Ac, sa);
+      float wg[NT];
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
@@ -446,6 +486,12 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
         }
         interleave();
         __builtin_amdgcn_sched_barrier(0);
+        if (nt == 0) {
+#pragma unroll
+          for (int n2 = 0; n2 < NT; ++n2) wg[n2] = lv[n2] * rf[n2] * sf;
+          mid();
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
       if constexpr (NT == 1) {
 #pragma unroll
@@ -453,34 +499,40 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
       }
       wP = wg[NT - 1];
     };
-    auto step = [&](int J, Pre& pr) __attribute__((always_inline)) {
-      u32x4* rb = ring + (J & 1) * 2 * SL16;
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2)
-#pragma unroll
-        for (int u = 0; u < V16; ++u) {
-          const int pi = tid + RTHR * u;
-          if (SL16 % RTHR == 0 || pi < SL16) rb[s2 * SL16 + pi] = pr.x[s2][u];
-        }
-      float* wt = sW + (J & 1) * 2 * RL;
-      if (RL == RTHR || tid < RL) {
-        wt[tid] = to_f32(lam0) * rfw * sSf[2 * J];
-        wt[RL + tid] = to_f32(lam1) * rfw * sSf[2 * J + 1];
+    auto nothing = []() __attribute__((always_inline)) {};
+    FT saX[KS], saY[KS];
+    // Before the barrier of step J the slices of step J (and of step J+1, whose
+    // first operand the step reads ahead with PREF) and the lambda entries of
+    // step J must be in LDS.  Step J' requests, between the first and second
+    // chains of its first state, the lambda entries of step J'+LAM_D and then
+    // the slices of step J'+LEAD; so the wave waits for its requests up to
+    // the slices of step J+PF-LEAD, and the later ones stay in flight: per
+    // step two lambda requests and 2 V16 slice pieces.  The wave's LDS reads
+    // are complete before the barrier, so a pair or lambda slot is rewritten
+    // only after it was read.
+    constexpr int VM_AFTER = (LEAD - 1 - P::PF) * (2 + 2 * V16);
+    static_assert(VM_AFTER >= 0 && VM_AFTER < 64, "vmcnt range");
+    static_assert(P::LAM_D >= LEAD - P::PF, "lambda requests precede the slices waited for");
+    constexpr int WAIT = (VM_AFTER & 15) | (7 << 4) | (0 << 8) | ((VM_AFTER >> 4) << 14);
+    __syncthreads();  // (waits for every request: the first LEAD steps' slices are in LDS)
+    if constexpr (P::PREF) opload(reinterpret_cast<const Tin*>(ring), saX);
+    for (int J = 0; 2 * J < m; ++J) {
+      if (J > 0) {
+        __builtin_amdgcn_s_waitcnt(WAIT);
+        __builtin_amdgcn_s_barrier();
       }
-      lam0 = lam_req(2 * J + 2);
-      lam1 = lam_req(2 * J + 3);
       __builtin_amdgcn_sched_barrier(0);
-      prefetch2(2 * J + 4, pr);
+      const Tin* A0 = reinterpret_cast<const Tin*>(ring + (J % P::NPAIR) * 2 * SL16);
+      const Tin* A2 = reinterpret_cast<const Tin*>(ring + ((J + 1) % P::NPAIR) * 2 * SL16);
+      const int jl = 2 * (J + P::LAM_D);
+      const int dt0 = lam_dt(jl), dt1 = lam_dt(jl + 1);
+      sub(2 * J, saX, A0, A0 + P::SLICE, saY, [&]() __attribute__((always_inline)) {
+        lam_dma(jl, dt0);
+        lam_dma(jl + 1, dt1);
+        dma2(2 * (J + LEAD), (J + LEAD) % P::NPAIR);
+      });
       __builtin_amdgcn_sched_barrier(0);
-      __syncthreads();
-      const Tin* A = reinterpret_cast<const Tin*>(rb);
-      sub(A, wt);
-      __builtin_amdgcn_sched_barrier(0);
-      sub(A + P::SLICE, wt + RL);
-    };
-    for (int J0 = 0; 2 * J0 < m; J0 += 2) {
-      step(J0, preA);
-      step(J0 + 1, preB);
+      sub(2 * J + 1, saY, A0 + P::SLICE, A2, saX, nothing);
     }
     if constexpr (NT > 1) {
 #pragma unroll
