@@ -144,7 +144,8 @@ def frac(achieved, peak):
     return round(achieved / peak, 4)
 
 
-def prefill_bench(args, torch, dla, W, steps, warmup, with_events=True, serial_steps=3):
+def prefill_bench(args, torch, dla, W, steps, warmup, with_events=True, serial_steps=3,
+                  pool_budget_log2=0):
     from paper_2606_10650_amd.workloads import make_inputs
     t0 = time.time()
     x = make_inputs(W)
@@ -165,8 +166,9 @@ def prefill_bench(args, torch, dla, W, steps, warmup, with_events=True, serial_s
     g = torch.from_numpy(x["g"]).reshape(B, H, T).cuda()
     del x
     cache = dla.cache_alloc(B, H, W.C, W.dk, W.dv)
-    ws_pipe = dla.workspace_bytes(cache, T, k.dtype)
-    ws_serial = dla.workspace_bytes(cache, T, k.dtype, serial=True)
+    ws_pipe = dla.workspace_bytes(cache, T, k.dtype, pool_budget_log2=pool_budget_log2)
+    ws_serial = dla.workspace_bytes(cache, T, k.dtype, serial=True,
+                                    pool_budget_log2=pool_budget_log2)
     ws = torch.empty(max(ws_pipe, ws_serial), dtype=torch.uint8, device="cuda")
     out = torch.empty((B, H, T, W.dv), dtype=k.dtype, device="cuda")
     bnd = torch.empty((B, H, T), dtype=torch.int8, device="cuda")
@@ -183,14 +185,14 @@ def prefill_bench(args, torch, dla, W, steps, warmup, with_events=True, serial_s
                    "cache init")
         dla.prefill(cache, q, k, v, g, lam, tau=W.tau, out=out, boundary=bnd, merge_idx=mrg,
                     score=scr, workspace=ws, stage_events=events, readout_events=rev,
-                    serial=serial)
+                    serial=serial, pool_budget_log2=pool_budget_log2)
 
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
     # the timed steps: the pipelined prefill, with every readout launch
     # bracketed by a pair of events on the stream it runs on
-    nseg = dla.prefill_segments(cache, T, k.dtype)
+    nseg = dla.prefill_segments(cache, T, k.dtype, pool_budget_log2=pool_budget_log2)
     revs = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * nseg)]
             for _ in range(steps)] if with_events else [None] * steps
     start = torch.cuda.Event(enable_timing=True)
@@ -209,7 +211,7 @@ def prefill_bench(args, torch, dla, W, steps, warmup, with_events=True, serial_s
     log(f"[bench] {W.name} prefill wall clock {ms:.3f} ms/step, "
         f"events {start.elapsed_time(stop) / steps:.3f} ms/step")
     res = {"ms_per_step": ms, "value": B * T / (ms * 1e-3), "workspace_bytes": ws_pipe,
-           "cache_bytes": nbytes}
+           "cache_bytes": nbytes, "segments": nseg}
     # algorithmic work from this run's exports: per token and head 2 m_t d_k d_v
     # (the readout over the m_t live states) + 4 d_k d_v (accumulate and score)
     b = bnd.cpu().numpy().reshape(B * H, T).astype(np.int64)
@@ -561,6 +563,17 @@ def main():
                 "roofline_call_frac_at_m_eq_C": r["roofline_call"]["frac_at_m_eq_C"],
                 "workspace_bytes": r["workspace_bytes"], "decisions": r["decisions"]}
         res["prefill_workloads"] = others
+    if not args.no_others:
+        # the prefill's state copies under smaller budgets (flags bits 8..15):
+        # less workspace, more segments, identical results
+        pb = {}
+        for kb in (31, 30):
+            r = prefill_bench(args, torch, dla, W, args.other_steps, 1, with_events=False,
+                              serial_steps=0, pool_budget_log2=kb)
+            pb[f"2^{kb}"] = {"workspace_bytes": r["workspace_bytes"], "segments": r["segments"],
+                             "ms_per_step": round(r["ms_per_step"], 4)}
+            log(f"[bench] pool budget 2^{kb}: {pb[f'2^{kb}']}")
+        res["memory"]["pool_budget"] = pb
     cache5 = None
     if not args.no_decode:
         W5 = WORKLOADS["cfg5"]

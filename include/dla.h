@@ -134,6 +134,17 @@ typedef struct {
 
 #define DLA_SKIP_READOUT 1u
 #define DLA_SERIAL_STAGES 2u
+/* Bits 8..15 of the flags set the budget of the readout's state copies (see
+ * dla_prefill_workspace_size): DLA_POOL_BUDGET_LOG2(k) bounds them to 2^k
+ * bytes per call, 20 <= k <= 40 (1 MiB .. 1 TiB); 0 keeps the default of
+ * 8 GiB.  A smaller budget splits the call into more segments of whole
+ * chunks (at least one chunk each, whatever the budget); results are
+ * identical.  The same flags must reach dla_prefill_workspace_size,
+ * dla_prefill_segment_count, dla_prefill_segment_starts and dla_prefill.
+ * Any other k is DLA_ERR_INVALID_ARG. */
+#define DLA_POOL_BUDGET_SHIFT 8
+#define DLA_POOL_BUDGET_MASK 0xFF00u
+#define DLA_POOL_BUDGET_LOG2(k) (((uint32_t)(k) << DLA_POOL_BUDGET_SHIFT) & DLA_POOL_BUDGET_MASK)
 
 /* Device flags kept in the cache header (read with dla_cache_flags).
  * DLA_FLAG_BAD_MERGE_OVERRIDE: a merge override outside [0, C-2] was ignored.
@@ -204,8 +215,9 @@ dla_status dla_cache_header_check(const dla_cache_desc* desc, const void* header
  * bytes per head (token frames, death tokens) and O(C) per head and chunk of
  * 512 tokens (256 for float32 inputs; the state list of every chunk), the
  * readout needs copies of the states in the input dtype: up to C per head and
- * chunk, d_k*d_v elements each.  They are bounded to 8 GiB per call: above
- * that the call is split into segments of whole chunks that reuse the space.
+ * chunk, d_k*d_v elements each.  They are bounded to 8 GiB per call (or the
+ * budget set in the flags, DLA_POOL_BUDGET_LOG2): above that the call is split
+ * into segments of whole chunks that reuse the space.
  * A pipelined call (see dla_params) splits into segments that grow by half
  * from one sixteenth of the chunks (2, 3, 5, 8 and 14 chunks at 16384 tokens).
  * Its segments share one pool when all its copies fit the budget; otherwise

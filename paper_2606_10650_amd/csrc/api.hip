@@ -214,9 +214,10 @@ dla_status dla_prefill_workspace_size(const dla_cache_desc* desc, int32_t T, dla
                                       uint32_t flags, size_t* bytes) {
   dla_status s = check_desc(desc);
   if (s != DLA_OK) return ret(s);
-  if (!bytes || T < 0 || !dtype_ok(in_dtype)) return ret(DLA_ERR_INVALID_ARG);
+  const size_t budget = pool_budget_of(flags);
+  if (!bytes || T < 0 || !dtype_ok(in_dtype) || !budget) return ret(DLA_ERR_INVALID_ARG);
   *bytes = prefill_workspace_bytes(*desc, T, in_dtype, (flags & DLA_SKIP_READOUT) == 0,
-                                   (flags & DLA_SERIAL_STAGES) != 0);
+                                   (flags & DLA_SERIAL_STAGES) != 0, budget);
   return ret(DLA_OK);
 }
 
@@ -224,9 +225,10 @@ dla_status dla_prefill_segment_count(const dla_cache_desc* desc, int32_t T, dla_
                                      uint32_t flags, int32_t* nseg) {
   dla_status s = check_desc(desc);
   if (s != DLA_OK) return ret(s);
-  if (!nseg || T < 0 || !dtype_ok(in_dtype)) return ret(DLA_ERR_INVALID_ARG);
+  const size_t budget = pool_budget_of(flags);
+  if (!nseg || T < 0 || !dtype_ok(in_dtype) || !budget) return ret(DLA_ERR_INVALID_ARG);
   *nseg = seg_plan(*desc, T, in_dtype, (flags & DLA_SKIP_READOUT) == 0,
-                   (flags & DLA_SERIAL_STAGES) != 0).nseg;
+                   (flags & DLA_SERIAL_STAGES) != 0, budget).nseg;
   return ret(DLA_OK);
 }
 
@@ -234,9 +236,10 @@ dla_status dla_prefill_segment_starts(const dla_cache_desc* desc, int32_t T, dla
                                       uint32_t flags, int32_t* starts, int32_t n) {
   dla_status s = check_desc(desc);
   if (s != DLA_OK) return ret(s);
-  if (!starts || n < 0 || T < 0 || !dtype_ok(in_dtype)) return ret(DLA_ERR_INVALID_ARG);
+  const size_t budget = pool_budget_of(flags);
+  if (!starts || n < 0 || T < 0 || !dtype_ok(in_dtype) || !budget) return ret(DLA_ERR_INVALID_ARG);
   const SegPlan p = seg_plan(*desc, T, in_dtype, (flags & DLA_SKIP_READOUT) == 0,
-                             (flags & DLA_SERIAL_STAGES) != 0);
+                             (flags & DLA_SERIAL_STAGES) != 0, budget);
   for (int seg = 0; seg < p.nseg && seg < n; ++seg) {
     int cs, ce;
     seg_range(p, seg, &cs, &ce);
@@ -268,9 +271,11 @@ static dla_status prefill_impl(const dla_cache_desc* desc, void* cache, const vo
       ((int64_t)1 << 40))
     return ret(DLA_ERR_UNSUPPORTED);
   const bool serial = static_ws || (params->flags & DLA_SERIAL_STAGES) != 0;
+  const size_t budget = pool_budget_of(params->flags);
+  if (!budget) return ret(DLA_ERR_INVALID_ARG);
   if (params->n_readout_events < 0 || (params->n_readout_events > 0 && !params->readout_events))
     return ret(DLA_ERR_INVALID_ARG);
-  const size_t need = prefill_workspace_bytes(*desc, T, in_dtype, !skip, serial);
+  const size_t need = prefill_workspace_bytes(*desc, T, in_dtype, !skip, serial, budget);
   if (static_ws) {
     if (need > DLA_STATIC_SCRATCH_BYTES) return ret(DLA_ERR_WORKSPACE);
     if (static_scratch((hipStream_t)stream, &workspace) != hipSuccess) return ret(DLA_ERR_HIP);
@@ -306,6 +311,7 @@ static dla_status prefill_impl(const dla_cache_desc* desc, void* cache, const vo
   a.in_dtype = in_dtype;
   a.out_dtype = out_dtype;
   a.serial = serial ? 1 : 0;
+  a.pool_budget = budget;
   a.workspace = (char*)workspace;
   StageEvents se;
   se.ev = params->stage_events;

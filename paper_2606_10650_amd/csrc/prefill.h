@@ -25,6 +25,7 @@ struct PrefillArgs {
   int skip_readout;
   dla_dtype in_dtype, out_dtype;
   int serial;  // stages one after another on the caller's stream
+  size_t pool_budget;  // bytes of state copies per call (pool_budget_of)
   char* workspace;
 };
 
@@ -46,7 +47,16 @@ constexpr int NTHR = 64 * NWAVE;
 constexpr int RWAVE = 8;  // waves per workgroup of the readout stage (two per SIMD)
 constexpr int RTHR = 64 * RWAVE;
 constexpr int NC = 32;    // value columns per workgroup
-constexpr size_t kPoolBudget = (size_t)8 << 30;  // bytes of state copies per segment
+constexpr size_t kPoolBudget = (size_t)8 << 30;  // default bytes of state copies per call
+
+// The budget of state copies that the flags select (bits 8..15: log2 of the
+// bytes, 0 for the default), or 0 when the field is out of range.
+inline size_t pool_budget_of(uint32_t flags) {
+  const uint32_t k = (flags & DLA_POOL_BUDGET_MASK) >> DLA_POOL_BUDGET_SHIFT;
+  if (k == 0) return kPoolBudget;
+  if (k < 20 || k > 40) return 0;
+  return (size_t)1 << k;
+}
 // A pipelined call runs the scan segment by segment on a second stream while
 // the first stream updates and reads out the segments already scanned, so only
 // the first segment's scan is exposed; its segments grow as a ramp (seg_range).
@@ -106,7 +116,7 @@ inline bool pipelined(int T, dla_dtype in, bool readout, bool serial) {
 }
 
 inline SegPlan seg_plan(const dla_cache_desc& d, int T, dla_dtype in, bool readout,
-                        bool serial) {
+                        bool serial, size_t budget) {
   SegPlan p;
   const int E = (int)dtype_bytes(in);
   p.RL = chunk_len(E);
@@ -121,7 +131,8 @@ inline SegPlan seg_plan(const dla_cache_desc& d, int T, dla_dtype in, bool reado
     return p;
   }
   const size_t per_chunk = (size_t)d.B * d.H * d.C * d.d_k * d.d_v * E;
-  int fit = (int)(kPoolBudget / per_chunk);
+  const size_t fit_z = budget / per_chunk;
+  int fit = fit_z > (size_t)p.nch ? p.nch : (int)fit_z;
   if (fit < 1) fit = 1;
   if (pipelined(T, in, readout, serial)) {
     p.first = p.nch / 16 > 1 ? p.nch / 16 : 1;
@@ -219,9 +230,9 @@ __host__ __device__ inline PrefillWS ws_layout(char* base, int nh, int T, int C,
 }
 
 inline size_t prefill_workspace_bytes(const dla_cache_desc& d, int T, dla_dtype in, bool readout,
-                                      bool serial) {
+                                      bool serial, size_t budget) {
   const size_t nh = (size_t)d.B * d.H;
-  const SegPlan p = seg_plan(d, T, in, readout, serial);
+  const SegPlan p = seg_plan(d, T, in, readout, serial, budget);
   size_t off = round_up(nh * T * sizeof(double), 256);
   off = round_up(off + nh * T * sizeof(int32_t), 256);
   off = round_up(off + nh * ws_init_stride(d.C), 256);
@@ -327,7 +338,8 @@ struct StageEvents {
 // its last update, so the call joins on s.
 inline hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s, const StageEvents& se) {
   const bool pipe = pipelined(a.T, a.in_dtype, !a.skip_readout, a.serial != 0);
-  const SegPlan p = seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout, a.serial != 0);
+  const SegPlan p = seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout, a.serial != 0,
+                             a.pool_budget);
   auto rec = [&](int i, hipStream_t st) -> hipError_t {
     if (se.ev && hipEventRecord((hipEvent_t)se.ev[i], st) != hipSuccess) return hipErrorInvalidValue;
     return hipSuccess;

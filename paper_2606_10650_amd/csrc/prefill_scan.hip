@@ -89,7 +89,7 @@ __global__ __launch_bounds__(256) void prefill_prep_kernel(PrefillArgs a, Prefil
 hipError_t launch_prefill_prep(const PrefillArgs& a, hipStream_t s) {
   const int nh = a.desc.B * a.desc.H;
   PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C, a.desc.d_k * a.desc.d_v,
-                          seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout, a.serial != 0).nch);
+                          seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout, a.serial != 0, a.pool_budget).nch);
   hipLaunchKernelGGL(prefill_prep_kernel, dim3(nh), dim3(256), 0, s, a, w);
   return hipGetLastError();
 }
@@ -794,7 +794,7 @@ hipError_t launch_prefill_scan(const PrefillArgs& a, int tb, int te, hipStream_t
   const int nh = a.desc.B * a.desc.H;
   const int dk = a.desc.d_k, dv = a.desc.d_v;
   PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C, dk * dv,
-                          seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout, a.serial != 0).nch);
+                          seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout, a.serial != 0, a.pool_budget).nch);
   if (tb < 0 || te > a.T || tb >= te || tb % SL != 0) return hipErrorInvalidValue;
   if (dk == 128 && dv == 128) return launch_scan_dims<128, 128>(a, w, nh, tb, te, s);
   if (dk == 64 && dv == 64) return launch_scan_dims<64, 64>(a, w, nh, tb, te, s);

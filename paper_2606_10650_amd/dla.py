@@ -21,6 +21,7 @@ DLA_OK, DLA_ERR_INVALID_ARG, DLA_ERR_UNSUPPORTED, DLA_ERR_CACHE_MISMATCH, DLA_ER
 DLA_F32, DLA_BF16 = 0, 1
 DLA_SKIP_READOUT = 1
 DLA_SERIAL_STAGES = 2
+DLA_POOL_BUDGET_SHIFT = 8  # flags bits 8..15: log2 of the state-copy budget in bytes
 DLA_FLAG_BAD_MERGE_OVERRIDE = 1
 DLA_FLAG_CACHE_MISMATCH = 2
 
@@ -203,40 +204,42 @@ def cache_flags(cache: StateCache) -> int:
     return int(f.value)
 
 
-def _flags(skip_readout: bool, serial: bool) -> int:
-    return (DLA_SKIP_READOUT if skip_readout else 0) | (DLA_SERIAL_STAGES if serial else 0)
+def _flags(skip_readout: bool, serial: bool, pool_budget_log2: int = 0) -> int:
+    """params flags; pool_budget_log2: DLA_POOL_BUDGET_LOG2 (0: the default budget)."""
+    return ((DLA_SKIP_READOUT if skip_readout else 0) | (DLA_SERIAL_STAGES if serial else 0) |
+            ((int(pool_budget_log2) & 0xFF) << DLA_POOL_BUDGET_SHIFT))
 
 
 def workspace_bytes(cache: StateCache, T: int, dtype=None, skip_readout: bool = False,
-                    serial: bool = False) -> int:
+                    serial: bool = False, pool_budget_log2: int = 0) -> int:
     """Prefill workspace for T tokens of input dtype (torch dtype, default bf16)."""
     code = DLA_BF16 if dtype is None else _dtype_code(dtype)
     n = ctypes.c_size_t(0)
     _check(lib().dla_prefill_workspace_size(ctypes.byref(cache.desc), int(T), code,
-                                            _flags(skip_readout, serial),
+                                            _flags(skip_readout, serial, pool_budget_log2),
                                             ctypes.byref(n)), "dla_prefill_workspace_size")
     return int(n.value)
 
 
 def prefill_segments(cache: StateCache, T: int, dtype=None, skip_readout: bool = False,
-                     serial: bool = False) -> int:
+                     serial: bool = False, pool_budget_log2: int = 0) -> int:
     """Segments (readout launches) of a prefill of T tokens."""
     code = DLA_BF16 if dtype is None else _dtype_code(dtype)
     n = ctypes.c_int32(0)
     _check(lib().dla_prefill_segment_count(ctypes.byref(cache.desc), int(T), code,
-                                           _flags(skip_readout, serial), ctypes.byref(n)),
+                                           _flags(skip_readout, serial, pool_budget_log2), ctypes.byref(n)),
            "dla_prefill_segment_count")
     return int(n.value)
 
 
 def prefill_segment_starts(cache: StateCache, T: int, dtype=None, skip_readout: bool = False,
-                           serial: bool = False) -> list:
+                           serial: bool = False, pool_budget_log2: int = 0) -> list:
     """First token of each segment of a prefill of T tokens."""
     code = DLA_BF16 if dtype is None else _dtype_code(dtype)
-    n = prefill_segments(cache, T, dtype, skip_readout, serial)
+    n = prefill_segments(cache, T, dtype, skip_readout, serial, pool_budget_log2)
     arr = (ctypes.c_int32 * n)()
     _check(lib().dla_prefill_segment_starts(ctypes.byref(cache.desc), int(T), code,
-                                            _flags(skip_readout, serial), arr, n),
+                                            _flags(skip_readout, serial, pool_budget_log2), arr, n),
            "dla_prefill_segment_starts")
     return list(arr)
 
@@ -247,8 +250,9 @@ def _event_array(events):
 
 
 def _params(tau, eps, eps_rms, skip_readout, serial=False, stage_events=None,
-            readout_events=None):
-    p = Params(float(tau), float(eps), float(eps_rms), _flags(skip_readout, serial), None, None, 0)
+            readout_events=None, pool_budget_log2=0):
+    p = Params(float(tau), float(eps), float(eps_rms),
+               _flags(skip_readout, serial, pool_budget_log2), None, None, 0)
     keep = []
     if stage_events is not None:
         assert len(stage_events) == len(PREFILL_STAGES) + 1
@@ -268,12 +272,13 @@ def prefill(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5, eps: f
             eps_rms: float = 1e-6, out=None, out_dtype=None, skip_readout: bool = False,
             boundary=None, merge_idx=None, score=None, boundary_override=None,
             merge_override=None, workspace=None, want_exports: bool = True, stage_events=None,
-            serial: bool = False, readout_events=None):
+            serial: bool = False, readout_events=None, pool_budget_log2: int = 0):
     """Absorb T tokens per head.  q, k: [B, H, T, d_k]; v: [B, H, T, d_v]; g:
     [B, H, T] float32; lam: [B, H, T, C] or None.  serial: run the stages one
     after another on the current stream (otherwise the scan of long inputs is
-    overlapped with the later stages on a second stream).  Returns (out,
-    boundary, merge_idx, score); exports not requested are None."""
+    overlapped with the later stages on a second stream).  pool_budget_log2:
+    log2 of the bytes of state copies per call (0: the library's default).
+    Returns (out, boundary, merge_idx, score); exports not requested are None."""
     torch = _torch()
     B, H, C = cache.B, cache.H, cache.C
     T = k.shape[2]
@@ -296,13 +301,14 @@ def prefill(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5, eps: f
                                                                         device=dev)
         score = score if score is not None else torch.empty((B, H, T), dtype=torch.float32,
                                                             device=dev)
-    wsb = workspace_bytes(cache, T, k.dtype, skip_readout, serial)
+    wsb = workspace_bytes(cache, T, k.dtype, skip_readout, serial, pool_budget_log2)
     if workspace is None or workspace.numel() < wsb:
         workspace = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
     for e in list(stage_events or ()) + list(readout_events or ()):
         if not e.cuda_event:
             e.record()   # torch creates an event on its first record
-    p = _params(tau, eps, eps_rms, skip_readout, serial, stage_events, readout_events)
+    p = _params(tau, eps, eps_rms, skip_readout, serial, stage_events, readout_events,
+                pool_budget_log2)
     st = lib().dla_prefill(ctypes.byref(cache.desc), _ptr(cache.buf), _ptr(q), _ptr(k), _ptr(v),
                            _ptr(g), _ptr(lam), int(T), _dtype_code(k.dtype), ctypes.byref(p),
                            _ptr(out), _dtype_code(out.dtype) if out is not None else DLA_F32,
@@ -316,7 +322,7 @@ def prefill(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5, eps: f
 def prefill_static(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5,
                    eps: float = 1e-6, eps_rms: float = 1e-6, out, boundary=None, merge_idx=None,
                    score=None, boundary_override=None, merge_override=None,
-                   skip_readout: bool = False):
+                   skip_readout: bool = False, pool_budget_log2: int = 0):
     """dla_prefill_static: prefill with the library's static device scratch as
     workspace (stages serial).  Allocates nothing: the caller passes the output
     and any export buffers.  Shapes as prefill."""
@@ -328,7 +334,7 @@ def prefill_static(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5,
     for t in (q, k, v, g, lam, out, boundary, merge_idx, score, boundary_override,
               merge_override):
         assert t is None or (t.is_contiguous() and t.device == dev)
-    p = _params(tau, eps, eps_rms, skip_readout, serial=True)
+    p = _params(tau, eps, eps_rms, skip_readout, serial=True, pool_budget_log2=pool_budget_log2)
     st = lib().dla_prefill_static(ctypes.byref(cache.desc), _ptr(cache.buf), _ptr(q), _ptr(k),
                                   _ptr(v), _ptr(g), _ptr(lam), int(T), _dtype_code(k.dtype),
                                   ctypes.byref(p), _ptr(out),

@@ -187,6 +187,27 @@ def test_prefill_segment_counts():
     assert count(1, 2, 16, 128, 1100, dla.DLA_BF16, 0) == 2
     assert count(1, 2, 16, 128, 0, dla.DLA_BF16, 0) == 1
     assert count(1, 2, 16, 128, 1100, dla.DLA_BF16, dla.DLA_SKIP_READOUT) == 1
+    # a state-copy budget in the flags: 1 GiB splits the 16k-token workload
+    # (256 MiB of copies per chunk) into segments of at most 4 chunks, 256 MiB
+    # into single chunks; the workspace shrinks with it; bad budgets are refused
+    serial = dla.DLA_SERIAL_STAGES
+    assert count(4, 16, 128, 128, 16384, dla.DLA_BF16, serial | dla._flags(False, False, 30)) == 8
+    assert count(4, 16, 128, 128, 16384, dla.DLA_BF16, serial | dla._flags(False, False, 28)) == 32
+    assert count(4, 16, 128, 128, 16384, dla.DLA_BF16, dla._flags(False, False, 30)) == 9
+    ws = []
+    for kb in (0, 31, 30, 29):
+        d = dla.CacheDesc(4, 16, 128, 128, 128)
+        n = ctypes.c_size_t(0)
+        assert L.dla_prefill_workspace_size(ctypes.byref(d), 16384, dla.DLA_BF16,
+                                            dla._flags(False, False, kb), ctypes.byref(n)) == 0
+        ws.append(n.value)
+    assert ws == sorted(ws, reverse=True) and ws[-1] < (1 << 30) < ws[0]
+    for kb in (19, 41, 255):
+        d = dla.CacheDesc(4, 16, 128, 128, 128)
+        n = ctypes.c_size_t(0)
+        assert L.dla_prefill_workspace_size(ctypes.byref(d), 16384, dla.DLA_BF16,
+                                            dla._flags(False, False, kb),
+                                            ctypes.byref(n)) == dla.DLA_ERR_INVALID_ARG
     # segment starts: the ramp of the 16k-token workload (2, 3, 5, 8, 14 chunks of 512)
     desc = dla.CacheDesc(4, 16, 128, 128, 128)
     arr = (ctypes.c_int32 * 8)(*([-7] * 8))

@@ -427,44 +427,49 @@ def test_skip_readout_builds_the_same_cache():
     H.assert_cache(dla.cache_export(cache), ref["cache"], 1e-4, what="skip")
 
 
-def _run_modes(w, x, T_split=None):
+def _run_modes(w, x, T_split=None, budgets=(0, 0)):
     """Prefill the same inputs twice, pipelined and serial (optionally as two
     calls split at T_split), and return both runs' outputs, exports, caches
-    and the pipelined run's readout-launch event count."""
+    and the pipelined run's readout-launch event count.  budgets: the state-copy
+    budgets (log2 bytes, 0 = default) of the pipelined and the serial run."""
     torch = _torch()
     dla = _dla()
     q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
     cuts = [0, w.T] if T_split is None else [0, T_split, w.T]
     res = {}
     for serial in (False, True):
+        kb = budgets[1 if serial else 0]
         cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
         outs = []
         for a, b in zip(cuts[:-1], cuts[1:]):
             sl = lambda t: t[:, :, a:b].contiguous()
             rev = None
+            nseg = dla.prefill_segments(cache, b - a, k.dtype, serial=serial, pool_budget_log2=kb)
             if not serial:
-                rev = [torch.cuda.Event(enable_timing=True) for _ in range(16)]
+                rev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * nseg)]
             o, bd, mi, sc = dla.prefill(cache, sl(q), sl(k), sl(v), sl(g), sl(lam), tau=w.tau,
-                                        serial=serial, readout_events=rev)
+                                        serial=serial, readout_events=rev, pool_budget_log2=kb)
             torch.cuda.synchronize()
             outs.append((o.cpu(), bd.cpu(), mi.cpu(), sc.cpu()))
             if rev is not None:
                 # every readout launch of the call is bracketed by a pair of events
-                for i in range(dla.prefill_segments(cache, b - a, k.dtype)):
+                for i in range(nseg):
                     assert rev[2 * i].elapsed_time(rev[2 * i + 1]) > 0.0
         res[serial] = (outs, dla.cache_export(cache))
     return res
 
 
 @pytest.mark.parametrize("case", ["bf16_ragged", "bf16_three_chunks", "f32", "continuation",
-                                  "bf16_16k", "bf16_64k"])
+                                  "bf16_16k", "bf16_64k", "small_budgets"])
 def test_pipelined_prefill_matches_serial(case):
     """The pipelined prefill (scan segments on a second stream, resuming from
     the scan carry) gives bit-identical outputs, exports and cache to the serial
     one: ragged last chunk, fewer chunks than segments, float32 inputs (256-token
     chunks), a continuation on a non-empty cache, the 16k-token shape (one
-    shared pool), and the 64k-token workload (segments that restart their
-    pool, serial and pipelined)."""
+    shared pool), the 64k-token workload (segments that restart their pool,
+    serial and pipelined), and small state-copy budgets that split both calls
+    into many segments, differently."""
+    budgets = (0, 0)
     if case == "bf16_ragged":
         w, cut = WORKLOADS["cfg3"].replace(B=1, H=3, T=2600, C=24, span_mean=200.0), None
     elif case == "bf16_three_chunks":
@@ -475,6 +480,11 @@ def test_pipelined_prefill_matches_serial(case):
         w, cut = WORKLOADS["cfg2"].replace(B=1, H=2, T=2900, C=16), 1100
     elif case == "bf16_16k":
         w, cut = WORKLOADS["cfg3"].replace(B=1, H=4), None
+    elif case == "small_budgets":
+        # 4 heads x 128 states x 32 KiB: 16 MiB of copies per chunk; budgets of
+        # 64 MiB (pipelined) and 32 MiB (serial) give segments of 4 and 2 chunks
+        w, cut = WORKLOADS["cfg3"].replace(B=1, H=4, T=9000), None
+        budgets = (26, 25)
     else:
         # 64k tokens at C = 256: the state copies exceed the pool budget, so
         # both calls run segments that restart their pool (4 serial, 6
@@ -482,7 +492,7 @@ def test_pipelined_prefill_matches_serial(case):
         w, cut = WORKLOADS["cfg4"], None
     _report("pipe-vs-serial", case=case, T=w.T, C=w.C, dtype=w.dtype)
     x = make_inputs(w)
-    res = _run_modes(w, x, cut)
+    res = _run_modes(w, x, cut, budgets)
     (op, cp), (os_, cs) = res[False], res[True]
     for a, b in zip(op, os_):
         for ta, tb in zip(a, b):
