@@ -23,6 +23,15 @@
  *              (Alg. 2, Sec. 3.2), then append s_t as a new state.
  *     readout o_t = sum_j lambda_{t,j} S_j^T q_t     (eq. capacity_bounded_output)
  *
+ * With a step size beta_t (the Gated DeltaNet form of the base model, Sec. 2.2,
+ * eq. delta_rule_rnn, in this orientation S = sum k v^T, o = S^T q), the newest
+ * state follows the delta rule while it accumulates, and a token writes
+ * beta_t s_t:
+ *     b_t = 0: S <- (I - beta_t k_t k_t^T) S + beta_t s_t   (S already decayed)
+ *     b_t = 1: the new state is beta_t s_t
+ * Closed states only decay.  The score still compares s_t with the newest state
+ * before this token's update (it is scale-invariant, so beta does not enter it).
+ *
  * Readings where the paper is silent or inconsistent (each one is listed with
  * its reasons in the design notes of the repository):
  *   - the score compares the RMS-normalised token state with the RMS-normalised
@@ -75,6 +84,17 @@ static double frob(const double* x, int64_t n) {
   return sqrt(acc);
 }
 
+/* Delta-rule erase of a d_k x d_v state: S <- (I - beta k k^T) S, through
+ * u = S^T k (work: dv doubles). */
+static void delta_erase(double* S, const double* k, double beta, int32_t dk, int32_t dv,
+                        double* u) {
+  for (int32_t c = 0; c < dv; ++c) u[c] = 0.0;
+  for (int32_t a = 0; a < dk; ++a)
+    for (int32_t c = 0; c < dv; ++c) u[c] += k[a] * S[a * dv + c];
+  for (int32_t a = 0; a < dk; ++a)
+    for (int32_t c = 0; c < dv; ++c) S[a * dv + c] -= beta * k[a] * u[c];
+}
+
 /* State Information Score of token state s against state S (both D values),
  * with RMSNorm (unit weight, over the whole flattened state) on both. */
 static double info_score(const double* s, const double* S, int64_t D, double eps,
@@ -99,8 +119,8 @@ static double info_score(const double* s, const double* S, int64_t D, double eps
 }
 
 static int run_head(int64_t T, int32_t C, int32_t dk, int32_t dv, const double* q,
-                    const double* k, const double* v, const double* g, const double* lam,
-                    double tau, double eps, double eps_rms, const int8_t* b_ovr,
+                    const double* k, const double* v, const double* g, const double* beta,
+                    const double* lam, double tau, double eps, double eps_rms, const int8_t* b_ovr,
                     const int32_t* m_ovr, int32_t full, double* out, int8_t* b_out,
                     int32_t* merge_out, double* score_out, int32_t* m_out, double* margin_b,
                     double* margin_m, double* mag_out, int32_t* cache_m, int64_t* n,
@@ -151,10 +171,15 @@ static int run_head(int64_t T, int32_t C, int32_t dk, int32_t dv, const double* 
       }
     }
 
+    /* the token's write (the score above used the unscaled token state) */
+    if (beta)
+      for (int64_t i = 0; i < D; ++i) s[i] *= beta[t];
+
     int32_t merged = -1;
     double mgap = INFINITY;
     if (!b) {
       double* So = S + (int64_t)(m - 1) * D;
+      if (beta) delta_erase(So, kt, beta[t], dk, dv, y);
       for (int64_t i = 0; i < D; ++i) So[i] += s[i];
       n[m - 1] += 1;
       ibar[m - 1] += I;
@@ -235,6 +260,7 @@ static int run_head(int64_t T, int32_t C, int32_t dk, int32_t dv, const double* 
  * Run the layer forward over n_heads independent heads of T tokens.
  *
  * Layouts (row-major): q, k [n_heads][T][dk]; v [n_heads][T][dv]; g [n_heads][T];
+ * beta [n_heads][T] or NULL (NULL: no delta rule, a token writes s_t);
  * lam [n_heads][T][C] or NULL; overrides [n_heads][T] or NULL (-1 = free);
  * outputs out [n_heads][T][dv]; b_out, merge_out, score_out, m_out, margin_b,
  * margin_m, mag_out [n_heads][T]; each output may be NULL (mag_out is written
@@ -250,8 +276,9 @@ static int run_head(int64_t T, int32_t C, int32_t dk, int32_t dv, const double* 
  */
 int dla_oracle_forward(int64_t n_heads, int64_t T, int32_t C, int32_t dk, int32_t dv,
                        const double* q, const double* k, const double* v, const double* g,
-                       const double* lam, double tau, double eps, double eps_rms,
-                       const int8_t* b_ovr, const int32_t* m_ovr, int32_t full, double* out,
+                       const double* beta, const double* lam, double tau, double eps,
+                       double eps_rms, const int8_t* b_ovr, const int32_t* m_ovr, int32_t full,
+                       double* out,
                        int8_t* b_out, int32_t* merge_out, double* score_out, int32_t* m_out,
                        double* margin_b, double* margin_m, double* mag_out, int32_t* cache_m,
                        int64_t* cache_n, double* cache_ibar, double* cache_S) {
@@ -265,7 +292,7 @@ int dla_oracle_forward(int64_t n_heads, int64_t T, int32_t C, int32_t dk, int32_
   for (int64_t h = 0; h < n_heads; ++h) {
     const int64_t tok = h * T;
     int r = run_head(T, C, dk, dv, q ? q + tok * dk : NULL, k + tok * dk, v + tok * dv, g + tok,
-                     lam ? lam + tok * C : NULL, tau, eps, eps_rms, b_ovr ? b_ovr + tok : NULL,
+                     beta ? beta + tok : NULL, lam ? lam + tok * C : NULL, tau, eps, eps_rms, b_ovr ? b_ovr + tok : NULL,
                      m_ovr ? m_ovr + tok : NULL, full, out ? out + tok * dv : NULL,
                      b_out ? b_out + tok : NULL, merge_out ? merge_out + tok : NULL,
                      score_out ? score_out + tok : NULL, m_out ? m_out + tok : NULL,

@@ -40,7 +40,7 @@ def _load(path: Optional[str] = None):
     P = ctypes.c_void_p
     lib.dla_oracle_forward.restype = ctypes.c_int
     lib.dla_oracle_forward.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
-                                       ctypes.c_int32, ctypes.c_int32, P, P, P, P, P,
+                                       ctypes.c_int32, ctypes.c_int32, P, P, P, P, P, P,
                                        ctypes.c_double, ctypes.c_double, ctypes.c_double, P, P,
                                        ctypes.c_int32, P, P, P, P, P, P, P, P, P, P, P, P]
     lib.dla_oracle_threads.restype = ctypes.c_int
@@ -74,12 +74,13 @@ def _p(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
 
-def oracle_forward(k, v, g, C: int, tau: float, *, q=None, lam=None, eps: float = 1e-6,
+def oracle_forward(k, v, g, C: int, tau: float, *, q=None, lam=None, beta=None, eps: float = 1e-6,
                    eps_rms: float = 1e-6, b_override=None, m_override=None, full: bool = True,
                    want_out: bool = True, want_mag: bool = False,
                    cache: Optional[OracleCache] = None, lib_path: Optional[str] = None):
     """Run the oracle on float64 inputs shaped [n_heads, T, d] (g: [n_heads, T],
-    lam: [n_heads, T, C]).  Returns a dict with out, b, merge, score, m,
+    lam: [n_heads, T, C]; beta: [n_heads, T] step sizes of the delta rule, or
+    None for the gated form).  Returns a dict with out, b, merge, score, m,
     margin_b, margin_m, mag (with want_mag: the sum over states of |lambda|
     ||S_j||_F ||q||, which bounds the sizes of the readout's terms; with out)
     and the final cache.  The cache argument is
@@ -94,6 +95,9 @@ def oracle_forward(k, v, g, C: int, tau: float, *, q=None, lam=None, eps: float 
     if lam is not None:
         lam = np.ascontiguousarray(lam, np.float64)
         assert lam.shape == (nh, T, C)
+    if beta is not None:
+        beta = np.ascontiguousarray(beta, np.float64)
+        assert beta.shape == (nh, T)
     if cache is None:
         cache = OracleCache.empty(nh, C, dk, dv)
     want_out = want_out and full and q is not None
@@ -110,7 +114,8 @@ def oracle_forward(k, v, g, C: int, tau: float, *, q=None, lam=None, eps: float 
     bo = None if b_override is None else np.ascontiguousarray(b_override, np.int8)
     mo = None if m_override is None else np.ascontiguousarray(m_override, np.int32)
     lib = _load(lib_path)
-    rc = lib.dla_oracle_forward(nh, T, C, dk, dv, _p(q), _p(k), _p(v), _p(g), _p(lam), tau, eps,
+    rc = lib.dla_oracle_forward(nh, T, C, dk, dv, _p(q), _p(k), _p(v), _p(g), _p(beta), _p(lam),
+                                tau, eps,
                                 eps_rms, _p(bo), _p(mo), 1 if full else 0, _p(res["out"]),
                                 _p(res["b"]), _p(res["merge"]), _p(res["score"]), _p(res["m"]),
                                 _p(res["margin_b"]), _p(res["margin_m"]), _p(res["mag"]), _p(cache.m),

@@ -20,7 +20,11 @@ What pins what (paper passages in brackets):
     the score  [eq. importance_score, RMSNorm remark of Sec. 3.1];
   * hand-computed merge schedules on scalar states  (tests/golden/), including
     the near-tie margins of the parity protocol and the merge override;
-  * conservation (counts, scores, states) and C-independence of boundaries.
+  * conservation (counts, scores, states) and C-independence of boundaries;
+  * the delta-rule form (Gated DeltaNet, Sec. 2.2, eq. delta_rule_rnn): C = 1
+    is the textbook recurrence, a unit key with step 1 is overwritten with its
+    value, step 0 writes nothing, and with boundaries and merges every state is
+    the sum of its ranges' own recurrences (Alg. 2 replayed on membership lists).
 """
 from __future__ import annotations
 
@@ -509,6 +513,115 @@ def pin_direct_evaluation_matches_the_recurrence(lib_path=None):
             assert np.abs(S[:m] - c.S[h, :m]).max() < 1e-11 * np.abs(c.S[h, :m]).max()
 
 
+# ----------------------------------------------------------------------------
+# the delta-rule form (Gated DeltaNet base model, Sec. 2.2, eq. delta_rule_rnn)
+# ----------------------------------------------------------------------------
+
+def gated_deltanet(q, k, v, g, beta):
+    """Textbook recurrence of one head, S = sum k v^T orientation:
+    S_t = exp(g_t) (I - beta_t k_t k_t^T) S_{t-1} + beta_t k_t v_t^T, o_t = S_t^T q_t."""
+    dk, dv = k.shape[1], v.shape[1]
+    S = np.zeros((dk, dv))
+    out = np.zeros((len(k), dv))
+    for t in range(len(k)):
+        A = np.exp(g[t]) * (np.eye(dk) - beta[t] * np.outer(k[t], k[t]))
+        S = A @ S + beta[t] * np.outer(k[t], v[t])
+        out[t] = S.T @ q[t]
+    return out, S
+
+
+def delta_range_states(k, v, g, beta, b, upto):
+    """The state of every token range (a run of tokens opened by a boundary) at
+    token `upto`: the delta-rule recurrence over the range's own tokens, then
+    decay only once the range is closed.  Returns {first token: state}."""
+    G = cum_gate(g)
+    dk, dv = k.shape[1], v.shape[1]
+    starts = [t for t in range(upto + 1) if b[t] or t == 0]
+    out = {}
+    for i, a in enumerate(starts):
+        e = (starts[i + 1] - 1) if i + 1 < len(starts) else upto
+        S = beta[a] * np.outer(k[a], v[a])
+        for s in range(a + 1, e + 1):
+            S = np.exp(g[s]) * (S - beta[s] * np.outer(k[s], k[s] @ S)) + beta[s] * np.outer(k[s], v[s])
+        out[a] = np.exp(G[upto] - G[e]) * S
+    return out
+
+
+def _delta_inputs(name, T, C, seed, **kw):
+    w, q, k, v, g, lam = f64_inputs(name, T=T, **kw)
+    beta = np.random.default_rng(seed).uniform(0.05, 1.0, size=g.shape)
+    return w, q, k, v, g, lam[:, :, :C], beta
+
+
+def pin_delta_single_state_is_gated_deltanet(lib_path=None):
+    """C = 1 with lambda = 1: the layer is the Gated DeltaNet recurrence (the
+    first token's write opens the one state, every later token accumulates)."""
+    w, q, k, v, g, _, beta = _delta_inputs("cfg1", 160, 1, 3)
+    r = oracle_forward(k, v, g, 1, w.tau, q=q, beta=beta, lib_path=lib_path)
+    for h in range(len(q)):
+        ref, S = gated_deltanet(q[h], k[h], v[h], g[h], beta[h])
+        assert np.abs(r["out"][h] - ref).max() < 1e-11 * np.abs(ref).max(), h
+        assert np.abs(r["cache"].S[h, 0] - S).max() < 1e-11 * np.abs(S).max(), h
+
+
+def pin_delta_rule_overwrites_a_unit_key(lib_path=None):
+    """beta = 1 and a unit key: after the token, the accumulating state maps that
+    key to exactly its value (S^T k = v), whatever it held before."""
+    w, q, k, v, g, _, beta = _delta_inputs("cfg1", 64, 4, 5)
+    beta[:] = 0.3
+    beta[:, -1] = 1.0
+    k[:, -1] /= np.linalg.norm(k[:, -1], axis=-1, keepdims=True)   # exactly unit in float64
+    r = oracle_forward(k, v, g, 4, 1e30, q=q, beta=beta, lib_path=lib_path)
+    for h in range(len(q)):
+        assert r["cache"].m[h] == 1
+        got = r["cache"].S[h, 0].T @ k[h, -1]
+        assert np.abs(got - v[h, -1]).max() < 1e-12 * np.abs(v[h, -1]).max(), h
+
+
+def pin_delta_zero_step_writes_nothing(lib_path=None):
+    """beta = 0: no token writes anything, so every state and output is 0."""
+    w, q, k, v, g, lam, beta = _delta_inputs("cfg1", 80, 4, 7)
+    r = oracle_forward(k, v, g, 4, w.tau, q=q, lam=lam, beta=np.zeros_like(beta),
+                       lib_path=lib_path)
+    assert np.abs(r["out"]).max() == 0.0 and np.abs(r["cache"].S).max() == 0.0
+
+
+def pin_delta_ranges_and_merges(lib_path=None):
+    """With boundaries and capacity merges: each state is the sum of the token
+    ranges merged into it (Alg. 2 replayed on membership lists), each range the
+    delta-rule recurrence over its own tokens while it was the newest state and
+    decayed only after it closed; outputs as in eq. capacity_bounded_output."""
+    for name, T, C, kw in (("cfg1", 140, 4, dict(n_seg=12, rho2=0.9)), ("cfg1_iid", 60, 3, {})):
+        w, q, k, v, g, lam, beta = _delta_inputs(name, T, C, 11, **kw)
+        r = oracle_forward(k, v, g, C, w.tau, q=q, lam=lam, beta=beta, lib_path=lib_path)
+        for h in range(len(q)):
+            b, mg = r["b"][h], r["merge"][h]
+            assert (mg >= 0).sum() > 0, "the case must merge"
+            hist = replay_membership(b, mg, C)
+            for t in (0, 1, T // 2, T - 1):
+                rs = delta_range_states(k[h], v[h], g[h], beta[h], b, t)
+                o = np.zeros(v.shape[2])
+                for j, slot in enumerate(hist[t]):
+                    Sj = sum(rs[a] for a in slot if a in rs)
+                    o += lam[h, t, j] * (Sj.T @ q[h, t])
+                ref = r["out"][h, t]
+                assert np.abs(o - ref).max() < 1e-10 * max(np.abs(ref).max(), 1e-30), (name, h, t)
+            rs = delta_range_states(k[h], v[h], g[h], beta[h], b, T - 1)
+            for j, slot in enumerate(hist[T - 1]):
+                Sj = sum(rs[a] for a in slot if a in rs)
+                assert np.abs(Sj - r["cache"].S[h, j]).max() < 1e-10 * np.abs(Sj).max(), (name, h, j)
+
+
+def pin_delta_decisions_mode(lib_path=None):
+    """The decisions mode (newest state only) takes the full mode's decisions
+    with the delta rule too."""
+    w, q, k, v, g, lam, beta = _delta_inputs("cfg1", 200, 4, 13, n_seg=10)
+    full = oracle_forward(k, v, g, 4, w.tau, q=q, lam=lam, beta=beta, lib_path=lib_path)
+    dec = oracle_forward(k, v, g, 4, w.tau, beta=beta, full=False, lib_path=lib_path)
+    assert np.array_equal(full["b"], dec["b"]) and np.array_equal(full["merge"], dec["merge"])
+    assert np.abs(full["score"] - dec["score"]).max() < 1e-12
+
+
 ALL_PINS = [
     pin_lambda_one_is_gated_linear_attention,
     pin_single_state_and_one_state_per_token,
@@ -524,4 +637,9 @@ ALL_PINS = [
     pin_margins_and_merge_overrides,
     pin_margin_b_chord_distance,
     pin_direct_evaluation_matches_the_recurrence,
+    pin_delta_single_state_is_gated_deltanet,
+    pin_delta_rule_overwrites_a_unit_key,
+    pin_delta_zero_step_writes_nothing,
+    pin_delta_ranges_and_merges,
+    pin_delta_decisions_mode,
 ]

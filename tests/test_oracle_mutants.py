@@ -17,6 +17,14 @@ SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), 
                    "dla_oracle.c")
 
 MUTANTS = {
+    # the delta-rule form (Sec. 2.2, eq. delta_rule_rnn)
+    "delta_erase_sign": ("S[a * dv + c] -= beta * k[a] * u[c];", "S[a * dv + c] += beta * k[a] * u[c];"),
+    "delta_erase_without_key": ("u[c] += k[a] * S[a * dv + c];", "u[c] += S[a * dv + c];"),
+    "delta_erase_skipped": ("      if (beta) delta_erase(So, kt, beta[t], dk, dv, y);\n", "\n"),
+    "delta_write_unscaled": ("      for (int64_t i = 0; i < D; ++i) s[i] *= beta[t];\n", "      ;\n"),
+    "delta_on_closing_state": ("      memcpy(S + (int64_t)m * D, s, sizeof(double) * D);",
+                               "      if (beta && m > 0) delta_erase(S + (int64_t)(m - 1) * D, kt, beta[t], dk, dv, y);\n"
+                               "      memcpy(S + (int64_t)m * D, s, sizeof(double) * D);"),
     "no_decay": ("S[j * D + i] *= alpha;", "S[j * D + i] *= 1.0;"),
     "decay_only_newest": ("for (int32_t j = full ? 0 : (m > 0 ? m - 1 : 0); j < m; ++j)",
                           "for (int32_t j = (m > 0 ? m - 1 : 0); j < m; ++j)"),
