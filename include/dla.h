@@ -299,6 +299,42 @@ dla_status dla_decode_step(const dla_cache_desc* desc, void* cache, const void* 
                            float* score, const int8_t* boundary_override,
                            const int32_t* merge_override, void* stream);
 
+/*
+ * Gated DeltaNet form of the layer (Sec. 2.2, eq. delta_rule_rnn; the paper
+ * applies DLA to that backbone as well).  beta: float32 step sizes, [B][H] for
+ * a decode step, [B][H][T] for a sequence, not null.  The newest state follows
+ * the delta rule while tokens accumulate into it (Sec. 3.1 update rule, b_t =
+ * 0): with every state first decayed by exp(g_t),
+ *   S <- (I - beta_t k_t k_t^T) S + beta_t k_t v_t^T,
+ * and a boundary opens the new state beta_t k_t v_t^T (b_t = 1).  Closed states
+ * are summaries and only decay; merges (Alg. 2), scores, decisions and the
+ * readout are those of dla_decode_step (the score compares k_t v_t^T with the
+ * newest state before the token's update; it is scale-invariant, so beta does
+ * not enter it).  With C = 1 the layer is the Gated DeltaNet recurrence.
+ * Same cache as dla_prefill / dla_decode_step (either may continue a cache
+ * the other built, in the same form).
+ */
+dla_status dla_decode_step_delta(const dla_cache_desc* desc, void* cache, const void* q,
+                                 const void* k, const void* v, const float* log_gate,
+                                 const float* beta, const void* lambda, dla_dtype in_dtype,
+                                 const dla_params* params, void* out, dla_dtype out_dtype,
+                                 int8_t* boundary, int32_t* merge_idx, float* score,
+                                 const int8_t* boundary_override, const int32_t* merge_override,
+                                 void* stream);
+
+/* T tokens per head in the Gated DeltaNet form: the arrays of dla_prefill
+ * ([B][H][T][d] tokens, [B][H][T] log_gate, beta, exports and overrides,
+ * [B][H][T][C] lambda), run as T decode steps enqueued on `stream` (one token
+ * of every head per step; no workspace).  A chunked form of this prefill is
+ * not built: it costs one or two kernel launches per token. */
+dla_status dla_prefill_delta(const dla_cache_desc* desc, void* cache, const void* q, const void* k,
+                             const void* v, const float* log_gate, const float* beta,
+                             const void* lambda, int32_t T, dla_dtype in_dtype,
+                             const dla_params* params, void* out, dla_dtype out_dtype,
+                             int8_t* boundary, int32_t* merge_idx, float* score,
+                             const int8_t* boundary_override, const int32_t* merge_override,
+                             void* stream);
+
 const char* dla_status_string(dla_status s);
 dla_status dla_get_last_error(void);
 

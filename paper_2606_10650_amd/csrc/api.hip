@@ -345,18 +345,17 @@ dla_status dla_prefill_static(const dla_cache_desc* desc, void* cache, const voi
                       stream, true);
 }
 
-dla_status dla_decode_step(const dla_cache_desc* desc, void* cache, const void* q, const void* k,
-                           const void* v, const float* log_gate, const void* lambda,
-                           dla_dtype in_dtype, const dla_params* params, void* out,
-                           dla_dtype out_dtype, int8_t* boundary, int32_t* merge_idx,
-                           float* score, const int8_t* boundary_override,
-                           const int32_t* merge_override, void* stream) {
-  dla_status s = check_desc(desc);
-  if (s != DLA_OK) return ret(s);
-  if (!params || !dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return ret(DLA_ERR_INVALID_ARG);
+}  // extern "C"
+
+// One decode step for every head, or step t of a sequence (hs = T): the
+// per-token arrays are passed already offset to the step's token.
+static dla_status decode_impl(const dla_cache_desc* desc, void* cache, const void* q, const void* k,
+                              const void* v, const float* log_gate, const float* beta,
+                              const void* lambda, dla_dtype in_dtype, const dla_params* params,
+                              void* out, dla_dtype out_dtype, int8_t* boundary, int32_t* merge_idx,
+                              float* score, const int8_t* boundary_override,
+                              const int32_t* merge_override, long long hs, void* stream) {
   const bool skip = (params->flags & DLA_SKIP_READOUT) != 0;
-  if (!cache || !k || !v || !log_gate) return ret(DLA_ERR_INVALID_ARG);
-  if (!skip && (!q || !out)) return ret(DLA_ERR_INVALID_ARG);
   const dla_cache_layout L = layout_of(*desc);
   DecodeArgs a;
   memset(&a, 0, sizeof(a));
@@ -378,13 +377,85 @@ dla_status dla_decode_step(const dla_cache_desc* desc, void* cache, const void* 
   a.score_out = score;
   a.b_ovr = boundary_override;
   a.m_ovr = merge_override;
+  a.beta = beta;
+  a.hs = hs;
   a.tau = params->tau;
   a.eps = params->eps;
   a.eps_rms = params->eps_rms;
   a.skip_readout = skip ? 1 : 0;
   if (launch_decode(a, desc->B * desc->H, desc->d_k, desc->d_v, in_dtype, out_dtype,
                     (hipStream_t)stream) != hipSuccess)
-    return ret(DLA_ERR_HIP);
+    return DLA_ERR_HIP;
+  return DLA_OK;
+}
+
+static dla_status decode_check(const dla_cache_desc* desc, void* cache, const void* q,
+                               const void* k, const void* v, const float* log_gate,
+                               dla_dtype in_dtype, const dla_params* params, void* out,
+                               dla_dtype out_dtype) {
+  dla_status s = check_desc(desc);
+  if (s != DLA_OK) return s;
+  if (!params || !dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return DLA_ERR_INVALID_ARG;
+  const bool skip = (params->flags & DLA_SKIP_READOUT) != 0;
+  if (!cache || !k || !v || !log_gate) return DLA_ERR_INVALID_ARG;
+  if (!skip && (!q || !out)) return DLA_ERR_INVALID_ARG;
+  return DLA_OK;
+}
+
+extern "C" {
+
+dla_status dla_decode_step(const dla_cache_desc* desc, void* cache, const void* q, const void* k,
+                           const void* v, const float* log_gate, const void* lambda,
+                           dla_dtype in_dtype, const dla_params* params, void* out,
+                           dla_dtype out_dtype, int8_t* boundary, int32_t* merge_idx,
+                           float* score, const int8_t* boundary_override,
+                           const int32_t* merge_override, void* stream) {
+  dla_status s = decode_check(desc, cache, q, k, v, log_gate, in_dtype, params, out, out_dtype);
+  if (s != DLA_OK) return ret(s);
+  return ret(decode_impl(desc, cache, q, k, v, log_gate, nullptr, lambda, in_dtype, params, out,
+                         out_dtype, boundary, merge_idx, score, boundary_override, merge_override,
+                         1, stream));
+}
+
+dla_status dla_decode_step_delta(const dla_cache_desc* desc, void* cache, const void* q,
+                                 const void* k, const void* v, const float* log_gate,
+                                 const float* beta, const void* lambda, dla_dtype in_dtype,
+                                 const dla_params* params, void* out, dla_dtype out_dtype,
+                                 int8_t* boundary, int32_t* merge_idx, float* score,
+                                 const int8_t* boundary_override, const int32_t* merge_override,
+                                 void* stream) {
+  dla_status s = decode_check(desc, cache, q, k, v, log_gate, in_dtype, params, out, out_dtype);
+  if (s != DLA_OK) return ret(s);
+  if (!beta) return ret(DLA_ERR_INVALID_ARG);
+  return ret(decode_impl(desc, cache, q, k, v, log_gate, beta, lambda, in_dtype, params, out,
+                         out_dtype, boundary, merge_idx, score, boundary_override, merge_override,
+                         1, stream));
+}
+
+dla_status dla_prefill_delta(const dla_cache_desc* desc, void* cache, const void* q, const void* k,
+                             const void* v, const float* log_gate, const float* beta,
+                             const void* lambda, int32_t T, dla_dtype in_dtype,
+                             const dla_params* params, void* out, dla_dtype out_dtype,
+                             int8_t* boundary, int32_t* merge_idx, float* score,
+                             const int8_t* boundary_override, const int32_t* merge_override,
+                             void* stream) {
+  dla_status s = decode_check(desc, cache, q, k, v, log_gate, in_dtype, params, out, out_dtype);
+  if (s != DLA_OK) return ret(s);
+  if (!beta || T < 0) return ret(DLA_ERR_INVALID_ARG);
+  const size_t ei = dtype_bytes(in_dtype), eo = dtype_bytes(out_dtype);
+  const size_t dk = desc->d_k, dv = desc->d_v, C = desc->C;
+  auto at = [](const void* p, size_t off) -> const void* {
+    return p ? static_cast<const char*>(p) + off : nullptr;
+  };
+  for (int32_t t = 0; t < T; ++t) {
+    s = decode_impl(desc, cache, at(q, t * dk * ei), at(k, t * dk * ei), at(v, t * dv * ei),
+                    log_gate + t, beta + t, at(lambda, t * C * ei), in_dtype, params,
+                    out ? static_cast<char*>(out) + t * dv * eo : nullptr, out_dtype,
+                    boundary ? boundary + t : nullptr, merge_idx ? merge_idx + t : nullptr,
+                    score ? score + t : nullptr, boundary_override ? boundary_override + t : nullptr,
+                    merge_override ? merge_override + t : nullptr, T, stream);
+    if (s != DLA_OK) return ret(s);
+  }
   return ret(DLA_OK);
 }
 

@@ -20,6 +20,13 @@ struct DecodeArgs {
   float* score_out;
   const int8_t* b_ovr;
   const int32_t* m_ovr;
+  // Gated DeltaNet form (Sec. 2.2, eq. delta_rule_rnn): beta [B*H] step sizes
+  // of the delta rule on the newest state, or null for the gated form
+  const float* beta;
+  // tokens between consecutive heads in every per-token array (q, k, v, g,
+  // beta, lambda, out, exports, overrides): 1 for a decode step, T for a step
+  // of a sequence of T tokens laid out [B][H][T]
+  long long hs;
   float tau, eps, eps_rms;
   int skip_readout;
 };

@@ -24,6 +24,11 @@
 // another, and no device-scope fence is needed (one per workgroup, with the L2
 // write-back it implies, made the split step 2.4 times slower).
 //
+// Gated DeltaNet form (with step sizes beta): the newest state follows the
+// delta rule while it accumulates, S <- (I - beta k k^T) S + beta k v^T, and a
+// new state is beta k v^T; closed states only decay.  The erase needs S^T k,
+// reduced from the newest state's registers at the end of the step.
+//
 // Thread mapping inside a state: element group tid + 256 r (4 consecutive
 // elements) of the row-major d_k x d_v array, i.e. thread tid owns the 4
 // columns 4*(tid % (d_v/4)) .. +3 of the rows (tid / (d_v/4)) + r * (256 /
@@ -123,7 +128,39 @@ __device__ __forceinline__ void finish_step(const DecodeArgs& a, int h, int m, i
   const int cq = tid % ST::CQ;
   const int rg = tid / ST::CQ;
   const int C = a.desc.C;
+  const size_t ht = (size_t)h * a.hs;
   const int m_post = b ? (istar >= 0 ? m : m + 1) : m;
+  // Delta rule (Gated DeltaNet form): the token writes beta k v^T, and an
+  // accumulating newest state is first erased along k: with the true old
+  // state f S~ (f = exp(Gn - F)) and u = S~^T k, the new state is
+  //   f S~ + beta k (v - f u)^T.
+  const bool delta = a.beta != nullptr;
+  const float beta = delta ? a.beta[ht] : 1.f;
+  const float fo = (!b && m > 0) ? __expf((float)(Gn - sF[m - 1])) : 0.f;
+  __shared__ float sUp[ST::RG][DV];
+  __shared__ float sU[DV];
+  if (delta && !b) {
+    float up[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < ST::NV; ++r) {
+      const float kr = sk[rg + ST::RG * r];
+      const float4 o = open_at(r);
+      up[0] += kr * o.x;
+      up[1] += kr * o.y;
+      up[2] += kr * o.z;
+      up[3] += kr * o.w;
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) sUp[rg][4 * cq + c] = up[c];
+    __syncthreads();
+    if (tid < DV) {
+      float u = 0.f;
+#pragma unroll
+      for (int g2 = 0; g2 < ST::RG; ++g2) u += sUp[g2][tid];
+      sU[tid] = fo * u;   // (f u: the true state's S^T k)
+    }
+    __syncthreads();
+  }
   {
     float* dst;
     if (SB)
@@ -132,7 +169,13 @@ __device__ __forceinline__ void finish_step(const DecodeArgs& a, int h, int m, i
       dst = reinterpret_cast<float*>(states) + (size_t)sP[m - 1] * D;
     else
       dst = reinterpret_cast<float*>(states) + (size_t)((istar >= 0) ? sP[istar + 1] : sP[m]) * D;
-    const float4 vq = reinterpret_cast<const float4*>(sv)[cq];
+    // the token's write beta (v - f u) (beta = 1, u = 0 in the gated form)
+    float4 vq = reinterpret_cast<const float4*>(sv)[cq];
+    if (delta) {
+      const float4 uq = b ? make_float4(0.f, 0.f, 0.f, 0.f) : reinterpret_cast<const float4*>(sU)[cq];
+      vq = make_float4(beta * (vq.x - uq.x), beta * (vq.y - uq.y), beta * (vq.z - uq.z),
+                       beta * (vq.w - uq.w));
+    }
     if (b) {
 #pragma unroll
       for (int r = 0; r < ST::NV; ++r) {
@@ -140,7 +183,7 @@ __device__ __forceinline__ void finish_step(const DecodeArgs& a, int h, int m, i
         st_group(dst, tid + 256 * r, make_float4(kr * vq.x, kr * vq.y, kr * vq.z, kr * vq.w));
       }
     } else {
-      const float f = __expf((float)(Gn - sF[m - 1]));
+      const float f = fo;
 #pragma unroll
       for (int r = 0; r < ST::NV; ++r) {
         const float kr = sk[rg + ST::RG * r];
@@ -154,15 +197,16 @@ __device__ __forceinline__ void finish_step(const DecodeArgs& a, int h, int m, i
       }
     }
   }
-  // the new token's own contribution lambda_{m'-1} (q.k) v
+  // the new token's own contribution lambda_{m'-1} (q.k) times its write
   if (!a.skip_readout && tid < DV) {
-    acc += sLam[m_post - 1] * qk2 * sv[tid];
-    static_cast<Tout*>(a.out)[(size_t)h * DV + tid] = from_f32<Tout>(acc);
+    const float wv = delta ? beta * (sv[tid] - (b ? 0.f : sU[tid])) : sv[tid];
+    acc += sLam[m_post - 1] * qk2 * wv;
+    static_cast<Tout*>(a.out)[ht * DV + tid] = from_f32<Tout>(acc);
   }
   if (tid == 0) {
-    if (a.b_out) a.b_out[h] = (int8_t)b;
-    if (a.merge_out) a.merge_out[h] = istar;
-    if (a.score_out) a.score_out[h] = (float)I;
+    if (a.b_out) a.b_out[ht] = (int8_t)b;
+    if (a.merge_out) a.merge_out[ht] = istar;
+    if (a.score_out) a.score_out[ht] = (float)I;
   }
   // metadata update (chronological arrays, parallel over slots)
   if (!b) {
@@ -238,9 +282,10 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
   __shared__ double sScal[4];
   __shared__ int sDec[4];
 
-  const Tin* q = static_cast<const Tin*>(a.q) + (size_t)h * DK;
-  const Tin* k = static_cast<const Tin*>(a.k) + (size_t)h * DK;
-  const Tin* v = static_cast<const Tin*>(a.v) + (size_t)h * DV;
+  const size_t ht = (size_t)h * a.hs;
+  const Tin* q = static_cast<const Tin*>(a.q) + ht * DK;
+  const Tin* k = static_cast<const Tin*>(a.k) + ht * DK;
+  const Tin* v = static_cast<const Tin*>(a.v) + ht * DV;
   for (int i = tid; i < DK; i += 256) {
     sk[i] = to_f32(k[i]);
     sq[i] = a.skip_readout ? 0.f : to_f32(q[i]);
@@ -256,11 +301,11 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     sI[j] = M.ibar[j];
     sN[j] = M.n[j];
     sP[j] = min(max(M.perm[j], 0), C - 1);
-    sLam[j] = a.lam ? to_f32(static_cast<const Tin*>(a.lam)[(size_t)h * C + j]) : 1.f;
+    sLam[j] = a.lam ? to_f32(static_cast<const Tin*>(a.lam)[ht * C + j]) : 1.f;
   }
   __syncthreads();
 
-  const double Gn = G0 + (double)a.g[h];
+  const double Gn = G0 + (double)a.g[ht];
   TS* states = reinterpret_cast<TS*>(a.cache + a.states_offset) + (size_t)h * C * D;
   float* open = SB ? reinterpret_cast<float*>(a.cache + a.open_offset) + (size_t)h * D : nullptr;
   // the newest state's storage: its slot, or the open region
@@ -306,7 +351,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
       const double a2 = (double)kk2 * (double)vv2;
       I = info_score(a2, f * f * (double)bt, f * (double)ct, (double)D, a.eps, a.eps_rms);
       b = (I >= (double)a.tau) ? 1 : 0;
-      if (a.b_ovr && a.b_ovr[h] != -1) b = a.b_ovr[h] ? 1 : 0;
+      if (a.b_ovr && a.b_ovr[ht] != -1) b = a.b_ovr[ht] ? 1 : 0;
       if (C == 1) b = 0;
     }
     sScal[0] = I;
@@ -355,8 +400,8 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
       // at pair 0 when pair 0's density is NaN or none is a number
       if (ii < 0 || ii > C - 2) ii = 0;
       if (__builtin_isnan((sI[0] + sI[1]) / (double)(sN[0] + sN[1]))) ii = 0;
-      if (a.m_ovr && a.m_ovr[h] != -1) {
-        const int f = a.m_ovr[h];
+      if (a.m_ovr && a.m_ovr[ht] != -1) {
+        const int f = a.m_ovr[ht];
         if (f >= 0 && f <= C - 2)
           ii = f;
         else if (sp == 0)
@@ -497,9 +542,10 @@ __global__ __launch_bounds__(256) void decode_finish_kernel(DecodeArgs a) {
   float* sLam = reinterpret_cast<float*>(sP + C);       // [C]
   __shared__ float sk[DK], sv[DV];
   __shared__ float red[8];
-  const Tin* q = static_cast<const Tin*>(a.q) + (size_t)h * DK;
-  const Tin* k = static_cast<const Tin*>(a.k) + (size_t)h * DK;
-  const Tin* v = static_cast<const Tin*>(a.v) + (size_t)h * DV;
+  const size_t ht = (size_t)h * a.hs;
+  const Tin* q = static_cast<const Tin*>(a.q) + ht * DK;
+  const Tin* k = static_cast<const Tin*>(a.k) + ht * DK;
+  const Tin* v = static_cast<const Tin*>(a.v) + ht * DV;
   float qk = 0.f;
   for (int i = tid; i < DK; i += 256) {
     sk[i] = to_f32(k[i]);
@@ -509,13 +555,13 @@ __global__ __launch_bounds__(256) void decode_finish_kernel(DecodeArgs a) {
   char* mbase = a.cache + a.meta_offset + (size_t)h * a.meta_stride;
   Meta M = meta_at(mbase, C);
   const int m = min(max(*M.m, 0), C);
-  const double Gn = *M.G + (double)a.g[h];
+  const double Gn = *M.G + (double)a.g[ht];
   for (int j = tid; j < C; j += 256) {
     sF[j] = M.F[j];
     sI[j] = M.ibar[j];
     sN[j] = M.n[j];
     sP[j] = min(max(M.perm[j], 0), C - 1);
-    sLam[j] = a.lam ? to_f32(static_cast<const Tin*>(a.lam)[(size_t)h * C + j]) : 1.f;
+    sLam[j] = a.lam ? to_f32(static_cast<const Tin*>(a.lam)[ht * C + j]) : 1.f;
   }
   const DecodeRecord rec = *reinterpret_cast<const DecodeRecord*>(decode_record(mbase, C));
   float dummy = 0.f;

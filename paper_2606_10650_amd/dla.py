@@ -28,6 +28,7 @@ DLA_FLAG_CACHE_MISMATCH = 2
 EXPORTED = ("dla_cache_layout_of", "dla_state_cache_alloc", "dla_cache_flags",
             "dla_cache_header_check", "dla_prefill_workspace_size", "dla_prefill_segment_count",
             "dla_prefill_segment_starts", "dla_prefill", "dla_prefill_static", "dla_decode_step",
+            "dla_decode_step_delta", "dla_prefill_delta",
             "dla_status_string", "dla_get_last_error", "dla_peak_mfma_bf16", "dla_peak_hbm_read")
 STATIC_SCRATCH_BYTES = 128 << 20   # DLA_STATIC_SCRATCH_BYTES
 
@@ -90,6 +91,11 @@ def lib():
                                          P, P, P]
         L.dla_decode_step.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, I,
                                       ctypes.POINTER(Params), P, I, P, P, P, P, P, P]
+        L.dla_decode_step_delta.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, P, I,
+                                            ctypes.POINTER(Params), P, I, P, P, P, P, P, P]
+        L.dla_prefill_delta.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, P,
+                                        ctypes.c_int32, I, ctypes.POINTER(Params), P, I, P, P, P,
+                                        P, P, P]
         L.dla_peak_mfma_bf16.argtypes = [ctypes.c_int32, ctypes.c_int32, P, P]
         L.dla_peak_hbm_read.argtypes = [P, ctypes.c_size_t, ctypes.c_int32, P, P]
         L.dla_status_string.argtypes = [I]
@@ -98,7 +104,8 @@ def lib():
         for name in ("dla_cache_layout_of", "dla_state_cache_alloc", "dla_cache_flags",
                      "dla_cache_header_check", "dla_prefill_workspace_size",
                      "dla_prefill_segment_count", "dla_prefill_segment_starts", "dla_prefill",
-                     "dla_prefill_static", "dla_decode_step", "dla_get_last_error",
+                     "dla_prefill_static", "dla_decode_step", "dla_decode_step_delta",
+                     "dla_prefill_delta", "dla_get_last_error",
                      "dla_peak_mfma_bf16", "dla_peak_hbm_read"):
             getattr(L, name).restype = I
         _lib = L
@@ -376,6 +383,77 @@ def decode_step(cache: StateCache, q, k, v, g, lam=None, *, tau: float = 0.5, ep
                                _ptr(boundary), _ptr(merge_idx), _ptr(score),
                                _ptr(boundary_override), _ptr(merge_override), _stream(dev))
     _check(st, "dla_decode_step")
+    return out, boundary, merge_idx, score
+
+
+def decode_step_delta(cache: StateCache, q, k, v, g, beta, lam=None, *, tau: float = 0.5,
+                      eps: float = 1e-6, eps_rms: float = 1e-6, out=None, out_dtype=None,
+                      skip_readout: bool = False, boundary=None, merge_idx=None, score=None,
+                      boundary_override=None, merge_override=None, want_exports: bool = True):
+    """dla_decode_step_delta: one token per head in the Gated DeltaNet form.
+    Shapes as decode_step; beta: [B, H] float32 step sizes."""
+    torch = _torch()
+    B, H = cache.B, cache.H
+    dev = cache.device
+    assert beta is not None and beta.shape == (B, H) and beta.dtype == torch.float32
+    assert k.shape == (B, H, cache.d_k) and v.shape == (B, H, cache.d_v) and g.shape == (B, H)
+    for t in (q, k, v, g, beta, lam, boundary_override, merge_override):
+        assert t is None or (t.is_contiguous() and t.device == dev)
+    if out is None and not skip_readout:
+        out = torch.empty((B, H, cache.d_v), dtype=out_dtype or k.dtype, device=dev)
+    if want_exports:
+        boundary = boundary if boundary is not None else torch.empty((B, H), dtype=torch.int8,
+                                                                      device=dev)
+        merge_idx = merge_idx if merge_idx is not None else torch.empty((B, H), dtype=torch.int32,
+                                                                        device=dev)
+        score = score if score is not None else torch.empty((B, H), dtype=torch.float32,
+                                                            device=dev)
+    p = _params(tau, eps, eps_rms, skip_readout)
+    st = lib().dla_decode_step_delta(ctypes.byref(cache.desc), _ptr(cache.buf), _ptr(q), _ptr(k),
+                                     _ptr(v), _ptr(g), _ptr(beta), _ptr(lam), _dtype_code(k.dtype),
+                                     ctypes.byref(p), _ptr(out),
+                                     _dtype_code(out.dtype) if out is not None else DLA_F32,
+                                     _ptr(boundary), _ptr(merge_idx), _ptr(score),
+                                     _ptr(boundary_override), _ptr(merge_override), _stream(dev))
+    _check(st, "dla_decode_step_delta")
+    return out, boundary, merge_idx, score
+
+
+def prefill_delta(cache: StateCache, q, k, v, g, beta, lam=None, *, tau: float = 0.5,
+                  eps: float = 1e-6, eps_rms: float = 1e-6, out=None, out_dtype=None,
+                  skip_readout: bool = False, boundary=None, merge_idx=None, score=None,
+                  boundary_override=None, merge_override=None, want_exports: bool = True):
+    """dla_prefill_delta: T tokens per head in the Gated DeltaNet form (run as
+    T decode steps).  Shapes as prefill; beta: [B, H, T] float32."""
+    torch = _torch()
+    B, H, C = cache.B, cache.H, cache.C
+    T = k.shape[2]
+    dev = cache.device
+    assert k.shape == (B, H, T, cache.d_k) and v.shape == (B, H, T, cache.d_v)
+    assert g.shape == (B, H, T) and beta is not None and beta.shape == (B, H, T)
+    assert beta.dtype == torch.float32
+    for t in (q, k, v, g, beta, lam, boundary_override, merge_override):
+        assert t is None or (t.is_contiguous() and t.device == dev)
+    if lam is not None:
+        assert lam.shape == (B, H, T, C) and lam.dtype == k.dtype
+    if out is None and not skip_readout:
+        out = torch.empty((B, H, T, cache.d_v), dtype=out_dtype or k.dtype, device=dev)
+    if want_exports:
+        boundary = boundary if boundary is not None else torch.empty((B, H, T), dtype=torch.int8,
+                                                                      device=dev)
+        merge_idx = merge_idx if merge_idx is not None else torch.empty((B, H, T),
+                                                                        dtype=torch.int32,
+                                                                        device=dev)
+        score = score if score is not None else torch.empty((B, H, T), dtype=torch.float32,
+                                                            device=dev)
+    p = _params(tau, eps, eps_rms, skip_readout)
+    st = lib().dla_prefill_delta(ctypes.byref(cache.desc), _ptr(cache.buf), _ptr(q), _ptr(k),
+                                 _ptr(v), _ptr(g), _ptr(beta), _ptr(lam), int(T),
+                                 _dtype_code(k.dtype), ctypes.byref(p), _ptr(out),
+                                 _dtype_code(out.dtype) if out is not None else DLA_F32,
+                                 _ptr(boundary), _ptr(merge_idx), _ptr(score),
+                                 _ptr(boundary_override), _ptr(merge_override), _stream(dev))
+    _check(st, "dla_prefill_delta")
     return out, boundary, merge_idx, score
 
 

@@ -28,7 +28,7 @@ from typing import Optional
 import numpy as np
 
 # Stream ids used as the last word of the RNG key.
-_S_SEG, _S_MU, _S_K, _S_V, _S_Q, _S_G, _S_W = range(7)
+_S_SEG, _S_MU, _S_K, _S_V, _S_Q, _S_G, _S_W, _S_BETA = range(8)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -194,6 +194,18 @@ def _head_tokens(w: Workload, b: int, h: int, seg: np.ndarray, rho2: np.ndarray,
 def lambda_weights(w: Workload, h: int) -> np.ndarray:
     """Per-head readout projection w_j (C x dk), shared by all sequences."""
     return _rng(w.seed, 0, h, _S_W).standard_normal((w.C, w.dk))
+
+
+def make_beta(w: Workload, heads: Optional[list] = None, T: Optional[int] = None) -> np.ndarray:
+    """Step sizes of the delta-rule form (a sigmoid output in the Gated DeltaNet
+    backbone): beta ~ U(0.05, 1) i.i.d. per (b, h, t), float32 [n_heads, T]."""
+    T = w.T if T is None else T
+    if heads is None:
+        heads = [(b, h) for b in range(w.B) for h in range(w.H)]
+    out = np.empty((len(heads), T), np.float32)
+    for i, (b, h) in enumerate(heads):
+        out[i] = _rng(w.seed, b, h, _S_BETA).uniform(0.05, 1.0, size=T)
+    return out
 
 
 def _parallel(fn, n):
