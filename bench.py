@@ -274,7 +274,7 @@ def decode_bytes(W, m_live, state_dtype_bf16):
     return rd + wr + (2 * W.dk + W.dv + W.C + W.dv) * 2
 
 
-def decode_bench(args, torch, dla, W, steps, state_dtype, label):
+def decode_bench(args, torch, dla, W, steps, state_dtype, label, delta=False):
     from paper_2606_10650_amd.workloads import make_decode_tokens_torch, make_prefix_torch
     t0 = time.time()
     _, k, v, g = make_prefix_torch(W, "cuda")
@@ -286,6 +286,18 @@ def decode_bench(args, torch, dla, W, steps, state_dtype, label):
     del k, v, g
     torch.cuda.empty_cache()
     q, kk, vv, gg, lam = make_decode_tokens_torch(W, steps + 2, "cuda")
+    beta = None
+    if delta:
+        # step sizes of the delta rule, U(0.05, 1) per head and token
+        gen = torch.Generator(device="cuda").manual_seed(W.seed + 17)
+        beta = 0.05 + 0.95 * torch.rand((steps + 2, W.B, W.H), device="cuda", generator=gen)
+
+    def one(c, i, **kw):
+        if delta:
+            return dla.decode_step_delta(c, q[i], kk[i], vv[i], gg[i], beta[i], lam[i],
+                                         tau=W.tau, out=out, **kw)
+        return dla.decode_step(c, q[i], kk[i], vv[i], gg[i], lam[i], tau=W.tau, out=out, **kw)
+
     out = torch.empty((W.B, W.H, W.dv), dtype=torch.bfloat16, device="cuda")
     bnd = torch.empty((steps, W.B, W.H), dtype=torch.int8, device="cuda")
     mrg = torch.empty((steps, W.B, W.H), dtype=torch.int32, device="cuda")
@@ -293,8 +305,7 @@ def decode_bench(args, torch, dla, W, steps, state_dtype, label):
     # warm-up on a copy of the cache, then the timed steps on the prefix cache
     warm = dla.StateCache(W.B, W.H, W.C, W.dk, W.dv, cache.buf.clone(), state_dtype)
     for i in range(2):
-        dla.decode_step(warm, q[i], kk[i], vv[i], gg[i], lam[i], tau=W.tau, out=out,
-                        want_exports=False)
+        one(warm, i, want_exports=False)
     torch.cuda.synchronize()
     del warm
     torch.cuda.empty_cache()
@@ -310,8 +321,7 @@ def decode_bench(args, torch, dla, W, steps, state_dtype, label):
     t0 = time.perf_counter()
     evs[0].record()
     for i in range(steps):
-        dla.decode_step(cache, q[i + 2], kk[i + 2], vv[i + 2], gg[i + 2], lam[i + 2], tau=W.tau,
-                        out=out, boundary=bnd[i], merge_idx=mrg[i], score=None)
+        one(cache, i + 2, boundary=bnd[i], merge_idx=mrg[i], score=None)
         evs[i + 1].record()
     t_enq = time.perf_counter() - t0
     torch.cuda.synchronize()
@@ -324,7 +334,8 @@ def decode_bench(args, torch, dla, W, steps, state_dtype, label):
     ach = bytes_step / (np.mean(us) * 1e-6) / 1e9
     res = {
         "config": {"workload": (f"decode {W.B}x{W.H} heads, C={W.C}, d={W.dk}, prefix {W.T} "
-                                f"tokens, {'bf16' if sb else 'f32'} state storage"),
+                                f"tokens, {'bf16' if sb else 'f32'} state storage"
+                                + (", delta rule on the newest state" if delta else "")),
                    "B": W.B, "H": W.H, "C": W.C, "prefix_tokens": W.T, "steps": steps,
                    "state_dtype": "bf16" if sb else "f32"},
         "us_per_step_mean": round(float(np.mean(us)), 2),
@@ -335,7 +346,8 @@ def decode_bench(args, torch, dla, W, steps, state_dtype, label):
         "cache_bytes": cache.buf.numel(),
         "roofline": {"kernel": "decode_kernel", "bound": "hbm", "achieved": round(ach, 1),
                      "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": frac(ach, PEAK_HBM_GBS),
-                     "traffic": (counter_traffic("decode_kernel", W.name) if not sb else
+                     "traffic": (None if delta else
+                                 counter_traffic("decode_kernel", W.name) if not sb else
                                  counter_traffic("decode_kernel", W.name + "_bf16")),
                      "bytes_per_launch": bytes_step},
     }
@@ -589,8 +601,16 @@ def main():
         d = decode_bench(args, torch, dla, few, 64, dla.DLA_F32, "decode few heads")
         res["decode_few_heads"] = d
         log(f"[bench] decode (1x32 heads) {d['us_per_step_mean']} us/step")
+        # Gated DeltaNet form of the step (the prefix is absorbed by the gated
+        # prefill; only the timed steps take the delta rule)
+        d = decode_bench(args, torch, dla, W5, args.decode_steps, dla.DLA_BF16,
+                         "decode delta bf16", delta=True)
+        d.pop("_cache", None)
+        res["decode_delta_bf16_states"] = d
+        log(f"[bench] decode delta (bf16 states) {d['us_per_step_mean']} us/step")
         if pk := res.get("peaks_measured"):
-            for key in ("decode", "decode_bf16_states", "decode_few_heads"):
+            for key in ("decode", "decode_bf16_states", "decode_few_heads",
+                        "decode_delta_bf16_states"):
                 res[key]["roofline"]["frac_measured_peak"] = frac(res[key]["roofline"]["achieved"],
                                                                   pk["hbm_read_gbs"])
     if not args.no_sweep:
