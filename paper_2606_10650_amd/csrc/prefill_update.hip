@@ -55,13 +55,22 @@ struct UpdP {
   static_assert(VBYTES >= (size_t)3 * RL * 4 && VBYTES >= (size_t)NWAVE * 64 * 16 * 4, "aliases");
 };
 
+// Key groups of the token-range loop in flight per wave when the keys come
+// through LDS (KL): each group is the wave's 32 rows of d_k for 16 tokens, 1 KB
+// of 16-bit keys.
+constexpr int KDL = 4;
+
 template <int DK, typename Tin>
-static size_t update_smem_bytes(int C) {
+__host__ __device__ static size_t update_smem_base(int C) {
   using U = UpdP<DK, Tin>;
   size_t off = round_up(U::VBYTES, 16);  // staged values (and their aliases)
   off += (size_t)C * 8;                  // sF
   off += (size_t)C * 4 * 13 + 64;        // int arrays, reduction scratch
   return round_up(off, 16);
+}
+template <int DK, typename Tin, bool KL>
+static size_t update_smem_bytes(int C) {
+  return update_smem_base<DK, Tin>(C) + (KL ? (size_t)NWAVE * KDL * 1024 : 0);  // key rings
 }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, int bytes) {
@@ -69,7 +78,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, 
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
 }
 
-template <int DK, int DV, typename Tin, typename TS>
+// KL: the token-range loop reads its keys from a per-wave LDS ring that the
+// loads fill directly (16-bit inputs), with explicit waits; else straight from
+// global memory into registers.
+template <int DK, int DV, typename Tin, typename TS, bool KL>
 __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, PrefillWS w,
                                                               SegPlan plan, int seg) {
   if (!cache_matches(a.cache, a.desc)) return;  // refused call (see the prep kernel)
@@ -624,21 +636,87 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
       };
 
       const int g0 = ps >> 4, g1 = (pe + 15) >> 4;
-      uint32_t kw[U::KD][U::KW];
       BOp bb[2];
+      if constexpr (KL) {
+        // The wave's keys pass through its ring of KDL groups in LDS, each
+        // loaded straight from memory (lane i brings 16 bytes: token i / 4 of
+        // the group, piece (i % 4) ^ (token / 4 % 4) of the band's 32 rows, so
+        // that the reads below spread over the banks).  A range end inside the
+        // loop stores a state, so the number of memory operations between a
+        // group's request and its use varies: the waits count only the later
+        // key requests, which are a lower bound.
+        char* kring = smem + update_smem_base<DK, Tin>(C) + (size_t)wv * KDL * 1024;
+        auto kdma = [&](int g) __attribute__((always_inline)) {
+          const int t = lane >> 2, pc = (lane & 3) ^ ((t >> 2) & 3);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              kr, (__attribute__((address_space(3))) void*)(kring + (g % KDL) * 1024), 16,
+              ((16 * g + t) * DK + ib + 8 * pc) * 2, 0, 0, 0);
+        };
+        // the 32-bit words kload would read for group g, from the ring
+        auto kread = [&](int g, uint32_t (&dst)[U::KW]) __attribute__((always_inline)) {
+          const char* slot = kring + (g % KDL) * 1024;
+          const int r = l32 & ~1;
 #pragma unroll
-      for (int u = 0; u < U::KD; ++u)
-        if (g0 + u < g1) kload(g0 + u, kw[u]);
-      bload(g0, bb[0]);
-      for (int gb = g0; gb < g1; gb += U::KD) {
+          for (int u = 0; u < 4; ++u) {
+            const int tk = 8 * half + (odd ? 4 : 0) + u;
+            const int pos = 4 * tk + ((r >> 3) ^ ((tk >> 2) & 3));
+            dst[u] = *reinterpret_cast<const uint32_t*>(slot + pos * 16 + (r & 7) * 2);
+          }
+        };
+        // wait until the request of group g has landed: the requests issued
+        // after it, up to group e - 1, are a lower bound on those in flight
+        static_assert(KDL == 4, "wait counts");
+        auto kwait = [&](int later) __attribute__((always_inline)) {
+          if (later >= 3)
+            __builtin_amdgcn_s_waitcnt((3 & 15) | (7 << 4) | (15 << 8) | ((3 >> 4) << 14));
+          else if (later == 2)
+            __builtin_amdgcn_s_waitcnt((2 & 15) | (7 << 4) | (15 << 8) | ((2 >> 4) << 14));
+          else if (later == 1)
+            __builtin_amdgcn_s_waitcnt((1 & 15) | (7 << 4) | (15 << 8) | ((1 >> 4) << 14));
+          else
+            __builtin_amdgcn_s_waitcnt((0 & 15) | (7 << 4) | (15 << 8) | ((0 >> 4) << 14));
+        };
+        for (int u = 0; u < KDL; ++u)
+          if (g0 + u < g1) kdma(g0 + u);
+        bload(g0, bb[0]);
+        uint32_t kwa[U::KW], kwb[U::KW];
+        kwait(min(KDL - 1, g1 - 1 - g0));
+        kread(g0, kwa);
+        // Group g with its staged values in cur and its key words in kc; the
+        // next group's values and key words are read into nxt and kn.  The
+        // request of group g + KDL reuses group g's slot, whose reads have
+        // returned (their words are in av).
+        auto step = [&](int g, BOp& cur, BOp& nxt, uint32_t (&kc)[U::KW], uint32_t (&kn)[U::KW])
+            __attribute__((always_inline)) {
+          const FT av = kfrag(kc);
+          if (g + KDL < g1) kdma(g + KDL);
+          if (g + 1 < g1) {
+            bload(g + 1, nxt);
+            kwait(min(KDL - 1, g1 - 2 - g));
+            kread(g + 1, kn);
+          }
+          group(g, av, cur);
+        };
+        for (int g = g0; g < g1; g += 2) {
+          step(g, bb[0], bb[1], kwa, kwb);
+          if (g + 1 < g1) step(g + 1, bb[1], bb[0], kwb, kwa);
+        }
+      } else {
+        uint32_t kw[U::KD][U::KW];
 #pragma unroll
-        for (int u = 0; u < U::KD; ++u) {
-          const int g = gb + u;
-          if (g < g1) {
-            if (g + 1 < g1) bload(g + 1, bb[(u + 1) & 1]);
-            const FT av = kfrag(kw[u]);
-            if (g + U::KD < g1) kload(g + U::KD, kw[u]);
-            group(g, av, bb[u & 1]);
+        for (int u = 0; u < U::KD; ++u)
+          if (g0 + u < g1) kload(g0 + u, kw[u]);
+        bload(g0, bb[0]);
+        for (int gb = g0; gb < g1; gb += U::KD) {
+#pragma unroll
+          for (int u = 0; u < U::KD; ++u) {
+            const int g = gb + u;
+            if (g < g1) {
+              if (g + 1 < g1) bload(g + 1, bb[(u + 1) & 1]);
+              const FT av = kfrag(kw[u]);
+              if (g + U::KD < g1) kload(g + U::KD, kw[u]);
+              group(g, av, bb[u & 1]);
+            }
           }
         }
       }
@@ -742,14 +820,20 @@ static hipError_t launch_update_t(const PrefillArgs& a, const SegPlan& p, int se
   const int nh = a.desc.B * a.desc.H;
   PrefillWS w = ws_layout(a.workspace, nh, a.T, a.desc.C, a.desc.d_k * a.desc.d_v, p.nch);
   const int grid = (int)round_up(nh, 8) * (DV / NC);
-  const size_t shm = update_smem_bytes<DK, Tin>(a.desc.C);
-  if (shm > 160 * 1024) return hipErrorInvalidValue;
-  auto k = prefill_update_kernel<DK, DV, Tin, TS>;
-  if (hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm) !=
-      hipSuccess)
-    return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k, dim3(grid), dim3(NTHR), shm, s, a, w, p, seg);
-  return hipGetLastError();
+  auto launch = [&](auto k, size_t shm) -> hipError_t {
+    if (shm > 160 * 1024) return hipErrorInvalidValue;
+    if (hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm) !=
+        hipSuccess)
+      return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k, dim3(grid), dim3(NTHR), shm, s, a, w, p, seg);
+    return hipGetLastError();
+  };
+  // keys through LDS for 16-bit inputs when the rings fit beside the rest
+  constexpr bool E2 = sizeof(Tin) == 2;
+  const size_t shm_kl = update_smem_bytes<DK, Tin, E2>(a.desc.C);
+  if (E2 && shm_kl <= 160 * 1024) return launch(prefill_update_kernel<DK, DV, Tin, TS, E2>, shm_kl);
+  return launch(prefill_update_kernel<DK, DV, Tin, TS, false>,
+                update_smem_bytes<DK, Tin, false>(a.desc.C));
 }
 
 template <int DK, int DV>
@@ -765,10 +849,10 @@ static hipError_t launch_update_dims(const PrefillArgs& a, const SegPlan& p, int
 
 bool prefill_update_supported(const dla_cache_desc& d, dla_dtype in_dtype) {
   const bool f = in_dtype == DLA_F32;
-  const size_t b = d.d_k == 128 ? (f ? update_smem_bytes<128, float>(d.C)
-                                     : update_smem_bytes<128, bf16_t>(d.C))
-                                : (f ? update_smem_bytes<64, float>(d.C)
-                                     : update_smem_bytes<64, bf16_t>(d.C));
+  const size_t b = d.d_k == 128 ? (f ? update_smem_bytes<128, float, false>(d.C)
+                                     : update_smem_bytes<128, bf16_t, false>(d.C))
+                                : (f ? update_smem_bytes<64, float, false>(d.C)
+                                     : update_smem_bytes<64, bf16_t, false>(d.C));
   return b <= 160 * 1024;
 }
 
