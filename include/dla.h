@@ -322,18 +322,36 @@ dla_status dla_decode_step_delta(const dla_cache_desc* desc, void* cache, const 
                                  const int8_t* boundary_override, const int32_t* merge_override,
                                  void* stream);
 
-/* T tokens per head in the Gated DeltaNet form: the arrays of dla_prefill
- * ([B][H][T][d] tokens, [B][H][T] log_gate, beta, exports and overrides,
- * [B][H][T][C] lambda), run as T decode steps enqueued on `stream` (one token
- * of every head per step; no workspace).  A chunked form of this prefill is
- * not built: it costs one or two kernel launches per token. */
+/*
+ * Workspace of dla_prefill_delta for T tokens per head (same meaning of flags
+ * as dla_prefill_workspace_size: DLA_SKIP_READOUT, DLA_POOL_BUDGET_LOG2).
+ */
+dla_status dla_prefill_delta_workspace_size(const dla_cache_desc* desc, int32_t T,
+                                            dla_dtype in_dtype, uint32_t flags, size_t* bytes);
+
+/*
+ * T tokens per head in the Gated DeltaNet form (the rule of
+ * dla_decode_step_delta), with the arrays of dla_prefill ([B][H][T][d] tokens,
+ * [B][H][T] log_gate, beta, exports and overrides, [B][H][T][C] lambda).
+ * A token that joins the newest state adds k_t u_t^T to the decayed state,
+ * with pseudo-value u_t = beta_t (v_t - (alpha_t S)^T k_t); a token that opens
+ * one starts it at k_t (beta_t v_t)^T.  Every state is therefore the decayed
+ * sum of k_s u_s^T over its tokens: a sequential scan (one workgroup per head,
+ * the newest state on chip) makes the decisions and the pseudo-values, and the
+ * chunked update and readout stages of dla_prefill run on (q, k, u, lambda) in
+ * float32 (16-bit inputs are widened into the workspace first).  Stages run
+ * in order on `stream`; the workspace (dla_prefill_delta_workspace_size bytes,
+ * 256-byte aligned, caller-owned) must not be used by another call until the
+ * stream has passed this one.  Errors as dla_prefill; DLA_ERR_UNSUPPORTED
+ * where the float32 stages do not fit.
+ */
 dla_status dla_prefill_delta(const dla_cache_desc* desc, void* cache, const void* q, const void* k,
                              const void* v, const float* log_gate, const float* beta,
                              const void* lambda, int32_t T, dla_dtype in_dtype,
                              const dla_params* params, void* out, dla_dtype out_dtype,
                              int8_t* boundary, int32_t* merge_idx, float* score,
                              const int8_t* boundary_override, const int32_t* merge_override,
-                             void* stream);
+                             void* workspace, size_t workspace_bytes, void* stream);
 
 const char* dla_status_string(dla_status s);
 dla_status dla_get_last_error(void);

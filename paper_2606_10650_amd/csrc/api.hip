@@ -432,30 +432,72 @@ dla_status dla_decode_step_delta(const dla_cache_desc* desc, void* cache, const 
                          1, stream));
 }
 
+dla_status dla_prefill_delta_workspace_size(const dla_cache_desc* desc, int32_t T,
+                                            dla_dtype in_dtype, uint32_t flags, size_t* bytes) {
+  dla_status s = check_desc(desc);
+  if (s != DLA_OK) return ret(s);
+  const size_t budget = pool_budget_of(flags);
+  if (!bytes || T < 0 || !dtype_ok(in_dtype) || !budget) return ret(DLA_ERR_INVALID_ARG);
+  *bytes = prefill_delta_workspace_bytes(*desc, T, in_dtype, (flags & DLA_SKIP_READOUT) == 0, budget);
+  return ret(DLA_OK);
+}
+
 dla_status dla_prefill_delta(const dla_cache_desc* desc, void* cache, const void* q, const void* k,
                              const void* v, const float* log_gate, const float* beta,
                              const void* lambda, int32_t T, dla_dtype in_dtype,
                              const dla_params* params, void* out, dla_dtype out_dtype,
                              int8_t* boundary, int32_t* merge_idx, float* score,
                              const int8_t* boundary_override, const int32_t* merge_override,
-                             void* stream) {
-  dla_status s = decode_check(desc, cache, q, k, v, log_gate, in_dtype, params, out, out_dtype);
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  dla_status s = check_desc(desc);
   if (s != DLA_OK) return ret(s);
-  if (!beta || T < 0) return ret(DLA_ERR_INVALID_ARG);
-  const size_t ei = dtype_bytes(in_dtype), eo = dtype_bytes(out_dtype);
-  const size_t dk = desc->d_k, dv = desc->d_v, C = desc->C;
-  auto at = [](const void* p, size_t off) -> const void* {
-    return p ? static_cast<const char*>(p) + off : nullptr;
-  };
-  for (int32_t t = 0; t < T; ++t) {
-    s = decode_impl(desc, cache, at(q, t * dk * ei), at(k, t * dk * ei), at(v, t * dv * ei),
-                    log_gate + t, beta + t, at(lambda, t * C * ei), in_dtype, params,
-                    out ? static_cast<char*>(out) + t * dv * eo : nullptr, out_dtype,
-                    boundary ? boundary + t : nullptr, merge_idx ? merge_idx + t : nullptr,
-                    score ? score + t : nullptr, boundary_override ? boundary_override + t : nullptr,
-                    merge_override ? merge_override + t : nullptr, T, stream);
-    if (s != DLA_OK) return ret(s);
-  }
+  if (!params || T < 0 || !dtype_ok(in_dtype) || !dtype_ok(out_dtype)) return ret(DLA_ERR_INVALID_ARG);
+  const bool skip = (params->flags & DLA_SKIP_READOUT) != 0;
+  if (!cache || !k || !v || !log_gate || !beta) return ret(DLA_ERR_INVALID_ARG);
+  if (!skip && (!q || !out)) return ret(DLA_ERR_INVALID_ARG);
+  if (T == 0) return ret(DLA_OK);
+  // the float32 update and readout stages, and the sequential scan's LDS
+  if (!prefill_chunks_supported(*desc, DLA_F32) || prefill_delta_scan_smem(*desc) > 160 * 1024)
+    return ret(DLA_ERR_UNSUPPORTED);
+  if ((int64_t)desc->B * desc->H * (int64_t)T * (desc->C > 128 ? desc->C : 128) >
+      ((int64_t)1 << 40))
+    return ret(DLA_ERR_UNSUPPORTED);
+  const size_t budget = pool_budget_of(params->flags);
+  if (!budget) return ret(DLA_ERR_INVALID_ARG);
+  const size_t need = prefill_delta_workspace_bytes(*desc, T, in_dtype, !skip, budget);
+  if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 255u))
+    return ret(DLA_ERR_WORKSPACE);
+  PrefillArgs a;
+  memset(&a, 0, sizeof(a));
+  const dla_cache_layout L = layout_of(*desc);
+  a.desc = *desc;
+  a.cache = (char*)cache;
+  a.meta_offset = L.meta_offset;
+  a.meta_stride = L.meta_stride;
+  a.states_offset = L.states_offset;
+  a.open_offset = L.open_offset;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.g = log_gate;
+  a.lam = lambda;
+  a.out = skip ? nullptr : out;
+  a.b_out = boundary;
+  a.merge_out = merge_idx;
+  a.score_out = score;
+  a.b_ovr = boundary_override;
+  a.m_ovr = merge_override;
+  a.T = T;
+  a.tau = params->tau;
+  a.eps = params->eps;
+  a.eps_rms = params->eps_rms;
+  a.skip_readout = skip ? 1 : 0;
+  a.in_dtype = in_dtype;
+  a.out_dtype = out_dtype;
+  a.serial = 1;
+  a.pool_budget = budget;
+  a.workspace = (char*)workspace;
+  if (launch_prefill_delta(a, beta, (hipStream_t)stream) != hipSuccess) return ret(DLA_ERR_HIP);
   return ret(DLA_OK);
 }
 

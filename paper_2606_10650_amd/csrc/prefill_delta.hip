@@ -1,0 +1,420 @@
+// Prefill in the Gated DeltaNet form of the layer (Sec. 2.2, eq. delta_rule_rnn,
+// with the decisions and merges of Sec. 3.1-3.2).
+//
+// With every state decayed by alpha_t = exp(g_t) first, a token that joins the
+// newest state S takes the delta rule
+//   S <- (I - beta_t k_t k_t^T) alpha_t S + beta_t k_t v_t^T
+//      = alpha_t S + k_t u_t^T,   u_t = beta_t (v_t - (alpha_t S)^T k_t),
+// and a token that opens a state starts it at beta_t k_t v_t^T, i.e. u_t =
+// beta_t v_t.  So every state is the same decayed sum of rank-one terms k_s
+// u_s^T over its tokens as the gated form with v_s replaced by u_s, and once the
+// pseudo-values u_s are known the chunked update and readout stages apply
+// unchanged.  The pseudo-values depend on the newest state before each token,
+// which depends on every earlier decision, so they come from a sequential scan
+// that keeps the newest state on chip: one 256-thread workgroup per head, each
+// thread holding a (d_k / 16) x (d_v / 16) block of the state in registers.
+// Per token it forms y = (alpha S)^T k and the score's three scalars (a =
+// |k|^2 |v|^2, b = |alpha S|^2, c = y . v), decides (Alg. 1, with Alg. 2 at a
+// full cache), and applies the rank-one step with u.  It emits the decisions,
+// scores and merge indices, the death token of every state leader (the same
+// bookkeeping as the gated scan), the cache's per-state counts and aggregated
+// scores, and u as float32.
+//
+// The call then runs the float32 update and readout stages over (q, k, u,
+// lambda), with float32 copies of 16-bit inputs made first.
+#include "prefill.h"
+
+namespace dla {
+
+constexpr int DTHR = 256;  // threads of the delta scan (4 waves)
+constexpr int DSL = 64;    // tokens staged in LDS per round
+
+template <int DK, int DV>
+struct DeltaP {
+  static constexpr int RB = DK / 16;  // state rows per thread
+  static constexpr int CB = DV / 16;  // state columns per thread
+  static size_t smem_bytes(int C) {
+    size_t off = (size_t)DSL * (DK + DV) * 4;  // sK, sV
+    off += (size_t)DSL * 4 * 5;                 // sAl, sBeta, sA, sBo, sMo
+    off += (size_t)(4 + 1) * DV * 4;            // sY, sU
+    off += 16 * 4;                              // sRed
+    off = round_up(off, 8);
+    off += (size_t)C * 8;                       // sIb
+    off += (size_t)C * 4 * 2;                   // sN, sLead
+    return round_up(off, 16);
+  }
+};
+
+template <int DK, int DV, typename Tin>
+__global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a, PrefillWS w,
+                                                                  const float* __restrict__ beta,
+                                                                  float* __restrict__ U) {
+  if (!cache_matches(a.cache, a.desc)) return;  // refused call (see the prep kernel)
+  using P = DeltaP<DK, DV>;
+  constexpr int RB = P::RB, CB = P::CB;
+  constexpr int D = DK * DV;
+  const int h = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wv = tid >> 6;
+  const int rb = tid >> 4;  // row block of the thread's state block
+  const int cb = tid & 15;  // column block
+  const int C = a.desc.C;
+  const int T = a.T;
+  const size_t tok0 = (size_t)h * T;
+
+  extern __shared__ __align__(16) char smem[];
+  float* sK = reinterpret_cast<float*>(smem);  // [DSL][DK]
+  float* sV = sK + DSL * DK;                   // [DSL][DV]
+  float* sAl = sV + DSL * DV;                  // alpha_t
+  float* sBeta = sAl + DSL;
+  float* sA = sBeta + DSL;                     // |k|^2 |v|^2
+  int32_t* sBo = reinterpret_cast<int32_t*>(sA + DSL);
+  int32_t* sMo = sBo + DSL;
+  float* sY = reinterpret_cast<float*>(sMo + DSL);  // [4 waves][DV] partial y
+  float* sU = sY + 4 * DV;                          // [DV] pseudo-values
+  float* sRed = sU + DV;                            // [16]
+  double* sIb = reinterpret_cast<double*>(smem + round_up((size_t)((char*)(sRed + 16) - smem), 8));
+  int32_t* sN = reinterpret_cast<int32_t*>(sIb + C);
+  int32_t* sLead = sN + C;
+
+  Meta M = meta_at(a.cache + a.meta_offset + (size_t)h * a.meta_stride, C);
+  InitView iv = init_at(w, h, C);
+  const int m0 = min(max(*iv.m0, 0), C);
+  for (int j = tid; j < C; j += DTHR) {
+    sIb[j] = j < m0 ? M.ibar[j] : 0.0;
+    sN[j] = j < m0 ? M.n[j] : 0;
+    sLead[j] = j - m0;  // states present before the call: negative leaders
+  }
+  // the newest state at the start of the call, true (decayed) values
+  float S[RB][CB];
+#pragma unroll
+  for (int i = 0; i < RB; ++i)
+#pragma unroll
+    for (int j = 0; j < CB; ++j) S[i][j] = 0.f;
+  if (m0 > 0) {
+    const float* src =
+        a.desc.state_dtype == DLA_BF16
+            ? reinterpret_cast<const float*>(a.cache + a.open_offset) + (size_t)h * D
+            : reinterpret_cast<const float*>(a.cache + a.states_offset) +
+                  ((size_t)h * C + min(max(M.perm[m0 - 1], 0), C - 1)) * D;
+    const float f = (float)exp(*M.G - M.F[m0 - 1]);
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+#pragma unroll
+      for (int j = 0; j < CB; ++j) S[i][j] = f * src[(size_t)(rb * RB + i) * DV + cb * CB + j];
+  }
+  int m = m0;
+
+  const Tin* Kin = static_cast<const Tin*>(a.k) + tok0 * DK;
+  const Tin* Vin = static_cast<const Tin*>(a.v) + tok0 * DV;
+  const float* g = a.g + tok0;
+  const float* bt = beta + tok0;
+  int32_t* death = w.death + tok0;
+  float* Uh = U + tok0 * DV;
+
+  for (int c0 = 0; c0 < T; c0 += DSL) {
+    const int nr = min(DSL, T - c0);
+    __syncthreads();  // the previous round is done with the staged tokens
+    for (int i = tid; i < nr * DK; i += DTHR) sK[i] = to_f32(Kin[(size_t)c0 * DK + i]);
+    for (int i = tid; i < nr * DV; i += DTHR) sV[i] = to_f32(Vin[(size_t)c0 * DV + i]);
+    for (int t = tid; t < nr; t += DTHR) {
+      sAl[t] = __expf(g[c0 + t]);
+      sBeta[t] = bt[c0 + t];
+      sBo[t] = a.b_ovr ? (int)a.b_ovr[tok0 + c0 + t] : -1;
+      sMo[t] = a.m_ovr ? a.m_ovr[tok0 + c0 + t] : -1;
+    }
+    __syncthreads();
+    // a_t = |k_t|^2 |v_t|^2, one wave per token
+    for (int t = wv; t < nr; t += 4) {
+      float kk = 0.f, vv = 0.f;
+      for (int i = lane; i < DK; i += 64) kk += sK[t * DK + i] * sK[t * DK + i];
+      for (int i = lane; i < DV; i += 64) vv += sV[t * DV + i] * sV[t * DV + i];
+      kk = wave_sum(kk);
+      vv = wave_sum(vv);
+      if (lane == 0) sA[t] = kk * vv;
+    }
+    __syncthreads();
+
+    for (int tt = 0; tt < nr; ++tt) {
+      const int t = c0 + tt;
+      const float al = sAl[tt];
+      float kr[RB];
+#pragma unroll
+      for (int i = 0; i < RB; ++i) kr[i] = sK[tt * DK + rb * RB + i];
+      // decay, the block's share of y = S^T k, and of |S|^2
+      float yp[CB];
+#pragma unroll
+      for (int j = 0; j < CB; ++j) yp[j] = 0.f;
+      float bp = 0.f;
+#pragma unroll
+      for (int i = 0; i < RB; ++i)
+#pragma unroll
+        for (int j = 0; j < CB; ++j) {
+          S[i][j] *= al;
+          yp[j] += kr[i] * S[i][j];
+          bp += S[i][j] * S[i][j];
+        }
+      // the wave's four row blocks (lanes 16 apart), then the four waves
+#pragma unroll
+      for (int j = 0; j < CB; ++j) {
+        yp[j] += __shfl_xor(yp[j], 16, 64);
+        yp[j] += __shfl_xor(yp[j], 32, 64);
+      }
+      bp = wave_sum(bp);
+      if (lane < 16) {
+#pragma unroll
+        for (int j = 0; j < CB; ++j) sY[wv * DV + cb * CB + j] = yp[j];
+      }
+      if (lane == 0) sRed[wv] = bp;
+      __syncthreads();
+      float yj = 0.f, cj = 0.f;
+      if (tid < DV) {
+        yj = (sY[tid] + sY[DV + tid]) + (sY[2 * DV + tid] + sY[3 * DV + tid]);
+        cj = yj * sV[tt * DV + tid];
+      }
+      cj = wave_sum(cj);
+      if (lane == 0) sRed[4 + wv] = cj;
+      __syncthreads();
+      const double b = ((double)sRed[0] + sRed[1]) + ((double)sRed[2] + sRed[3]);
+      const double c = ((double)sRed[4] + sRed[5]) + ((double)sRed[6] + sRed[7]);
+      // the decision, identical in every thread
+      int bd;
+      float It;
+      if (m == 0) {  // the first token of an empty cache opens a state with score 0
+        bd = 1;
+        It = 0.f;
+      } else {
+        It = (float)info_score((double)sA[tt], b, c, (double)D, a.eps, a.eps_rms);
+        bd = (It >= a.tau) ? 1 : 0;
+        if (sBo[tt] != -1) bd = sBo[tt] ? 1 : 0;
+        if (C == 1) bd = 0;
+      }
+      if (bd) {
+        int istar = -1;
+        if (m == C) {
+          // Alg. 2 on wave 0: the adjacent pair of lowest density, ties to the
+          // lowest index (the gated scan's rules, overrides included)
+          if (wv == 0) {
+            double best = INFINITY;
+            int bi = 0x7fffffff;
+            for (int i = lane; i + 1 < C; i += 64) {
+              const double d = (sIb[i] + sIb[i + 1]) / (double)(sN[i] + sN[i + 1]);
+              if (d < best) {
+                best = d;
+                bi = i;
+              }
+            }
+            wave_argmin_d(best, bi);
+            istar = (bi >= 0 && bi <= C - 2) ? bi : 0;
+            if (__builtin_isnan((sIb[0] + sIb[1]) / (double)(sN[0] + sN[1]))) istar = 0;
+            const int fo = sMo[tt];
+            if (fo != -1) {
+              if (fo >= 0 && fo <= C - 2)
+                istar = fo;
+              else if (lane == 0)
+                atomicOr(&reinterpret_cast<CacheHeader*>(a.cache)->flags,
+                         DLA_FLAG_BAD_MERGE_OVERRIDE);
+            }
+            // the right state of the pair dies at token t
+            const int ld = sLead[istar + 1];
+            if (lane == 0) {
+              if (ld >= 0)
+                death[ld] = t;
+              else
+                iv.death0[ld + m0] = t;
+            }
+            for (int j0 = istar; j0 + 1 < m; j0 += 64) {
+              const int j = j0 + lane;
+              const bool act = j + 1 < m;
+              double nI = 0.0;
+              int nN = 0, nL = 0;
+              if (act) {
+                nI = (j == istar) ? sIb[j] + sIb[j + 1] : sIb[j + 1];
+                nN = (j == istar) ? sN[j] + sN[j + 1] : sN[j + 1];
+                nL = (j == istar) ? sLead[j] : sLead[j + 1];
+              }
+              __builtin_amdgcn_wave_barrier();
+              if (act) {
+                sIb[j] = nI;
+                sN[j] = nN;
+                sLead[j] = nL;
+              }
+              __builtin_amdgcn_wave_barrier();
+            }
+          }
+          m -= 1;
+        }
+        if (tid == 0) {
+          sN[m] = 1;
+          sIb[m] = (double)It;
+          sLead[m] = t;
+          death[t] = T;
+          if (a.b_out) a.b_out[tok0 + t] = 1;
+          if (a.merge_out) a.merge_out[tok0 + t] = istar;
+          if (a.score_out) a.score_out[tok0 + t] = It;
+        }
+        m += 1;
+      } else {
+        if (tid == 0) {
+          sN[m - 1] += 1;
+          sIb[m - 1] += (double)It;
+          death[t] = -1;
+          if (a.b_out) a.b_out[tok0 + t] = 0;
+          if (a.merge_out) a.merge_out[tok0 + t] = -1;
+          if (a.score_out) a.score_out[tok0 + t] = It;
+        }
+      }
+      // pseudo-values, then the rank-one step (a new state starts from zero)
+      if (tid < DV) {
+        const float u = sBeta[tt] * (sV[tt * DV + tid] - (bd ? 0.f : yj));
+        sU[tid] = u;
+        Uh[(size_t)t * DV + tid] = u;
+      }
+      __syncthreads();
+      float uc[CB];
+#pragma unroll
+      for (int j = 0; j < CB; ++j) uc[j] = sU[cb * CB + j];
+#pragma unroll
+      for (int i = 0; i < RB; ++i)
+#pragma unroll
+        for (int j = 0; j < CB; ++j) S[i][j] = (bd ? 0.f : S[i][j]) + kr[i] * uc[j];
+    }
+  }
+  __syncthreads();
+  for (int j = tid; j < m; j += DTHR) {
+    M.n[j] = sN[j];
+    M.ibar[j] = sIb[j];
+  }
+}
+
+// float32 copy of n 16-bit values
+__global__ __launch_bounds__(256) void widen_kernel(const bf16_t* __restrict__ src,
+                                                    float* __restrict__ dst, size_t n) {
+  const size_t stride = (size_t)gridDim.x * 256 * 4;
+  for (size_t i = ((size_t)blockIdx.x * 256 + threadIdx.x) * 4; i < n; i += stride) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (i + e < n) dst[i + e] = to_f32(src[i + e]);
+  }
+}
+
+template <int DK, int DV>
+static size_t delta_smem(int C) {
+  return DeltaP<DK, DV>::smem_bytes(C);
+}
+
+size_t prefill_delta_scan_smem(const dla_cache_desc& d) {
+  if (d.d_k == 128 && d.d_v == 128) return delta_smem<128, 128>(d.C);
+  if (d.d_k == 64 && d.d_v == 64) return delta_smem<64, 64>(d.C);
+  if (d.d_k == 128 && d.d_v == 64) return delta_smem<128, 64>(d.C);
+  return delta_smem<64, 128>(d.C);
+}
+
+template <int DK, int DV, typename Tin>
+static hipError_t launch_delta_scan_t(const PrefillArgs& a, const PrefillWS& w, const float* beta,
+                                      float* U, hipStream_t s) {
+  const size_t shm = DeltaP<DK, DV>::smem_bytes(a.desc.C);
+  if (shm > 160 * 1024) return hipErrorInvalidValue;
+  auto k = prefill_delta_scan_kernel<DK, DV, Tin>;
+  if (hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm) !=
+      hipSuccess)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k, dim3(a.desc.B * a.desc.H), dim3(DTHR), shm, s, a, w, beta, U);
+  return hipGetLastError();
+}
+
+template <int DK, int DV>
+static hipError_t launch_delta_scan_dims(const PrefillArgs& a, const PrefillWS& w,
+                                         const float* beta, float* U, hipStream_t s) {
+  if (a.in_dtype == DLA_F32) return launch_delta_scan_t<DK, DV, float>(a, w, beta, U, s);
+  return launch_delta_scan_t<DK, DV, bf16_t>(a, w, beta, U, s);
+}
+
+static hipError_t widen(const void* src, float* dst, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const size_t blocks = (n + 1023) / 1024;
+  hipLaunchKernelGGL(widen_kernel, dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(256), 0, s,
+                     static_cast<const bf16_t*>(src), dst, n);
+  return hipGetLastError();
+}
+
+// Workspace of a delta-form prefill: the float32 stages' workspace (serial),
+// then the pseudo-values, then float32 copies of q, k and lambda for 16-bit
+// inputs.
+struct DeltaWS {
+  size_t stages, u, q, k, lam, total;
+};
+
+static DeltaWS delta_ws(const dla_cache_desc& d, int T, dla_dtype in, bool readout, size_t budget) {
+  DeltaWS r;
+  const size_t nh = (size_t)d.B * d.H;
+  const bool wide = in != DLA_F32;
+  r.stages = 0;
+  size_t off = round_up(prefill_workspace_bytes(d, T, DLA_F32, readout, true, budget), 256);
+  r.u = off;
+  off = round_up(off + nh * T * d.d_v * 4, 256);
+  r.q = off;
+  off = round_up(off + (wide && readout ? nh * T * d.d_k * 4 : 0), 256);
+  r.k = off;
+  off = round_up(off + (wide ? nh * T * d.d_k * 4 : 0), 256);
+  r.lam = off;
+  off = round_up(off + (wide && readout ? nh * T * d.C * 4 : 0), 256);
+  r.total = off;
+  return r;
+}
+
+size_t prefill_delta_workspace_bytes(const dla_cache_desc& d, int T, dla_dtype in, bool readout,
+                                     size_t budget) {
+  return delta_ws(d, T, in, readout, budget).total;
+}
+
+hipError_t launch_prefill_delta(const PrefillArgs& a, const float* beta, hipStream_t s) {
+  const bool readout = !a.skip_readout;
+  const DeltaWS L = delta_ws(a.desc, a.T, a.in_dtype, readout, a.pool_budget);
+  const size_t nh = (size_t)a.desc.B * a.desc.H;
+  char* base = a.workspace;
+  float* U = reinterpret_cast<float*>(base + L.u);
+  // the float32 stages: q, k and lambda widened, u for the values
+  PrefillArgs f = a;
+  f.in_dtype = DLA_F32;
+  f.serial = 1;
+  f.v = U;
+  hipError_t e;
+  if (a.in_dtype != DLA_F32) {
+    float* kf = reinterpret_cast<float*>(base + L.k);
+    if ((e = widen(a.k, kf, nh * a.T * a.desc.d_k, s)) != hipSuccess) return e;
+    f.k = kf;
+    if (readout) {
+      float* qf = reinterpret_cast<float*>(base + L.q);
+      if ((e = widen(a.q, qf, nh * a.T * a.desc.d_k, s)) != hipSuccess) return e;
+      f.q = qf;
+      if (a.lam) {
+        float* lf = reinterpret_cast<float*>(base + L.lam);
+        if ((e = widen(a.lam, lf, nh * a.T * a.desc.C, s)) != hipSuccess) return e;
+        f.lam = lf;
+      }
+    }
+  }
+  const SegPlan p = seg_plan(a.desc, a.T, DLA_F32, readout, true, a.pool_budget);
+  const PrefillWS w = ws_layout(base, nh, a.T, a.desc.C, a.desc.d_k * a.desc.d_v, p.nch);
+  if ((e = launch_prefill_prep(f, s)) != hipSuccess) return e;
+  const int dk = a.desc.d_k, dv = a.desc.d_v;
+  // (the scan reads the keys and values in the caller's type)
+  if (dk == 128 && dv == 128)
+    e = launch_delta_scan_dims<128, 128>(a, w, beta, U, s);
+  else if (dk == 64 && dv == 64)
+    e = launch_delta_scan_dims<64, 64>(a, w, beta, U, s);
+  else if (dk == 128 && dv == 64)
+    e = launch_delta_scan_dims<128, 64>(a, w, beta, U, s);
+  else
+    e = launch_delta_scan_dims<64, 128>(a, w, beta, U, s);
+  if (e != hipSuccess) return e;
+  for (int seg = 0; seg < p.nseg; ++seg) {
+    if ((e = launch_prefill_update(f, p, seg, s)) != hipSuccess) return e;
+    if (readout && (e = launch_prefill_readout(f, p, seg, s)) != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace dla

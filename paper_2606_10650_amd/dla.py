@@ -28,7 +28,7 @@ DLA_FLAG_CACHE_MISMATCH = 2
 EXPORTED = ("dla_cache_layout_of", "dla_state_cache_alloc", "dla_cache_flags",
             "dla_cache_header_check", "dla_prefill_workspace_size", "dla_prefill_segment_count",
             "dla_prefill_segment_starts", "dla_prefill", "dla_prefill_static", "dla_decode_step",
-            "dla_decode_step_delta", "dla_prefill_delta",
+            "dla_decode_step_delta", "dla_prefill_delta_workspace_size", "dla_prefill_delta",
             "dla_status_string", "dla_get_last_error", "dla_peak_mfma_bf16", "dla_peak_hbm_read")
 STATIC_SCRATCH_BYTES = 128 << 20   # DLA_STATIC_SCRATCH_BYTES
 
@@ -93,9 +93,12 @@ def lib():
                                       ctypes.POINTER(Params), P, I, P, P, P, P, P, P]
         L.dla_decode_step_delta.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, P, I,
                                             ctypes.POINTER(Params), P, I, P, P, P, P, P, P]
+        L.dla_prefill_delta_workspace_size.argtypes = [ctypes.POINTER(CacheDesc), ctypes.c_int32,
+                                                       I, ctypes.c_uint32,
+                                                       ctypes.POINTER(ctypes.c_size_t)]
         L.dla_prefill_delta.argtypes = [ctypes.POINTER(CacheDesc), P, P, P, P, P, P, P,
                                         ctypes.c_int32, I, ctypes.POINTER(Params), P, I, P, P, P,
-                                        P, P, P]
+                                        P, P, P, ctypes.c_size_t, P]
         L.dla_peak_mfma_bf16.argtypes = [ctypes.c_int32, ctypes.c_int32, P, P]
         L.dla_peak_hbm_read.argtypes = [P, ctypes.c_size_t, ctypes.c_int32, P, P]
         L.dla_status_string.argtypes = [I]
@@ -105,7 +108,7 @@ def lib():
                      "dla_cache_header_check", "dla_prefill_workspace_size",
                      "dla_prefill_segment_count", "dla_prefill_segment_starts", "dla_prefill",
                      "dla_prefill_static", "dla_decode_step", "dla_decode_step_delta",
-                     "dla_prefill_delta", "dla_get_last_error",
+                     "dla_prefill_delta_workspace_size", "dla_prefill_delta", "dla_get_last_error",
                      "dla_peak_mfma_bf16", "dla_peak_hbm_read"):
             getattr(L, name).restype = I
         _lib = L
@@ -225,6 +228,18 @@ def workspace_bytes(cache: StateCache, T: int, dtype=None, skip_readout: bool = 
     _check(lib().dla_prefill_workspace_size(ctypes.byref(cache.desc), int(T), code,
                                             _flags(skip_readout, serial, pool_budget_log2),
                                             ctypes.byref(n)), "dla_prefill_workspace_size")
+    return int(n.value)
+
+
+def delta_workspace_bytes(cache: StateCache, T: int, dtype=None, skip_readout: bool = False,
+                          pool_budget_log2: int = 0) -> int:
+    """dla_prefill_delta workspace for T tokens of input dtype (default bf16)."""
+    code = DLA_BF16 if dtype is None else _dtype_code(dtype)
+    n = ctypes.c_size_t(0)
+    _check(lib().dla_prefill_delta_workspace_size(ctypes.byref(cache.desc), int(T), code,
+                                                  _flags(skip_readout, False, pool_budget_log2),
+                                                  ctypes.byref(n)),
+           "dla_prefill_delta_workspace_size")
     return int(n.value)
 
 
@@ -422,9 +437,11 @@ def decode_step_delta(cache: StateCache, q, k, v, g, beta, lam=None, *, tau: flo
 def prefill_delta(cache: StateCache, q, k, v, g, beta, lam=None, *, tau: float = 0.5,
                   eps: float = 1e-6, eps_rms: float = 1e-6, out=None, out_dtype=None,
                   skip_readout: bool = False, boundary=None, merge_idx=None, score=None,
-                  boundary_override=None, merge_override=None, want_exports: bool = True):
-    """dla_prefill_delta: T tokens per head in the Gated DeltaNet form (run as
-    T decode steps).  Shapes as prefill; beta: [B, H, T] float32."""
+                  boundary_override=None, merge_override=None, workspace=None,
+                  want_exports: bool = True, pool_budget_log2: int = 0):
+    """dla_prefill_delta: T tokens per head in the Gated DeltaNet form.  Shapes
+    as prefill; beta: [B, H, T] float32.  The workspace is allocated when none
+    (or one too small) is given."""
     torch = _torch()
     B, H, C = cache.B, cache.H, cache.C
     T = k.shape[2]
@@ -446,13 +463,17 @@ def prefill_delta(cache: StateCache, q, k, v, g, beta, lam=None, *, tau: float =
                                                                         device=dev)
         score = score if score is not None else torch.empty((B, H, T), dtype=torch.float32,
                                                             device=dev)
-    p = _params(tau, eps, eps_rms, skip_readout)
+    wsb = delta_workspace_bytes(cache, T, k.dtype, skip_readout, pool_budget_log2)
+    if workspace is None or workspace.numel() < wsb:
+        workspace = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
+    p = _params(tau, eps, eps_rms, skip_readout, pool_budget_log2=pool_budget_log2)
     st = lib().dla_prefill_delta(ctypes.byref(cache.desc), _ptr(cache.buf), _ptr(q), _ptr(k),
                                  _ptr(v), _ptr(g), _ptr(beta), _ptr(lam), int(T),
                                  _dtype_code(k.dtype), ctypes.byref(p), _ptr(out),
                                  _dtype_code(out.dtype) if out is not None else DLA_F32,
                                  _ptr(boundary), _ptr(merge_idx), _ptr(score),
-                                 _ptr(boundary_override), _ptr(merge_override), _stream(dev))
+                                 _ptr(boundary_override), _ptr(merge_override), _ptr(workspace),
+                                 workspace.numel(), _stream(dev))
     _check(st, "dla_prefill_delta")
     return out, boundary, merge_idx, score
 

@@ -27,7 +27,7 @@ def _oracle(w, x, beta, b_override=None, m_override=None):
                           m_override=m_override, want_mag=True)
 
 
-def _case(w, mode, state_dtype=0, no_lambda=False):
+def _case(w, mode, state_dtype=0, no_lambda=False, pool_budget_log2=0):
     """mode: 'prefill' (dla_prefill_delta) or 'decode' (T steps of
     dla_decode_step_delta)."""
     torch = _torch()
@@ -46,7 +46,8 @@ def _case(w, mode, state_dtype=0, no_lambda=False):
     cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv, state_dtype=state_dtype)
     if mode == "prefill":
         out, b, mi, sc = dla.prefill_delta(cache, q, k, v, g, bt, lam, tau=w.tau,
-                                           boundary_override=bo_d, merge_override=mo_d)
+                                           boundary_override=bo_d, merge_override=mo_d,
+                                           pool_budget_log2=pool_budget_log2)
     else:
         outs, bs, ms, ss = [], [], [], []
         for t in range(w.T):
@@ -102,8 +103,112 @@ def test_delta_bf16_state_storage():
 
 
 def test_delta_one_workgroup_per_head():
-    """1024 heads: the step runs one workgroup per head (no split)."""
+    """1024 heads: the decode step runs one workgroup per head (no split), and
+    the prefill's scan one workgroup per head."""
     from paper_2606_10650_amd import dla
-    w = WORKLOADS["cfg1"].replace(B=64, H=16, T=40, C=4)
+    w = WORKLOADS["cfg1"].replace(B=64, H=16, T=24, C=4)
     assert dla.lib() and w.B * w.H >= 1024
-    _case(w, "prefill")
+    _case(w, "decode")
+    _case(w.replace(T=300), "prefill")
+
+
+def test_delta_prefill_long_bf16():
+    """Spans and bursts over 2600 tokens: many float32 chunks (256 tokens) of
+    the update and readout stages, merges at a full cache of 24."""
+    _case(WORKLOADS["cfg3"].replace(B=1, H=2, T=2600, C=24), "prefill")
+
+
+def test_delta_prefill_long_f32():
+    _case(WORKLOADS["cfg1"].replace(T=1500, n_seg=24, C=8), "prefill")
+
+
+def test_delta_prefill_small_pool_budget():
+    """A state-copy budget of 8 MiB splits the float32 stages into segments of
+    two chunks."""
+    from paper_2606_10650_amd import dla
+    w = WORKLOADS["cfg3"].replace(B=1, H=2, T=2600, C=24)
+    c = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+    assert dla.delta_workspace_bytes(c, w.T, pool_budget_log2=23) < dla.delta_workspace_bytes(c, w.T)
+    _case(w, "prefill", pool_budget_log2=23)
+
+
+def test_delta_prefill_split_then_decode():
+    """Two prefill calls and then decode steps continue one sequence: the
+    second call starts from the cache (and the newest state) the first left,
+    and the steps from the second's, against one oracle run."""
+    torch = _torch()
+    from paper_2606_10650_amd import dla
+    w = WORKLOADS["cfg2"].replace(B=1, H=2, T=900, C=10)
+    T1, T2 = 333, 850
+    x = make_inputs(w)
+    beta = make_beta(w)
+    ref = _oracle(w, x, beta)
+    bo, mo, nb, nm = H.near_tie_overrides(ref, what="delta split")
+    q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    shp = (w.B, w.H, w.T)
+    bt = torch.from_numpy(beta).reshape(shp).cuda()
+    bo_d = torch.from_numpy(bo).reshape(shp).cuda()
+    mo_d = torch.from_numpy(mo).reshape(shp).cuda()
+    cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+    parts = []
+    for a0, a1 in ((0, T1), (T1, T2)):
+        sl = lambda z: z[:, :, a0:a1].contiguous()
+        parts.append(dla.prefill_delta(cache, sl(q), sl(k), sl(v), sl(g), sl(bt), sl(lam),
+                                       tau=w.tau, boundary_override=sl(bo_d),
+                                       merge_override=sl(mo_d)))
+    for t in range(T2, w.T):
+        sl = lambda z: z[:, :, t].contiguous()
+        o, bb, mm, s_ = dla.decode_step_delta(cache, sl(q), sl(k), sl(v), sl(g), sl(bt), sl(lam),
+                                              tau=w.tau, boundary_override=sl(bo_d),
+                                              merge_override=sl(mo_d))
+        parts.append((o.unsqueeze(2), bb.unsqueeze(2), mm.unsqueeze(2), s_.unsqueeze(2)))
+    torch.cuda.synchronize()
+    out, b, mi, sc = (torch.cat([p_[i] for p_ in parts], 2) for i in range(4))
+    nh = w.B * w.H
+    H.assert_decisions(b.cpu().numpy().reshape(nh, -1), mi.cpu().numpy().reshape(nh, -1), ref,
+                       "delta split")
+    rel = H.assert_outputs(out.float().cpu().numpy().reshape(nh, w.T, w.dv), ref["out"],
+                           H.TOL["bf16"], "delta split", mag=ref["mag"], mag_tol=0.0)
+    srel = H.assert_cache(dla.cache_export(cache), ref["cache"], H.STATE_TOL[False],
+                          what="delta split")
+    assert dla.cache_flags(cache) == 0
+    print(f"[delta-ok] split {T1}+{T2 - T1}+{w.T - T2} near={nb}+{nm} max_rel_out={rel:.2e} "
+          f"max_rel_state={srel:.2e}", flush=True)
+
+
+def test_delta_prefill_skip_readout_and_refusals():
+    """SKIP_READOUT builds the same cache; a missing beta, a short workspace
+    and an unaligned one are refused before any work."""
+    torch = _torch()
+    import ctypes
+    from paper_2606_10650_amd import dla
+    w = WORKLOADS["cfg2"].replace(B=1, H=2, T=700, C=8)
+    x = make_inputs(w)
+    beta = make_beta(w)
+    ref = _oracle(w, x, beta)
+    bo, mo, nb, nm = H.near_tie_overrides(ref, what="delta skip")
+    q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    shp = (w.B, w.H, w.T)
+    bt = torch.from_numpy(beta).reshape(shp).cuda()
+    cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+    dla.prefill_delta(cache, None, k, v, g, bt, None, tau=w.tau, skip_readout=True,
+                      boundary_override=torch.from_numpy(bo).reshape(shp).cuda(),
+                      merge_override=torch.from_numpy(mo).reshape(shp).cuda())
+    torch.cuda.synchronize()
+    H.assert_cache(dla.cache_export(cache), ref["cache"], H.STATE_TOL[False], what="delta skip")
+    L = dla.lib()
+    p = dla._params(w.tau, 1e-6, 1e-6, False)
+    need = dla.delta_workspace_bytes(cache, w.T)
+    ws = torch.empty(need + 512, dtype=torch.uint8, device="cuda")
+    out = torch.empty((w.B, w.H, w.T, w.dv), dtype=k.dtype, device="cuda")
+    def call(beta_ptr, wptr, wbytes):
+        return L.dla_prefill_delta(ctypes.byref(cache.desc), dla._ptr(cache.buf), dla._ptr(q),
+                                   dla._ptr(k), dla._ptr(v), dla._ptr(g), beta_ptr, dla._ptr(lam),
+                                   w.T, dla.DLA_BF16, ctypes.byref(p), dla._ptr(out), dla.DLA_BF16,
+                                   None, None, None, None, None, wptr, wbytes, dla._stream(q.device))
+    before = cache.buf.clone()
+    assert call(None, dla._ptr(ws), need) == dla.DLA_ERR_INVALID_ARG
+    assert call(dla._ptr(bt), dla._ptr(ws), need - 1) == dla.DLA_ERR_WORKSPACE
+    assert call(dla._ptr(bt), ctypes.c_void_p(ws.data_ptr() + 128), need) == dla.DLA_ERR_WORKSPACE
+    torch.cuda.synchronize()
+    assert torch.equal(before, cache.buf)
