@@ -259,6 +259,49 @@ def prefill_bench(args, torch, dla, W, steps, warmup, with_events=True, serial_s
     return res
 
 
+def delta_prefill_bench(args, torch, dla, W, steps):
+    """The Gated DeltaNet form of the prefill (dla_prefill_delta) on workload W,
+    step sizes beta ~ U(0.05, 1): ms per call and tokens/s, with the
+    sequential scan's share measured in a skip-readout call."""
+    from paper_2606_10650_amd.workloads import make_prefix_torch
+    t0 = time.time()
+    q, k, v, g, lam = make_prefix_torch(W, "cuda", with_lambda=True)
+    gen = torch.Generator(device="cuda").manual_seed(W.seed + 29)
+    beta = 0.05 + 0.95 * torch.rand((W.B, W.H, W.T), device="cuda", generator=gen)
+    torch.cuda.synchronize()
+    log(f"[bench] delta prefill: {W.label} drawn in {time.time() - t0:.1f}s")
+    cache = dla.cache_alloc(W.B, W.H, W.C, W.dk, W.dv)
+    ws = torch.empty(dla.delta_workspace_bytes(cache, W.T, k.dtype), dtype=torch.uint8,
+                     device="cuda")
+    out = torch.empty((W.B, W.H, W.T, W.dv), dtype=k.dtype, device="cuda")
+
+    def run(skip=False):
+        dla.cache_reset(cache)
+        dla.prefill_delta(cache, None if skip else q, k, v, g, beta, None if skip else lam,
+                          tau=W.tau, out=None if skip else out, skip_readout=skip, workspace=ws,
+                          want_exports=False)
+
+    run()
+    torch.cuda.synchronize()
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    e[0].record()
+    for _ in range(steps):
+        run()
+    e[1].record()
+    e[2].record()
+    run(skip=True)
+    e[3].record()
+    torch.cuda.synchronize()
+    ms = e[0].elapsed_time(e[1]) / steps
+    res = {"workload": f"prefill, Gated DeltaNet form, {W.label}, beta ~ U(0.05, 1)",
+           "ms_per_call": round(ms, 3), "tokens_per_s": round(W.B * W.T / (ms * 1e-3), 1),
+           "ms_without_readout": round(e[2].elapsed_time(e[3]), 3),
+           "workspace_bytes": ws.numel(), "calls": steps}
+    del q, k, v, g, lam, beta, ws, out, cache
+    torch.cuda.empty_cache()
+    return res
+
+
 def decode_bytes(W, m_live, state_dtype_bf16):
     """HBM bytes of one decode step per head on a full cache with a boundary
     and a merge: every live state read once; the merged pair written, with
@@ -613,6 +656,13 @@ def main():
                         "decode_delta_bf16_states"):
                 res[key]["roofline"]["frac_measured_peak"] = frac(res[key]["roofline"]["achieved"],
                                                                   pk["hbm_read_gbs"])
+    if not args.no_others:
+        # the Gated DeltaNet form's prefill on the 4k-token and the 16k-token workloads
+        dp = {}
+        for name in ("cfg2", "cfg3"):
+            dp[name] = delta_prefill_bench(args, torch, dla, WORKLOADS[name], 2)
+            log(f"[bench] delta prefill {name}: {dp[name]}")
+        res["prefill_delta"] = dp
     if not args.no_sweep:
         res["policy_sweep"] = policy_sweep(args, torch, dla)
     if not args.no_cpu_baseline:

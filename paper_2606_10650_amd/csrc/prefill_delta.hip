@@ -11,8 +11,8 @@
 // pseudo-values u_s are known the chunked update and readout stages apply
 // unchanged.  The pseudo-values depend on the newest state before each token,
 // which depends on every earlier decision, so they come from a sequential scan
-// that keeps the newest state on chip: one 256-thread workgroup per head, each
-// thread holding a (d_k / 16) x (d_v / 16) block of the state in registers.
+// that keeps the newest state on chip: one 512-thread workgroup per head, each
+// thread holding a (d_k / 16) x (d_v / 32) block of the state in registers.
 // Per token it forms y = (alpha S)^T k and the score's three scalars (a =
 // |k|^2 |v|^2, b = |alpha S|^2, c = y . v), decides (Alg. 1, with Alg. 2 at a
 // full cache), and applies the rank-one step with u.  It emits the decisions,
@@ -26,18 +26,21 @@
 
 namespace dla {
 
-constexpr int DTHR = 256;  // threads of the delta scan (4 waves)
-constexpr int DSL = 64;    // tokens staged in LDS per round
+constexpr int DTHR = 512;        // threads of the delta scan (256: 10% slower, 1024: 20% slower)
+constexpr int DWAVE = DTHR / 64;
+constexpr int DNCB = DTHR / 16;  // column blocks of the state (16 row blocks)
+constexpr int DSL = 64;          // tokens staged in LDS per round
 
 template <int DK, int DV>
 struct DeltaP {
-  static constexpr int RB = DK / 16;  // state rows per thread
-  static constexpr int CB = DV / 16;  // state columns per thread
+  static constexpr int RB = DK / 16;    // state rows per thread
+  static constexpr int CB = DV / DNCB;  // state columns per thread
+  static_assert(CB >= 1 && CB * DNCB == DV, "column blocks");
   static size_t smem_bytes(int C) {
     size_t off = (size_t)DSL * (DK + DV) * 4;  // sK, sV
     off += (size_t)DSL * 4 * 5;                 // sAl, sBeta, sA, sBo, sMo
-    off += (size_t)(4 + 1) * DV * 4;            // sY, sU
-    off += 16 * 4;                              // sRed
+    off += (size_t)(DWAVE + 1) * DV * 4;        // sY, sU
+    off += 2 * DWAVE * 4;                       // sRed
     off = round_up(off, 8);
     off += (size_t)C * 8;                       // sIb
     off += (size_t)C * 4 * 2;                   // sN, sLead
@@ -57,8 +60,8 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wv = tid >> 6;
-  const int rb = tid >> 4;  // row block of the thread's state block
-  const int cb = tid & 15;  // column block
+  const int rb = tid / DNCB;  // row block of the thread's state block
+  const int cb = tid % DNCB;  // column block
   const int C = a.desc.C;
   const int T = a.T;
   const size_t tok0 = (size_t)h * T;
@@ -71,10 +74,11 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
   float* sA = sBeta + DSL;                     // |k|^2 |v|^2
   int32_t* sBo = reinterpret_cast<int32_t*>(sA + DSL);
   int32_t* sMo = sBo + DSL;
-  float* sY = reinterpret_cast<float*>(sMo + DSL);  // [4 waves][DV] partial y
-  float* sU = sY + 4 * DV;                          // [DV] pseudo-values
-  float* sRed = sU + DV;                            // [16]
-  double* sIb = reinterpret_cast<double*>(smem + round_up((size_t)((char*)(sRed + 16) - smem), 8));
+  float* sY = reinterpret_cast<float*>(sMo + DSL);  // [waves][DV] partial y
+  float* sU = sY + DWAVE * DV;                      // [DV] pseudo-values
+  float* sRed = sU + DV;                            // [2 waves]
+  double* sIb =
+      reinterpret_cast<double*>(smem + round_up((size_t)((char*)(sRed + 2 * DWAVE) - smem), 8));
   int32_t* sN = reinterpret_cast<int32_t*>(sIb + C);
   int32_t* sLead = sN + C;
 
@@ -126,7 +130,7 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
     }
     __syncthreads();
     // a_t = |k_t|^2 |v_t|^2, one wave per token
-    for (int t = wv; t < nr; t += 4) {
+    for (int t = wv; t < nr; t += DWAVE) {
       float kk = 0.f, vv = 0.f;
       for (int i = lane; i < DK; i += 64) kk += sK[t * DK + i] * sK[t * DK + i];
       for (int i = lane; i < DV; i += 64) vv += sV[t * DV + i] * sV[t * DV + i];
@@ -142,7 +146,7 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
       float kr[RB];
 #pragma unroll
       for (int i = 0; i < RB; ++i) kr[i] = sK[tt * DK + rb * RB + i];
-      // decay, the block's share of y = S^T k, and of |S|^2
+      // decay, and the block's shares of y = S^T k, |S|^2 and c = k^T S v
       float yp[CB];
 #pragma unroll
       for (int j = 0; j < CB; ++j) yp[j] = 0.f;
@@ -155,29 +159,36 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
           yp[j] += kr[i] * S[i][j];
           bp += S[i][j] * S[i][j];
         }
-      // the wave's four row blocks (lanes 16 apart), then the four waves
+      float cp = 0.f;
 #pragma unroll
-      for (int j = 0; j < CB; ++j) {
-        yp[j] += __shfl_xor(yp[j], 16, 64);
-        yp[j] += __shfl_xor(yp[j], 32, 64);
-      }
+      for (int j = 0; j < CB; ++j) cp += yp[j] * sV[tt * DV + cb * CB + j];
+      // the wave's row blocks (lanes DNCB apart), then the waves
+#pragma unroll
+      for (int o = DNCB; o < 64; o <<= 1)
+#pragma unroll
+        for (int j = 0; j < CB; ++j) yp[j] += __shfl_xor(yp[j], o, 64);
       bp = wave_sum(bp);
-      if (lane < 16) {
+      cp = wave_sum(cp);
+      if (lane < DNCB) {
 #pragma unroll
         for (int j = 0; j < CB; ++j) sY[wv * DV + cb * CB + j] = yp[j];
       }
-      if (lane == 0) sRed[wv] = bp;
-      __syncthreads();
-      float yj = 0.f, cj = 0.f;
-      if (tid < DV) {
-        yj = (sY[tid] + sY[DV + tid]) + (sY[2 * DV + tid] + sY[3 * DV + tid]);
-        cj = yj * sV[tt * DV + tid];
+      if (lane == 0) {
+        sRed[wv] = bp;
+        sRed[DWAVE + wv] = cp;
       }
-      cj = wave_sum(cj);
-      if (lane == 0) sRed[4 + wv] = cj;
       __syncthreads();
-      const double b = ((double)sRed[0] + sRed[1]) + ((double)sRed[2] + sRed[3]);
-      const double c = ((double)sRed[4] + sRed[5]) + ((double)sRed[6] + sRed[7]);
+      float yj = 0.f;
+      if (tid < DV) {
+#pragma unroll
+        for (int w2 = 0; w2 < DWAVE; ++w2) yj += sY[w2 * DV + tid];
+      }
+      double b = 0.0, c = 0.0;
+#pragma unroll
+      for (int w2 = 0; w2 < DWAVE; ++w2) {
+        b += (double)sRed[w2];
+        c += (double)sRed[DWAVE + w2];
+      }
       // the decision, identical in every thread
       int bd;
       float It;
