@@ -123,8 +123,8 @@ static int run_head(int64_t T, int32_t C, int32_t dk, int32_t dv, const double* 
                     const double* lam, double tau, double eps, double eps_rms, const int8_t* b_ovr,
                     const int32_t* m_ovr, int32_t full, double* out, int8_t* b_out,
                     int32_t* merge_out, double* score_out, int32_t* m_out, double* margin_b,
-                    double* margin_m, double* mag_out, int32_t* cache_m, int64_t* n,
-                    double* ibar, double* S) {
+                    double* margin_m, double* mag_out, double* u_out, int32_t* cache_m,
+                    int64_t* n, double* ibar, double* S) {
   const int64_t D = (int64_t)dk * dv;
   double* s = (double*)malloc(sizeof(double) * (D * 3 + dv));
   double* dens = (double*)malloc(sizeof(double) * (C > 1 ? C : 1));
@@ -183,7 +183,15 @@ static int run_head(int64_t T, int32_t C, int32_t dk, int32_t dv, const double* 
       for (int64_t i = 0; i < D; ++i) So[i] += s[i];
       n[m - 1] += 1;
       ibar[m - 1] += I;
+      /* the newest state took k_t u_t^T: u_t = beta_t (v_t - y), y the
+       * decayed state's S^T k_t (with no beta, u_t = v_t) */
+      if (u_out)
+        for (int32_t c = 0; c < dv; ++c)
+          u_out[t * dv + c] = beta ? beta[t] * (vt[c] - y[c]) : vt[c];
     } else {
+      /* the new state is k_t u_t^T with u_t = beta_t v_t (or v_t) */
+      if (u_out)
+        for (int32_t c = 0; c < dv; ++c) u_out[t * dv + c] = beta ? beta[t] * vt[c] : vt[c];
       if (m == C) {
         /* Alg. 2: lowest-density adjacent pair among the C cached states */
         int32_t best = 0;
@@ -263,7 +271,9 @@ static int run_head(int64_t T, int32_t C, int32_t dk, int32_t dv, const double* 
  * beta [n_heads][T] or NULL (NULL: no delta rule, a token writes s_t);
  * lam [n_heads][T][C] or NULL; overrides [n_heads][T] or NULL (-1 = free);
  * outputs out [n_heads][T][dv]; b_out, merge_out, score_out, m_out, margin_b,
- * margin_m, mag_out [n_heads][T]; each output may be NULL (mag_out is written
+ * margin_m, mag_out [n_heads][T]; u_out [n_heads][T][dv], the vector u_t with
+ * which the token's write is k_t u_t^T (beta_t (v_t - S^T k_t) joining, beta_t
+ * v_t opening; v_t without beta); each output may be NULL (mag_out is written
  * only with out).
  *
  * The cache is read and written: cache_m [n_heads], cache_n and cache_ibar
@@ -280,8 +290,9 @@ int dla_oracle_forward(int64_t n_heads, int64_t T, int32_t C, int32_t dk, int32_
                        double eps_rms, const int8_t* b_ovr, const int32_t* m_ovr, int32_t full,
                        double* out,
                        int8_t* b_out, int32_t* merge_out, double* score_out, int32_t* m_out,
-                       double* margin_b, double* margin_m, double* mag_out, int32_t* cache_m,
-                       int64_t* cache_n, double* cache_ibar, double* cache_S) {
+                       double* margin_b, double* margin_m, double* mag_out, double* u_out,
+                       int32_t* cache_m, int64_t* cache_n, double* cache_ibar,
+                       double* cache_S) {
   if (n_heads < 0 || T < 0 || C < 1 || dk < 1 || dv < 1 || !k || !v || !g || !cache_m ||
       !cache_n || !cache_ibar || !cache_S)
     return ORACLE_BAD_ARG;
@@ -297,7 +308,8 @@ int dla_oracle_forward(int64_t n_heads, int64_t T, int32_t C, int32_t dk, int32_
                      b_out ? b_out + tok : NULL, merge_out ? merge_out + tok : NULL,
                      score_out ? score_out + tok : NULL, m_out ? m_out + tok : NULL,
                      margin_b ? margin_b + tok : NULL, margin_m ? margin_m + tok : NULL,
-                     mag_out ? mag_out + tok : NULL, cache_m + h, cache_n + h * C,
+                     mag_out ? mag_out + tok : NULL, u_out ? u_out + tok * dv : NULL,
+                     cache_m + h, cache_n + h * C,
                      cache_ibar + h * C, cache_S + h * C * D);
     if (r != ORACLE_OK) {
 #pragma omp critical

@@ -42,7 +42,7 @@ def _load(path: Optional[str] = None):
     lib.dla_oracle_forward.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
                                        ctypes.c_int32, ctypes.c_int32, P, P, P, P, P, P,
                                        ctypes.c_double, ctypes.c_double, ctypes.c_double, P, P,
-                                       ctypes.c_int32, P, P, P, P, P, P, P, P, P, P, P, P]
+                                       ctypes.c_int32, P, P, P, P, P, P, P, P, P, P, P, P, P]
     lib.dla_oracle_threads.restype = ctypes.c_int
     if path is None:
         _lib = lib
@@ -76,14 +76,15 @@ def _p(a):
 
 def oracle_forward(k, v, g, C: int, tau: float, *, q=None, lam=None, beta=None, eps: float = 1e-6,
                    eps_rms: float = 1e-6, b_override=None, m_override=None, full: bool = True,
-                   want_out: bool = True, want_mag: bool = False,
+                   want_out: bool = True, want_mag: bool = False, want_u: bool = False,
                    cache: Optional[OracleCache] = None, lib_path: Optional[str] = None):
     """Run the oracle on float64 inputs shaped [n_heads, T, d] (g: [n_heads, T],
     lam: [n_heads, T, C]; beta: [n_heads, T] step sizes of the delta rule, or
     None for the gated form).  Returns a dict with out, b, merge, score, m,
     margin_b, margin_m, mag (with want_mag: the sum over states of |lambda|
-    ||S_j||_F ||q||, which bounds the sizes of the readout's terms; with out)
-    and the final cache.  The cache argument is
+    ||S_j||_F ||q||, which bounds the sizes of the readout's terms; with out),
+    u (with want_u: [n_heads, T, d_v], the vector of each token's write k_t
+    u_t^T) and the final cache.  The cache argument is
     updated in place when given."""
     k = np.ascontiguousarray(k, np.float64)
     v = np.ascontiguousarray(v, np.float64)
@@ -110,6 +111,7 @@ def oracle_forward(k, v, g, C: int, tau: float, *, q=None, lam=None, beta=None, 
         "margin_b": np.zeros((nh, T)),
         "margin_m": np.zeros((nh, T)),
         "mag": np.zeros((nh, T)) if (want_out and want_mag) else None,
+        "u": np.zeros((nh, T, dv)) if want_u else None,
     }
     bo = None if b_override is None else np.ascontiguousarray(b_override, np.int8)
     mo = None if m_override is None else np.ascontiguousarray(m_override, np.int32)
@@ -118,7 +120,8 @@ def oracle_forward(k, v, g, C: int, tau: float, *, q=None, lam=None, beta=None, 
                                 tau, eps,
                                 eps_rms, _p(bo), _p(mo), 1 if full else 0, _p(res["out"]),
                                 _p(res["b"]), _p(res["merge"]), _p(res["score"]), _p(res["m"]),
-                                _p(res["margin_b"]), _p(res["margin_m"]), _p(res["mag"]), _p(cache.m),
+                                _p(res["margin_b"]), _p(res["margin_m"]), _p(res["mag"]),
+                                _p(res["u"]), _p(cache.m),
                                 _p(cache.n), _p(cache.ibar), _p(cache.S))
     if rc != 0:
         raise ValueError(f"oracle error {rc}")

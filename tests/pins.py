@@ -622,6 +622,43 @@ def pin_delta_decisions_mode(lib_path=None):
     assert np.abs(full["score"] - dec["score"]).max() < 1e-12
 
 
+def pin_delta_pseudo_values(lib_path=None):
+    """The exported write vectors u_t (each token adds k_t u_t^T): at C = 1
+    they are beta_t (v_t - (exp(g_t) S_{t-1})^T k_t) of the textbook Gated
+    DeltaNet states (beta_t v_t at the first token); with boundaries and
+    merges, the direct evaluator given u in place of v reproduces the delta
+    recurrence's outputs and final cache in decisions mode too."""
+    from oracle import direct
+    w, q, k, v, g, _, beta = _delta_inputs("cfg1", 120, 1, 17)
+    r = oracle_forward(k, v, g, 1, w.tau, q=q, beta=beta, want_u=True, lib_path=lib_path)
+    for h in range(len(q)):
+        dk, dv = k.shape[2], v.shape[2]
+        S = np.zeros((dk, dv))
+        for t in range(q.shape[1]):
+            want = beta[h, t] * (v[h, t] - (np.exp(g[h, t]) * S).T @ k[h, t])
+            assert np.abs(r["u"][h, t] - want).max() < 1e-12 * max(np.abs(want).max(), 1e-30)
+            A = np.exp(g[h, t]) * (np.eye(dk) - beta[h, t] * np.outer(k[h, t], k[h, t]))
+            S = A @ S + beta[h, t] * np.outer(k[h, t], v[h, t])
+    for name, T, C, kw in (("cfg1", 220, 4, dict(n_seg=14, rho2=0.9)), ("cfg1_iid", 70, 3, {})):
+        w, q, k, v, g, lam, beta = _delta_inputs(name, T, C, 19, **kw)
+        r = oracle_forward(k, v, g, C, w.tau, q=q, lam=lam, beta=beta, want_u=True,
+                           lib_path=lib_path)
+        dec = oracle_forward(k, v, g, C, w.tau, beta=beta, full=False, want_u=True,
+                             lib_path=lib_path)
+        assert np.abs(r["u"] - dec["u"]).max() < 1e-12 * np.abs(r["u"]).max()
+        tokens = [0, 1, T // 3, T // 2 + 1, T - 2, T - 1]
+        for h in range(len(q)):
+            assert (r["merge"][h] >= 0).sum() > 0, "the case must merge"
+            o = direct.outputs_at(q[h], k[h], r["u"][h], g[h], lam[h], r["b"][h], r["merge"][h], C,
+                                  tokens)
+            ref = r["out"][h, tokens]
+            assert np.abs(o - ref).max() < 1e-10 * max(np.abs(ref).max(), 1e-30), (name, h)
+            m, n, S = direct.final_states(k[h], r["u"][h], g[h], r["b"][h], r["merge"][h], C)
+            c = r["cache"]
+            assert m == c.m[h] and (n[:m] == c.n[h, :m]).all(), (name, h)
+            assert np.abs(S[:m] - c.S[h, :m]).max() < 1e-10 * np.abs(c.S[h, :m]).max(), (name, h)
+
+
 ALL_PINS = [
     pin_lambda_one_is_gated_linear_attention,
     pin_single_state_and_one_state_per_token,
@@ -642,4 +679,5 @@ ALL_PINS = [
     pin_delta_zero_step_writes_nothing,
     pin_delta_ranges_and_merges,
     pin_delta_decisions_mode,
+    pin_delta_pseudo_values,
 ]

@@ -212,3 +212,64 @@ def test_delta_prefill_skip_readout_and_refusals():
     assert call(dla._ptr(bt), ctypes.c_void_p(ws.data_ptr() + 128), need) == dla.DLA_ERR_WORKSPACE
     torch.cuda.synchronize()
     assert torch.equal(before, cache.buf)
+
+
+def test_delta_prefill_full_size_sampled_heads():
+    """The delta form at the 16k-token workload's full size (B=4, H=16,
+    T=16384, C=128), the call the benchmark times.  Six heads spread over batch
+    and head: every decision and score, the outputs of four windows and the
+    final cache, against the oracle's decisions mode with its write vectors u
+    and the direct evaluation over them (both pinned to the delta
+    recurrence)."""
+    torch = _torch()
+    from oracle import OracleCache, direct
+    from paper_2606_10650_amd import dla
+    from tests.test_gpu_full_size import spread_heads, windows
+    w = WORKLOADS["cfg3"]
+    nh = w.B * w.H
+    heads = spread_heads(w.B, w.H, 6)
+    x = make_inputs(w)
+    beta = make_beta(w)
+    xs = H.f64({key: x[key][heads] for key in ("q", "k", "v", "lam", "g")}, w)
+    dec = oracle_forward(xs["k"], xs["v"], xs["g"], w.C, w.tau, beta=beta[heads].astype(np.float64),
+                         full=False, want_u=True)
+    bo_s, mo_s, nb, nm = H.near_tie_overrides(dec, what=f"delta {w.label} full size")
+    bo = np.full((nh, w.T), -1, np.int8)
+    mo = np.full((nh, w.T), -1, np.int32)
+    bo[heads], mo[heads] = bo_s, mo_s
+    q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    del x
+    shp = (w.B, w.H, w.T)
+    cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+    out, b, mi, sc = dla.prefill_delta(cache, q, k, v, g, torch.from_numpy(beta).reshape(shp).cuda(),
+                                       lam, tau=w.tau,
+                                       boundary_override=torch.from_numpy(bo).reshape(shp).cuda(),
+                                       merge_override=torch.from_numpy(mo).reshape(shp).cuda())
+    torch.cuda.synchronize()
+    H.assert_decisions(b.cpu().numpy().reshape(nh, w.T)[heads],
+                       mi.cpu().numpy().reshape(nh, w.T)[heads], dec, w.label)
+    serr = np.abs(sc.cpu().numpy().reshape(nh, w.T)[heads] - dec["score"]).max()
+    assert serr < H.DELTA_B / 10, f"score error {serr}"
+    # windows inside a chunk of the float32 stages (256 tokens), across the
+    # start of a later segment, the last segment's first tokens and the end
+    f32_starts = dla.prefill_segment_starts(cache, w.T, torch.float32, serial=True)
+    toks, wins = windows(w.T, 256, f32_starts)
+    og = out.float().reshape(nh, w.T, w.dv)[heads][:, toks].cpu().numpy()
+    del q, k, v, g, lam, out
+    oc = OracleCache.empty(len(heads), w.C, w.dk, w.dv)
+    ref_o = np.zeros((len(heads), len(toks), w.dv))
+    for i in range(len(heads)):
+        u = dec["u"][i]
+        ref_o[i] = direct.outputs_at(xs["q"][i], xs["k"][i], u, xs["g"][i], xs["lam"][i],
+                                     dec["b"][i], dec["merge"][i], w.C, toks)
+        m, n, S = direct.final_states(xs["k"][i], u, xs["g"][i], dec["b"][i], dec["merge"][i], w.C)
+        assert m == dec["cache"].m[i] and (n[:m] == dec["cache"].n[i, :m]).all()
+        oc.m[i], oc.n[i], oc.S[i] = m, n, S
+        oc.ibar[i] = dec["cache"].ibar[i]
+    rel = H.assert_outputs(og, ref_o, H.TOL[w.dtype], f"delta {w.label} windows {wins}")
+    exp = dla.cache_export(cache, heads=heads)
+    H.assert_cache(exp, oc, 1e-4, what=f"delta {w.label}")
+    print(f"[delta-full-ok] {w.label} heads={heads} near={nb}+{nm} "
+          f"boundaries={int(dec['b'].sum())} merges={int((dec['merge'] >= 0).sum())} "
+          f"segments={len(f32_starts)} windows={wins} max_rel_out={rel:.2e} "
+          f"max_score_err={serr:.2e}", flush=True)

@@ -18,6 +18,10 @@ SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), 
 
 MUTANTS = {
     # the delta-rule form (Sec. 2.2, eq. delta_rule_rnn)
+    "delta_u_without_erase_term": ("u_out[t * dv + c] = beta ? beta[t] * (vt[c] - y[c]) : vt[c];",
+                                   "u_out[t * dv + c] = beta ? beta[t] * vt[c] : vt[c];"),
+    "delta_u_unscaled": ("u_out[t * dv + c] = beta ? beta[t] * vt[c] : vt[c];",
+                         "u_out[t * dv + c] = vt[c];"),
     "delta_erase_sign": ("S[a * dv + c] -= beta * k[a] * u[c];", "S[a * dv + c] += beta * k[a] * u[c];"),
     "delta_erase_without_key": ("u[c] += k[a] * S[a * dv + c];", "u[c] += S[a * dv + c];"),
     "delta_erase_skipped": ("      if (beta) delta_erase(So, kt, beta[t], dk, dv, y);\n", "\n"),
