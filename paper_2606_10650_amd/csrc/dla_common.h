@@ -193,6 +193,18 @@ __device__ __forceinline__ void wave_scan_affine(float& A, float& B) {
   affine_step<0x143, 0xC>(A, B);
 }
 
+// Sum of a float over the wavefront through DPP row shifts and broadcasts
+// (every lane gets it).
+__device__ __forceinline__ float wave_total_dpp(float x) {
+  x += dpp_f<0x111, 0xF>(0.f, x);
+  x += dpp_f<0x112, 0xF>(0.f, x);
+  x += dpp_f<0x114, 0xF>(0.f, x);
+  x += dpp_f<0x118, 0xF>(0.f, x);
+  x += dpp_f<0x142, 0xA>(0.f, x);
+  x += dpp_f<0x143, 0xC>(0.f, x);
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+
 // Sum of a double over the wavefront (every lane gets it).
 template <int CTRL, int RMASK>
 __device__ __forceinline__ void sum_step_d(double& x) {
@@ -258,6 +270,17 @@ __device__ __forceinline__ double info_score(double a, double b, double c, doubl
   // rounding can take num a little below 0; a NaN (non-finite inputs) passes
   // through, as the score of the definition would be NaN
   return sqrt(num < 0.0 ? 0.0 : num) / (sqrt(b / rS2) + eps);
+}
+
+// The same score in float32 (the prefill scans).
+__device__ __forceinline__ float score_f(float a, float b, float c, float D, float eps,
+                                         float eps_rms) {
+  const float rs2 = a / D + eps_rms;
+  const float rS2 = b / D + eps_rms;
+  const float num = a / rs2 + b / rS2 - 2.f * c * rsqrtf(rs2 * rS2);
+  // rounding can take num a little below 0; a NaN (non-finite inputs) passes
+  // through, as the score of the definition would be NaN
+  return sqrtf(num < 0.f ? 0.f : num) / (sqrtf(b / rS2) + eps);
 }
 
 }  // namespace dla

@@ -26,16 +26,27 @@
 
 namespace dla {
 
-constexpr int DTHR = 512;        // threads of the delta scan (256: 10% slower, 1024: 20% slower)
+constexpr int DTHR = 512;        // threads of the delta scan
 constexpr int DWAVE = DTHR / 64;
-constexpr int DNCB = DTHR / 16;  // column blocks of the state (16 row blocks)
 constexpr int DSL = 64;          // tokens staged in LDS per round
+
+// Barrier for the per-token exchanges through LDS: waits for the wave's LDS
+// operations only, so that the pseudo-values and exports stored to global
+// memory stay in flight (a full __syncthreads would wait for those stores at
+// every token).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt((63 & 15) | (7 << 4) | (0 << 8) | ((63 >> 4) << 14));
+  __builtin_amdgcn_s_barrier();
+}
 
 template <int DK, int DV>
 struct DeltaP {
-  static constexpr int RB = DK / 16;    // state rows per thread
-  static constexpr int CB = DV / DNCB;  // state columns per thread
-  static_assert(CB >= 1 && CB * DNCB == DV, "column blocks");
+  // wave w holds rows [w RB, (w + 1) RB) of the state, lane l columns
+  // [l CB, (l + 1) CB): a wave's share of S^T k covers every column, so it
+  // needs no exchange between lanes
+  static constexpr int RB = DK / DWAVE;  // state rows per thread
+  static constexpr int CB = DV / 64;     // state columns per thread
+  static_assert(RB * DWAVE == DK && CB * 64 == DV, "state blocks");
   static size_t smem_bytes(int C) {
     size_t off = (size_t)DSL * (DK + DV) * 4;  // sK, sV
     off += (size_t)DSL * 4 * 5;                 // sAl, sBeta, sA, sBo, sMo
@@ -60,8 +71,8 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wv = tid >> 6;
-  const int rb = tid / DNCB;  // row block of the thread's state block
-  const int cb = tid % DNCB;  // column block
+  const int rb = wv;    // row block of the thread's state block
+  const int cb = lane;  // column block
   const int C = a.desc.C;
   const int T = a.T;
   const size_t tok0 = (size_t)h * T;
@@ -162,22 +173,16 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
       float cp = 0.f;
 #pragma unroll
       for (int j = 0; j < CB; ++j) cp += yp[j] * sV[tt * DV + cb * CB + j];
-      // the wave's row blocks (lanes DNCB apart), then the waves
+      // the waves' shares are added below; |S|^2 and c over the wave
+      bp = wave_total_dpp(bp);
+      cp = wave_total_dpp(cp);
 #pragma unroll
-      for (int o = DNCB; o < 64; o <<= 1)
-#pragma unroll
-        for (int j = 0; j < CB; ++j) yp[j] += __shfl_xor(yp[j], o, 64);
-      bp = wave_sum(bp);
-      cp = wave_sum(cp);
-      if (lane < DNCB) {
-#pragma unroll
-        for (int j = 0; j < CB; ++j) sY[wv * DV + cb * CB + j] = yp[j];
-      }
+      for (int j = 0; j < CB; ++j) sY[wv * DV + cb * CB + j] = yp[j];
       if (lane == 0) {
         sRed[wv] = bp;
         sRed[DWAVE + wv] = cp;
       }
-      __syncthreads();
+      lds_barrier();
       float yj = 0.f;
       if (tid < DV) {
 #pragma unroll
@@ -196,7 +201,7 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
         bd = 1;
         It = 0.f;
       } else {
-        It = (float)info_score((double)sA[tt], b, c, (double)D, a.eps, a.eps_rms);
+        It = score_f(sA[tt], (float)b, (float)c, (float)D, a.eps, a.eps_rms);
         bd = (It >= a.tau) ? 1 : 0;
         if (sBo[tt] != -1) bd = sBo[tt] ? 1 : 0;
         if (C == 1) bd = 0;
@@ -282,7 +287,7 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
         sU[tid] = u;
         Uh[(size_t)t * DV + tid] = u;
       }
-      __syncthreads();
+      lds_barrier();
       float uc[CB];
 #pragma unroll
       for (int j = 0; j < CB; ++j) uc[j] = sU[cb * CB + j];

@@ -136,19 +136,6 @@ struct ScanP {
   }
 };
 
-// Score of a rank-one token state (|k|^2|v|^2 = a) against a state S with
-// |S|^2 = b and k^T S v = c, both RMS-normalised (closed form of the
-// State Information Score).
-__device__ __forceinline__ float score_f(float a, float b, float c, float D, float eps,
-                                         float eps_rms) {
-  const float rs2 = a / D + eps_rms;
-  const float rS2 = b / D + eps_rms;
-  const float num = a / rs2 + b / rS2 - 2.f * c * rsqrtf(rs2 * rS2);
-  // rounding can take num a little below 0; a NaN (non-finite inputs) passes
-  // through, as the score of the definition would be NaN
-  return sqrtf(num < 0.f ? 0.f : num) / (sqrtf(b / rS2) + eps);
-}
-
 template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(STHR) void prefill_scan_kernel(PrefillArgs a, PrefillWS w, int tb,
                                                             int te) {
