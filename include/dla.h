@@ -338,8 +338,9 @@ dla_status dla_prefill_delta_workspace_size(const dla_cache_desc* desc, int32_t 
  * one starts it at k_t (beta_t v_t)^T.  Every state is therefore the decayed
  * sum of k_s u_s^T over its tokens: a sequential scan (one workgroup per head,
  * the newest state on chip) makes the decisions and the pseudo-values, and the
- * chunked update and readout stages of dla_prefill run on (q, k, u, lambda) in
- * float32 (16-bit inputs are widened into the workspace first).  Stages run
+ * chunked update and readout stages of dla_prefill run on (q, k, u, lambda)
+ * (u kept in float32 for the states; a bfloat16 copy for the readout of
+ * 16-bit inputs).  Stages run
  * in order on `stream`; the workspace (dla_prefill_delta_workspace_size bytes,
  * 256-byte aligned, caller-owned) must not be used by another call until the
  * stream has passed this one.  Errors as dla_prefill; DLA_ERR_UNSUPPORTED

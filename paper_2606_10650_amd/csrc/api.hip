@@ -456,8 +456,8 @@ dla_status dla_prefill_delta(const dla_cache_desc* desc, void* cache, const void
   if (!cache || !k || !v || !log_gate || !beta) return ret(DLA_ERR_INVALID_ARG);
   if (!skip && (!q || !out)) return ret(DLA_ERR_INVALID_ARG);
   if (T == 0) return ret(DLA_OK);
-  // the float32 update and readout stages, and the sequential scan's LDS
-  if (!prefill_chunks_supported(*desc, DLA_F32) || prefill_delta_scan_smem(*desc) > 160 * 1024)
+  // the update and readout stages in the inputs' type, and the sequential scan's LDS
+  if (!prefill_chunks_supported(*desc, in_dtype) || prefill_delta_scan_smem(*desc) > 160 * 1024)
     return ret(DLA_ERR_UNSUPPORTED);
   if ((int64_t)desc->B * desc->H * (int64_t)T * (desc->C > 128 ? desc->C : 128) >
       ((int64_t)1 << 40))

@@ -27,6 +27,9 @@ struct PrefillArgs {
   int serial;  // stages one after another on the caller's stream
   size_t pool_budget;  // bytes of state copies per call (pool_budget_of)
   char* workspace;
+  // values given as float32 with 16-bit keys (the update stage of the Gated
+  // DeltaNet form, whose values are the delta rule's write vectors)
+  int v_f32;
 };
 
 // ---------------------------------------------------------------------------

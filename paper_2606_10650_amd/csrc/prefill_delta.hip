@@ -20,8 +20,12 @@
 // bookkeeping as the gated scan), the cache's per-state counts and aggregated
 // scores, and u as float32.
 //
-// The call then runs the float32 update and readout stages over (q, k, u,
-// lambda), with float32 copies of 16-bit inputs made first.
+// The call then runs the chunked update and readout stages of the gated form
+// over (q, k, u, lambda).  For 16-bit inputs the update takes u in float32 (it
+// stages every value as three bfloat16 terms, so the states stay float32
+// exact) and the readout a bfloat16 copy of u (for its in-chunk part, which
+// rounds values to bfloat16 in the gated form too); float32 inputs run the
+// float32 stages on u.
 #include "prefill.h"
 
 namespace dla {
@@ -62,7 +66,8 @@ struct DeltaP {
 template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a, PrefillWS w,
                                                                   const float* __restrict__ beta,
-                                                                  float* __restrict__ U) {
+                                                                  float* __restrict__ U,
+                                                                  bf16_t* __restrict__ U16) {
   if (!cache_matches(a.cache, a.desc)) return;  // refused call (see the prep kernel)
   using P = DeltaP<DK, DV>;
   constexpr int RB = P::RB, CB = P::CB;
@@ -127,6 +132,7 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
   const float* bt = beta + tok0;
   int32_t* death = w.death + tok0;
   float* Uh = U + tok0 * DV;
+  bf16_t* U16h = U16 ? U16 + tok0 * DV : nullptr;  // bfloat16 copy (16-bit inputs)
 
   for (int c0 = 0; c0 < T; c0 += DSL) {
     const int nr = min(DSL, T - c0);
@@ -286,6 +292,7 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
         const float u = sBeta[tt] * (sV[tt * DV + tid] - (bd ? 0.f : yj));
         sU[tid] = u;
         Uh[(size_t)t * DV + tid] = u;
+        if (U16h) U16h[(size_t)t * DV + tid] = from_f32<bf16_t>(u);
       }
       lds_barrier();
       float uc[CB];
@@ -304,17 +311,6 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
   }
 }
 
-// float32 copy of n 16-bit values
-__global__ __launch_bounds__(256) void widen_kernel(const bf16_t* __restrict__ src,
-                                                    float* __restrict__ dst, size_t n) {
-  const size_t stride = (size_t)gridDim.x * 256 * 4;
-  for (size_t i = ((size_t)blockIdx.x * 256 + threadIdx.x) * 4; i < n; i += stride) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-      if (i + e < n) dst[i + e] = to_f32(src[i + e]);
-  }
-}
-
 template <int DK, int DV>
 static size_t delta_smem(int C) {
   return DeltaP<DK, DV>::smem_bytes(C);
@@ -329,53 +325,40 @@ size_t prefill_delta_scan_smem(const dla_cache_desc& d) {
 
 template <int DK, int DV, typename Tin>
 static hipError_t launch_delta_scan_t(const PrefillArgs& a, const PrefillWS& w, const float* beta,
-                                      float* U, hipStream_t s) {
+                                      float* U, bf16_t* U16, hipStream_t s) {
   const size_t shm = DeltaP<DK, DV>::smem_bytes(a.desc.C);
   if (shm > 160 * 1024) return hipErrorInvalidValue;
   auto k = prefill_delta_scan_kernel<DK, DV, Tin>;
   if (hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm) !=
       hipSuccess)
     return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k, dim3(a.desc.B * a.desc.H), dim3(DTHR), shm, s, a, w, beta, U);
+  hipLaunchKernelGGL(k, dim3(a.desc.B * a.desc.H), dim3(DTHR), shm, s, a, w, beta, U, U16);
   return hipGetLastError();
 }
 
 template <int DK, int DV>
 static hipError_t launch_delta_scan_dims(const PrefillArgs& a, const PrefillWS& w,
-                                         const float* beta, float* U, hipStream_t s) {
-  if (a.in_dtype == DLA_F32) return launch_delta_scan_t<DK, DV, float>(a, w, beta, U, s);
-  return launch_delta_scan_t<DK, DV, bf16_t>(a, w, beta, U, s);
+                                         const float* beta, float* U, bf16_t* U16,
+                                         hipStream_t s) {
+  if (a.in_dtype == DLA_F32) return launch_delta_scan_t<DK, DV, float>(a, w, beta, U, U16, s);
+  return launch_delta_scan_t<DK, DV, bf16_t>(a, w, beta, U, U16, s);
 }
 
-static hipError_t widen(const void* src, float* dst, size_t n, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  const size_t blocks = (n + 1023) / 1024;
-  hipLaunchKernelGGL(widen_kernel, dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(256), 0, s,
-                     static_cast<const bf16_t*>(src), dst, n);
-  return hipGetLastError();
-}
-
-// Workspace of a delta-form prefill: the float32 stages' workspace (serial),
-// then the pseudo-values, then float32 copies of q, k and lambda for 16-bit
-// inputs.
+// Workspace of a delta-form prefill: the stages' workspace (serial; the
+// float32 stages for float32 inputs), then the write vectors u (float32), and
+// for 16-bit inputs a bfloat16 copy of them.
 struct DeltaWS {
-  size_t stages, u, q, k, lam, total;
+  size_t u, u16, total;
 };
 
 static DeltaWS delta_ws(const dla_cache_desc& d, int T, dla_dtype in, bool readout, size_t budget) {
   DeltaWS r;
   const size_t nh = (size_t)d.B * d.H;
-  const bool wide = in != DLA_F32;
-  r.stages = 0;
-  size_t off = round_up(prefill_workspace_bytes(d, T, DLA_F32, readout, true, budget), 256);
+  size_t off = round_up(prefill_workspace_bytes(d, T, in, readout, true, budget), 256);
   r.u = off;
   off = round_up(off + nh * T * d.d_v * 4, 256);
-  r.q = off;
-  off = round_up(off + (wide && readout ? nh * T * d.d_k * 4 : 0), 256);
-  r.k = off;
-  off = round_up(off + (wide ? nh * T * d.d_k * 4 : 0), 256);
-  r.lam = off;
-  off = round_up(off + (wide && readout ? nh * T * d.C * 4 : 0), 256);
+  r.u16 = off;
+  off = round_up(off + (in != DLA_F32 && readout ? nh * T * d.d_v * 2 : 0), 256);
   r.total = off;
   return r;
 }
@@ -387,48 +370,37 @@ size_t prefill_delta_workspace_bytes(const dla_cache_desc& d, int T, dla_dtype i
 
 hipError_t launch_prefill_delta(const PrefillArgs& a, const float* beta, hipStream_t s) {
   const bool readout = !a.skip_readout;
+  const bool wide = a.in_dtype != DLA_F32;
   const DeltaWS L = delta_ws(a.desc, a.T, a.in_dtype, readout, a.pool_budget);
   const size_t nh = (size_t)a.desc.B * a.desc.H;
   char* base = a.workspace;
   float* U = reinterpret_cast<float*>(base + L.u);
-  // the float32 stages: q, k and lambda widened, u for the values
-  PrefillArgs f = a;
-  f.in_dtype = DLA_F32;
-  f.serial = 1;
-  f.v = U;
-  hipError_t e;
-  if (a.in_dtype != DLA_F32) {
-    float* kf = reinterpret_cast<float*>(base + L.k);
-    if ((e = widen(a.k, kf, nh * a.T * a.desc.d_k, s)) != hipSuccess) return e;
-    f.k = kf;
-    if (readout) {
-      float* qf = reinterpret_cast<float*>(base + L.q);
-      if ((e = widen(a.q, qf, nh * a.T * a.desc.d_k, s)) != hipSuccess) return e;
-      f.q = qf;
-      if (a.lam) {
-        float* lf = reinterpret_cast<float*>(base + L.lam);
-        if ((e = widen(a.lam, lf, nh * a.T * a.desc.C, s)) != hipSuccess) return e;
-        f.lam = lf;
-      }
-    }
-  }
-  const SegPlan p = seg_plan(a.desc, a.T, DLA_F32, readout, true, a.pool_budget);
+  bf16_t* U16 = wide && readout ? reinterpret_cast<bf16_t*>(base + L.u16) : nullptr;
+  // the update takes u (float32), the readout u in the inputs' type
+  PrefillArgs fu = a;
+  fu.serial = 1;
+  fu.v = U;
+  fu.v_f32 = wide ? 1 : 0;
+  PrefillArgs fr = fu;
+  fr.v_f32 = 0;
+  if (wide) fr.v = U16;
+  const SegPlan p = seg_plan(a.desc, a.T, a.in_dtype, readout, true, a.pool_budget);
   const PrefillWS w = ws_layout(base, nh, a.T, a.desc.C, a.desc.d_k * a.desc.d_v, p.nch);
-  if ((e = launch_prefill_prep(f, s)) != hipSuccess) return e;
+  hipError_t e;
+  if ((e = launch_prefill_prep(fu, s)) != hipSuccess) return e;
   const int dk = a.desc.d_k, dv = a.desc.d_v;
-  // (the scan reads the keys and values in the caller's type)
   if (dk == 128 && dv == 128)
-    e = launch_delta_scan_dims<128, 128>(a, w, beta, U, s);
+    e = launch_delta_scan_dims<128, 128>(a, w, beta, U, U16, s);
   else if (dk == 64 && dv == 64)
-    e = launch_delta_scan_dims<64, 64>(a, w, beta, U, s);
+    e = launch_delta_scan_dims<64, 64>(a, w, beta, U, U16, s);
   else if (dk == 128 && dv == 64)
-    e = launch_delta_scan_dims<128, 64>(a, w, beta, U, s);
+    e = launch_delta_scan_dims<128, 64>(a, w, beta, U, U16, s);
   else
-    e = launch_delta_scan_dims<64, 128>(a, w, beta, U, s);
+    e = launch_delta_scan_dims<64, 128>(a, w, beta, U, U16, s);
   if (e != hipSuccess) return e;
   for (int seg = 0; seg < p.nseg; ++seg) {
-    if ((e = launch_prefill_update(f, p, seg, s)) != hipSuccess) return e;
-    if (readout && (e = launch_prefill_readout(f, p, seg, s)) != hipSuccess) return e;
+    if ((e = launch_prefill_update(fu, p, seg, s)) != hipSuccess) return e;
+    if (readout && (e = launch_prefill_readout(fr, p, seg, s)) != hipSuccess) return e;
   }
   return hipSuccess;
 }

@@ -81,7 +81,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, 
 // KL: the token-range loop reads its keys from a per-wave LDS ring that the
 // loads fill directly (16-bit inputs), with explicit waits; else straight from
 // global memory into registers.
-template <int DK, int DV, typename Tin, typename TS, bool KL>
+// VF: float32 values with 16-bit keys (a.v_f32), staged through the same three
+// bfloat16 terms.
+template <int DK, int DV, typename Tin, typename TS, bool KL, bool VF>
 __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, PrefillWS w,
                                                               SegPlan plan, int seg) {
   if (!cache_matches(a.cache, a.desc)) return;  // refused call (see the prep kernel)
@@ -177,6 +179,8 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
   const int32_t* death = w.death + (size_t)h * T;
   const Tin* Kin = static_cast<const Tin*>(a.k) + (size_t)h * T * DK;
   const Tin* Vin = static_cast<const Tin*>(a.v) + (size_t)h * T * DV;
+  const float* Vf = static_cast<const float*>(a.v) + (size_t)h * T * DV;  // (VF)
+  static_assert(!VF || E == 2, "float32 values go with 16-bit keys");
   auto obj_slice = [&](int obj) -> Tin* {
     return pool_slice<Tin>(w.pool, h, plan.P_cap, obj, cg, NCG, U::CP::SLICE);
   };
@@ -323,9 +327,12 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
     // now, staged in LDS once the leader tables no longer need the region.
     // Item i covers TPW consecutive tokens and one 16-byte piece.
     u32x4 vraw[U::VIPT][U::TPW];
+    u32x4 vhi[VF ? U::VIPT : 1][VF ? U::TPW : 1];  // (VF) the piece's last four values
     double vg[U::VIPT][U::TPW];
     {
-      const __amdgpu_buffer_rsrc_t vr = buffer_rsrc(Vin + (size_t)c0 * DV, nrow * DV * E);
+      const __amdgpu_buffer_rsrc_t vr =
+          VF ? buffer_rsrc(Vf + (size_t)c0 * DV, nrow * DV * 4)
+             : buffer_rsrc(Vin + (size_t)c0 * DV, nrow * DV * E);
 #pragma unroll
       for (int u = 0; u < U::VIPT; ++u) {
         const int item = tid + NTHR * u;
@@ -333,8 +340,14 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
 #pragma unroll
         for (int t = 0; t < U::TPW; ++t) {
           const int tok = U::TPW * tp + t;
-          vraw[u][t] = __builtin_amdgcn_raw_buffer_load_b128(
-              vr, (tok * DV + cg * NC + p * U::EPP) * E, 0, 0);
+          if constexpr (VF) {
+            const int off = (tok * DV + cg * NC + p * U::EPP) * 4;
+            vraw[u][t] = __builtin_amdgcn_raw_buffer_load_b128(vr, off, 0, 0);
+            vhi[u][t] = __builtin_amdgcn_raw_buffer_load_b128(vr, off + 16, 0, 0);
+          } else {
+            vraw[u][t] = __builtin_amdgcn_raw_buffer_load_b128(
+                vr, (tok * DV + cg * NC + p * U::EPP) * E, 0, 0);
+          }
           vg[u][t] = Gtok[c0 + min(tok, nrow - 1)];
         }
       }
@@ -454,8 +467,15 @@ __global__ __launch_bounds__(NTHR) void prefill_update_kernel(PrefillArgs a, Pre
         uint32_t* row = reinterpret_cast<uint32_t*>(sV + (p * U::EPP) * VTS) + tp;
 #pragma unroll
         for (int q = 0; q < U::EPP; ++q) {
-          const float x0 = ef[0] * to_f32(piece_elem<bf16_t>(vraw[u][0], q));
-          const float x1 = ef[1] * to_f32(piece_elem<bf16_t>(vraw[u][1], q));
+          // element q of the token's piece (float32 values: four per 16 bytes)
+          auto val = [&](int t) __attribute__((always_inline)) -> float {
+            if constexpr (VF)
+              return __uint_as_float(q < 4 ? vraw[u][t][q & 3] : vhi[u][t][q & 3]);
+            else
+              return to_f32(piece_elem<bf16_t>(vraw[u][t], q));
+          };
+          const float x0 = ef[0] * val(0);
+          const float x1 = ef[1] * val(1);
           const bf16x2 hi = {(__bf16)x0, (__bf16)x1};
           const float y0 = x0 - (float)hi[0], y1 = x1 - (float)hi[1];
           const bf16x2 mid = {(__bf16)y0, (__bf16)y1};
@@ -831,9 +851,14 @@ static hipError_t launch_update_t(const PrefillArgs& a, const SegPlan& p, int se
   // keys through LDS for 16-bit inputs when the rings fit beside the rest
   constexpr bool E2 = sizeof(Tin) == 2;
   const size_t shm_kl = update_smem_bytes<DK, Tin, E2>(a.desc.C);
-  if (E2 && shm_kl <= 160 * 1024) return launch(prefill_update_kernel<DK, DV, Tin, TS, E2>, shm_kl);
-  return launch(prefill_update_kernel<DK, DV, Tin, TS, false>,
-                update_smem_bytes<DK, Tin, false>(a.desc.C));
+  const size_t shm = update_smem_bytes<DK, Tin, false>(a.desc.C);
+  if (E2 && a.v_f32) {
+    if (shm_kl <= 160 * 1024) return launch(prefill_update_kernel<DK, DV, Tin, TS, E2, E2>, shm_kl);
+    return launch(prefill_update_kernel<DK, DV, Tin, TS, false, E2>, shm);
+  }
+  if (a.v_f32) return hipErrorInvalidValue;  // (float32 values go with 16-bit keys)
+  if (E2 && shm_kl <= 160 * 1024) return launch(prefill_update_kernel<DK, DV, Tin, TS, E2, false>, shm_kl);
+  return launch(prefill_update_kernel<DK, DV, Tin, TS, false, false>, shm);
 }
 
 template <int DK, int DV>

@@ -113,8 +113,8 @@ def test_delta_one_workgroup_per_head():
 
 
 def test_delta_prefill_long_bf16():
-    """Spans and bursts over 2600 tokens: many float32 chunks (256 tokens) of
-    the update and readout stages, merges at a full cache of 24."""
+    """Spans and bursts over 2600 tokens: several chunks of the update and
+    readout stages, merges at a full cache of 24."""
     _case(WORKLOADS["cfg3"].replace(B=1, H=2, T=2600, C=24), "prefill")
 
 
@@ -123,8 +123,8 @@ def test_delta_prefill_long_f32():
 
 
 def test_delta_prefill_small_pool_budget():
-    """A state-copy budget of 8 MiB splits the float32 stages into segments of
-    two chunks."""
+    """A state-copy budget of 8 MiB splits the stages into segments of a
+    chunk or two."""
     from paper_2606_10650_amd import dla
     w = WORKLOADS["cfg3"].replace(B=1, H=2, T=2600, C=24)
     c = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
@@ -250,10 +250,10 @@ def test_delta_prefill_full_size_sampled_heads():
                        mi.cpu().numpy().reshape(nh, w.T)[heads], dec, w.label)
     serr = np.abs(sc.cpu().numpy().reshape(nh, w.T)[heads] - dec["score"]).max()
     assert serr < H.DELTA_B / 10, f"score error {serr}"
-    # windows inside a chunk of the float32 stages (256 tokens), across the
-    # start of a later segment, the last segment's first tokens and the end
-    f32_starts = dla.prefill_segment_starts(cache, w.T, torch.float32, serial=True)
-    toks, wins = windows(w.T, 256, f32_starts)
+    # windows inside a chunk (512 tokens), across the start of a later segment
+    # of the serial stages, the last segment's first tokens and the end
+    seg_starts = dla.prefill_segment_starts(cache, w.T, torch.bfloat16, serial=True)
+    toks, wins = windows(w.T, 512, seg_starts)
     og = out.float().reshape(nh, w.T, w.dv)[heads][:, toks].cpu().numpy()
     del q, k, v, g, lam, out
     oc = OracleCache.empty(len(heads), w.C, w.dk, w.dv)
@@ -271,5 +271,5 @@ def test_delta_prefill_full_size_sampled_heads():
     H.assert_cache(exp, oc, 1e-4, what=f"delta {w.label}")
     print(f"[delta-full-ok] {w.label} heads={heads} near={nb}+{nm} "
           f"boundaries={int(dec['b'].sum())} merges={int((dec['merge'] >= 0).sum())} "
-          f"segments={len(f32_starts)} windows={wins} max_rel_out={rel:.2e} "
+          f"segments={len(seg_starts)} windows={wins} max_rel_out={rel:.2e} "
           f"max_score_err={serr:.2e}", flush=True)
