@@ -308,12 +308,14 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   // pool_h + obj * NCG * SLICE (the object index is wave-uniform, so the
   // address is formed in scalar registers)
   const Tin* pool_h = pool_slice<Tin>(w.pool, h, plan.P_cap, 0, cg, NCG, P::SLICE);
-  // slices of states jb, jb + 1 into ring pair pr, straight from memory into
+  // pool object of state j (the last state's past the list)
+  auto obj_of = [&](int j) __attribute__((always_inline)) -> int { return sObj[min(j, m - 1)]; };
+  // slices of pool objects o0, o1 into ring pair pr, straight from memory into
   // LDS (each lane's 16 bytes land at the wave's base plus 16 bytes per lane)
-  auto dma2 = [&](int jb, int pr) __attribute__((always_inline)) {
+  auto dma2 = [&](int pr, int o0, int o1) __attribute__((always_inline)) {
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
-      const int obj = __builtin_amdgcn_readfirstlane(sObj[min(jb + s2, m - 1)]);
+      const int obj = __builtin_amdgcn_readfirstlane(s2 ? o1 : o0);
       const __amdgpu_buffer_rsrc_t src = __builtin_amdgcn_make_buffer_rsrc(
           const_cast<Tin*>(pool_h + (size_t)obj * (NCG * P::SLICE)), (short)0, SL16 * 16,
           0x00020000);
@@ -332,7 +334,7 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
 #pragma unroll
     for (int j = 0; j < 2 * P::LAM_D; ++j) lam_dma(j, lam_dt(j));
 #pragma unroll
-    for (int J = 0; J < LEAD; ++J) dma2(2 * J, J);
+    for (int J = 0; J < LEAD; ++J) dma2(J, obj_of(2 * J), obj_of(2 * J + 1));
   }
   // old states alive at each token: m minus the states of the list whose death
   // token is at or before it (a state lives while its death token is later)
@@ -526,10 +528,13 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
       const Tin* A2 = reinterpret_cast<const Tin*>(ring + ((J + 1) % P::NPAIR) * 2 * SL16);
       const int jl = 2 * (J + P::LAM_D);
       const int dt0 = lam_dt(jl), dt1 = lam_dt(jl + 1);
+      // (the object numbers are read here, so that the requests below need not
+      // wait for an LDS read behind the operand reads)
+      const int ob0 = obj_of(2 * (J + LEAD)), ob1 = obj_of(2 * (J + LEAD) + 1);
       sub(2 * J, saX, A0, A0 + P::SLICE, saY, [&]() __attribute__((always_inline)) {
         lam_dma(jl, dt0);
         lam_dma(jl + 1, dt1);
-        dma2(2 * (J + LEAD), (J + LEAD) % P::NPAIR);
+        dma2((J + LEAD) % P::NPAIR, ob0, ob1);
       });
       __builtin_amdgcn_sched_barrier(0);
       sub(2 * J + 1, saY, A0 + P::SLICE, A2, saX, nothing);
