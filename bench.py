@@ -254,6 +254,12 @@ def prefill_bench(args, torch, dla, W, steps, warmup, with_events=True, serial_s
         stages = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(ns)] for e in evs])
         res["stages_ms_serial"] = dict(zip(dla.PREFILL_STAGES,
                                            [round(float(s), 4) for s in stages.mean(axis=0)]))
+        if "roofline" in res:
+            # the same launches alone on the chip: in the timed (pipelined) steps
+            # the scan and the next segment's update share the CUs with them
+            ser = res["stages_ms_serial"]["readout"]
+            res["roofline"]["readout_ms_per_step_serial"] = ser
+            res["roofline"]["frac_serial"] = frac(flops_ro / (ser * 1e-3) / 1e12, PEAK_BF16_TFLOPS)
     del q, k, v, lam, g, out, ws, cache
     torch.cuda.empty_cache()
     return res
