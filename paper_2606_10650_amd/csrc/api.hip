@@ -15,10 +15,9 @@ namespace dla {
 // Pipelined prefills fork a second stream from the caller's.  Each host thread
 // gets its own stream and events per device, so concurrent calls from several
 // threads never share an event; they live until the process ends.
-hipError_t pipe_resources(hipStream_t caller, int n, hipStream_t* side, hipStream_t* side2,
-                          hipEvent_t** evs) {
+hipError_t pipe_resources(hipStream_t caller, int n, hipStream_t* side, hipEvent_t** evs) {
   struct PerDevice {
-    hipStream_t side = nullptr, side2 = nullptr;
+    hipStream_t side = nullptr;
     std::vector<hipEvent_t> ev;
   };
   static thread_local std::vector<PerDevice> per;
@@ -30,14 +29,11 @@ hipError_t pipe_resources(hipStream_t caller, int n, hipStream_t* side, hipStrea
   if (dev < 0) return hipErrorInvalidDevice;
   if ((int)per.size() <= dev) per.resize(dev + 1);
   PerDevice& pd = per[dev];
-  if (!pd.side || !pd.side2 || (int)pd.ev.size() < n) {
+  if (!pd.side || (int)pd.ev.size() < n) {
     if ((e = hipGetDevice(&cur)) != hipSuccess) return e;
     if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
     if (!pd.side && (e = hipStreamCreateWithFlags(&pd.side, hipStreamNonBlocking)) != hipSuccess)
       pd.side = nullptr;
-    if (e == hipSuccess && !pd.side2 &&
-        (e = hipStreamCreateWithFlags(&pd.side2, hipStreamNonBlocking)) != hipSuccess)
-      pd.side2 = nullptr;
     while (e == hipSuccess && (int)pd.ev.size() < n) {
       hipEvent_t x;
       if ((e = hipEventCreateWithFlags(&x, hipEventDisableTiming)) == hipSuccess) pd.ev.push_back(x);
@@ -47,7 +43,6 @@ hipError_t pipe_resources(hipStream_t caller, int n, hipStream_t* side, hipStrea
     if (r != hipSuccess) return r;
   }
   *side = pd.side;
-  *side2 = pd.side2;
   *evs = pd.ev.data();
   return hipSuccess;
 }

@@ -326,11 +326,10 @@ size_t prefill_delta_workspace_bytes(const dla_cache_desc& d, int T, dla_dtype i
                                      size_t budget);
 size_t prefill_delta_scan_smem(const dla_cache_desc& d);
 
-// The second and third streams of a pipelined call on the device of the
-// caller's stream, and n events for ordering the streams (owned by the
-// library, one set per host thread and device; created on first use).
-hipError_t pipe_resources(hipStream_t caller, int n, hipStream_t* side, hipStream_t* side2,
-                          hipEvent_t** evs);
+// The second stream of a pipelined call on the device of the caller's stream,
+// and n events for ordering the two streams (owned by the library, one set per
+// host thread and device; created on first use).
+hipError_t pipe_resources(hipStream_t caller, int n, hipStream_t* side, hipEvent_t** evs);
 
 // Event hooks of a call: ev (nullable) receives an event before the first
 // stage and after the token frames, the scan, the state updates and the
@@ -344,13 +343,9 @@ struct StageEvents {
 
 // Stages in order.  Serial: frames, the whole scan, then update and readout
 // segment by segment, all on s.  Pipelined: the scan segments run on a second
-// stream, forked from s after the token frames.  With one pool for the whole
-// call the updates run on a third stream, segment k's after segment k's scan,
-// and segment k's readout on s waits for segment k's update, so the next
-// segment's update overlaps this readout (it only adds pool objects and lists
-// of later chunks); otherwise segment k's update and readout both run on s
-// after segment k's scan.  s waits for the last segment's scan or update,
-// which follow every other launch on the other streams, so the call joins on s.
+// stream, forked from s after the token frames, and segment k's update and
+// readout on s wait for segment k's scan; s waits for the whole scan before
+// its last update, so the call joins on s.
 inline hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s, const StageEvents& se) {
   const bool pipe = pipelined(a.T, a.in_dtype, !a.skip_readout, a.serial != 0);
   const SegPlan p = seg_plan(a.desc, a.T, a.in_dtype, !a.skip_readout, a.serial != 0,
@@ -369,26 +364,20 @@ inline hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s, const Stag
   if ((e = rec(0, s)) != hipSuccess) return e;
   if ((e = launch_prefill_prep(a, s)) != hipSuccess) return e;
   if ((e = rec(1, s)) != hipSuccess) return e;
-  hipStream_t side = s, ups = s;
+  hipStream_t side = s;
   hipEvent_t* pev = nullptr;
   bool forked = false;
-  const bool upd_side = pipe && p.shared;
-  // After the fork, an error still joins the other streams into s before it
-  // is returned, so that nothing enqueued on them can outlive the call's
-  // ordering on s (the caller may free the workspace once s is done).
+  // After the fork, an error still joins the second stream into s before it
+  // is returned, so that nothing enqueued on the second stream can outlive the
+  // call's ordering on s (the caller may free the workspace once s is done).
   auto fail = [&](hipError_t err) -> hipError_t {
     if (forked && hipEventRecord(pev[0], side) == hipSuccess) (void)hipStreamWaitEvent(s, pev[0], 0);
-    if (forked && upd_side && hipEventRecord(pev[0], ups) == hipSuccess)
-      (void)hipStreamWaitEvent(s, pev[0], 0);
     return err;
   };
   if (pipe) {
     // event 0 forks the side stream after the frames; event 1 + k marks the
-    // end of scan segment k, event 1 + nseg + k the end of update segment k
-    // (updates on the third stream)
-    hipStream_t third = s;
-    if ((e = pipe_resources(s, 2 * p.nseg + 1, &side, &third, &pev)) != hipSuccess) return e;
-    if (upd_side) ups = third;
+    // end of scan segment k
+    if ((e = pipe_resources(s, p.nseg + 1, &side, &pev)) != hipSuccess) return e;
     if ((e = hipEventRecord(pev[0], s)) != hipSuccess) return e;
     if ((e = hipStreamWaitEvent(side, pev[0], 0)) != hipSuccess) return e;
     forked = true;
@@ -406,21 +395,16 @@ inline hipError_t launch_prefill(const PrefillArgs& a, hipStream_t s, const Stag
     if ((e = rec(2, s)) != hipSuccess) return e;
   }
   for (int seg = 0; seg < p.nseg; ++seg) {
-    if (pipe && (e = hipStreamWaitEvent(ups, pev[1 + seg], 0)) != hipSuccess) return fail(e);
-    if ((e = launch_prefill_update(a, p, seg, ups)) != hipSuccess) return fail(e);
-    if (seg == p.nseg - 1 && (e = rec(3, ups)) != hipSuccess) return fail(e);
-    if (upd_side) {
-      if ((e = hipEventRecord(pev[1 + p.nseg + seg], ups)) != hipSuccess) return fail(e);
-      if ((e = hipStreamWaitEvent(s, pev[1 + p.nseg + seg], 0)) != hipSuccess) return fail(e);
-    }
+    if (pipe && (e = hipStreamWaitEvent(s, pev[1 + seg], 0)) != hipSuccess) return fail(e);
+    if ((e = launch_prefill_update(a, p, seg, s)) != hipSuccess) return fail(e);
+    if (seg == p.nseg - 1 && (e = rec(3, s)) != hipSuccess) return fail(e);
     if (!a.skip_readout) {
       if ((e = rrec(seg, 0)) != hipSuccess) return fail(e);
       if ((e = launch_prefill_readout(a, p, seg, s)) != hipSuccess) return fail(e);
       if ((e = rrec(seg, 1)) != hipSuccess) return fail(e);
     }
   }
-  // (the last segment's wait on pev[nseg], or on pev[2 nseg] with the updates
-  // on the third stream, has joined the other streams)
+  // (the last segment's wait on pev[nseg] has joined the second stream)
   return rec(4, s);
 }
 
