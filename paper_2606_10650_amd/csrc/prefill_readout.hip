@@ -13,12 +13,12 @@
 //     state that absorbed it).  The tile S~_j^T Q^T (32 columns x 32 tokens,
 //     K = d_k) is an MFMA chain; each lane owns one token of a tile, so the
 //     weight is a per-lane scalar applied to the chain's result.  States are
-//     streamed from the pool two per step through a 4-slot LDS ring, up to
-//     four states ahead in registers, with one barrier per step; each wave reads a
-//     state's operand from LDS once for all of its tiles.  The weights are
-//     computed once per (token, state), by the thread of that token, into a
-//     small LDS ring (the lambda entries are requested one step ahead), and
-//     each lane reads the weights of its tiles' tokens from there.
+//     streamed from the pool two per step through an LDS ring of state pairs,
+//     loaded straight from memory into LDS a few steps ahead, with one barrier
+//     per step; each wave reads a state's operand from LDS once for all of its
+//     tiles.  The lambda entries of a state at the lane's tokens come the same
+//     way into a small LDS ring, two steps ahead, and each lane forms the
+//     weights of its own tokens.
 //   * intra-chunk part: (Q K^T (.) M) V with M[t][s] = [s <= t] exp(G_t - G_s)
 //     lambda[t][slot_t(s)] over the chunk's own keys.  The keys pass through
 //     an LDS ring of 32-token blocks, KU blocks per barrier, requested one
@@ -419,16 +419,14 @@ __global__ __launch_bounds__(RTHR) void prefill_readout_kernel(PrefillArgs a, Pr
   }
 
   // ------------------------------------------------ inter-chunk readout
-  // Ring pair p of the LDS holds states 2J and 2J+1 for every step J = p mod 3.
-  // Step J starts with a barrier and runs the MFMA chains of states 2J and
-  // 2J+1 with their operands in registers; meanwhile the operand of the state
-  // after each is read from LDS (for 16-bit inputs), and the slices of states
-  // 2J+4 and 2J+5, loaded into registers three steps earlier, are stored into
-  // pair (J+2) % 3, whose last reader was step J-1 (before this barrier), and
-  // the registers reloaded with states 2J+10 and 2J+11.  A state's slices are
-  // thus written two steps before its chains run.  Each lane forms the weights
-  // of its own tokens from lambda entries requested six states ahead, so no
-  // step waits on a load.  Steps past the last state have sSf = 0.
+  // Ring pair p of the LDS (NPAIR pairs) holds states 2J and 2J+1 for every
+  // step J = p mod NPAIR.  Step J starts with a barrier and runs the MFMA
+  // chains of states 2J and 2J+1 with their operands in registers; meanwhile
+  // the operand of the state after each is read from LDS (for 16-bit inputs),
+  // and the step requests, straight from memory into LDS, the slices of step
+  // J + LEAD (into the pair that step J - 1 read, before this barrier) and the
+  // lambda entries of step J + LAM_D.  Each lane forms the weights of its own
+  // tokens from those entries.  Steps past the last state have sSf = 0.
   // The weight of state j at token t is lambda[t][x] exp(G_t - F_j), x = (live
   // states up to j) - 1 (a state merged away at or before t is weighted as the
   // live state that absorbed it).
