@@ -524,7 +524,9 @@ def cache_export(cache: StateCache, heads=None) -> dict:
         else:
             slots = raw.view(np.float32)
         slots = slots.reshape(C, dk, dv)
-        for j in range(m):
+        # (with bfloat16 storage the newest state lives in the float32 open
+        # region, and its slot holds nothing)
+        for j in range(m - 1 if sd == DLA_BF16 else m):
             res["stored"][i, j] = slots[perm[j]]
         if sd == DLA_BF16 and m > 0:
             o0 = L.open_offset + h * D * 4

@@ -569,3 +569,36 @@ def torch_equal_bits(a, b):
     if a.dtype == torch.float32:
         return torch.equal(a.view(torch.int32), b.view(torch.int32))
     return torch.equal(a, b)
+
+
+def _random_cases(n, seed):
+    """Seeded mixes of the shape parameters the kernels branch on: head counts
+    that are not a multiple of the 8-head workgroup groups, token counts at and
+    around the 64-token scan blocks and the readout chunks (256 tokens for
+    float32 inputs, 512 for bfloat16), capacities from 1 to past the 128-state
+    DPP range, both head sizes and both input types, with and without lambda,
+    float32 or bfloat16 state storage."""
+    rng = np.random.default_rng(seed)
+    structures = ["cuts", "geom", "spans_bursts", "iid"]
+    cases = []
+    for i in range(n):
+        dtype = ["f32", "bf16"][i % 2]
+        rl = 256 if dtype == "f32" else 512
+        T = int(rng.choice([1, 63, 64, 65, rl - 1, rl, rl + 1, 2 * rl + 37, 3 * rl - 5]))
+        dk, dv = [(64, 64), (128, 128), (64, 128), (128, 64)][int(rng.integers(4))]
+        C = int(rng.choice([1, 2, 3, 7, 33, 130]))
+        B, Hh = int(rng.choice([1, 2, 3])), int(rng.choice([1, 3, 5]))
+        st = structures[int(rng.integers(len(structures)))]
+        w = WORKLOADS["cfg1"].replace(
+            name=f"random{i}", B=B, H=Hh, T=T, dk=dk, dv=dv, C=C, dtype=dtype,
+            tau=round(float(rng.uniform(0.1, 0.9)), 2), seed=1000 + i, structure=st,
+            n_seg=max(1, T // 50), mean_len=40.0, span_mean=200.0, burst_mean=8.0,
+            g_lo=float(rng.choice([-0.05, -0.01])))
+        cases.append((w, bool(rng.integers(2)), (i // 2) % 2))
+    return cases
+
+
+@pytest.mark.parametrize("w,no_lambda,state_dtype", _random_cases(24, 20261202),
+                         ids=[f"random{i}" for i in range(24)])
+def test_prefill_random_shapes(w, no_lambda, state_dtype):
+    _prefill_case(w, no_lambda=no_lambda, state_dtype=state_dtype)
