@@ -273,3 +273,41 @@ def test_delta_prefill_full_size_sampled_heads():
           f"boundaries={int(dec['b'].sum())} merges={int((dec['merge'] >= 0).sum())} "
           f"segments={len(seg_starts)} windows={wins} max_rel_out={rel:.2e} "
           f"max_score_err={serr:.2e}", flush=True)
+
+
+def _random_cases(n, seed):
+    """Seeded shape mixes for the delta form: head counts off the 8-head
+    groups of the update and readout grids, token counts around the 64-token
+    staging rounds and the readout chunks, capacities from 1 to past 128, all
+    head sizes, both input types, with and without lambda, both state types;
+    decode runs the shorter ones step by step.  i.i.d. tokens keep capacities
+    up to 33: at 130 their merge densities tie too often for the harness's
+    bound on near-tie pins."""
+    rng = np.random.default_rng(seed)
+    structures = ["cuts", "geom", "spans_bursts", "iid"]
+    cases = []
+    for i in range(n):
+        dtype = ["f32", "bf16"][i % 2]
+        mode = "decode" if i % 4 == 3 else "prefill"
+        rl = 256 if dtype == "f32" else 512
+        choices = [1, 63, 64, 65, 130] if mode == "decode" else [1, 63, 65, rl - 1, rl + 1, 2 * rl + 37]
+        T = int(rng.choice(choices))
+        dk, dv = [(64, 64), (128, 128), (64, 128), (128, 64)][int(rng.integers(4))]
+        C = int(rng.choice([1, 2, 3, 7, 33, 130]))
+        B, Hh = int(rng.choice([1, 2, 3])), int(rng.choice([1, 3, 5]))
+        st = structures[int(rng.integers(len(structures)))]
+        if st == "iid":
+            C = min(C, 33)
+        w = WORKLOADS["cfg1"].replace(
+            name=f"delta_random{i}", B=B, H=Hh, T=T, dk=dk, dv=dv, C=C, dtype=dtype,
+            tau=round(float(rng.uniform(0.1, 0.9)), 2), seed=2000 + i, structure=st,
+            n_seg=max(1, T // 50), mean_len=40.0, span_mean=200.0, burst_mean=8.0,
+            g_lo=float(rng.choice([-0.05, -0.01])))
+        cases.append((w, mode, bool(rng.integers(2)), (i // 2) % 2))
+    return cases
+
+
+@pytest.mark.parametrize("w,mode,no_lambda,state_dtype", _random_cases(16, 20261203),
+                         ids=[f"delta_random{i}" for i in range(16)])
+def test_delta_random_shapes(w, mode, no_lambda, state_dtype):
+    _case(w, mode, state_dtype=state_dtype, no_lambda=no_lambda)
