@@ -602,3 +602,36 @@ def _random_cases(n, seed):
                          ids=[f"random{i}" for i in range(24)])
 def test_prefill_random_shapes(w, no_lambda, state_dtype):
     _prefill_case(w, no_lambda=no_lambda, state_dtype=state_dtype)
+
+
+def _random_decode_cases(n, seed):
+    """Seeded mixes for decode: head counts from 1 (the step split over up to
+    16 workgroups per head) to 15, capacities 1 to 130, all head sizes, both
+    input and state types, steps from an empty cache or after a prefill."""
+    rng = np.random.default_rng(seed)
+    structures = ["cuts", "geom", "spans_bursts", "iid"]
+    cases = []
+    for i in range(n):
+        dtype = ["f32", "bf16"][i % 2]
+        dk, dv = [(64, 64), (128, 128), (64, 128), (128, 64)][int(rng.integers(4))]
+        C = int(rng.choice([1, 2, 3, 7, 33, 130]))
+        B, Hh = int(rng.choice([1, 2, 3])), int(rng.choice([1, 3, 5]))
+        st = structures[int(rng.integers(len(structures)))]
+        if st == "iid":
+            C = min(C, 7)  # (i.i.d. tokens merging at larger capacities tie densities
+            # too often for the harness's bound on near-tie pins)
+        T1 = int(rng.choice([0, 1, 70, 300]))
+        T = T1 + int(rng.integers(1, 60))
+        w = WORKLOADS["cfg1"].replace(
+            name=f"decode_random{i}", B=B, H=Hh, T=T, dk=dk, dv=dv, C=C, dtype=dtype,
+            tau=round(float(rng.uniform(0.1, 0.9)), 2), seed=3000 + i, structure=st,
+            n_seg=max(1, T // 40), mean_len=30.0, span_mean=120.0, burst_mean=6.0,
+            g_lo=float(rng.choice([-0.05, -0.01])))
+        cases.append((w, T1, (i // 2) % 2))
+    return cases
+
+
+@pytest.mark.parametrize("w,T1,state_dtype", _random_decode_cases(12, 20261205),
+                         ids=[f"decode_random{i}" for i in range(12)])
+def test_decode_random_shapes(w, T1, state_dtype):
+    _decode_case(w, T1=T1, state_dtype=state_dtype)
