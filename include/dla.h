@@ -324,7 +324,8 @@ dla_status dla_decode_step_delta(const dla_cache_desc* desc, void* cache, const 
 
 /*
  * Workspace of dla_prefill_delta for T tokens per head (same meaning of flags
- * as dla_prefill_workspace_size: DLA_SKIP_READOUT, DLA_POOL_BUDGET_LOG2).
+ * as dla_prefill_workspace_size: DLA_SKIP_READOUT, DLA_SERIAL_STAGES,
+ * DLA_POOL_BUDGET_LOG2).
  */
 dla_status dla_prefill_delta_workspace_size(const dla_cache_desc* desc, int32_t T,
                                             dla_dtype in_dtype, uint32_t flags, size_t* bytes);
@@ -340,11 +341,14 @@ dla_status dla_prefill_delta_workspace_size(const dla_cache_desc* desc, int32_t 
  * the newest state on chip) makes the decisions and the pseudo-values, and the
  * chunked update and readout stages of dla_prefill run on (q, k, u, lambda)
  * (u kept in float32 for the states; a bfloat16 copy for the readout of
- * 16-bit inputs).  Stages run
- * in order on `stream`; the workspace (dla_prefill_delta_workspace_size bytes,
- * 256-byte aligned, caller-owned) must not be used by another call until the
- * stream has passed this one.  Errors as dla_prefill; DLA_ERR_UNSUPPORTED
- * where the float32 stages do not fit.
+ * 16-bit inputs).  The stages follow dla_prefill's schedule: pipelined (the
+ * scan in segments on the library's second stream, joined back into `stream`
+ * before the call's last stage), or in order on `stream` with
+ * DLA_SERIAL_STAGES; results are identical either way.  The workspace
+ * (dla_prefill_delta_workspace_size bytes for the same flags, 256-byte
+ * aligned, caller-owned) must not be used by another call until the stream
+ * has passed this one.  Errors as dla_prefill; DLA_ERR_UNSUPPORTED where the
+ * stages do not fit.
  */
 dla_status dla_prefill_delta(const dla_cache_desc* desc, void* cache, const void* q, const void* k,
                              const void* v, const float* log_gate, const float* beta,

@@ -438,7 +438,8 @@ dla_status dla_prefill_delta_workspace_size(const dla_cache_desc* desc, int32_t 
   if (s != DLA_OK) return ret(s);
   const size_t budget = pool_budget_of(flags);
   if (!bytes || T < 0 || !dtype_ok(in_dtype) || !budget) return ret(DLA_ERR_INVALID_ARG);
-  *bytes = prefill_delta_workspace_bytes(*desc, T, in_dtype, (flags & DLA_SKIP_READOUT) == 0, budget);
+  *bytes = prefill_delta_workspace_bytes(*desc, T, in_dtype, (flags & DLA_SKIP_READOUT) == 0,
+                                         (flags & DLA_SERIAL_STAGES) != 0, budget);
   return ret(DLA_OK);
 }
 
@@ -464,7 +465,8 @@ dla_status dla_prefill_delta(const dla_cache_desc* desc, void* cache, const void
     return ret(DLA_ERR_UNSUPPORTED);
   const size_t budget = pool_budget_of(params->flags);
   if (!budget) return ret(DLA_ERR_INVALID_ARG);
-  const size_t need = prefill_delta_workspace_bytes(*desc, T, in_dtype, !skip, budget);
+  const bool serial = (params->flags & DLA_SERIAL_STAGES) != 0;
+  const size_t need = prefill_delta_workspace_bytes(*desc, T, in_dtype, !skip, serial, budget);
   if (!workspace || workspace_bytes < need || ((uintptr_t)workspace & 255u))
     return ret(DLA_ERR_WORKSPACE);
   PrefillArgs a;
@@ -494,7 +496,7 @@ dla_status dla_prefill_delta(const dla_cache_desc* desc, void* cache, const void
   a.skip_readout = skip ? 1 : 0;
   a.in_dtype = in_dtype;
   a.out_dtype = out_dtype;
-  a.serial = 1;
+  a.serial = serial ? 1 : 0;
   a.pool_budget = budget;
   a.workspace = (char*)workspace;
   if (launch_prefill_delta(a, beta, (hipStream_t)stream) != hipSuccess) return ret(DLA_ERR_HIP);

@@ -320,10 +320,11 @@ hipError_t launch_prefill_readout(const PrefillArgs& a, const SegPlan& p, int se
 bool prefill_chunks_supported(const dla_cache_desc& d, dla_dtype in_dtype);
 
 // Gated DeltaNet form (prefill_delta.hip): the sequential scan that yields the
-// pseudo-values, then the float32 update and readout stages over them.
+// pseudo-values, then the update and readout stages over them (pipelined
+// unless a.serial).
 hipError_t launch_prefill_delta(const PrefillArgs& a, const float* beta, hipStream_t s);
 size_t prefill_delta_workspace_bytes(const dla_cache_desc& d, int T, dla_dtype in, bool readout,
-                                     size_t budget);
+                                     bool serial, size_t budget);
 size_t prefill_delta_scan_smem(const dla_cache_desc& d);
 
 // The second stream of a pipelined call on the device of the caller's stream,

@@ -21,7 +21,9 @@
 // scores, and u as float32.
 //
 // The call then runs the chunked update and readout stages of the gated form
-// over (q, k, u, lambda).  For 16-bit inputs the update takes u in float32 (it
+// over (q, k, u, lambda), on the gated prefill's schedule: with the scan in
+// segments on a second stream, overlapped with the update and readout of the
+// segments already scanned, unless the caller asks for serial stages.  For 16-bit inputs the update takes u in float32 (it
 // stages every value as three bfloat16 terms, so the states stay float32
 // exact) and the readout a bfloat16 copy of u (for its in-chunk part, which
 // rounds values to bfloat16 in the gated form too); float32 inputs run the
@@ -65,6 +67,7 @@ struct DeltaP {
 
 template <int DK, int DV, typename Tin>
 __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a, PrefillWS w,
+                                                                  int tb, int te,
                                                                   const float* __restrict__ beta,
                                                                   float* __restrict__ U,
                                                                   bf16_t* __restrict__ U16) {
@@ -100,11 +103,21 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
 
   Meta M = meta_at(a.cache + a.meta_offset + (size_t)h * a.meta_stride, C);
   InitView iv = init_at(w, h, C);
+  // tokens [tb, te); a segment after the first resumes from the carry the
+  // previous one left in the workspace (the bookkeeping, and the newest state
+  // in this kernel's own thread order)
+  ScarryView sv = scarry_at(w, h, C);
   const int m0 = min(max(*iv.m0, 0), C);
   for (int j = tid; j < C; j += DTHR) {
-    sIb[j] = j < m0 ? M.ibar[j] : 0.0;
-    sN[j] = j < m0 ? M.n[j] : 0;
-    sLead[j] = j - m0;  // states present before the call: negative leaders
+    if (tb == 0) {
+      sIb[j] = j < m0 ? M.ibar[j] : 0.0;
+      sN[j] = j < m0 ? M.n[j] : 0;
+      sLead[j] = j - m0;  // states present before the call: negative leaders
+    } else {
+      sIb[j] = sv.ibar[j];
+      sN[j] = sv.n[j];
+      sLead[j] = sv.lead[j];
+    }
   }
   // the newest state at the start of the call, true (decayed) values
   float S[RB][CB];
@@ -112,7 +125,12 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
   for (int i = 0; i < RB; ++i)
 #pragma unroll
     for (int j = 0; j < CB; ++j) S[i][j] = 0.f;
-  if (m0 > 0) {
+  if (tb > 0) {
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+#pragma unroll
+      for (int j = 0; j < CB; ++j) S[i][j] = sv.S[((size_t)tid * RB + i) * CB + j];
+  } else if (m0 > 0) {
     const float* src =
         a.desc.state_dtype == DLA_BF16
             ? reinterpret_cast<const float*>(a.cache + a.open_offset) + (size_t)h * D
@@ -124,7 +142,7 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
 #pragma unroll
       for (int j = 0; j < CB; ++j) S[i][j] = f * src[(size_t)(rb * RB + i) * DV + cb * CB + j];
   }
-  int m = m0;
+  int m = tb > 0 ? min(max(*sv.m, 0), C) : m0;
 
   const Tin* Kin = static_cast<const Tin*>(a.k) + tok0 * DK;
   const Tin* Vin = static_cast<const Tin*>(a.v) + tok0 * DV;
@@ -134,8 +152,8 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
   float* Uh = U + tok0 * DV;
   bf16_t* U16h = U16 ? U16 + tok0 * DV : nullptr;  // bfloat16 copy (16-bit inputs)
 
-  for (int c0 = 0; c0 < T; c0 += DSL) {
-    const int nr = min(DSL, T - c0);
+  for (int c0 = tb; c0 < te; c0 += DSL) {
+    const int nr = min(DSL, te - c0);
     __syncthreads();  // the previous round is done with the staged tokens
     for (int i = tid; i < nr * DK; i += DTHR) sK[i] = to_f32(Kin[(size_t)c0 * DK + i]);
     for (int i = tid; i < nr * DV; i += DTHR) sV[i] = to_f32(Vin[(size_t)c0 * DV + i]);
@@ -305,6 +323,20 @@ __global__ __launch_bounds__(DTHR) void prefill_delta_scan_kernel(PrefillArgs a,
     }
   }
   __syncthreads();
+  if (te < T) {
+    // the carry for the next segment
+    for (int j = tid; j < C; j += DTHR) {
+      sv.ibar[j] = sIb[j];
+      sv.n[j] = sN[j];
+      sv.lead[j] = sLead[j];
+    }
+    if (tid == 0) *sv.m = m;
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+#pragma unroll
+      for (int j = 0; j < CB; ++j) sv.S[((size_t)tid * RB + i) * CB + j] = S[i][j];
+    return;
+  }
   for (int j = tid; j < m; j += DTHR) {
     M.n[j] = sN[j];
     M.ibar[j] = sIb[j];
@@ -324,37 +356,47 @@ size_t prefill_delta_scan_smem(const dla_cache_desc& d) {
 }
 
 template <int DK, int DV, typename Tin>
-static hipError_t launch_delta_scan_t(const PrefillArgs& a, const PrefillWS& w, const float* beta,
-                                      float* U, bf16_t* U16, hipStream_t s) {
+static hipError_t launch_delta_scan_t(const PrefillArgs& a, const PrefillWS& w, int tb, int te,
+                                      const float* beta, float* U, bf16_t* U16, hipStream_t s) {
   const size_t shm = DeltaP<DK, DV>::smem_bytes(a.desc.C);
   if (shm > 160 * 1024) return hipErrorInvalidValue;
   auto k = prefill_delta_scan_kernel<DK, DV, Tin>;
   if (hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm) !=
       hipSuccess)
     return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k, dim3(a.desc.B * a.desc.H), dim3(DTHR), shm, s, a, w, beta, U, U16);
+  hipLaunchKernelGGL(k, dim3(a.desc.B * a.desc.H), dim3(DTHR), shm, s, a, w, tb, te, beta, U, U16);
   return hipGetLastError();
 }
 
 template <int DK, int DV>
-static hipError_t launch_delta_scan_dims(const PrefillArgs& a, const PrefillWS& w,
+static hipError_t launch_delta_scan_dims(const PrefillArgs& a, const PrefillWS& w, int tb, int te,
                                          const float* beta, float* U, bf16_t* U16,
                                          hipStream_t s) {
-  if (a.in_dtype == DLA_F32) return launch_delta_scan_t<DK, DV, float>(a, w, beta, U, U16, s);
-  return launch_delta_scan_t<DK, DV, bf16_t>(a, w, beta, U, U16, s);
+  if (a.in_dtype == DLA_F32) return launch_delta_scan_t<DK, DV, float>(a, w, tb, te, beta, U, U16, s);
+  return launch_delta_scan_t<DK, DV, bf16_t>(a, w, tb, te, beta, U, U16, s);
 }
 
-// Workspace of a delta-form prefill: the stages' workspace (serial; the
-// float32 stages for float32 inputs), then the write vectors u (float32), and
-// for 16-bit inputs a bfloat16 copy of them.
+static hipError_t launch_delta_scan(const PrefillArgs& a, const PrefillWS& w, int tb, int te,
+                                    const float* beta, float* U, bf16_t* U16, hipStream_t s) {
+  const int dk = a.desc.d_k, dv = a.desc.d_v;
+  if (dk == 128 && dv == 128) return launch_delta_scan_dims<128, 128>(a, w, tb, te, beta, U, U16, s);
+  if (dk == 64 && dv == 64) return launch_delta_scan_dims<64, 64>(a, w, tb, te, beta, U, U16, s);
+  if (dk == 128 && dv == 64) return launch_delta_scan_dims<128, 64>(a, w, tb, te, beta, U, U16, s);
+  return launch_delta_scan_dims<64, 128>(a, w, tb, te, beta, U, U16, s);
+}
+
+// Workspace of a delta-form prefill: the stages' workspace (for the serial or
+// the pipelined plan; the float32 stages for float32 inputs), then the write
+// vectors u (float32), and for 16-bit inputs a bfloat16 copy of them.
 struct DeltaWS {
   size_t u, u16, total;
 };
 
-static DeltaWS delta_ws(const dla_cache_desc& d, int T, dla_dtype in, bool readout, size_t budget) {
+static DeltaWS delta_ws(const dla_cache_desc& d, int T, dla_dtype in, bool readout, bool serial,
+                        size_t budget) {
   DeltaWS r;
   const size_t nh = (size_t)d.B * d.H;
-  size_t off = round_up(prefill_workspace_bytes(d, T, in, readout, true, budget), 256);
+  size_t off = round_up(prefill_workspace_bytes(d, T, in, readout, serial, budget), 256);
   r.u = off;
   off = round_up(off + nh * T * d.d_v * 4, 256);
   r.u16 = off;
@@ -364,44 +406,81 @@ static DeltaWS delta_ws(const dla_cache_desc& d, int T, dla_dtype in, bool reado
 }
 
 size_t prefill_delta_workspace_bytes(const dla_cache_desc& d, int T, dla_dtype in, bool readout,
-                                     size_t budget) {
-  return delta_ws(d, T, in, readout, budget).total;
+                                     bool serial, size_t budget) {
+  return delta_ws(d, T, in, readout, serial, budget).total;
 }
 
+// The stages of the gated prefill's schedule: serial (frames, the whole scan,
+// then update and readout segment by segment, on s), or pipelined (the scan
+// segment by segment on a second stream forked from s after the frames, and
+// segment k's update and readout on s after scan segment k; the last
+// segment's wait joins the second stream into s, and so does every error
+// path after the fork).
 hipError_t launch_prefill_delta(const PrefillArgs& a, const float* beta, hipStream_t s) {
   const bool readout = !a.skip_readout;
   const bool wide = a.in_dtype != DLA_F32;
-  const DeltaWS L = delta_ws(a.desc, a.T, a.in_dtype, readout, a.pool_budget);
+  const bool serial = a.serial != 0;
+  const DeltaWS L = delta_ws(a.desc, a.T, a.in_dtype, readout, serial, a.pool_budget);
   const size_t nh = (size_t)a.desc.B * a.desc.H;
   char* base = a.workspace;
   float* U = reinterpret_cast<float*>(base + L.u);
   bf16_t* U16 = wide && readout ? reinterpret_cast<bf16_t*>(base + L.u16) : nullptr;
   // the update takes u (float32), the readout u in the inputs' type
   PrefillArgs fu = a;
-  fu.serial = 1;
   fu.v = U;
   fu.v_f32 = wide ? 1 : 0;
   PrefillArgs fr = fu;
   fr.v_f32 = 0;
   if (wide) fr.v = U16;
-  const SegPlan p = seg_plan(a.desc, a.T, a.in_dtype, readout, true, a.pool_budget);
+  const bool pipe = pipelined(a.T, a.in_dtype, readout, serial);
+  SegPlan p = seg_plan(a.desc, a.T, a.in_dtype, readout, serial, a.pool_budget);
+  if (pipe && p.shared) {
+    // Here the scan is the long stage (its sequential chain per token takes
+    // about three times the update and readout), so the segments stay at the
+    // ramp's first size instead of growing: what remains after the scan, the
+    // last segment's update and readout, is then short.  The pool is shared,
+    // so the segments change neither the workspace nor the results.
+    p.fit = p.first;
+    p.nseg = 0;
+    p.nch_seg = 0;
+    for (int b = 0; b < p.nch; ++p.nseg) {
+      const int n = ramp_size(p.first, p.fit, p.nseg, p.nch - b);
+      p.nch_seg = n > p.nch_seg ? n : p.nch_seg;
+      b += n;
+    }
+  }
   const PrefillWS w = ws_layout(base, nh, a.T, a.desc.C, a.desc.d_k * a.desc.d_v, p.nch);
   hipError_t e;
   if ((e = launch_prefill_prep(fu, s)) != hipSuccess) return e;
-  const int dk = a.desc.d_k, dv = a.desc.d_v;
-  if (dk == 128 && dv == 128)
-    e = launch_delta_scan_dims<128, 128>(a, w, beta, U, U16, s);
-  else if (dk == 64 && dv == 64)
-    e = launch_delta_scan_dims<64, 64>(a, w, beta, U, U16, s);
-  else if (dk == 128 && dv == 64)
-    e = launch_delta_scan_dims<128, 64>(a, w, beta, U, U16, s);
-  else
-    e = launch_delta_scan_dims<64, 128>(a, w, beta, U, U16, s);
-  if (e != hipSuccess) return e;
-  for (int seg = 0; seg < p.nseg; ++seg) {
-    if ((e = launch_prefill_update(fu, p, seg, s)) != hipSuccess) return e;
-    if (readout && (e = launch_prefill_readout(fr, p, seg, s)) != hipSuccess) return e;
+  hipStream_t side = s;
+  hipEvent_t* pev = nullptr;
+  bool forked = false;
+  auto fail = [&](hipError_t err) -> hipError_t {
+    if (forked && hipEventRecord(pev[0], side) == hipSuccess) (void)hipStreamWaitEvent(s, pev[0], 0);
+    return err;
+  };
+  if (pipe) {
+    if ((e = pipe_resources(s, p.nseg + 1, &side, &pev)) != hipSuccess) return e;
+    if ((e = hipEventRecord(pev[0], s)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(side, pev[0], 0)) != hipSuccess) return e;
+    forked = true;
+    for (int seg = 0; seg < p.nseg; ++seg) {
+      int cs, ce;
+      seg_range(p, seg, &cs, &ce);
+      const int te = (seg + 1 == p.nseg) ? a.T : ce * p.RL;
+      if ((e = launch_delta_scan(a, w, cs * p.RL, te, beta, U, U16, side)) != hipSuccess)
+        return fail(e);
+      if ((e = hipEventRecord(pev[1 + seg], side)) != hipSuccess) return fail(e);
+    }
+  } else if ((e = launch_delta_scan(a, w, 0, a.T, beta, U, U16, s)) != hipSuccess) {
+    return e;
   }
+  for (int seg = 0; seg < p.nseg; ++seg) {
+    if (pipe && (e = hipStreamWaitEvent(s, pev[1 + seg], 0)) != hipSuccess) return fail(e);
+    if ((e = launch_prefill_update(fu, p, seg, s)) != hipSuccess) return fail(e);
+    if (readout && (e = launch_prefill_readout(fr, p, seg, s)) != hipSuccess) return fail(e);
+  }
+  // (the last segment's wait on pev[nseg] has joined the second stream)
   return hipSuccess;
 }
 

@@ -232,12 +232,12 @@ def workspace_bytes(cache: StateCache, T: int, dtype=None, skip_readout: bool = 
 
 
 def delta_workspace_bytes(cache: StateCache, T: int, dtype=None, skip_readout: bool = False,
-                          pool_budget_log2: int = 0) -> int:
+                          pool_budget_log2: int = 0, serial: bool = False) -> int:
     """dla_prefill_delta workspace for T tokens of input dtype (default bf16)."""
     code = DLA_BF16 if dtype is None else _dtype_code(dtype)
     n = ctypes.c_size_t(0)
     _check(lib().dla_prefill_delta_workspace_size(ctypes.byref(cache.desc), int(T), code,
-                                                  _flags(skip_readout, False, pool_budget_log2),
+                                                  _flags(skip_readout, serial, pool_budget_log2),
                                                   ctypes.byref(n)),
            "dla_prefill_delta_workspace_size")
     return int(n.value)
@@ -438,10 +438,10 @@ def prefill_delta(cache: StateCache, q, k, v, g, beta, lam=None, *, tau: float =
                   eps: float = 1e-6, eps_rms: float = 1e-6, out=None, out_dtype=None,
                   skip_readout: bool = False, boundary=None, merge_idx=None, score=None,
                   boundary_override=None, merge_override=None, workspace=None,
-                  want_exports: bool = True, pool_budget_log2: int = 0):
+                  want_exports: bool = True, pool_budget_log2: int = 0, serial: bool = False):
     """dla_prefill_delta: T tokens per head in the Gated DeltaNet form.  Shapes
-    as prefill; beta: [B, H, T] float32.  The workspace is allocated when none
-    (or one too small) is given."""
+    as prefill; beta: [B, H, T] float32; serial: DLA_SERIAL_STAGES.  The
+    workspace is allocated when none (or one too small) is given."""
     torch = _torch()
     B, H, C = cache.B, cache.H, cache.C
     T = k.shape[2]
@@ -463,10 +463,10 @@ def prefill_delta(cache: StateCache, q, k, v, g, beta, lam=None, *, tau: float =
                                                                         device=dev)
         score = score if score is not None else torch.empty((B, H, T), dtype=torch.float32,
                                                             device=dev)
-    wsb = delta_workspace_bytes(cache, T, k.dtype, skip_readout, pool_budget_log2)
+    wsb = delta_workspace_bytes(cache, T, k.dtype, skip_readout, pool_budget_log2, serial)
     if workspace is None or workspace.numel() < wsb:
         workspace = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
-    p = _params(tau, eps, eps_rms, skip_readout, pool_budget_log2=pool_budget_log2)
+    p = _params(tau, eps, eps_rms, skip_readout, serial=serial, pool_budget_log2=pool_budget_log2)
     st = lib().dla_prefill_delta(ctypes.byref(cache.desc), _ptr(cache.buf), _ptr(q), _ptr(k),
                                  _ptr(v), _ptr(g), _ptr(beta), _ptr(lam), int(T),
                                  _dtype_code(k.dtype), ctypes.byref(p), _ptr(out),

@@ -251,8 +251,8 @@ def test_delta_prefill_full_size_sampled_heads():
     serr = np.abs(sc.cpu().numpy().reshape(nh, w.T)[heads] - dec["score"]).max()
     assert serr < H.DELTA_B / 10, f"score error {serr}"
     # windows inside a chunk (512 tokens), across the start of a later segment
-    # of the serial stages, the last segment's first tokens and the end
-    seg_starts = dla.prefill_segment_starts(cache, w.T, torch.bfloat16, serial=True)
+    # of the pipelined call, the last segment's first tokens and the end
+    seg_starts = dla.prefill_segment_starts(cache, w.T, torch.bfloat16)
     toks, wins = windows(w.T, 512, seg_starts)
     og = out.float().reshape(nh, w.T, w.dv)[heads][:, toks].cpu().numpy()
     del q, k, v, g, lam, out
@@ -311,3 +311,66 @@ def _random_cases(n, seed):
                          ids=[f"delta_random{i}" for i in range(16)])
 def test_delta_random_shapes(w, mode, no_lambda, state_dtype):
     _case(w, mode, state_dtype=state_dtype, no_lambda=no_lambda)
+
+
+def _bits_equal(a, b):
+    torch = _torch()
+    if a.dtype in (torch.bfloat16, torch.float16):
+        return torch.equal(a.view(torch.int16), b.view(torch.int16))
+    if a.dtype == torch.float32:
+        return torch.equal(a.view(torch.int32), b.view(torch.int32))
+    return torch.equal(a, b)
+
+
+@pytest.mark.parametrize("case", ["bf16_ragged", "f32", "continuation", "small_budgets"])
+def test_delta_pipelined_matches_serial(case):
+    """The delta form's pipelined prefill (scan segments on a second stream,
+    each resuming from the carry of the one before) gives bit-identical
+    outputs, exports and caches to the serial one: ragged last chunk, float32
+    inputs (256-token chunks), a continuation on a non-empty cache, and small
+    state-copy budgets that split both calls into many segments, differently."""
+    torch = _torch()
+    from paper_2606_10650_amd import dla
+    budgets = (0, 0)
+    cut = None
+    if case == "bf16_ragged":
+        w = WORKLOADS["cfg3"].replace(B=1, H=3, T=2600, C=24, span_mean=200.0)
+    elif case == "f32":
+        w = WORKLOADS["cfg1"].replace(T=1000)
+    elif case == "continuation":
+        w, cut = WORKLOADS["cfg2"].replace(B=1, H=2, T=2900, C=16), 1100
+    else:
+        # 4 heads x 128 states x 32 KiB: 16 MiB of copies per chunk; budgets of
+        # 64 MiB (pipelined) and 32 MiB (serial)
+        w = WORKLOADS["cfg3"].replace(B=1, H=4, T=5000)
+        budgets = (26, 25)
+    x = make_inputs(w)
+    beta = make_beta(w)
+    q, k, v, g, lam = H.inputs_to_device(w, x, w.B, w.H)
+    bt = torch.from_numpy(beta).reshape(w.B, w.H, w.T).cuda()
+    cuts = [0, w.T] if cut is None else [0, cut, w.T]
+    res = {}
+    for serial in (False, True):
+        kb = budgets[1 if serial else 0]
+        cache = dla.cache_alloc(w.B, w.H, w.C, w.dk, w.dv)
+        outs = []
+        for a, b in zip(cuts[:-1], cuts[1:]):
+            sl = lambda t: t[:, :, a:b].contiguous()
+            nseg = dla.prefill_segments(cache, b - a, k.dtype, serial=serial, pool_budget_log2=kb)
+            o, bd, mi, sc = dla.prefill_delta(cache, sl(q), sl(k), sl(v), sl(g), sl(bt), sl(lam),
+                                              tau=w.tau, serial=serial, pool_budget_log2=kb)
+            torch.cuda.synchronize()
+            outs.append((o.cpu(), bd.cpu(), mi.cpu(), sc.cpu(), nseg))
+        res[serial] = (outs, dla.cache_export(cache))
+    (op, cp), (os_, cs) = res[False], res[True]
+    print(f"[delta-pipe] {case} segments pipelined={[o[4] for o in op]} serial={[o[4] for o in os_]}",
+          flush=True)
+    # (the counts are dla_prefill's plan; the delta call splits a shared pool's
+    # call into at least as many segments)
+    assert any(o[4] > 1 for o in op)
+    for a, b in zip(op, os_):
+        for ta, tb in zip(a[:4], b[:4]):
+            assert _bits_equal(ta, tb), case
+    for key in cp:
+        assert np.array_equal(cp[key], cs[key]), (case, key)
+    assert int(os_[-1][1].sum()) > 1
