@@ -567,8 +567,8 @@ def main():
                     help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the DLA layer shards over (batch, head) with no "
-              "exchange between GPUs, and this build runs on a single MI355X (--gpus 1).",
+        print("bench.py measures one GPU only (--gpus 1): the DLA layer shards over (batch, head) "
+              "with no exchange between GPUs, so N GPUs run N independent shares of the heads.",
               file=sys.stderr)
         sys.exit(2)
     import torch
