@@ -12,7 +12,7 @@
 // unchanged.  The pseudo-values depend on the newest state before each token,
 // which depends on every earlier decision, so they come from a sequential scan
 // that keeps the newest state on chip: one 512-thread workgroup per head, each
-// thread holding a (d_k / 16) x (d_v / 32) block of the state in registers.
+// thread holding a (d_k / 8) x (d_v / 64) block of the state in registers.
 // Per token it forms y = (alpha S)^T k and the score's three scalars (a =
 // |k|^2 |v|^2, b = |alpha S|^2, c = y . v), decides (Alg. 1, with Alg. 2 at a
 // full cache), and applies the rank-one step with u.  It emits the decisions,
@@ -23,11 +23,11 @@
 // The call then runs the chunked update and readout stages of the gated form
 // over (q, k, u, lambda), on the gated prefill's schedule: with the scan in
 // segments on a second stream, overlapped with the update and readout of the
-// segments already scanned, unless the caller asks for serial stages.  For 16-bit inputs the update takes u in float32 (it
-// stages every value as three bfloat16 terms, so the states stay float32
-// exact) and the readout a bfloat16 copy of u (for its in-chunk part, which
-// rounds values to bfloat16 in the gated form too); float32 inputs run the
-// float32 stages on u.
+// segments already scanned, unless the caller asks for serial stages.  For
+// 16-bit inputs the update takes u in float32 (it stages every value as three
+// bfloat16 terms, so the states stay float32 exact) and the readout a bfloat16
+// copy of u (for its in-chunk part, which rounds values to bfloat16 in the
+// gated form too); float32 inputs run the float32 stages on u.
 #include "prefill.h"
 
 namespace dla {
