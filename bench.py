@@ -567,7 +567,7 @@ def main():
                     help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only (--gpus 1): the DLA layer shards over (batch, head) "
+        print("bench.py measures a single GPU (--gpus 1): the DLA layer shards over (batch, head) "
               "with no exchange between GPUs, so N GPUs run N independent shares of the heads.",
               file=sys.stderr)
         sys.exit(2)
